@@ -1,0 +1,245 @@
+/*
+ * spla.h - C ABI of the SPLA decode-step library for AMD Instinct MI355X
+ * (gfx950).
+ *
+ * SPLA ("Block Sparse Plus Linear Attention", arXiv 2601.22379) answers one
+ * decode query per attention head by
+ *   1. scoring every KV block with a second-order Taylor estimate of its
+ *      attention mass built from the block's key mean and diagonal
+ *      covariance (Sec. 3.1, Eqs. 8-10), summed over the GQA group after a
+ *      per-head normalisation (Sec. 2.2, Eq. 6);
+ *   2. selecting the top-k blocks per KV head, with a forced sink block and
+ *      the most recent blocks (Sec. 2.1 Eq. 3; Sec. 4 "Sparsity
+ *      Specifications");
+ *   3. running exact softmax attention over the selected blocks (Eq. 5) and,
+ *      from the same read of those blocks, their linear-attention term
+ *      (Eq. 16);
+ *   4. forming the residual linear attention by subtraction from the global
+ *      linear-attention state (Eqs. 14-15) and adding its RMSNorm to the exact
+ *      output (Sec. 3.3).
+ * The append call maintains what step 1 and step 4 read: the per-block key
+ * statistics and the global state S_bar = sum_t phi(k_t)^T v_t (Eq. 15),
+ * with phi the softmax over the feature dimension (Sec. 3.2).
+ *
+ * Conventions shared by every call:
+ *  - The library owns no memory. Every buffer is allocated by the caller;
+ *    "device" pointers are HIP device memory of the current device, "host"
+ *    pointers are ordinary host memory.
+ *  - Every argument check happens on the host before anything is enqueued
+ *    and returns a negative spla_status; nothing is enqueued on failure.
+ *  - Work is enqueued on `stream` (a hipStream_t; NULL is the null stream)
+ *    and is asynchronous. Calls on one stream execute in order. Two calls
+ *    that share a cache or a workspace must not run concurrently.
+ *  - No C++ exception crosses this interface.
+ *  - Conditions only the device can see (an append that would overflow the
+ *    capacity) set bits in cache->err_flags (if non-NULL) and are otherwise
+ *    handled as documented at the call.
+ */
+#ifndef SPLA_H_
+#define SPLA_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ------------------------------------------------------------------ status */
+typedef enum spla_status {
+  SPLA_OK = 0,
+  SPLA_ERR_INVALID_ARG = -1, /* NULL pointer, inconsistent or out-of-range value */
+  SPLA_ERR_UNSUPPORTED = -2, /* valid, but a shape this build does not implement */
+  SPLA_ERR_CAPACITY = -3,    /* a size exceeds the cache capacity or a library limit */
+  SPLA_ERR_WORKSPACE = -4,   /* workspace NULL, too small or misaligned */
+  SPLA_ERR_HIP = -5          /* the HIP runtime reported an error at launch */
+} spla_status;
+
+typedef enum spla_dtype { SPLA_F32 = 0, SPLA_BF16 = 1 } spla_dtype;
+
+/* cfg.flags: the ablations of Sec. 4 "Baselines" */
+enum {
+  SPLA_FLAG_NO_RLA = 1u,        /* SPA: output = exact sparse branch only */
+  SPLA_FLAG_FIRST_ORDER = 2u,   /* block score with Eq. 11 (mean only) instead of Eq. 10 */
+  SPLA_FLAG_RLA_NORMALIZE = 4u  /* divide the residual by <phi(q), z_bar - z_selected> */
+};
+
+/* err_flags bits written by the device */
+enum { SPLA_DEVERR_CAPACITY = 1 };
+
+/* Library limits of this build. */
+enum {
+  SPLA_MAX_GROUP = 16,      /* query heads per KV head */
+  SPLA_MAX_TOP_K = 256,     /* selected blocks per KV head */
+  SPLA_MAX_BLOCKS = 32768,  /* blocks per sequence (max_seq_len / block_size) */
+  SPLA_WORKSPACE_ALIGN = 256
+};
+
+/* ------------------------------------------------------------------ config */
+typedef struct spla_config {
+  int32_t batch;          /* sequences decoded together, >= 1 */
+  int32_t n_q_heads;      /* Hq, a multiple of n_kv_heads */
+  int32_t n_kv_heads;     /* Hkv; G = Hq / Hkv query heads share a KV head and one
+                             block selection (Sec. 2.2); 1 <= G <= SPLA_MAX_GROUP */
+  int32_t head_dim;       /* d: 64 or 128 */
+  int32_t block_size;     /* B, the selection granularity (Sec. 2.1): 32, 64 or 128 */
+  int32_t top_k;          /* k blocks selected per KV head, forced blocks included;
+                             n_sink + n_local <= k <= SPLA_MAX_TOP_K */
+  int32_t n_sink_blocks;  /* always-selected leading blocks (paper: 1) */
+  int32_t n_local_blocks; /* always-selected most recent blocks (paper: 4) */
+  int32_t max_seq_len;    /* per-sequence capacity in tokens, a multiple of B,
+                             at most SPLA_MAX_BLOCKS * B */
+  int32_t dtype;          /* spla_dtype of q, out and the K/V cache */
+  float softmax_scale;    /* s; <= 0 selects 1/sqrt(head_dim). Scales the exact
+                             logits and the query inside the block score */
+  float rms_eps;          /* epsilon of the RMSNorm on the residual, >= 0 (1e-6) */
+  uint32_t flags;         /* SPLA_FLAG_* */
+} spla_config;
+
+/* ------------------------------------------------------------------- cache
+ * Caller-owned device buffers that persist across calls. Sizes in bytes are
+ * given by spla_cache_bytes (index in brackets). Let nb_cap = max_seq_len / B
+ * and n_tiles = ceil(nb_cap / 64).
+ *  [0] k_cache   dtype [batch][Hkv][max_seq_len][d]       token-major keys
+ *  [1] v_cache   dtype [batch][Hkv][nb_cap][d][B]         values, transposed
+ *                inside each block: element (token t, coord c) is at
+ *                [t / B][c][t % B]
+ *  [2] blk_stats fp32  [batch][Hkv][n_tiles][2][d/4][64][4]
+ *                part 0 the block key mean, part 1 the block's sum of
+ *                squared deviations from it (M2; variance = M2 / n_i). Block
+ *                i of a sequence is entry i % 64 of tile i / 64: for each
+ *                group of four coordinates, 64 consecutive blocks are stored
+ *                side by side
+ *  [3] lin_state fp32  [batch][Hkv][d][d]  S_bar[j][c] = sum_t phi(k_t)_j v_t,c (Eq. 15)
+ *  [4] lin_norm  fp32  [batch][Hkv][d]     z_bar = sum_t phi(k_t)
+ *  [5] seq_lens  int32 [batch]             tokens held by each sequence
+ * err_flags: int32 [1] or NULL; SPLA_DEVERR_* bits are OR-ed in, never cleared
+ * by the library.
+ * A zero-filled cache (spla_reset) is the empty cache.
+ */
+typedef struct spla_cache {
+  void* k_cache;
+  void* v_cache;
+  float* blk_stats;
+  float* lin_state;
+  float* lin_norm;
+  int32_t* seq_lens;
+  int32_t* err_flags;
+} spla_cache;
+
+enum { SPLA_CACHE_NUM_BUFFERS = 6 };
+
+/* Kernel phases that spla_decode_ex / spla_step_ex can bracket with events. */
+enum {
+  SPLA_PHASE_APPEND = 0, /* single-token append of spla_step */
+  SPLA_PHASE_SCORE = 1,  /* block statistics stream -> per-head block mass */
+  SPLA_PHASE_SELECT = 2, /* group score, top-k */
+  SPLA_PHASE_SPARSE = 3, /* fused exact + selected-linear pass over the selected blocks */
+  SPLA_PHASE_MERGE = 4,  /* split merge, residual, RMSNorm, output */
+  SPLA_PHASE_LINEAR = 5, /* o_bar = phi(q) S_bar */
+  SPLA_NUM_PHASES = 8
+};
+
+/* Optional timing hooks: each non-NULL start[p] / stop[p] (a hipEvent_t) is
+ * recorded on the call's stream right before / after the launch(es) of phase
+ * p. A phase the library does not launch separately records nothing. */
+typedef struct spla_events {
+  void* start[SPLA_NUM_PHASES];
+  void* stop[SPLA_NUM_PHASES];
+} spla_events;
+
+/* ---------------------------------------------------------- host-only calls */
+
+/* Text of a status code (static storage). */
+const char* spla_status_string(int32_t status);
+
+/* Name of a phase id ("score", ...), or NULL for an unused id. */
+const char* spla_phase_name(int32_t phase);
+
+/* Checks cfg against the limits above. Host only; touches no device. */
+int32_t spla_validate(const spla_config* cfg);
+
+/* Bytes of each cache buffer, out_bytes[SPLA_CACHE_NUM_BUFFERS] (host array),
+ * in the order listed at spla_cache. Host only. */
+int32_t spla_cache_bytes(const spla_config* cfg, size_t* out_bytes);
+
+/* Device workspace that spla_decode / spla_step need (host-only query). */
+int32_t spla_workspace_bytes(const spla_config* cfg, size_t* out_bytes);
+
+/* Device workspace that spla_append needs for up to max_new tokens per
+ * sequence (host-only query). */
+int32_t spla_append_workspace_bytes(const spla_config* cfg, int32_t max_new, size_t* out_bytes);
+
+/* ---------------------------------------------------------- device calls */
+
+/* Empties the cache: zero-fills blk_stats, lin_state, lin_norm and seq_lens
+ * (K/V rows are left as they are; they are never read past seq_lens). */
+int32_t spla_reset(const spla_config* cfg, const spla_cache* cache, void* stream);
+
+/* Appends tokens to every (sequence, KV head) (Sec. 3.1 statistics; Eq. 15).
+ *  k_new, v_new: device, dtype [batch][Hkv][max_new][d], token-major; only the
+ *                first n_b rows of sequence b are read.
+ *  n_new:        device int32 [batch] (n_b, 0 <= n_b <= max_new), or NULL for
+ *                n_b = max_new for every sequence.
+ *  workspace:    device, at least spla_append_workspace_bytes(cfg, max_new),
+ *                256-byte aligned.
+ * For each sequence b with length L_b = seq_lens[b], the tokens land at
+ * positions L_b .. L_b + n_b - 1: key rows go to k_cache, value rows to
+ * v_cache, the statistics of every touched block are updated (Chan's
+ * parallel combination of mean and M2, computed in fp64), S_bar and z_bar
+ * receive phi(k_t)^T v_t and phi(k_t) of every new token (partial sums over
+ * token chunks, reduced in a fixed order: deterministic), and seq_lens[b]
+ * becomes L_b + n_b. Tokens that would exceed max_seq_len are dropped and
+ * SPLA_DEVERR_CAPACITY is set in err_flags. */
+int32_t spla_append(const spla_config* cfg, const spla_cache* cache,
+                    const void* k_new, const void* v_new, int32_t max_new,
+                    const int32_t* n_new, void* workspace, size_t workspace_bytes,
+                    void* stream);
+
+/* One SPLA decode step for every sequence (Secs. 2.1-2.2, 3.1-3.3).
+ *  q:          device, dtype [batch][Hq][d]; query head m reads KV head m / G.
+ *  rms_weight: device fp32 [Hq][d], the RMSNorm weight gamma.
+ *  out:        device, dtype [batch][Hq][d] (may not alias q).
+ *  sel_idx:    device int32 [batch][Hkv][top_k] or NULL: the selected block
+ *              ids of each KV head in ascending order, padded with -1 when a
+ *              sequence has fewer than top_k blocks.
+ *  workspace:  device, at least spla_workspace_bytes(cfg), 256-byte aligned.
+ * For each sequence with L = seq_lens[b] tokens, nb = ceil(L / B) blocks:
+ * if nb <= top_k every block is selected and the output is exact attention;
+ * otherwise the sink and local blocks plus the top-scored remaining blocks
+ * (ties to the lower block id) are selected, and
+ *   out = o_sparse + gamma * r / sqrt(mean(r^2) + eps),  r = o_bar - o_tilde.
+ * A sequence with L = 0 yields a zero output and no selection.
+ * The cache is only read. */
+int32_t spla_decode(const spla_config* cfg, const spla_cache* cache, const void* q,
+                    const float* rms_weight, void* out, int32_t* sel_idx,
+                    void* workspace, size_t workspace_bytes, void* stream);
+
+/* spla_decode with optional timing events (events may be NULL). */
+int32_t spla_decode_ex(const spla_config* cfg, const spla_cache* cache, const void* q,
+                       const float* rms_weight, void* out, int32_t* sel_idx,
+                       void* workspace, size_t workspace_bytes, const spla_events* events,
+                       void* stream);
+
+/* Appends one token per (sequence, KV head), then decodes (Sec. 2: the query
+ * at position N attends to tokens 1..N, the new one included).
+ *  k_new, v_new: device, dtype [batch][Hkv][d].
+ * Equivalent to spla_append with max_new = 1 followed by spla_decode, with
+ * the single-token update done in place (no append workspace). A sequence
+ * already at capacity is not extended (SPLA_DEVERR_CAPACITY) and decodes
+ * over its current tokens. */
+int32_t spla_step(const spla_config* cfg, const spla_cache* cache, const void* k_new,
+                  const void* v_new, const void* q, const float* rms_weight, void* out,
+                  int32_t* sel_idx, void* workspace, size_t workspace_bytes, void* stream);
+
+/* spla_step with optional timing events (events may be NULL). */
+int32_t spla_step_ex(const spla_config* cfg, const spla_cache* cache, const void* k_new,
+                     const void* v_new, const void* q, const float* rms_weight, void* out,
+                     int32_t* sel_idx, void* workspace, size_t workspace_bytes,
+                     const spla_events* events, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SPLA_H_ */

@@ -1,0 +1,323 @@
+// Append path: key/value rows into the cache, block key statistics, and the
+// global linear-attention state S_bar = sum_t phi(k_t)^T v_t, z_bar =
+// sum_t phi(k_t) (Sec. 3.1 statistics, Sec. 3.2 Eq. 15, phi = softmax over
+// the feature dimension).
+#include "spla_device.h"
+#include "spla_kernels.h"
+
+namespace spla {
+
+// Tokens of sequence b this append really adds (clamped to the capacity).
+__device__ __forceinline__ int appended_count(const Dims& m, int L0, int max_new,
+                                              const int32_t* __restrict__ n_new, int b,
+                                              bool* clipped) {
+  int n = n_new ? n_new[b] : max_new;
+  n = n < 0 ? 0 : (n > max_new ? max_new : n);
+  int room = m.cap - L0;
+  room = room < 0 ? 0 : room;
+  *clipped = n > room;
+  return n < room ? n : room;
+}
+
+// One workgroup per touched block: copies the new rows of that block into
+// the caches and merges the block's statistics. The new tokens' mean and M2
+// are computed two-pass in fp64 and combined with the stored ones by Chan's
+// formula, then rounded to fp32.
+template <typename T>
+__global__ __launch_bounds__(128) void append_blocks_kernel(
+    Dims m, T* __restrict__ kc, T* __restrict__ vc, float* __restrict__ stats,
+    const int32_t* __restrict__ seq_lens, int32_t* __restrict__ err, const T* __restrict__ k_new,
+    const T* __restrict__ v_new, int max_new, const int32_t* __restrict__ n_new) {
+  const int bh = blockIdx.y;
+  const int b = bh / m.hkv;
+  const int L0 = seq_lens[b];
+  bool clipped;
+  const int ne = appended_count(m, L0, max_new, n_new, b, &clipped);
+  if (clipped && err && blockIdx.x == 0 && bh % m.hkv == 0 && threadIdx.x == 0)
+    atomicOr(err, (int)SPLA_DEVERR_CAPACITY);
+  const int i = L0 / m.B + (int)blockIdx.x;
+  const int t_lo = max(L0, i * m.B);
+  const int t_hi = min(L0 + ne, (i + 1) * m.B);
+  const int j = threadIdx.x;
+  if (t_hi <= t_lo || j >= m.d) return;
+  const int64_t src0 = ((int64_t)bh * max_new - L0) * m.d + j;  // row t at src0 + t*d
+
+  double sum = 0.0;
+  for (int t = t_lo; t < t_hi; ++t) {
+    const T kv = k_new[src0 + (int64_t)t * m.d];
+    kc[k_off(m, bh, t, j)] = kv;
+    vc[v_off(m, bh, t, j)] = v_new[src0 + (int64_t)t * m.d];
+    sum += (double)Elem<T>::load(&kv, 0);
+  }
+  const int nc = t_hi - t_lo;
+  const double mean_c = sum / nc;
+  double m2_c = 0.0;
+  for (int t = t_lo; t < t_hi; ++t) {
+    const double x = (double)Elem<T>::load(k_new, src0 + (int64_t)t * m.d) - mean_c;
+    m2_c += x * x;
+  }
+  const int na = t_lo - i * m.B;
+  const int64_t o_mean = stats_off4(m, bh, i, 0, j / 4) + (j & 3);
+  const int64_t o_m2 = stats_off4(m, bh, i, 1, j / 4) + (j & 3);
+  double mean = mean_c, m2 = m2_c;
+  if (na > 0) {
+    const double mean_a = stats[o_mean], m2_a = stats[o_m2];
+    const double n = (double)(na + nc);
+    const double delta = mean_c - mean_a;
+    mean = mean_a + delta * (nc / n);
+    m2 = m2_a + m2_c + delta * delta * ((double)na * nc / n);
+  }
+  stats[o_mean] = (float)mean;
+  stats[o_m2] = (float)m2;
+}
+
+// Partial linear-attention state of one chunk of new tokens:
+// P[j][c] = sum_t phi(k_t)_j v_t,c and Pz[j] = sum_t phi(k_t)_j, fp32.
+template <typename T, int D>
+__global__ __launch_bounds__(256) void append_state_partial_kernel(
+    Dims m, const int32_t* __restrict__ seq_lens, const T* __restrict__ k_new,
+    const T* __restrict__ v_new, int max_new, const int32_t* __restrict__ n_new, int n_chunks,
+    int chunk_tokens, float* __restrict__ part_s, float* __restrict__ part_z) {
+  constexpr int R = D / 16;
+  __shared__ float sE[kSubTokens][D + 1];
+  __shared__ float sV[kSubTokens][D + 1];
+  const int bh = blockIdx.y;
+  const int b = bh / m.hkv;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  bool clipped;
+  const int ne = appended_count(m, seq_lens[b], max_new, n_new, b, &clipped);
+  const int t0 = blockIdx.x * chunk_tokens;
+  const int t1 = min(t0 + chunk_tokens, ne);
+  const int tr = tid / 16, tc = tid % 16;
+  float acc[R][R];
+  float zacc[R];
+#pragma unroll
+  for (int a = 0; a < R; ++a) {
+    zacc[a] = 0.f;
+#pragma unroll
+    for (int c = 0; c < R; ++c) acc[a][c] = 0.f;
+  }
+  for (int tt = t0; tt < t1; tt += kSubTokens) {
+    const int nt = min(kSubTokens, t1 - tt);
+    for (int e = tid; e < kSubTokens * D; e += 256) {
+      const int row = e / D, col = e % D;
+      const int64_t src = ((int64_t)bh * max_new + tt + row) * D + col;
+      sE[row][col] = row < nt ? Elem<T>::load(k_new, src) : 0.f;
+      sV[row][col] = row < nt ? Elem<T>::load(v_new, src) : 0.f;
+    }
+    __syncthreads();
+    // phi(k) = softmax over the feature dimension, one row per wave step
+    for (int r = 0; r < kSubTokens / 4; ++r) {
+      const int row = w * (kSubTokens / 4) + r;
+      float x[D / 64];
+      float mx = -INFINITY;
+#pragma unroll
+      for (int e = 0; e < D / 64; ++e) {
+        x[e] = sE[row][lane + 64 * e];
+        mx = fmaxf(mx, x[e]);
+      }
+      mx = wave_max(mx);
+      float s = 0.f;
+#pragma unroll
+      for (int e = 0; e < D / 64; ++e) {
+        x[e] = expf(x[e] - mx);
+        s += x[e];
+      }
+      s = wave_sum(s);
+      const float inv = row < nt ? 1.0f / s : 0.f;
+#pragma unroll
+      for (int e = 0; e < D / 64; ++e) sE[row][lane + 64 * e] = x[e] * inv;
+    }
+    __syncthreads();
+    for (int t = 0; t < nt; ++t) {
+      float pv[R], vv[R];
+#pragma unroll
+      for (int a = 0; a < R; ++a) {
+        pv[a] = sE[t][tr * R + a];
+        vv[a] = sV[t][tc * R + a];
+      }
+#pragma unroll
+      for (int a = 0; a < R; ++a) {
+        zacc[a] += pv[a];
+#pragma unroll
+        for (int c = 0; c < R; ++c) acc[a][c] = fmaf(pv[a], vv[c], acc[a][c]);
+      }
+    }
+    __syncthreads();
+  }
+  float* ps = part_s + ((int64_t)bh * n_chunks + blockIdx.x) * D * D;
+#pragma unroll
+  for (int a = 0; a < R; ++a)
+#pragma unroll
+    for (int c = 0; c < R; ++c) ps[(tr * R + a) * D + tc * R + c] = acc[a][c];
+  if (tc == 0) {
+    float* pz = part_z + ((int64_t)bh * n_chunks + blockIdx.x) * D;
+#pragma unroll
+    for (int a = 0; a < R; ++a) pz[tr * R + a] = zacc[a];
+  }
+}
+
+// S_bar += sum of the chunk partials, accumulated in fp64 in chunk order.
+__global__ __launch_bounds__(256) void append_state_reduce_kernel(
+    Dims m, int n_chunks, const float* __restrict__ part_s, const float* __restrict__ part_z,
+    float* __restrict__ S, float* __restrict__ z) {
+  const int bh = blockIdx.y;
+  const int D = m.d;
+  const int row0 = blockIdx.x * 16;
+  for (int e = threadIdx.x; e < 16 * D; e += 256) {
+    const int row = row0 + e / D, col = e % D;
+    const int64_t o = ((int64_t)bh * D + row) * D + col;
+    double s = S[o];
+    for (int c = 0; c < n_chunks; ++c) s += part_s[(((int64_t)bh * n_chunks + c) * D + row) * D + col];
+    S[o] = (float)s;
+  }
+  if (threadIdx.x < 16) {
+    const int row = row0 + threadIdx.x;
+    double s = z[(int64_t)bh * D + row];
+    for (int c = 0; c < n_chunks; ++c) s += part_z[((int64_t)bh * n_chunks + c) * D + row];
+    z[(int64_t)bh * D + row] = (float)s;
+  }
+}
+
+// Single-token state update: S_bar += phi(k)^T v, z_bar += phi(k) (fp32).
+template <typename T, int D>
+__global__ __launch_bounds__(256) void append_state_rank1_kernel(
+    Dims m, const int32_t* __restrict__ seq_lens, const T* __restrict__ k_new,
+    const T* __restrict__ v_new, float* __restrict__ S, float* __restrict__ z) {
+  __shared__ float sphi[D];
+  __shared__ float sv[D];
+  const int bh = blockIdx.y;
+  const int b = bh / m.hkv;
+  if (seq_lens[b] >= m.cap) return;
+  const int tid = threadIdx.x;
+  if (tid < 64) {
+    float x[D / 64];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int e = 0; e < D / 64; ++e) {
+      x[e] = Elem<T>::load(k_new, (int64_t)bh * D + tid + 64 * e);
+      mx = fmaxf(mx, x[e]);
+    }
+    mx = wave_max(mx);
+    float s = 0.f;
+#pragma unroll
+    for (int e = 0; e < D / 64; ++e) {
+      x[e] = expf(x[e] - mx);
+      s += x[e];
+    }
+    s = wave_sum(s);
+#pragma unroll
+    for (int e = 0; e < D / 64; ++e) sphi[tid + 64 * e] = x[e] / s;
+  }
+  for (int c = tid; c < D; c += 256) sv[c] = Elem<T>::load(v_new, (int64_t)bh * D + c);
+  __syncthreads();
+  const int row0 = blockIdx.x * 16;
+  for (int e = tid; e < 16 * D; e += 256) {
+    const int row = row0 + e / D, col = e % D;
+    const int64_t o = ((int64_t)bh * D + row) * D + col;
+    S[o] = fmaf(sphi[row], sv[col], S[o]);
+  }
+  if (tid < 16) z[(int64_t)bh * D + row0 + tid] += sphi[row0 + tid];
+}
+
+__global__ void append_finish_kernel(Dims m, int32_t* __restrict__ seq_lens, int max_new,
+                                     const int32_t* __restrict__ n_new) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= m.batch) return;
+  bool clipped;
+  const int L0 = seq_lens[b];
+  seq_lens[b] = L0 + appended_count(m, L0, max_new, n_new, b, &clipped);
+}
+
+__global__ void fill_zero_kernel(uint32_t* __restrict__ p, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = 0u;
+}
+
+// ------------------------------------------------------------- launchers
+hipError_t launch_append_blocks(const Dims& m, const spla_cache& c, const void* k_new,
+                                const void* v_new, int max_new, const int32_t* n_new,
+                                hipStream_t st) {
+  dim3 grid((unsigned)(ceil_div(max_new, m.B) + 1), (unsigned)m.bh);
+  if (m.elem == 4)
+    hipLaunchKernelGGL(append_blocks_kernel<float>, grid, dim3(128), 0, st, m, (float*)c.k_cache,
+                       (float*)c.v_cache, c.blk_stats, c.seq_lens, c.err_flags,
+                       (const float*)k_new, (const float*)v_new, max_new, n_new);
+  else
+    hipLaunchKernelGGL(append_blocks_kernel<bf16_t>, grid, dim3(128), 0, st, m,
+                       (bf16_t*)c.k_cache, (bf16_t*)c.v_cache, c.blk_stats, c.seq_lens,
+                       c.err_flags, (const bf16_t*)k_new, (const bf16_t*)v_new, max_new, n_new);
+  return hipGetLastError();
+}
+
+template <typename T, int D>
+static void state_partial(const Dims& m, const spla_cache& c, const void* k_new, const void* v_new,
+                          int max_new, const int32_t* n_new, const AppendWs& ws, char* base,
+                          hipStream_t st) {
+  hipLaunchKernelGGL((append_state_partial_kernel<T, D>), dim3(ws.n_chunks, m.bh), dim3(256), 0,
+                     st, m, c.seq_lens, (const T*)k_new, (const T*)v_new, max_new, n_new,
+                     ws.n_chunks, ws.chunk_tokens, (float*)(base + ws.part_s),
+                     (float*)(base + ws.part_z));
+}
+
+hipError_t launch_append_state(const Dims& m, const spla_cache& c, const void* k_new,
+                               const void* v_new, int max_new, const int32_t* n_new,
+                               const AppendWs& ws, char* base, hipStream_t st) {
+  if (m.elem == 4) {
+    if (m.d == 64) state_partial<float, 64>(m, c, k_new, v_new, max_new, n_new, ws, base, st);
+    else state_partial<float, 128>(m, c, k_new, v_new, max_new, n_new, ws, base, st);
+  } else {
+    if (m.d == 64) state_partial<bf16_t, 64>(m, c, k_new, v_new, max_new, n_new, ws, base, st);
+    else state_partial<bf16_t, 128>(m, c, k_new, v_new, max_new, n_new, ws, base, st);
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(append_state_reduce_kernel, dim3(m.d / 16, m.bh), dim3(256), 0, st, m,
+                     ws.n_chunks, (const float*)(base + ws.part_s),
+                     (const float*)(base + ws.part_z), c.lin_state, c.lin_norm);
+  return hipGetLastError();
+}
+
+hipError_t launch_append_state_rank1(const Dims& m, const spla_cache& c, const void* k_new,
+                                     const void* v_new, hipStream_t st) {
+  dim3 grid(m.d / 16, m.bh);
+  if (m.elem == 4) {
+    if (m.d == 64)
+      hipLaunchKernelGGL((append_state_rank1_kernel<float, 64>), grid, dim3(256), 0, st, m,
+                         c.seq_lens, (const float*)k_new, (const float*)v_new, c.lin_state,
+                         c.lin_norm);
+    else
+      hipLaunchKernelGGL((append_state_rank1_kernel<float, 128>), grid, dim3(256), 0, st, m,
+                         c.seq_lens, (const float*)k_new, (const float*)v_new, c.lin_state,
+                         c.lin_norm);
+  } else {
+    if (m.d == 64)
+      hipLaunchKernelGGL((append_state_rank1_kernel<bf16_t, 64>), grid, dim3(256), 0, st, m,
+                         c.seq_lens, (const bf16_t*)k_new, (const bf16_t*)v_new, c.lin_state,
+                         c.lin_norm);
+    else
+      hipLaunchKernelGGL((append_state_rank1_kernel<bf16_t, 128>), grid, dim3(256), 0, st, m,
+                         c.seq_lens, (const bf16_t*)k_new, (const bf16_t*)v_new, c.lin_state,
+                         c.lin_norm);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_append_finish(const Dims& m, const spla_cache& c, int max_new,
+                                const int32_t* n_new, hipStream_t st) {
+  hipLaunchKernelGGL(append_finish_kernel, dim3((unsigned)ceil_div(m.batch, 256)), dim3(256), 0,
+                     st, m, c.seq_lens, max_new, n_new);
+  return hipGetLastError();
+}
+
+hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t st) {
+  const int64_t n = (int64_t)(bytes / 4);
+  if (n == 0) return hipSuccess;
+  int64_t blocks = ceil_div(n, 256);
+  if (blocks > 8192) blocks = 8192;
+  hipLaunchKernelGGL(fill_zero_kernel, dim3((unsigned)blocks), dim3(256), 0, st, (uint32_t*)p, n);
+  return hipGetLastError();
+}
+
+}  // namespace spla

@@ -1,0 +1,160 @@
+// Device entry points of the C ABI: argument checks, then the kernel
+// launches of each call on the caller's stream.
+#include <hip/hip_runtime.h>
+
+#include "spla_kernels.h"
+
+using spla::Dims;
+
+namespace {
+
+int32_t check_cache(const spla_cache* c) {
+  if (!c) return SPLA_ERR_INVALID_ARG;
+  if (!c->k_cache || !c->v_cache || !c->blk_stats || !c->lin_state || !c->lin_norm || !c->seq_lens)
+    return SPLA_ERR_INVALID_ARG;
+  return SPLA_OK;
+}
+
+int32_t check_ws(const void* ws, size_t have, size_t need) {
+  if (need == 0) return SPLA_OK;
+  if (!ws || have < need) return SPLA_ERR_WORKSPACE;
+  if (reinterpret_cast<uintptr_t>(ws) % SPLA_WORKSPACE_ALIGN != 0) return SPLA_ERR_WORKSPACE;
+  return SPLA_OK;
+}
+
+struct PhaseMark {
+  const spla_events* ev;
+  hipStream_t st;
+  int p;
+  PhaseMark(const spla_events* e, hipStream_t s, int phase) : ev(e), st(s), p(phase) {
+    if (ev && ev->start[p]) hipEventRecord((hipEvent_t)ev->start[p], st);
+  }
+  ~PhaseMark() {
+    if (ev && ev->stop[p]) hipEventRecord((hipEvent_t)ev->stop[p], st);
+  }
+};
+
+#define SPLA_TRY(expr)                               \
+  do {                                               \
+    hipError_t e_ = (expr);                          \
+    if (e_ != hipSuccess) return SPLA_ERR_HIP;       \
+  } while (0)
+
+int32_t run_decode(const spla_config* cfg, const spla_cache* cache, const void* q,
+                   const float* w, void* out, int32_t* sel_idx, void* ws, size_t ws_bytes,
+                   const spla_events* ev, hipStream_t st) {
+  const Dims m = spla::make_dims(*cfg);
+  const spla::DecodeWs L = spla::decode_ws_layout(m);
+  char* base = static_cast<char*>(ws);
+  {
+    PhaseMark pm(ev, st, SPLA_PHASE_SCORE);
+    SPLA_TRY(spla::launch_score(m, *cfg, *cache, q, L, base, st));
+  }
+  {
+    PhaseMark pm(ev, st, SPLA_PHASE_LINEAR);
+    SPLA_TRY(spla::launch_linear(m, *cfg, *cache, q, L, base, st));
+  }
+  {
+    PhaseMark pm(ev, st, SPLA_PHASE_SELECT);
+    SPLA_TRY(spla::launch_select(m, *cache, L, base, sel_idx, st));
+  }
+  {
+    PhaseMark pm(ev, st, SPLA_PHASE_SPARSE);
+    SPLA_TRY(spla::launch_sparse(m, *cfg, *cache, q, L, base, st));
+  }
+  {
+    PhaseMark pm(ev, st, SPLA_PHASE_MERGE);
+    SPLA_TRY(spla::launch_merge(m, *cfg, w, out, L, base, st));
+  }
+  return SPLA_OK;
+}
+
+int32_t check_decode_args(const spla_config* cfg, const spla_cache* cache, const void* q,
+                          const float* w, void* out, void* ws, size_t ws_bytes) {
+  int32_t s = spla_validate(cfg);
+  if (s != SPLA_OK) return s;
+  if ((s = check_cache(cache)) != SPLA_OK) return s;
+  if (!q || !w || !out) return SPLA_ERR_INVALID_ARG;
+  if (out == q) return SPLA_ERR_INVALID_ARG;
+  size_t need = 0;
+  spla_workspace_bytes(cfg, &need);
+  return check_ws(ws, ws_bytes, need);
+}
+
+}  // namespace
+
+extern "C" int32_t spla_reset(const spla_config* cfg, const spla_cache* cache, void* stream) {
+  int32_t s = spla_validate(cfg);
+  if (s != SPLA_OK) return s;
+  if ((s = check_cache(cache)) != SPLA_OK) return s;
+  size_t b[SPLA_CACHE_NUM_BUFFERS];
+  spla_cache_bytes(cfg, b);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  SPLA_TRY(spla::launch_fill_zero(cache->blk_stats, b[2], st));
+  SPLA_TRY(spla::launch_fill_zero(cache->lin_state, b[3], st));
+  SPLA_TRY(spla::launch_fill_zero(cache->lin_norm, b[4], st));
+  SPLA_TRY(spla::launch_fill_zero(cache->seq_lens, b[5], st));
+  return SPLA_OK;
+}
+
+extern "C" int32_t spla_append(const spla_config* cfg, const spla_cache* cache, const void* k_new,
+                               const void* v_new, int32_t max_new, const int32_t* n_new,
+                               void* workspace, size_t workspace_bytes, void* stream) {
+  int32_t s = spla_validate(cfg);
+  if (s != SPLA_OK) return s;
+  if ((s = check_cache(cache)) != SPLA_OK) return s;
+  if (max_new < 0) return SPLA_ERR_INVALID_ARG;
+  if (max_new > cfg->max_seq_len) return SPLA_ERR_CAPACITY;
+  if (max_new == 0) return SPLA_OK;
+  if (!k_new || !v_new) return SPLA_ERR_INVALID_ARG;
+  size_t need = 0;
+  spla_append_workspace_bytes(cfg, max_new, &need);
+  if ((s = check_ws(workspace, workspace_bytes, need)) != SPLA_OK) return s;
+  const Dims m = spla::make_dims(*cfg);
+  const spla::AppendWs L = spla::append_ws_layout(m, max_new);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  SPLA_TRY(spla::launch_append_blocks(m, *cache, k_new, v_new, max_new, n_new, st));
+  SPLA_TRY(spla::launch_append_state(m, *cache, k_new, v_new, max_new, n_new, L,
+                                     static_cast<char*>(workspace), st));
+  SPLA_TRY(spla::launch_append_finish(m, *cache, max_new, n_new, st));
+  return SPLA_OK;
+}
+
+extern "C" int32_t spla_decode_ex(const spla_config* cfg, const spla_cache* cache, const void* q,
+                                  const float* w, void* out, int32_t* sel_idx, void* ws,
+                                  size_t ws_bytes, const spla_events* ev, void* stream) {
+  int32_t s = check_decode_args(cfg, cache, q, w, out, ws, ws_bytes);
+  if (s != SPLA_OK) return s;
+  return run_decode(cfg, cache, q, w, out, sel_idx, ws, ws_bytes, ev,
+                    static_cast<hipStream_t>(stream));
+}
+
+extern "C" int32_t spla_decode(const spla_config* cfg, const spla_cache* cache, const void* q,
+                               const float* w, void* out, int32_t* sel_idx, void* ws,
+                               size_t ws_bytes, void* stream) {
+  return spla_decode_ex(cfg, cache, q, w, out, sel_idx, ws, ws_bytes, nullptr, stream);
+}
+
+extern "C" int32_t spla_step_ex(const spla_config* cfg, const spla_cache* cache, const void* k_new,
+                                const void* v_new, const void* q, const float* w, void* out,
+                                int32_t* sel_idx, void* ws, size_t ws_bytes,
+                                const spla_events* ev, void* stream) {
+  int32_t s = check_decode_args(cfg, cache, q, w, out, ws, ws_bytes);
+  if (s != SPLA_OK) return s;
+  if (!k_new || !v_new) return SPLA_ERR_INVALID_ARG;
+  const Dims m = spla::make_dims(*cfg);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  {
+    PhaseMark pm(ev, st, SPLA_PHASE_APPEND);
+    SPLA_TRY(spla::launch_append_blocks(m, *cache, k_new, v_new, 1, nullptr, st));
+    SPLA_TRY(spla::launch_append_state_rank1(m, *cache, k_new, v_new, st));
+    SPLA_TRY(spla::launch_append_finish(m, *cache, 1, nullptr, st));
+  }
+  return run_decode(cfg, cache, q, w, out, sel_idx, ws, ws_bytes, ev, st);
+}
+
+extern "C" int32_t spla_step(const spla_config* cfg, const spla_cache* cache, const void* k_new,
+                             const void* v_new, const void* q, const float* w, void* out,
+                             int32_t* sel_idx, void* ws, size_t ws_bytes, void* stream) {
+  return spla_step_ex(cfg, cache, k_new, v_new, q, w, out, sel_idx, ws, ws_bytes, nullptr, stream);
+}

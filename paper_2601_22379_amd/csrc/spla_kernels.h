@@ -1,0 +1,40 @@
+// Launchers of the SPLA kernels (host side). Each returns hipSuccess or the
+// launch error; the C ABI maps that to a spla_status.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "spla_layout.h"
+
+namespace spla {
+
+// append.hip
+hipError_t launch_append_blocks(const Dims& m, const spla_cache& c, const void* k_new,
+                                const void* v_new, int max_new, const int32_t* n_new,
+                                hipStream_t st);
+hipError_t launch_append_state(const Dims& m, const spla_cache& c, const void* k_new,
+                               const void* v_new, int max_new, const int32_t* n_new,
+                               const AppendWs& ws, char* wsbase, hipStream_t st);
+hipError_t launch_append_state_rank1(const Dims& m, const spla_cache& c, const void* k_new,
+                                     const void* v_new, hipStream_t st);
+hipError_t launch_append_finish(const Dims& m, const spla_cache& c, int max_new,
+                                const int32_t* n_new, hipStream_t st);
+hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t st);
+
+// score.hip
+hipError_t launch_score(const Dims& m, const spla_config& cfg, const spla_cache& c,
+                        const void* q, const DecodeWs& ws, char* wsbase, hipStream_t st);
+hipError_t launch_linear(const Dims& m, const spla_config& cfg, const spla_cache& c,
+                         const void* q, const DecodeWs& ws, char* wsbase, hipStream_t st);
+
+// select.hip
+hipError_t launch_select(const Dims& m, const spla_cache& c, const DecodeWs& ws, char* wsbase,
+                         int32_t* sel_out, hipStream_t st);
+
+// sparse.hip
+hipError_t launch_sparse(const Dims& m, const spla_config& cfg, const spla_cache& c,
+                         const void* q, const DecodeWs& ws, char* wsbase, hipStream_t st);
+hipError_t launch_merge(const Dims& m, const spla_config& cfg, const float* rms_weight,
+                        void* out, const DecodeWs& ws, char* wsbase, hipStream_t st);
+
+}  // namespace spla

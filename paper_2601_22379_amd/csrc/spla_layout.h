@@ -1,0 +1,136 @@
+// Memory layout of the caller-owned cache buffers and of the decode / append
+// workspaces. Shared by the host launch code and the kernels; plain C++ with
+// no HIP types so that the host-only validation build can use it too.
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/spla.h"
+
+#if defined(__HIPCC__)
+#define SPLA_HD __host__ __device__ inline
+#else
+#define SPLA_HD inline
+#endif
+
+namespace spla {
+
+constexpr int kTileBlocks = 64;   // blocks per statistics tile (one wavefront)
+constexpr int kSubTokens = 32;    // tokens per sparse-pass sub-tile
+constexpr int kAppendChunkTarget = 2048;  // append state-partial workgroups to aim for
+
+SPLA_HD int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+SPLA_HD int64_t align_up(int64_t a, int64_t b) { return ceil_div(a, b) * b; }
+
+// Shape numbers derived from a validated config.
+struct Dims {
+  int batch, hq, hkv, group, d, B, k, n_sink, n_local, cap;
+  int nb_cap;    // blocks per sequence at capacity
+  int n_tiles;   // statistics tiles per (sequence, kv head)
+  int bh;        // batch * hkv
+  int elem;      // bytes per q / K / V / out element
+};
+
+SPLA_HD Dims make_dims(const spla_config& c) {
+  Dims m;
+  m.batch = c.batch;
+  m.hq = c.n_q_heads;
+  m.hkv = c.n_kv_heads;
+  m.group = c.n_q_heads / c.n_kv_heads;
+  m.d = c.head_dim;
+  m.B = c.block_size;
+  m.k = c.top_k;
+  m.n_sink = c.n_sink_blocks;
+  m.n_local = c.n_local_blocks;
+  m.cap = c.max_seq_len;
+  m.nb_cap = c.max_seq_len / c.block_size;
+  m.n_tiles = (int)ceil_div(m.nb_cap, kTileBlocks);
+  m.bh = c.batch * c.n_kv_heads;
+  m.elem = c.dtype == SPLA_F32 ? 4 : 2;
+  return m;
+}
+
+// ---- cache buffers (element offsets) ---------------------------------------
+// k_cache [bh][cap][d]
+SPLA_HD int64_t k_off(const Dims& m, int64_t bh, int64_t t, int j) {
+  return (bh * m.cap + t) * m.d + j;
+}
+// v_cache [bh][nb_cap][d][B]
+SPLA_HD int64_t v_off(const Dims& m, int64_t bh, int64_t t, int c) {
+  return ((bh * m.nb_cap + t / m.B) * m.d + c) * m.B + (t % m.B);
+}
+// blk_stats [bh][n_tiles][2][d/4][64][4]; returns the offset of the float4
+// holding coordinates 4*j4 .. 4*j4+3 of block `blk`, part 0 (mean) or 1 (M2).
+SPLA_HD int64_t stats_off4(const Dims& m, int64_t bh, int64_t blk, int part, int j4) {
+  return ((((bh * m.n_tiles + blk / kTileBlocks) * 2 + part) * (m.d / 4) + j4) * kTileBlocks +
+          blk % kTileBlocks) * 4;
+}
+
+// ---- decode workspace ------------------------------------------------------
+struct DecodeWs {
+  int64_t e_vals;    // f32 [bh][G][n_tiles*64]   exp(ell - tile max)
+  int64_t tile_part; // f64 [bh][n_tiles][G][2]   (tile max, tile sum)
+  int64_t obar;      // f32 [bh][G][d]            phi(q) S_bar
+  int64_t zq;        // f32 [bh][G]               <phi(q), z_bar>
+  int64_t sel;       // i32 [bh][k]               selected blocks, ascending
+  int64_t meta;      // i32 [bh][4]               (n_selected, all_selected, length, 0)
+  int64_t split;     // f32 [bh][n_splits][G][split_stride]
+  int64_t counters;  // u32 [bh][4]
+  int64_t total;
+  int n_splits;
+  int blocks_per_split;
+  int split_stride;  // floats per (split, head): m, l, zw, pad, acc[d], accw[d]
+};
+
+SPLA_HD DecodeWs decode_ws_layout(const Dims& m) {
+  DecodeWs w;
+  const int64_t A = SPLA_WORKSPACE_ALIGN;
+  int64_t off = 0;
+  auto take = [&](int64_t bytes) {
+    int64_t o = off;
+    off = align_up(off + bytes, A);
+    return o;
+  };
+  w.blocks_per_split = 1;
+  w.n_splits = (int)ceil_div(m.k, w.blocks_per_split);
+  w.split_stride = 4 + 2 * m.d;
+  w.e_vals = take((int64_t)m.bh * m.group * m.n_tiles * kTileBlocks * 4);
+  w.tile_part = take((int64_t)m.bh * m.n_tiles * m.group * 2 * 8);
+  w.obar = take((int64_t)m.bh * m.group * m.d * 4);
+  w.zq = take((int64_t)m.bh * m.group * 4);
+  w.sel = take((int64_t)m.bh * m.k * 4);
+  w.meta = take((int64_t)m.bh * 4 * 4);
+  w.split = take((int64_t)m.bh * w.n_splits * m.group * w.split_stride * 4);
+  w.counters = take((int64_t)m.bh * 4 * 4);
+  w.total = off;
+  return w;
+}
+
+// ---- append workspace ------------------------------------------------------
+struct AppendWs {
+  int64_t part_s;  // f32 [bh][n_chunks][d][d]
+  int64_t part_z;  // f32 [bh][n_chunks][d]
+  int64_t total;
+  int n_chunks;
+  int chunk_tokens;
+};
+
+SPLA_HD AppendWs append_ws_layout(const Dims& m, int max_new) {
+  AppendWs w;
+  int64_t want = ceil_div(kAppendChunkTarget, m.bh);
+  int64_t most = ceil_div(max_new > 0 ? max_new : 1, kSubTokens);
+  int64_t n = want < most ? want : most;
+  if (n < 1) n = 1;
+  w.chunk_tokens = (int)align_up(ceil_div(max_new > 0 ? max_new : 1, n), kSubTokens);
+  w.n_chunks = (int)ceil_div(max_new > 0 ? max_new : 1, w.chunk_tokens);
+  const int64_t A = SPLA_WORKSPACE_ALIGN;
+  w.part_s = 0;
+  int64_t off = align_up((int64_t)m.bh * w.n_chunks * m.d * m.d * 4, A);
+  w.part_z = off;
+  off = align_up(off + (int64_t)m.bh * w.n_chunks * m.d * 4, A);
+  w.total = off;
+  return w;
+}
+
+}  // namespace spla
