@@ -1,0 +1,337 @@
+#!/usr/bin/env python3
+"""SPLA decode-step benchmark on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--config 3] [--replicas R]
+
+A step is one spla_decode call over the whole batch of the workload (for
+the appending workload, one spla_step): block scoring over every block's
+statistics, top-k selection, the fused exact + selected-linear pass over the
+selected blocks, and the merge. The cache is filled once through spla_append
+from the seeded synthetic generators (untimed). R identical copies of the
+cache are decoded in rotation so that the 256 MB last-level cache cannot
+serve a step from the previous visit; inputs are resident in HBM when the
+timed region starts.
+
+Prints one JSON line: whole-step throughput as algorithmic HBM bytes per
+second (value, GB/s), latency (ms_per_step), the roofline of the dominant
+kernel (the statistics scan, timed with HIP events on the library's stream
+over the timed region) and the fp64 CPU oracle timed on a bounded sample.
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "SPLA decode-step latency (µs) + achieved HBM GB/s vs peak at 128K ctx"
+PEAK_HBM_GBS = 8000.0
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "score_cfg3_traffic.json")
+SCORE_SOURCES = ["paper_2601_22379_amd/csrc/score.hip", "paper_2601_22379_amd/csrc/spla_layout.h",
+                 "paper_2601_22379_amd/csrc/spla_device.h"]
+
+
+def log(msg):
+    sys.stderr.write(f"[bench {time.strftime('%H:%M:%S')}] {msg}\n")
+    sys.stderr.flush()
+
+
+def source_hash(paths):
+    h = hashlib.sha256()
+    for p in paths:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def build_workload(w, replicas, dev):
+    import torch
+
+    from paper_2601_22379_amd import spla
+    import spla_inputs as si
+
+    cfg = spla.make_config(w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, w.block_size,
+                           w.top_k, w.capacity, w.dtype, n_sink=w.n_sink, n_local=w.n_local)
+    first = spla.SplaCache(cfg, dev)
+    dt = torch.float32 if w.dtype == "f32" else torch.bfloat16
+    lens = [w.prefill_length(b) for b in range(w.batch)]
+    per_tok = w.batch * w.n_kv_heads * w.head_dim * 8
+    T = int(min(w.capacity, max(256, 1 << (int((1 << 29) // per_tok).bit_length() - 1))))
+    t0 = time.time()
+    for a in range(0, max(lens), T):
+        K, V, n = si.gen_kv_slab(w, a, min(a + T, max(lens)), lengths=lens, threads=16)
+        first.append(torch.from_numpy(K).to(dt).to(dev), torch.from_numpy(V).to(dt).to(dev),
+                     torch.from_numpy(n).to(dev))
+    torch.cuda.synchronize()
+    log(f"filled {w.name} in {time.time() - t0:.1f}s")
+    caches = [first]
+    for _ in range(replicas - 1):
+        c = spla.SplaCache(cfg, dev)
+        for name in ("k", "v", "stats", "state", "norm", "seq_lens"):
+            getattr(c, name).copy_(getattr(first, name))
+        caches.append(c)
+    torch.cuda.synchronize()
+    return cfg, caches
+
+
+def cpu_baseline(w, seconds, n_units=2):
+    """The fp64 oracle's decode on a bounded sample of the workload: n_units
+    (sequence, KV head) units with their state prebuilt (untimed), decode
+    repeated until `seconds` of CPU time accumulate; one BLAS thread."""
+    import numpy as np
+    from threadpoolctl import threadpool_limits
+
+    import oracle as O
+    import spla_inputs as si
+
+    p = O.SplaParams(block_size=w.block_size, top_k=w.top_k, n_sink=w.n_sink, n_local=w.n_local)
+    rng = np.random.default_rng([w.code, 99])
+    allp = [(b, h) for b in range(w.batch) for h in range(w.n_kv_heads)]
+    pick = [allp[i] for i in rng.choice(len(allp), size=min(n_units, len(allp)), replace=False)]
+    gamma = si.gen_gamma(w)
+    units = []
+    with threadpool_limits(1):
+        for b, h in pick:
+            L = int(w.lengths[b])
+            K, V = si.gen_kv(w, b, h, 0, L, threads=8)
+            st = O.build_state(K, V, L, w.block_size)
+            q = si.gen_q(w, b)[h * w.group:(h + 1) * w.group]
+            units.append((q, st, K, V, gamma[h * w.group:(h + 1) * w.group]))
+        reps, busy = 0, 0.0
+        t_start = time.process_time()
+        while busy < seconds:
+            for u in units:
+                O.decode_kv_head(u[0], u[1], u[2], u[3], u[4], p)
+            reps += 1
+            busy = time.process_time() - t_start
+    wall_per_unit = busy / (reps * len(units))
+    import spla_inputs as si2
+    per_unit = si2.algorithmic_bytes(w)["total"] / (w.batch * w.n_kv_heads)
+    return {"value": round(per_unit / wall_per_unit / 1e9, 4), "unit": "GB/s", "cores": 1,
+            "kind": "oracle",
+            "sample": f"fp64 oracle decode of {len(units)} of {len(allp)} (sequence, KV head) "
+                      f"units of {w.name} (state prebuilt, untimed), repeated {reps}x "
+                      f"({busy:.1f}s CPU); {wall_per_unit * 1e3:.1f} ms per unit",
+            "cpu": _cpu_model()}
+
+
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--config", default="3")
+    ap.add_argument("--replicas", type=int, default=6)
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-graph", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run a plain 1 GiB copy kernel (for counter scaling)")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py: --gpus {args.gpus} (world size {world}) requested; this SPLA decode "
+              "library runs on a single GPU only (no multi-GPU path is built).", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2601_22379_amd import spla
+    import spla_inputs as si
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    spla.lib()  # fail loudly if the HIP library is missing
+    dev = torch.device("cuda:0")
+    w = si.config(args.config)
+    R = max(1, args.replicas)
+    cfg, caches = build_workload(w, R, dev)
+    dt = torch.float32 if w.dtype == "f32" else torch.bfloat16
+    K, W = args.steps, args.warmup
+    gamma = torch.from_numpy(si.gen_gamma(w)).to(dev)
+    appending = w.appends_per_step > 0
+    n_q = K + W + 2 * R + 1
+    if appending:
+        # per-step inputs generated before timing: token rows and queries
+        kn = np.zeros((n_q, w.batch, w.n_kv_heads, w.head_dim), np.float32)
+        vn = np.zeros_like(kn)
+        for s in range(n_q):
+            r = s % R
+            for b in range(w.batch):
+                pos = w.lengths[b] - 1 + s // R
+                for h in range(w.n_kv_heads):
+                    kk, vv = si.gen_kv(w, b, h, pos, pos + 1)
+                    kn[s, b, h], vn[s, b, h] = kk[0], vv[0]
+        kn_d = torch.from_numpy(kn).to(dt).to(dev)
+        vn_d = torch.from_numpy(vn).to(dt).to(dev)
+        qs = torch.from_numpy(np.stack([si.gen_q_batch(w, s) for s in range(min(n_q, 64))])).to(
+            dt).to(dev)
+    else:
+        qs = torch.from_numpy(si.gen_q_batch(w)[None]).to(dt).to(dev)
+    outs = [torch.empty((w.batch, w.n_q_heads, w.head_dim), dtype=dt, device=dev)
+            for _ in range(R)]
+    sels = [torch.empty((w.batch, w.n_kv_heads, w.top_k), dtype=torch.int32, device=dev)
+            for _ in range(R)]
+
+    def one(s, events=None):
+        r = s % R
+        q = qs[s % qs.shape[0]]
+        if appending:
+            return caches[r].step(kn_d[s], vn_d[s], q, gamma, outs[r], sels[r], events)
+        return caches[r].decode(q, gamma, outs[r], sels[r], events)
+
+    phase_names = ["append", "score", "linear", "select", "sparse", "merge"]
+    for s in range(W):
+        one(s)
+    torch.cuda.synchronize()
+
+    # timed region: K steps, each phase bracketed by HIP events on the call's stream
+    ev = [spla.make_events(phase_names) for _ in range(K)]
+    torch.cuda.synchronize()
+    t_a = torch.cuda.Event(enable_timing=True)
+    t_b = torch.cuda.Event(enable_timing=True)
+    wall0 = time.perf_counter()
+    t_a.record()
+    for s in range(K):
+        one(W + s, ev[s][0])
+    t_b.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    ms_per_step = t_a.elapsed_time(t_b) / K
+    phases = {}
+    for name in phase_names:
+        d = [e[1][name][0].elapsed_time(e[1][name][1]) for e in ev]
+        if appending or name != "append":
+            phases[name] = float(np.mean(d)) * 1e3
+    log(f"timed {K} steps: {ms_per_step * 1e3:.2f} us/step (wall {wall / K * 1e6:.2f} us/step); "
+        f"phases us: " + ", ".join(f"{k}={v:.2f}" for k, v in phases.items()))
+
+    # the same loop without per-phase events
+    torch.cuda.synchronize()
+    t_a.record()
+    for s in range(K):
+        one(W + K + s)
+    t_b.record()
+    torch.cuda.synchronize()
+    plain_us = t_a.elapsed_time(t_b) / K * 1e3
+
+    graph_us = None
+    if not args.no_graph and not appending:
+        try:
+            graphs = []
+            side = torch.cuda.Stream()
+            side.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(side):
+                for r in range(R):
+                    g = torch.cuda.CUDAGraph()
+                    with torch.cuda.graph(g, stream=side):
+                        one(r)
+                    graphs.append(g)
+            torch.cuda.current_stream().wait_stream(side)
+            torch.cuda.synchronize()
+            ref = [o.clone() for o in outs]
+            for r in range(R):
+                one(r)
+            torch.cuda.synchronize()
+            eager = [o.clone() for o in outs]
+            for _ in range(3):
+                for r in range(R):
+                    graphs[r].replay()
+                torch.cuda.synchronize()
+                for r in range(R):
+                    assert torch.equal(outs[r], eager[r]), "graph replay differs from eager"
+            t_a.record()
+            for s in range(K):
+                graphs[s % R].replay()
+            t_b.record()
+            torch.cuda.synchronize()
+            graph_us = t_a.elapsed_time(t_b) / K * 1e3
+            del ref
+        except Exception as e:  # graph capture is an extra measurement only
+            log(f"graph measurement skipped: {e!r}")
+
+    if args.copy_calibration:
+        n = 1 << 28
+        src = torch.ones(n, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        torch.mul(src, 1.0, out=dst)
+        torch.cuda.synchronize()
+        log("copy calibration: 1 GiB read + 1 GiB written by one elementwise kernel")
+
+    sel_counts = None
+    if not appending:
+        lens = caches[0].seq_lens.cpu().numpy()
+        sel_np = sels[0].cpu().numpy()
+        sel_counts = [[sum(min(w.block_size, int(lens[b]) - int(i) * w.block_size)
+                           for i in sel_np[b, h] if i >= 0) for h in range(w.n_kv_heads)]
+                      for b in range(w.batch)]
+    ab = si.algorithmic_bytes(w, sel_counts)
+    total = ab["total"]
+    value = total / (ms_per_step * 1e-3) / 1e9
+    score_bytes = ab["stats"] + w.batch * w.n_q_heads * w.head_dim * (4 if w.dtype == "f32" else 2)
+    score_us = phases["score"]
+    achieved = score_bytes / (score_us * 1e-6) / 1e9
+    traffic = None
+    if os.path.exists(TRAFFIC_FILE):
+        with open(TRAFFIC_FILE) as f:
+            tr = json.load(f)
+        if tr.get("source_sha") == source_hash(SCORE_SOURCES) and tr.get("workload") == w.name:
+            traffic = tr["hbm_bytes_per_launch"]
+    roofline = {"kernel": "score", "bound": "hbm", "achieved": round(achieved, 1),
+                "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4),
+                "traffic": traffic, "algorithmic_bytes_per_launch": score_bytes,
+                "avg_launch_us": round(score_us, 3)}
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle")
+        cpu = cpu_baseline(w, args.cpu_seconds)
+    line = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": W,
+        "ms_per_step": round(ms_per_step, 6),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic (seeded generators; no dataset)",
+        "config": {"workload": w.name, "batch": w.batch, "n_q_heads": w.n_q_heads,
+                   "n_kv_heads": w.n_kv_heads, "head_dim": w.head_dim,
+                   "context": int(max(w.lengths)), "block_size": w.block_size,
+                   "top_k": w.top_k, "n_sink": w.n_sink, "n_local": w.n_local,
+                   "cache_replicas": R, "appends_per_step": w.appends_per_step},
+        "latency_us": round(ms_per_step * 1e3, 3),
+        "latency_us_without_phase_events": round(plain_us, 3),
+        "latency_us_hip_graph": None if graph_us is None else round(graph_us, 3),
+        "frac_of_peak_hbm": round(value / PEAK_HBM_GBS, 4),
+        "algorithmic_bytes": ab,
+        "phases_us": {k: round(v, 3) for k, v in phases.items()},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -154,12 +154,15 @@ def test_decode_is_deterministic_and_leaves_cache_unchanged(dev):
 
 
 def test_capacity_overflow_is_clamped_and_flagged(dev):
-    w = si.custom("cap", 2, 4, 1, 64, 32, 4, [300, 100], kind="iid", capacity=256, code=125)
+    w = si.custom("cap", 2, 4, 1, 64, 32, 6, [300, 100], kind="iid", capacity=256, code=125)
     cfg = H.config_of(w)
     cache = spla.SplaCache(cfg, dev)
-    K, V, n = si.gen_kv_slab(w, 0, 300, lengths=[300, 100])
-    cache.append(H.to_dev(K, w, dev), H.to_dev(V, w, dev), torch.from_numpy(n).to(dev))
+    for t0, t1 in [(0, 200), (200, 300)]:
+        K, V, n = si.gen_kv_slab(w, t0, t1, lengths=[300, 100])
+        cache.append(H.to_dev(K, w, dev), H.to_dev(V, w, dev), torch.from_numpy(n).to(dev))
     torch.cuda.synchronize()
+    with pytest.raises(spla.SplaError):   # more rows than the capacity: rejected on the host
+        cache.append(*(H.to_dev(np.zeros((2, 1, 257, 64), np.float32), w, dev),) * 2)
     assert cache.seq_lens.cpu().tolist() == [256, 100]
     assert int(cache.err.item()) & spla.DEVERR_CAPACITY
     q = si.gen_q_batch(w)
@@ -174,7 +177,7 @@ def test_capacity_overflow_is_clamped_and_flagged(dev):
 def test_step_appends_then_decodes(dev):
     """spla_step: one token appended per (sequence, KV head), then the decode
     sees it; two consecutive steps."""
-    w = si.custom("step", 3, 8, 2, 128, 128, 4, [300, 1000, 129], kind="iid", code=126,
+    w = si.custom("step", 3, 8, 2, 128, 128, 6, [300, 1000, 129], kind="iid", code=126,
                   capacity=1152, appends_per_step=1)
     cfg = H.config_of(w)
     cache = spla.SplaCache(cfg, dev)
