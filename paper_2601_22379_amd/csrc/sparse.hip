@@ -1,24 +1,150 @@
-// Fused pass over the selected blocks and the merge (Secs. 2.2, 3.2, 3.3).
+// Fused pass over the selected blocks, and the merge (Secs. 2.2, 3.2, 3.3).
 //
-// sparse: workgroup (split, sequence x KV head) reads its selected blocks
-// once, 32 tokens at a time, and from that single read accumulates
-//   - the exact softmax branch of Eq. (5): online max m, normaliser l and
-//     acc = sum_t exp(s q.k_t - m) v_t for each of the G heads, and
+// Every selected block is read from HBM once. From that read the pass
+// accumulates, for each of the G query heads of the KV head,
+//   - the exact branch of Eq. (5): online max m, normaliser l and
+//     acc = sum_t exp(s q.k_t - m) v_t over the selected tokens, and
 //   - the selected-token linear term of Eq. (16):
-//     accw = sum_t <phi(q), phi(k_t)> v_t, zw = sum_t <phi(q), phi(k_t)>.
-// merge: combines the splits, forms r = o_bar - o_tilde (Eq. 14; exactly 0
-// when every token is selected), and writes
-//   out = o_sparse + gamma * r / sqrt(mean(r^2) + eps)   (Sec. 3.3).
+//     accw = sum_t <phi(q), phi(k_t)> v_t and zw = sum_t <phi(q), phi(k_t)>,
+//     phi being the softmax over the feature dimension.
+// Each workgroup writes one record (m, l, zw, acc, accw). The merge kernel
+// (one workgroup per sequence x KV head) combines the records, forms the
+// residual r = o_bar - o_tilde (Eq. 14; exactly 0 when every token is
+// selected) and writes out = o_sparse + gamma * r / sqrt(mean(r^2) + eps)
+// (Sec. 3.3).
+//
+// bf16 with G <= 8 runs on the matrix cores (v_mfma_f32_16x16x32_bf16, one
+// 32-token step per wavefront); fp32 and larger groups use a VALU pass that
+// writes the same records.
 #include "spla_device.h"
 #include "spla_kernels.h"
 
 namespace spla {
 
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+constexpr float kLog2e = 1.4426950408889634f;
+
+// ---------------------------------------------------------------- merge
+// Combines the n_rec records of a (sequence, KV head) (blockIdx.y) and
+// writes the output rows of the group's G heads.
+template <typename T, int D>
+__device__ void final_merge(const Dims& m, float eps, uint32_t flags,
+                            const float* __restrict__ gamma, const int32_t* __restrict__ meta,
+                            const float* __restrict__ rec, int n_rec, int stride,
+                            const float* __restrict__ obar_part, const float* __restrict__ zq_part,
+                            T* __restrict__ out) {
+  constexpr int E = D / 64;       // coordinates per lane
+  constexpr int NB = 8;           // records loaded per batch
+  constexpr int NL = D / kLinRows;
+  const int bh = blockIdx.y;
+  const int b = bh / m.hkv, h = bh % m.hkv;
+  const int G = m.group;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int all_sel = meta[bh * 4 + 1];
+  const int L = meta[bh * 4 + 2];
+  const bool rla = !(flags & SPLA_FLAG_NO_RLA);
+  for (int g = w; g < G; g += 4) {
+    const int64_t orow = ((int64_t)b * m.hq + h * G + g) * D;
+    if (L == 0) {
+#pragma unroll
+      for (int e = 0; e < E; ++e) Elem<T>::store(out, orow + lane + 64 * e, 0.f);
+      continue;
+    }
+    // the residual's ingredients do not depend on the records: load them first
+    float ob[E], zq = 0.f;
+#pragma unroll
+    for (int e = 0; e < E; ++e) ob[e] = 0.f;
+    {
+      float part[NL][E];
+#pragma unroll
+      for (int c = 0; c < NL; ++c)
+#pragma unroll
+        for (int e = 0; e < E; ++e)
+          part[c][e] = obar_part[(((int64_t)bh * NL + c) * G + g) * D + lane + 64 * e];
+#pragma unroll
+      for (int c = 0; c < NL; ++c)
+#pragma unroll
+        for (int e = 0; e < E; ++e) ob[e] += part[c][e];
+      if (flags & SPLA_FLAG_RLA_NORMALIZE) {
+        float zp[NL];
+#pragma unroll
+        for (int c = 0; c < NL; ++c) zp[c] = zq_part[((int64_t)bh * NL + c) * G + g];
+#pragma unroll
+        for (int c = 0; c < NL; ++c) zq += zp[c];
+      }
+    }
+    // records in batches; every load of a batch is issued before its math,
+    // and the running max is rescaled as in an online softmax
+    float M = -INFINITY, l = 0.f, zt = 0.f;
+    float osp[E], ot[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) osp[e] = ot[e] = 0.f;
+    for (int x0 = 0; x0 < n_rec; x0 += NB) {
+      float mx[NB], lx[NB], zx[NB], a[NB][E], aw[NB][E];
+#pragma unroll
+      for (int u = 0; u < NB; ++u) {
+        const bool ok = x0 + u < n_rec;
+        const float* r = rec + (int64_t)(ok ? x0 + u : 0) * stride;
+        mx[u] = ok ? r[g] : -INFINITY;
+        lx[u] = ok ? r[16 + g] : 0.f;
+        zx[u] = ok ? r[32 + g] : 0.f;
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          a[u][e] = ok ? r[kPartHead + g * D + lane + 64 * e] : 0.f;
+          aw[u][e] = ok ? r[kPartHead + (G + g) * D + lane + 64 * e] : 0.f;
+        }
+      }
+      float bm = M;
+#pragma unroll
+      for (int u = 0; u < NB; ++u) bm = fmaxf(bm, mx[u]);
+      const float alpha = M == -INFINITY ? 0.f : __expf(M - bm);
+      l *= alpha;
+#pragma unroll
+      for (int e = 0; e < E; ++e) osp[e] *= alpha;
+#pragma unroll
+      for (int u = 0; u < NB; ++u) {
+        const float sc = mx[u] == -INFINITY ? 0.f : __expf(mx[u] - bm);
+        l = fmaf(lx[u], sc, l);
+        zt += zx[u];
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          osp[e] = fmaf(a[u][e], sc, osp[e]);
+          ot[e] += aw[u][e];
+        }
+      }
+      M = bm;
+    }
+    const float den = (flags & SPLA_FLAG_RLA_NORMALIZE) ? zq - zt : 1.f;
+    float rr[E];
+    float ss = 0.f;
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      osp[e] /= l;
+      rr[e] = (rla && !all_sel) ? (ob[e] - ot[e]) / den : 0.f;
+      ss += rr[e] * rr[e];
+    }
+    ss = wave_sum(ss);
+    const float inv = 1.0f / sqrtf(ss / D + eps);
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      const int c = lane + 64 * e;
+      float o = osp[e];
+      if (rla) o = fmaf(gamma[(int64_t)(h * G + g) * D + c] * rr[e], inv, o);
+      Elem<T>::store(out, orow + c, o);
+    }
+  }
+}
+
+// ------------------------------------------------------------ VALU pass
 template <typename T, int D>
 __global__ __launch_bounds__(256) void sparse_valu_kernel(
-    Dims m, float s, const T* __restrict__ kc, const T* __restrict__ vc,
-    const T* __restrict__ q, const int32_t* __restrict__ sel, const int32_t* __restrict__ meta,
-    int n_splits, int bps, int stride, float* __restrict__ part) {
+    Dims m, float s, float eps, uint32_t flags, const T* __restrict__ kc,
+    const T* __restrict__ vc, const T* __restrict__ q, const float* __restrict__ gamma,
+    const int32_t* __restrict__ sel, const int32_t* __restrict__ meta, int bps, int stride,
+    float* __restrict__ part, const float* __restrict__ obar_part,
+    const float* __restrict__ zq_part, T* __restrict__ out) {
   constexpr int MG = SPLA_MAX_GROUP;
   constexpr int PER = (MG * D + 255) / 256;  // (head, coord) pairs per thread
   __shared__ float sq[MG][D];
@@ -35,6 +161,7 @@ __global__ __launch_bounds__(256) void sparse_valu_kernel(
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int nsel = meta[bh * 4 + 0];
   const int L = meta[bh * 4 + 2];
+  const int nb = (L + m.B - 1) / m.B;
   const int p0 = split * bps, p1 = min(p0 + bps, nsel);
 
   for (int mm = w; mm < G; mm += 4) {
@@ -68,7 +195,8 @@ __global__ __launch_bounds__(256) void sparse_valu_kernel(
   __syncthreads();
 
   for (int p = p0; p < p1; ++p) {
-    const int blk = sel[(int64_t)bh * m.k + p];
+    int blk = sel[(int64_t)bh * m.k + p];
+    blk = blk < 0 ? 0 : (blk >= nb ? nb - 1 : blk);
     const int n_i = block_count(L, m.B, blk);
     for (int sub = 0; sub * kSubTokens < n_i; ++sub) {
       const int t0 = blk * m.B + sub * kSubTokens;
@@ -148,121 +276,319 @@ __global__ __launch_bounds__(256) void sparse_valu_kernel(
       __syncthreads();
     }
   }
-  float* out = part + ((int64_t)bh * n_splits + split) * G * stride;
+  float* rec = part + ((int64_t)bh * gridDim.x + split) * stride;
 #pragma unroll
   for (int r = 0; r < PER; ++r) {
     const int idx = tid + 256 * r;
     if (idx < G * D) {
       const int mm = idx / D, c = idx % D;
-      out[mm * stride + 4 + c] = acc[r];
-      out[mm * stride + 4 + D + c] = accw[r];
+      rec[kPartHead + mm * D + c] = acc[r];
+      rec[kPartHead + (G + mm) * D + c] = accw[r];
     }
   }
   if (tid < G) {
-    out[tid * stride + 0] = s_m[tid];
-    out[tid * stride + 1] = s_l[tid];
-    out[tid * stride + 2] = s_zw[tid];
-    out[tid * stride + 3] = 0.f;
+    rec[tid] = s_m[tid];
+    rec[16 + tid] = s_l[tid];
+    rec[32 + tid] = s_zw[tid];
   }
 }
 
+// ------------------------------------------------------------ MFMA pass
+// One 32-token step of one selected block per wavefront (the workgroup's
+// four wavefronts take consecutive steps). With g = lane / 16 and
+// j = lane % 16 (the MFMA column), for the two 16-row tiles of a step the key
+// row loaded by lane l is token 8 (i / 4) + 4 tile + (i % 4), i = l % 16, so
+// that after S = K [Q | phi(Q)]^T the accumulator rows held by lane l are
+// exactly the tokens 8 g .. 8 g + 7 of the step, in order - the layout the
+// second product needs for its B operand. Columns 0..7 carry the exact-branch
+// logits of heads 0..G-1, columns 8..15 the linear weights
+// <phi(q), phi(k)> of the same heads; one accumulator holds both. phi(k) and
+// the probabilities enter the products as bf16 hi + lo pairs (about 16
+// mantissa bits); accumulation is fp32.
+template <int D, int BLK>
+__global__ __launch_bounds__(256) void sparse_mfma_kernel(
+    Dims m, float s, const bf16_t* __restrict__ kc, const bf16_t* __restrict__ vc,
+    const bf16_t* __restrict__ q, const int32_t* __restrict__ sel,
+    const int32_t* __restrict__ meta, int stride, float* __restrict__ part) {
+  constexpr int KS = D / 32;   // k-steps of the first product
+  constexpr int MT = D / 16;   // coordinate tiles of the second product
+  constexpr int CPB = BLK / 32;  // steps per block
+  __shared__ float s_o[kSparseWaves][D][17];
+  __shared__ float s_m[kSparseWaves][16], s_l[kSparseWaves][16];
+  const int bh = blockIdx.y;
+  const int b = bh / m.hkv, h = bh % m.hkv;
+  const int G = m.group;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int j = lane & 15, g = lane >> 4, i = lane & 15;
+  const int item = blockIdx.x * kSparseWaves + w;
+  const int p = item / CPB, ch = item % CPB;
+  const bool exact_col = j < 8;
+  const int head = exact_col ? j : j - 8;
+  const bool live = head < G;
+  // independent loads first: the block id (entries past the selection are
+  // -1), the sequence length and this lane's query slice
+  const int blk_sel = p < m.k ? sel[(int64_t)bh * m.k + p] : -1;
+  const int L = meta[bh * 4 + 2];
+  const bf16_t* qrow = q + ((int64_t)b * m.hq + h * G + (live ? head : 0)) * D;
+  bf16x8 qraw[KS];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) qraw[ks] = *reinterpret_cast<const bf16x8*>(qrow + 32 * ks + 8 * g);
+  const int nb = (L + BLK - 1) / BLK;
+  int n_valid = 0;  // tokens of this step that exist
+  bf16x8 ka[2][KS];
+  bf16x8 va[MT];
+  if (blk_sel >= 0) {
+    const int blk = blk_sel >= nb ? nb - 1 : blk_sel;
+    n_valid = min(32, block_count(L, BLK, blk) - ch * 32);
+    if (n_valid > 0) {
+      const bf16_t* kblk = kc + ((int64_t)bh * m.cap + (int64_t)blk * BLK + ch * 32) * D;
+      const bf16_t* vblk = vc + ((int64_t)bh * m.nb_cap + blk) * D * BLK + ch * 32;
+#pragma unroll
+      for (int mt = 0; mt < 2; ++mt) {
+        const int row = 8 * (i >> 2) + 4 * mt + (i & 3);
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+          ka[mt][ks] = *reinterpret_cast<const bf16x8*>(kblk + (int64_t)row * D + 32 * ks + 8 * g);
+      }
+#pragma unroll
+      for (int t = 0; t < MT; ++t)
+        va[t] = *reinterpret_cast<const bf16x8*>(vblk + (int64_t)(16 * t + i) * BLK + 8 * g);
+    }
+  }
+  floatx4 acc_o[MT];
+#pragma unroll
+  for (int t = 0; t < MT; ++t) acc_o[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+  float m_run = -INFINITY, l_run = 0.f;  // exact columns: max / sum; linear columns: sum
+  if (n_valid > 0) {
+    // B operands (while the key / value loads are in flight): [q | 0] for the
+    // logits, [0 | phi(q)_hi] and [0 | phi(q)_lo] for the linear weights
+    bf16x8 qb[KS], pqh[KS], pql[KS];
+    {
+      float x[KS][8];
+      float mx = -INFINITY;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          x[ks][e] = live ? (float)qraw[ks][e] : 0.f;
+          mx = fmaxf(mx, x[ks][e]);
+        }
+      }
+      mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
+      mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+      float sum = 0.f;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) sum += exp2f((x[ks][e] - mx) * kLog2e);
+      sum += __shfl_xor(sum, 16, kWave);
+      sum += __shfl_xor(sum, 32, kWave);
+      const float inv = 1.0f / sum;
+      const __bf16 zero = (__bf16)0.f;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float pq = exp2f((x[ks][e] - mx) * kLog2e) * inv;
+          const __bf16 hi = (__bf16)pq;
+          const __bf16 lo = (__bf16)(pq - (float)hi);
+          qb[ks][e] = (exact_col && live) ? (__bf16)x[ks][e] : zero;
+          pqh[ks][e] = (!exact_col && live) ? hi : zero;
+          pql[ks][e] = (!exact_col && live) ? lo : zero;
+        }
+    }
+    floatx4 sw[2];
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt) {
+      sw[mt] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks)
+        sw[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[mt][ks], qb[ks], sw[mt], 0, 0, 0);
+      // phi(k) of this lane's key row (row i of the tile), spread over lanes i + 16 g'
+      float kx[KS][8];
+      float mx = -INFINITY;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          kx[ks][e] = (float)ka[mt][ks][e];
+          mx = fmaxf(mx, kx[ks][e]);
+        }
+      mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
+      mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+      const float mxl = mx * kLog2e;
+      float sum = 0.f;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          kx[ks][e] = exp2f(fmaf(kx[ks][e], kLog2e, -mxl));
+          sum += kx[ks][e];
+        }
+      sum += __shfl_xor(sum, 16, kWave);
+      sum += __shfl_xor(sum, 32, kWave);
+      const float inv = 1.0f / sum;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        bf16x8 fh, fl;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float f = kx[ks][e] * inv;
+          const __bf16 hi = (__bf16)f;
+          fh[e] = hi;
+          fl[e] = (__bf16)(f - (float)hi);
+        }
+        sw[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fh, pqh[ks], sw[mt], 0, 0, 0);
+        sw[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fh, pql[ks], sw[mt], 0, 0, 0);
+        sw[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fl, pqh[ks], sw[mt], 0, 0, 0);
+      }
+    }
+    // tokens 8g .. 8g+7 of this step: tile 0 rows 4g..4g+3, tile 1 rows 4g..4g+3
+    float val[8];
+    float cmax = -INFINITY;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const bool ok = 8 * g + e < n_valid;
+      const float x = sw[e >> 2][e & 3];
+      val[e] = exact_col ? (ok ? x * s : -INFINITY) : (ok ? x : 0.f);
+      cmax = fmaxf(cmax, val[e]);
+    }
+    cmax = fmaxf(cmax, __shfl_xor(cmax, 16, kWave));
+    cmax = fmaxf(cmax, __shfl_xor(cmax, 32, kWave));
+    float psum = 0.f;
+    bf16x8 bh8, bl8;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float pv = exact_col ? exp2f((val[e] - cmax) * kLog2e) : val[e];
+      psum += pv;
+      const __bf16 hi = (__bf16)pv;
+      bh8[e] = hi;
+      bl8[e] = (__bf16)(pv - (float)hi);
+    }
+    psum += __shfl_xor(psum, 16, kWave);
+    psum += __shfl_xor(psum, 32, kWave);
+    m_run = exact_col ? cmax : -INFINITY;
+    l_run = psum;
+    if (n_valid < 32) {  // rows past the sequence end may hold anything: zero them
+#pragma unroll
+      for (int t = 0; t < MT; ++t)
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if (8 * g + e >= n_valid) va[t][e] = (__bf16)0.f;
+    }
+#pragma unroll
+    for (int t = 0; t < MT; ++t) {
+      acc_o[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va[t], bh8, acc_o[t], 0, 0, 0);
+      acc_o[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va[t], bl8, acc_o[t], 0, 0, 0);
+    }
+  }
+  // ---- merge the four wavefronts of the workgroup into one record
+#pragma unroll
+  for (int t = 0; t < MT; ++t)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) s_o[w][16 * t + 4 * g + r][j] = acc_o[t][r];
+  if (lane < 16) {
+    s_m[w][lane] = m_run;
+    s_l[w][lane] = l_run;
+  }
+  __syncthreads();
+  float* rec = part + ((int64_t)bh * gridDim.x + blockIdx.x) * stride;
+  for (int e = tid; e < G * D; e += 256) {
+    const int hh = e / D, c = e % D;
+    float M = -INFINITY;
+#pragma unroll
+    for (int x = 0; x < kSparseWaves; ++x) M = fmaxf(M, s_m[x][hh]);
+    float a = 0.f, aw = 0.f;
+#pragma unroll
+    for (int x = 0; x < kSparseWaves; ++x) {
+      const float sc = s_m[x][hh] == -INFINITY ? 0.f : __expf(s_m[x][hh] - M);
+      a = fmaf(s_o[x][c][hh], sc, a);
+      aw += s_o[x][c][8 + hh];
+    }
+    rec[kPartHead + hh * D + c] = a;
+    rec[kPartHead + (G + hh) * D + c] = aw;
+  }
+  if (tid < G) {
+    float M = -INFINITY;
+#pragma unroll
+    for (int x = 0; x < kSparseWaves; ++x) M = fmaxf(M, s_m[x][tid]);
+    float l = 0.f, zw = 0.f;
+#pragma unroll
+    for (int x = 0; x < kSparseWaves; ++x) {
+      l += s_m[x][tid] == -INFINITY ? 0.f : s_l[x][tid] * __expf(s_m[x][tid] - M);
+      zw += s_l[x][8 + tid];
+    }
+    rec[tid] = M;
+    rec[16 + tid] = l;
+    rec[32 + tid] = zw;
+  }
+}
+
+// One workgroup per (sequence, KV head): merges the records of the pass.
 template <typename T, int D>
 __global__ __launch_bounds__(256) void merge_kernel(
     Dims m, float eps, uint32_t flags, const float* __restrict__ gamma,
-    const int32_t* __restrict__ meta, const float* __restrict__ part, int n_splits, int bps,
-    int stride, const float* __restrict__ obar, const float* __restrict__ zq, T* __restrict__ out) {
-  const int bh = blockIdx.x;
-  const int b = bh / m.hkv, h = bh % m.hkv;
-  const int G = m.group;
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int nsel = meta[bh * 4 + 0];
-  const int all_sel = meta[bh * 4 + 1];
-  const int L = meta[bh * 4 + 2];
-  const int n_used = (nsel + bps - 1) / bps;
-  const float* pb = part + (int64_t)bh * n_splits * G * stride;
-  for (int mm = w; mm < G; mm += 4) {
-    const int64_t orow = ((int64_t)b * m.hq + h * G + mm) * D;
-    if (L == 0) {
-#pragma unroll
-      for (int e = 0; e < D / 64; ++e) Elem<T>::store(out, orow + lane + 64 * e, 0.f);
-      continue;
-    }
-    float M = -INFINITY;
-    for (int x = 0; x < n_used; ++x) M = fmaxf(M, pb[((int64_t)x * G + mm) * stride]);
-    float l = 0.f, zt = 0.f;
-    float osp[D / 64], ot[D / 64];
-#pragma unroll
-    for (int e = 0; e < D / 64; ++e) osp[e] = ot[e] = 0.f;
-    for (int x = 0; x < n_used; ++x) {
-      const float* px = pb + ((int64_t)x * G + mm) * stride;
-      const float sc = expf(px[0] - M);
-      l = fmaf(px[1], sc, l);
-      zt += px[2];
-#pragma unroll
-      for (int e = 0; e < D / 64; ++e) {
-        osp[e] = fmaf(px[4 + lane + 64 * e], sc, osp[e]);
-        ot[e] += px[4 + D + lane + 64 * e];
-      }
-    }
-    float r[D / 64];
-    float ss = 0.f;
-    const bool rla = !(flags & SPLA_FLAG_NO_RLA);
-#pragma unroll
-    for (int e = 0; e < D / 64; ++e) {
-      osp[e] /= l;
-      r[e] = 0.f;
-      if (rla && !all_sel) r[e] = obar[((int64_t)bh * G + mm) * D + lane + 64 * e] - ot[e];
-    }
-    if (rla && !all_sel && (flags & SPLA_FLAG_RLA_NORMALIZE)) {
-      const float den = zq[(int64_t)bh * G + mm] - zt;
-#pragma unroll
-      for (int e = 0; e < D / 64; ++e) r[e] /= den;
-    }
-#pragma unroll
-    for (int e = 0; e < D / 64; ++e) ss += r[e] * r[e];
-    ss = wave_sum(ss);
-    const float inv = 1.0f / sqrtf(ss / D + eps);
-#pragma unroll
-    for (int e = 0; e < D / 64; ++e) {
-      const int c = lane + 64 * e;
-      float o = osp[e];
-      if (rla) o = fmaf(gamma[(int64_t)(h * G + mm) * D + c] * r[e], inv, o);
-      Elem<T>::store(out, orow + c, o);
-    }
-  }
+    const int32_t* __restrict__ meta, const float* __restrict__ part, int n_rec, int stride,
+    const float* __restrict__ obar_part, const float* __restrict__ zq_part, T* __restrict__ out) {
+  final_merge<T, D>(m, eps, flags, gamma, meta, part + (int64_t)blockIdx.y * n_rec * stride, n_rec,
+                    stride, obar_part, zq_part, out);
 }
 
+// ------------------------------------------------------------- launchers
 template <typename T, int D>
-static void sparse_td(const Dims& m, float s, const spla_cache& c, const void* q,
-                      const DecodeWs& ws, char* base, hipStream_t st) {
-  hipLaunchKernelGGL((sparse_valu_kernel<T, D>), dim3(ws.n_splits, m.bh), dim3(256), 0, st, m, s,
-                     (const T*)c.k_cache, (const T*)c.v_cache, (const T*)q,
-                     (const int32_t*)(base + ws.sel), (const int32_t*)(base + ws.meta),
-                     ws.n_splits, ws.blocks_per_split, ws.split_stride,
-                     (float*)(base + ws.split));
+static void valu_td(const Dims& m, const spla_config& cfg, float s, const spla_cache& c,
+                    const void* q, const float* gamma, void* out, const DecodeWs& ws, char* base,
+                    hipStream_t st) {
+  hipLaunchKernelGGL((sparse_valu_kernel<T, D>), dim3(ws.n_wg, m.bh), dim3(256), 0, st, m, s,
+                     cfg.rms_eps, cfg.flags, (const T*)c.k_cache, (const T*)c.v_cache,
+                     (const T*)q, gamma, (const int32_t*)(base + ws.sel),
+                     (const int32_t*)(base + ws.meta), ws.blocks_per_wg, ws.part_stride,
+                     (float*)(base + ws.part), (const float*)(base + ws.obar_part),
+                     (const float*)(base + ws.zq_part), (T*)out);
 }
 
-hipError_t launch_sparse(const Dims& m, const spla_config& cfg, const spla_cache& c,
-                         const void* q, const DecodeWs& ws, char* base, hipStream_t st) {
-  const float s = cfg.softmax_scale > 0.f ? cfg.softmax_scale : (float)(1.0 / sqrt((double)m.d));
-  if (m.elem == 4) {
-    if (m.d == 64) sparse_td<float, 64>(m, s, c, q, ws, base, st);
-    else sparse_td<float, 128>(m, s, c, q, ws, base, st);
-  } else {
-    if (m.d == 64) sparse_td<bf16_t, 64>(m, s, c, q, ws, base, st);
-    else sparse_td<bf16_t, 128>(m, s, c, q, ws, base, st);
-  }
-  return hipGetLastError();
+template <int D, int BLK>
+static void mfma_db(const Dims& m, float s, const spla_cache& c, const void* q,
+                    const DecodeWs& ws, char* base, hipStream_t st) {
+  hipLaunchKernelGGL((sparse_mfma_kernel<D, BLK>), dim3(ws.n_wg, m.bh), dim3(256), 0, st, m, s,
+                     (const bf16_t*)c.k_cache, (const bf16_t*)c.v_cache, (const bf16_t*)q,
+                     (const int32_t*)(base + ws.sel), (const int32_t*)(base + ws.meta),
+                     ws.part_stride, (float*)(base + ws.part));
+}
+
+template <int D>
+static void mfma_d(const Dims& m, float s, const spla_cache& c, const void* q,
+                   const DecodeWs& ws, char* base, hipStream_t st) {
+  if (m.B == 32) mfma_db<D, 32>(m, s, c, q, ws, base, st);
+  else if (m.B == 64) mfma_db<D, 64>(m, s, c, q, ws, base, st);
+  else mfma_db<D, 128>(m, s, c, q, ws, base, st);
 }
 
 template <typename T, int D>
 static void merge_td(const Dims& m, const spla_config& cfg, const float* gamma, void* out,
                      const DecodeWs& ws, char* base, hipStream_t st) {
-  hipLaunchKernelGGL((merge_kernel<T, D>), dim3(m.bh), dim3(256), 0, st, m, cfg.rms_eps,
+  hipLaunchKernelGGL((merge_kernel<T, D>), dim3(1, m.bh), dim3(256), 0, st, m, cfg.rms_eps,
                      cfg.flags, gamma, (const int32_t*)(base + ws.meta),
-                     (const float*)(base + ws.split), ws.n_splits, ws.blocks_per_split,
-                     ws.split_stride, (const float*)(base + ws.obar),
-                     (const float*)(base + ws.zq), (T*)out);
+                     (const float*)(base + ws.part), ws.n_wg, ws.part_stride,
+                     (const float*)(base + ws.obar_part), (const float*)(base + ws.zq_part),
+                     (T*)out);
+}
+
+hipError_t launch_sparse(const Dims& m, const spla_config& cfg, const spla_cache& c,
+                         const void* q, const float* gamma, void* out, const DecodeWs& ws,
+                         char* base, hipStream_t st) {
+  const float s = cfg.softmax_scale > 0.f ? cfg.softmax_scale : (float)(1.0 / sqrt((double)m.d));
+  if (use_mfma_sparse(m)) {
+    if (m.d == 64) mfma_d<64>(m, s, c, q, ws, base, st);
+    else mfma_d<128>(m, s, c, q, ws, base, st);
+  } else if (m.elem == 4) {
+    if (m.d == 64) valu_td<float, 64>(m, cfg, s, c, q, gamma, out, ws, base, st);
+    else valu_td<float, 128>(m, cfg, s, c, q, gamma, out, ws, base, st);
+  } else {
+    if (m.d == 64) valu_td<bf16_t, 64>(m, cfg, s, c, q, gamma, out, ws, base, st);
+    else valu_td<bf16_t, 128>(m, cfg, s, c, q, gamma, out, ws, base, st);
+  }
+  return hipGetLastError();
 }
 
 hipError_t launch_merge(const Dims& m, const spla_config& cfg, const float* gamma, void* out,

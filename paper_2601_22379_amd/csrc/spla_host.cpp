@@ -27,7 +27,6 @@ extern "C" const char* spla_phase_name(int32_t p) {
     case SPLA_PHASE_SELECT: return "select";
     case SPLA_PHASE_SPARSE: return "sparse";
     case SPLA_PHASE_MERGE: return "merge";
-    case SPLA_PHASE_LINEAR: return "linear";
     default: return nullptr;
   }
 }

@@ -21,20 +21,19 @@ hipError_t launch_append_finish(const Dims& m, const spla_cache& c, int max_new,
                                 const int32_t* n_new, hipStream_t st);
 hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t st);
 
-// score.hip
+// score.hip: block scoring and the o_bar partials in one launch
 hipError_t launch_score(const Dims& m, const spla_config& cfg, const spla_cache& c,
                         const void* q, const DecodeWs& ws, char* wsbase, hipStream_t st);
-hipError_t launch_linear(const Dims& m, const spla_config& cfg, const spla_cache& c,
-                         const void* q, const DecodeWs& ws, char* wsbase, hipStream_t st);
 
 // select.hip
 hipError_t launch_select(const Dims& m, const spla_cache& c, const DecodeWs& ws, char* wsbase,
                          int32_t* sel_out, hipStream_t st);
 
-// sparse.hip
+// sparse.hip: fused pass over the selected blocks (records), then the merge
 hipError_t launch_sparse(const Dims& m, const spla_config& cfg, const spla_cache& c,
-                         const void* q, const DecodeWs& ws, char* wsbase, hipStream_t st);
-hipError_t launch_merge(const Dims& m, const spla_config& cfg, const float* rms_weight,
-                        void* out, const DecodeWs& ws, char* wsbase, hipStream_t st);
+                         const void* q, const float* rms_weight, void* out, const DecodeWs& ws,
+                         char* wsbase, hipStream_t st);
+hipError_t launch_merge(const Dims& m, const spla_config& cfg, const float* rms_weight, void* out,
+                        const DecodeWs& ws, char* wsbase, hipStream_t st);
 
 }  // namespace spla

@@ -6,7 +6,7 @@
 #include <stddef.h>
 #include <stdint.h>
 
-#include "../../include/spla.h"
+#include "spla.h"
 
 #if defined(__HIPCC__)
 #define SPLA_HD __host__ __device__ inline
@@ -68,20 +68,28 @@ SPLA_HD int64_t stats_off4(const Dims& m, int64_t bh, int64_t blk, int part, int
 }
 
 // ---- decode workspace ------------------------------------------------------
+constexpr int kLinRows = 16;      // rows of S_bar per linear-term workgroup
+constexpr int kPartHead = 48;     // per-record header: m[16], l[16], zw[16]
+constexpr int kSparseWaves = 4;   // waves per sparse workgroup
+
 struct DecodeWs {
-  int64_t e_vals;    // f32 [bh][G][n_tiles*64]   exp(ell - tile max)
-  int64_t tile_part; // f64 [bh][n_tiles][G][2]   (tile max, tile sum)
-  int64_t obar;      // f32 [bh][G][d]            phi(q) S_bar
-  int64_t zq;        // f32 [bh][G]               <phi(q), z_bar>
-  int64_t sel;       // i32 [bh][k]               selected blocks, ascending
-  int64_t meta;      // i32 [bh][4]               (n_selected, all_selected, length, 0)
-  int64_t split;     // f32 [bh][n_splits][G][split_stride]
-  int64_t counters;  // u32 [bh][4]
+  int64_t e_vals;     // f32 [bh][G][n_tiles*64]   exp(ell - tile max)
+  int64_t tile_part;  // f64 [bh][n_tiles][G][2]   (max, sum) per 64-block tile
+  int64_t obar_part;  // f32 [bh][d/16][G][d]      phi(q) S_bar, per 16-row chunk
+  int64_t zq_part;    // f32 [bh][d/16][G]         <phi(q), z_bar>, per chunk
+  int64_t sel;        // i32 [bh][k]               selected blocks, ascending
+  int64_t meta;       // i32 [bh][4]               (n_selected, all_selected, length, 0)
+  int64_t part;       // f32 [bh][n_wg][part_stride]  sparse workgroup partials
   int64_t total;
-  int n_splits;
-  int blocks_per_split;
-  int split_stride;  // floats per (split, head): m, l, zw, pad, acc[d], accw[d]
+  int n_wg;           // sparse workgroups per (sequence, kv head)
+  int blocks_per_wg;  // selected blocks per VALU-pass workgroup
+  int part_stride;    // floats per record: header + acc[G][d] + accw[G][d]
+  int n_lin;          // linear-term workgroups per (sequence, kv head)
 };
+
+// The MFMA sparse pass handles bf16 with G <= 8; everything else uses the
+// VALU pass. Both write records in the same format.
+SPLA_HD bool use_mfma_sparse(const Dims& m) { return m.elem == 2 && m.group <= 8; }
 
 SPLA_HD DecodeWs decode_ws_layout(const Dims& m) {
   DecodeWs w;
@@ -92,17 +100,18 @@ SPLA_HD DecodeWs decode_ws_layout(const Dims& m) {
     off = align_up(off + bytes, A);
     return o;
   };
-  w.blocks_per_split = 1;
-  w.n_splits = (int)ceil_div(m.k, w.blocks_per_split);
-  w.split_stride = 4 + 2 * m.d;
+  // MFMA pass: one 32-token step per wavefront; VALU pass: one block per workgroup
+  w.blocks_per_wg = 1;
+  w.n_wg = use_mfma_sparse(m) ? (int)ceil_div((int64_t)m.k * (m.B / 32), kSparseWaves) : m.k;
+  w.part_stride = kPartHead + 2 * m.group * m.d;
+  w.n_lin = m.d / kLinRows;
   w.e_vals = take((int64_t)m.bh * m.group * m.n_tiles * kTileBlocks * 4);
   w.tile_part = take((int64_t)m.bh * m.n_tiles * m.group * 2 * 8);
-  w.obar = take((int64_t)m.bh * m.group * m.d * 4);
-  w.zq = take((int64_t)m.bh * m.group * 4);
+  w.obar_part = take((int64_t)m.bh * w.n_lin * m.group * m.d * 4);
+  w.zq_part = take((int64_t)m.bh * w.n_lin * m.group * 4);
   w.sel = take((int64_t)m.bh * m.k * 4);
   w.meta = take((int64_t)m.bh * 4 * 4);
-  w.split = take((int64_t)m.bh * w.n_splits * m.group * w.split_stride * 4);
-  w.counters = take((int64_t)m.bh * 4 * 4);
+  w.part = take((int64_t)m.bh * w.n_wg * w.part_stride * 4);
   w.total = off;
   return w;
 }

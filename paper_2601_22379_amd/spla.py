@@ -23,7 +23,7 @@ F32, BF16 = 0, 1
 FLAG_NO_RLA, FLAG_FIRST_ORDER, FLAG_RLA_NORMALIZE = 1, 2, 4
 DEVERR_CAPACITY = 1
 MAX_GROUP, MAX_TOP_K, MAX_BLOCKS, WORKSPACE_ALIGN = 16, 256, 32768, 256
-PHASES = {"append": 0, "score": 1, "select": 2, "sparse": 3, "merge": 4, "linear": 5}
+PHASES = {"append": 0, "score": 1, "select": 2, "sparse": 3, "merge": 4}
 NUM_PHASES = 8
 STATUS = {0: "ok", -1: "invalid argument", -2: "unsupported shape",
           -3: "capacity or library limit exceeded", -4: "workspace missing, too small or misaligned",
@@ -294,8 +294,7 @@ class SplaCache:
                 self.norm.view(c.batch, c.n_kv_heads, c.head_dim))
 
 
-def make_events(phases: Sequence[str] = ("score", "select", "sparse", "merge", "linear",
-                                         "append")):
+def make_events(phases: Sequence[str] = ("score", "select", "sparse", "merge", "append")):
     """torch.cuda.Event pairs for the given phases, and the SplaEvents that
     points at their HIP events. Returns (events_struct, {phase: (start, stop)})."""
     ev = SplaEvents()
