@@ -58,6 +58,60 @@ __device__ __forceinline__ T wave_max(T v) {
   return v;
 }
 
+// ---- wavefront scans on DPP: shifts inside 16-lane rows, then the row
+// broadcasts of lanes 15 and 31. No LDS traffic; lane 63 ends with the total.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t old, uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp((int)old, (int)v, CTRL, ROW_MASK, 0xF, false);
+}
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ double dpp_f64(double old, double v) {
+  const uint64_t o = __double_as_longlong(old), x = __double_as_longlong(v);
+  const uint32_t lo = dpp_u32<CTRL, ROW_MASK>((uint32_t)o, (uint32_t)x);
+  const uint32_t hi = dpp_u32<CTRL, ROW_MASK>((uint32_t)(o >> 32), (uint32_t)(x >> 32));
+  return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+
+// Inclusive prefix sum over lanes 0 .. l.
+__device__ __forceinline__ uint32_t wave_incl_scan_u32(uint32_t x) {
+  x += dpp_u32<0x111, 0xF>(0u, x);  // row_shr:1
+  x += dpp_u32<0x112, 0xF>(0u, x);  // row_shr:2
+  x += dpp_u32<0x114, 0xF>(0u, x);  // row_shr:4
+  x += dpp_u32<0x118, 0xF>(0u, x);  // row_shr:8
+  x += dpp_u32<0x142, 0xA>(0u, x);  // row_bcast:15 into rows 1, 3
+  x += dpp_u32<0x143, 0xC>(0u, x);  // row_bcast:31 into rows 2, 3
+  return x;
+}
+
+__device__ __forceinline__ uint32_t lane_u32(uint32_t v, int lane) {
+  return (uint32_t)__builtin_amdgcn_readlane((int)v, lane);
+}
+__device__ __forceinline__ double lane_f64(double v, int lane) {
+  const uint64_t x = __double_as_longlong(v);
+  const uint32_t lo = lane_u32((uint32_t)x, lane), hi = lane_u32((uint32_t)(x >> 32), lane);
+  return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+
+// Wave-uniform sum / max of doubles (fixed association order).
+__device__ __forceinline__ double wave_sum_u(double x) {
+  x += dpp_f64<0x111, 0xF>(0.0, x);
+  x += dpp_f64<0x112, 0xF>(0.0, x);
+  x += dpp_f64<0x114, 0xF>(0.0, x);
+  x += dpp_f64<0x118, 0xF>(0.0, x);
+  x += dpp_f64<0x142, 0xA>(0.0, x);
+  x += dpp_f64<0x143, 0xC>(0.0, x);
+  return lane_f64(x, 63);
+}
+__device__ __forceinline__ double wave_max_u(double x) {
+  x = fmax(x, dpp_f64<0x111, 0xF>(-INFINITY, x));
+  x = fmax(x, dpp_f64<0x112, 0xF>(-INFINITY, x));
+  x = fmax(x, dpp_f64<0x114, 0xF>(-INFINITY, x));
+  x = fmax(x, dpp_f64<0x118, 0xF>(-INFINITY, x));
+  x = fmax(x, dpp_f64<0x142, 0xA>(-INFINITY, x));
+  x = fmax(x, dpp_f64<0x143, 0xC>(-INFINITY, x));
+  return lane_f64(x, 63);
+}
+
 // Number of tokens of block i in a sequence of length L.
 __device__ __forceinline__ int block_count(int L, int B, int i) {
   int n = L - i * B;
