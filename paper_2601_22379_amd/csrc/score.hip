@@ -1,190 +1,154 @@
-// Block scoring (Sec. 3.1) and the global linear term o_bar = phi(q) S_bar
-// (Sec. 3.2, Eq. 15), one kernel.
-//
-// Scoring workgroups: one per tile of 64 blocks of a (sequence, KV head);
-// each wavefront takes 16 blocks, lane = (block, quarter of the head
-// dimension). All of the lane's statistics loads are issued before any
-// arithmetic and before the query coefficients are read (16 x 16 B in
-// flight per lane), and every 16-byte load of the
-// tile-interleaved statistics is a contiguous 256 B run per 16 lanes. For
-// head m of the group the log block mass is
+// Block scoring (Sec. 3.1), one workgroup per (sequence, KV head, tile of 64
+// blocks) item; every item's loads are in flight from the start. Within a
+// tile each wavefront takes 16 blocks, lane =
+// (block, quarter of the head dimension); every 16-byte load of the
+// tile-interleaved statistics is a contiguous 256 B run per 16 lanes, and the
+// loads are nontemporal (each byte is read once per step). For head m of the
+// group the log block mass is
 //   ell_m(i) = s q_m.mu_i + ln n_i + ln(1 + 1/2 s^2 sum_j q_mj^2 M2_ij / n_i)
 // (Eqs. 8 and 10, diagonal covariance M2/n): four coordinates at a time in
 // fp32, those partial sums accumulated in fp64 and summed over the four
 // quarters with cross-lane shuffles; lane (block, quarter) then finishes
-// heads quarter, quarter+4, ... The workgroup writes exp(ell - tile max) per
-// head and block and the (max, sum) of its 64 blocks per head, from which
-// the selection forms each head's normaliser Z (Eq. 9) without another pass
-// over the statistics.
-//
-// Linear workgroups (blockIdx.x >= n_tiles): 16 rows of S_bar each,
-// o_bar partial[m][c] = sum_{j in rows} phi(q_m)_j S_bar[j][c] and
-// zq partial[m] = sum_{j in rows} phi(q_m)_j z_bar[j]; the merge adds the
-// partials.
+// heads quarter, quarter+4, ... Each tile yields exp(ell - tile max) per head
+// and block and the (max, sum) of its 64 blocks per head, from which the
+// selection forms each head's normaliser Z (Eq. 9) without another pass over
+// the statistics. For the matrix-core sparse pass, bh trailing workgroups
+// also lay out the query operands of its products.
 #include "spla_device.h"
 #include "spla_kernels.h"
 
 namespace spla {
 
 constexpr int kScoreGroup = 16;  // blocks per wavefront
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 
-template <int G, typename T, int D>
-__device__ __forceinline__ void linear_part(const Dims& m, const float* __restrict__ S,
-                                            const float* __restrict__ zbar, const T* __restrict__ q,
-                                            float* __restrict__ obar_part,
-                                            float* __restrict__ zq_part, float (*sphi)[D],
-                                            float (*sred)[G][D]) {
-  constexpr int NRG = 256 / D;
-  const int bh = blockIdx.y;
-  const int b = bh / m.hkv, h = bh % m.hkv;
-  const int chunk = blockIdx.x - m.n_tiles;
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  for (int mm = w; mm < G; mm += 4) {
-    float x[D / 64];
-    float mx = -INFINITY;
+template <int NJ>
+struct TileBuf {
+  float4 mu[NJ], m2[NJ];
+};
+
+// Issues the statistics loads of item t (sequence x KV head x tile) for this
+// lane; an item past the run (valid = false) re-reads the first 16 bytes of
+// the buffer, so every path issues the same loads and no wait depends on the
+// branch taken.
+template <int NJ>
+__device__ __forceinline__ void load_tile(const Dims& m, const float* __restrict__ stats, int t,
+                                          bool valid, int first_order, int bi, int qt,
+                                          TileBuf<NJ>& buf) {
+  const int bh = t / m.n_tiles, tile = t % m.n_tiles;
+  const int64_t blk = (int64_t)tile * kTileBlocks + bi;
+  // first order: the second-moment loads re-read the means (same lines)
+  const f32x4* pm = reinterpret_cast<const f32x4*>(
+      valid ? stats + stats_off4(m, bh, blk, 0, qt * NJ) : stats);
+  const f32x4* pv = reinterpret_cast<const f32x4*>(
+      valid ? stats + stats_off4(m, bh, blk, first_order ? 0 : 1, qt * NJ) : stats);
+  const int stride = valid ? kTileBlocks : 0;
 #pragma unroll
-    for (int e = 0; e < D / 64; ++e) {
-      x[e] = Elem<T>::load(q, ((int64_t)b * m.hq + h * G + mm) * D + lane + 64 * e);
-      mx = fmaxf(mx, x[e]);
-    }
-    mx = wave_max(mx);
-    float sum = 0.f;
-#pragma unroll
-    for (int e = 0; e < D / 64; ++e) {
-      x[e] = expf(x[e] - mx);
-      sum += x[e];
-    }
-    sum = wave_sum(sum);
-#pragma unroll
-    for (int e = 0; e < D / 64; ++e) sphi[mm][lane + 64 * e] = x[e] / sum;
-  }
-  __syncthreads();
-  const int col = tid % D, sub = tid / D;
-  const int row0 = chunk * kLinRows;
-  float acc[G];
-#pragma unroll
-  for (int mm = 0; mm < G; ++mm) acc[mm] = 0.f;
-  const float* Sb = S + (int64_t)bh * D * D;
-#pragma unroll
-  for (int r = sub; r < kLinRows; r += NRG) {
-    const float sv = Sb[(row0 + r) * D + col];
-#pragma unroll
-    for (int mm = 0; mm < G; ++mm) acc[mm] = fmaf(sphi[mm][row0 + r], sv, acc[mm]);
-  }
-#pragma unroll
-  for (int mm = 0; mm < G; ++mm) sred[sub][mm][col] = acc[mm];
-  __syncthreads();
-  float* op = obar_part + ((int64_t)bh * (D / kLinRows) + chunk) * G * D;
-  for (int e = tid; e < G * D; e += 256) {
-    const int mm = e / D, c = e % D;
-    float s = 0.f;
-#pragma unroll
-    for (int r = 0; r < NRG; ++r) s += sred[r][mm][c];
-    op[mm * D + c] = s;
-  }
-  if (tid < G) {
-    float s = 0.f;
-    for (int r = 0; r < kLinRows; ++r) s += sphi[tid][row0 + r] * zbar[(int64_t)bh * D + row0 + r];
-    zq_part[((int64_t)bh * (D / kLinRows) + chunk) * G + tid] = s;
+  for (int j = 0; j < NJ; ++j) {  // interleaved: group j is usable once its two loads land
+    const f32x4 x = __builtin_nontemporal_load(pm + j * stride);
+    const f32x4 y = __builtin_nontemporal_load(pv + j * stride);
+    buf.mu[j] = make_float4(x[0], x[1], x[2], x[3]);
+    buf.m2[j] = make_float4(y[0], y[1], y[2], y[3]);
   }
 }
 
+// Coefficient tables of sequence x KV head bh: s q and s^2 q^2 / 2 per head,
+// [head][group of 4 coordinates][quarter][4] (the four quarters read
+// adjacent 16-byte words). load_q issues the query loads, write_table fills
+// the tables; clamped entries rewrite the last element's value.
+template <int G, int D>
+struct QRegs {
+  float x[(G * D + 255) / 256];
+};
+
 template <int G, typename T, int D>
-__global__ __launch_bounds__(256) void score_linear_kernel(
-    Dims m, const float* __restrict__ stats, const float* __restrict__ S,
-    const float* __restrict__ zbar, const int32_t* __restrict__ seq_lens, const T* __restrict__ q,
-    double s, int first_order, float* __restrict__ e_vals, double* __restrict__ tile_part,
-    float* __restrict__ obar_part, float* __restrict__ zq_part) {
-  constexpr int Q = D / 4;         // coordinates per lane (one quarter of d)
-  constexpr int NJ = Q / 4;        // float4 loads per lane and statistics part
-  // coefficient tables, [head][group of 4 coordinates][quarter][4]: the four
-  // quarters read adjacent 16-byte words (distinct banks)
-  __shared__ float4 sq[G][NJ][4];
-  __shared__ float4 sq2[G][NJ][4];
-  __shared__ float sphi[G][D];
-  __shared__ float sred[256 / D][G][D];
-  __shared__ double s_part[4][G][2];
-  const int bh = blockIdx.y;
+__device__ __forceinline__ void load_q(const Dims& m, const T* __restrict__ q, int bh,
+                                       QRegs<G, D>& r) {
+  constexpr int QE = (G * D + 255) / 256;
   const int b = bh / m.hkv, h = bh % m.hkv;
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  if ((int)blockIdx.x >= m.n_tiles) {
-    linear_part<G, T, D>(m, S, zbar, q, obar_part, zq_part, sphi, sred);
-    return;
-  }
-  const int L = seq_lens[b];
-  const int nb = (L + m.B - 1) / m.B;
-  const int tile = blockIdx.x;
-  if (tile * kTileBlocks >= nb) return;
-  const int grp = tile * (kTileBlocks / kScoreGroup) + w;
-  const bool grp_live = grp * kScoreGroup < nb;
-  const int blk = grp * kScoreGroup + (lane & 15);
-  const int qt = lane >> 4;  // quarter of the head dimension
-  // statistics loads first; the coefficient table is built while they fly
-  float4 mu[NJ], m2[NJ];
-  if (grp_live) {
-    const float4* pm = reinterpret_cast<const float4*>(stats + stats_off4(m, bh, blk, 0, qt * NJ));
-    const float4* pv = reinterpret_cast<const float4*>(stats + stats_off4(m, bh, blk, 1, qt * NJ));
 #pragma unroll
-    for (int t = 0; t < NJ; ++t) mu[t] = pm[t * kTileBlocks];
-    if (!first_order) {
-#pragma unroll
-      for (int t = 0; t < NJ; ++t) m2[t] = pv[t * kTileBlocks];
-    }
+  for (int i = 0; i < QE; ++i) {
+    const int e = min((int)threadIdx.x + 256 * i, G * D - 1);
+    r.x[i] = Elem<T>::load(q, ((int64_t)b * m.hq + h * G + e / D) * D + e % D);
   }
-  for (int e = tid; e < G * D; e += 256) {
+}
+
+template <int G, int D>
+__device__ __forceinline__ void write_table(const QRegs<G, D>& r, double s, float4 (*sq)[D / 16][4],
+                                            float4 (*sq2)[D / 16][4]) {
+  constexpr int Q = D / 4;
+  constexpr int QE = (G * D + 255) / 256;
+#pragma unroll
+  for (int i = 0; i < QE; ++i) {
+    const int e = min((int)threadIdx.x + 256 * i, G * D - 1);
     const int mm = e / D, j = e % D;
-    const float x = Elem<T>::load(q, ((int64_t)b * m.hq + h * G + mm) * D + j);
     const int qq = j / Q, jj = j % Q;
+    const double x = (double)r.x[i];
     reinterpret_cast<float*>(&sq[mm][jj / 4][qq])[jj % 4] = (float)(s * x);
     reinterpret_cast<float*>(&sq2[mm][jj / 4][qq])[jj % 4] = (float)(0.5 * s * s * x * x);
   }
-  __syncthreads();
+}
+
+// Scores one tile from buf; s_part is this tile's half of the double-buffered
+// cross-wavefront scratch.
+template <int G, int D>
+__device__ __forceinline__ void score_tile(const Dims& m, const int32_t* __restrict__ seq_lens,
+                                           int first_order, int t, const TileBuf<D / 16>& buf,
+                                           const float4 (*sq)[D / 16][4],
+                                           const float4 (*sq2)[D / 16][4],
+                                           double (*s_part)[G][2], float* __restrict__ e_vals,
+                                           double* __restrict__ tile_part) {
+  constexpr int NJ = D / 16;
+  constexpr int U = (G + 3) / 4;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int qt = lane >> 4;
+  const int bh = t / m.n_tiles, tile = t % m.n_tiles;
+  const int blk = tile * kTileBlocks + kScoreGroup * w + (lane & 15);
+  const int L = seq_lens[bh / m.hkv];
+  const int nb = (L + m.B - 1) / m.B;
   double am[G], av[G];
 #pragma unroll
   for (int mm = 0; mm < G; ++mm) am[mm] = av[mm] = 0.0;
-  if (grp_live) {
-    // four coordinates at a time in fp32, accumulated across groups in fp64
+  // four coordinates at a time in fp32, accumulated across groups in fp64
 #pragma unroll
-    for (int t = 0; t < NJ; ++t) {
-#pragma unroll
-      for (int mm = 0; mm < G; ++mm) {
-        const float4 c = sq[mm][t][qt];
-        float pa = c.x * mu[t].x;
-        pa = fmaf(c.y, mu[t].y, pa);
-        pa = fmaf(c.z, mu[t].z, pa);
-        pa = fmaf(c.w, mu[t].w, pa);
-        am[mm] += (double)pa;
-        asm volatile("" : "+v"(am[mm]));  // add in coordinate order; keeps few partials live
-      }
-      if (!first_order) {
-#pragma unroll
-        for (int mm = 0; mm < G; ++mm) {
-          const float4 c = sq2[mm][t][qt];
-          float pb = c.x * m2[t].x;
-          pb = fmaf(c.y, m2[t].y, pb);
-          pb = fmaf(c.z, m2[t].z, pb);
-          pb = fmaf(c.w, m2[t].w, pb);
-          av[mm] += (double)pb;
-          asm volatile("" : "+v"(av[mm]));
-        }
-      }
-    }
+  for (int j = 0; j < NJ; ++j) {
 #pragma unroll
     for (int mm = 0; mm < G; ++mm) {
-      am[mm] += __shfl_xor(am[mm], 16, kWave);
-      am[mm] += __shfl_xor(am[mm], 32, kWave);
-      av[mm] += __shfl_xor(av[mm], 16, kWave);
-      av[mm] += __shfl_xor(av[mm], 32, kWave);
+      const float4 c = sq[mm][j][qt];
+      float pa = c.x * buf.mu[j].x;
+      pa = fmaf(c.y, buf.mu[j].y, pa);
+      pa = fmaf(c.z, buf.mu[j].z, pa);
+      pa = fmaf(c.w, buf.mu[j].w, pa);
+      am[mm] += (double)pa;
+      asm volatile("" : "+v"(am[mm]));  // add in coordinate order; keeps few partials live
     }
+    // (also in first-order mode, where the term is discarded: a branch here
+    // would let the compiler sink the second-moment loads into it)
+#pragma unroll
+    for (int mm = 0; mm < G; ++mm) {
+      const float4 c = sq2[mm][j][qt];
+      float pb = c.x * buf.m2[j].x;
+      pb = fmaf(c.y, buf.m2[j].y, pb);
+      pb = fmaf(c.z, buf.m2[j].z, pb);
+      pb = fmaf(c.w, buf.m2[j].w, pb);
+      av[mm] += (double)pb;
+      asm volatile("" : "+v"(av[mm]));
+    }
+  }
+#pragma unroll
+  for (int mm = 0; mm < G; ++mm) {
+    am[mm] += __shfl_xor(am[mm], 16, kWave);
+    am[mm] += __shfl_xor(am[mm], 32, kWave);
+    av[mm] += __shfl_xor(av[mm], 16, kWave);
+    av[mm] += __shfl_xor(av[mm], 32, kWave);
   }
   // every lane now holds all G sums of its block; lane (block, qt) finishes
   // heads qt, qt+4, ...: one fp64 log1p / exp per head and lane
-  const bool valid = grp_live && blk < nb;
+  const bool valid = blk < nb;
   const int n_i = valid ? block_count(L, m.B, blk) : 1;
   const double ln_n = log((double)n_i);
   const int nbp = m.n_tiles * kTileBlocks;
   float* ev = e_vals + (int64_t)bh * G * nbp;
-  constexpr int U = (G + 3) / 4;
   double ell[U];
 #pragma unroll
   for (int u = 0; u < U; ++u) {
@@ -217,7 +181,7 @@ __global__ __launch_bounds__(256) void score_linear_kernel(
       double sum = e;
 #pragma unroll
       for (int o = 1; o < 16; o <<= 1) sum += __shfl_xor(sum, o, kWave);
-      if (grp_live) ev[(int64_t)mm * nbp + blk] = (float)e;
+      ev[(int64_t)mm * nbp + blk] = (float)e;
       if ((lane & 15) == 0) s_part[w][mm][1] = sum;
     }
   }
@@ -235,17 +199,111 @@ __global__ __launch_bounds__(256) void score_linear_kernel(
   }
 }
 
+// Query operands of the sparse pass's matrix products for one sequence x KV
+// head, in the per-lane order the pass loads them (16 bytes per lane and
+// k-step): lane l = (g = l / 16, column j = l % 16) holds coordinates
+// 32 ks + 8 g .. +7 of head j (columns 0..7: q itself, the exact-branch
+// logits) or of head j - 8 (columns 8..15: phi(q) as a bf16 hi + lo pair,
+// the linear weights); absent heads are zero. phi is the softmax over the
+// feature dimension (Sec. 3.2).
+template <int G, int D>
+__device__ void prep_q_operands(const Dims& m, const bf16_t* __restrict__ q, int bh,
+                                uint4* __restrict__ qprep, float (*sphi)[D]) {
+  constexpr int KS = D / 32;
+  const int b = bh / m.hkv, h = bh % m.hkv;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  for (int mm = w; mm < G; mm += 4) {
+    float x[D / 64];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int e = 0; e < D / 64; ++e) {
+      x[e] = Elem<bf16_t>::load(q, ((int64_t)b * m.hq + h * G + mm) * D + lane + 64 * e);
+      mx = fmaxf(mx, x[e]);
+    }
+    mx = wave_max(mx);
+    float sum = 0.f;
+#pragma unroll
+    for (int e = 0; e < D / 64; ++e) {
+      x[e] = __expf(x[e] - mx);
+      sum += x[e];
+    }
+    sum = wave_sum(sum);
+    const float inv = 1.0f / sum;
+#pragma unroll
+    for (int e = 0; e < D / 64; ++e) sphi[mm][lane + 64 * e] = x[e] * inv;
+  }
+  __syncthreads();
+  for (int c = tid; c < 3 * KS * 64; c += 256) {
+    const int kind = c / (KS * 64), ks = (c / 64) % KS, l = c % 64;
+    const int g = l >> 4, j = l & 15;
+    const bool exact = j < 8;
+    const int head = exact ? j : j - 8;
+    const bool live = head < G && (kind == 0) == exact;
+    uint16_t v[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int coord = 32 * ks + 8 * g + e;
+      uint16_t bits = 0;
+      if (live) {
+        if (kind == 0) {
+          bits = q[((int64_t)b * m.hq + h * G + head) * D + coord].bits;
+        } else {
+          const float pq = sphi[head][coord];
+          const __bf16 hi = (__bf16)pq;
+          const __bf16 val = kind == 1 ? hi : (__bf16)(pq - (float)hi);
+          bits = __builtin_bit_cast(uint16_t, val);
+        }
+      }
+      v[e] = bits;
+    }
+    qprep[((int64_t)bh * 3 * KS + kind * KS + ks) * 64 + l] =
+        make_uint4(v[0] | ((uint32_t)v[1] << 16), v[2] | ((uint32_t)v[3] << 16),
+                   v[4] | ((uint32_t)v[5] << 16), v[6] | ((uint32_t)v[7] << 16));
+  }
+}
+
+template <int G, typename T, int D>
+__global__ __launch_bounds__(256) void score_kernel(
+    Dims m, const float* __restrict__ stats, const int32_t* __restrict__ seq_lens,
+    const T* __restrict__ q, double s, int first_order, float* __restrict__ e_vals,
+    double* __restrict__ tile_part, uint4* __restrict__ qprep) {
+  constexpr int NJ = D / 16;  // float4 loads per lane and statistics part
+  __shared__ float4 sq[G][NJ][4];
+  __shared__ float4 sq2[G][NJ][4];
+  __shared__ double s_part[4][G][2];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int t = blockIdx.x;  // item: sequence x KV head x tile
+  if (t >= m.bh * m.n_tiles) {  // trailing workgroups: query operands of the sparse pass
+    if constexpr (G <= 8 && sizeof(T) == 2) {
+      __shared__ float sphi[G][D];
+      prep_q_operands<G, D>(m, q, t - m.bh * m.n_tiles, qprep, sphi);
+    }
+    return;
+  }
+  // load order: the query elements of the coefficient table, then the
+  // statistics (16 x 16 B per lane); the table is built while the statistics
+  // are in flight. Items past the sequence end are scored and masked: an
+  // early exit would let the compiler sink the loads below the barrier.
+  QRegs<G, D> qr;
+  load_q<G, T, D>(m, q, t / m.n_tiles, qr);
+  TileBuf<NJ> A;
+  load_tile<NJ>(m, stats, t, true, first_order, kScoreGroup * w + (lane & 15), lane >> 4, A);
+  __builtin_amdgcn_sched_barrier(0);
+  write_table<G, D>(qr, s, sq, sq2);
+  __syncthreads();
+  score_tile<G, D>(m, seq_lens, first_order, t, A, sq, sq2, s_part, e_vals, tile_part);
+}
+
 template <int G, typename T, int D>
 static void score_gtd(const Dims& m, const spla_config& cfg, const spla_cache& c, const void* q,
                       const DecodeWs& ws, char* base, hipStream_t st) {
   const double s = cfg.softmax_scale > 0.f ? (double)cfg.softmax_scale : 1.0 / sqrt((double)m.d);
-  dim3 grid((unsigned)(m.n_tiles + ws.n_lin), (unsigned)m.bh);
-  hipLaunchKernelGGL((score_linear_kernel<G, T, D>), grid, dim3(256), 0, st, m,
-                     (const float*)c.blk_stats, (const float*)c.lin_state,
-                     (const float*)c.lin_norm, (const int32_t*)c.seq_lens, (const T*)q, s,
-                     (int)((cfg.flags & SPLA_FLAG_FIRST_ORDER) != 0), (float*)(base + ws.e_vals),
-                     (double*)(base + ws.tile_part), (float*)(base + ws.obar_part),
-                     (float*)(base + ws.zq_part));
+  const int n_prep = use_mfma_sparse(m) ? m.bh : 0;
+  hipLaunchKernelGGL((score_kernel<G, T, D>), dim3((unsigned)(m.bh * m.n_tiles + n_prep)),
+                     dim3(256), 0, st, m, (const float*)c.blk_stats, (const int32_t*)c.seq_lens,
+                     (const T*)q, s, (int)((cfg.flags & SPLA_FLAG_FIRST_ORDER) != 0),
+                     (float*)(base + ws.e_vals), (double*)(base + ws.tile_part),
+                     (uint4*)(base + ws.qprep));
 }
 
 template <typename T, int D>

@@ -110,7 +110,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
     Dims m, const int32_t* __restrict__ seq_lens, const float* __restrict__ e_vals,
     const double* __restrict__ tile_part, int32_t* __restrict__ sel_ws,
     int32_t* __restrict__ sel_out, int32_t* __restrict__ meta) {
-  constexpr int HC = R <= 2 ? 16 : 32 / R;  // heads per load batch
+  constexpr int HC = R <= 2 ? 16 / R : (R <= 8 ? 4 : 32 / R);  // heads per load batch
   constexpr int TJ = R <= 4 ? 1 : R / 4;      // tiles per lane: n_tiles <= 16 R
   __shared__ float sw[kMaxTiles * SPLA_MAX_GROUP];       // tile weights [tile][head]
   __shared__ __align__(16) uint32_t hist[4096];  // digit histograms: 2048 + 1024 + 1024 bins

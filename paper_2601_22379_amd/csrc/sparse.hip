@@ -7,10 +7,16 @@
 //   - the selected-token linear term of Eq. (16):
 //     accw = sum_t <phi(q), phi(k_t)> v_t and zw = sum_t <phi(q), phi(k_t)>,
 //     phi being the softmax over the feature dimension.
-// Each workgroup writes one record (m, l, zw, acc, accw). The merge kernel
-// (one workgroup per sequence x KV head) combines the records, forms the
-// residual r = o_bar - o_tilde (Eq. 14; exactly 0 when every token is
-// selected) and writes out = o_sparse + gamma * r / sqrt(mean(r^2) + eps)
+// The global linear term o_bar = phi(q) S_bar and <phi(q), z_bar> (Eq. 15) is
+// split over the same workgroups by rows of S_bar: workgroup x of a
+// (sequence, KV head) owns rows x*RW .. x*RW + RW - 1 (RW = ceil(d / n_wg)),
+// loads them at its start next to the key / value loads, and subtracts its
+// selected-token terms from its share, so each record carries
+// (m, l, zq_x - zw, acc, obar_x - accw). The merge kernel (one workgroup per
+// sequence x KV head) combines the records: the sum of the last fields is
+// the residual numerator o_bar - o_tilde of Eq. (14) (and its normaliser
+// <phi(q), z_bar> - z_tilde); the residual is exactly 0 when every token is
+// selected. It writes out = o_sparse + gamma * r / sqrt(mean(r^2) + eps)
 // (Sec. 3.3).
 //
 // bf16 with G <= 8 runs on the matrix cores (v_mfma_f32_16x16x32_bf16, one
@@ -33,11 +39,9 @@ template <typename T, int D>
 __device__ void final_merge(const Dims& m, float eps, uint32_t flags,
                             const float* __restrict__ gamma, const int32_t* __restrict__ meta,
                             const float* __restrict__ rec, int n_rec, int stride,
-                            const float* __restrict__ obar_part, const float* __restrict__ zq_part,
                             T* __restrict__ out) {
   constexpr int E = D / 64;       // coordinates per lane
   constexpr int NB = 8;           // records loaded per batch
-  constexpr int NL = D / kLinRows;
   const int bh = blockIdx.y;
   const int b = bh / m.hkv, h = bh % m.hkv;
   const int G = m.group;
@@ -51,29 +55,6 @@ __device__ void final_merge(const Dims& m, float eps, uint32_t flags,
 #pragma unroll
       for (int e = 0; e < E; ++e) Elem<T>::store(out, orow + lane + 64 * e, 0.f);
       continue;
-    }
-    // the residual's ingredients do not depend on the records: load them first
-    float ob[E], zq = 0.f;
-#pragma unroll
-    for (int e = 0; e < E; ++e) ob[e] = 0.f;
-    {
-      float part[NL][E];
-#pragma unroll
-      for (int c = 0; c < NL; ++c)
-#pragma unroll
-        for (int e = 0; e < E; ++e)
-          part[c][e] = obar_part[(((int64_t)bh * NL + c) * G + g) * D + lane + 64 * e];
-#pragma unroll
-      for (int c = 0; c < NL; ++c)
-#pragma unroll
-        for (int e = 0; e < E; ++e) ob[e] += part[c][e];
-      if (flags & SPLA_FLAG_RLA_NORMALIZE) {
-        float zp[NL];
-#pragma unroll
-        for (int c = 0; c < NL; ++c) zp[c] = zq_part[((int64_t)bh * NL + c) * G + g];
-#pragma unroll
-        for (int c = 0; c < NL; ++c) zq += zp[c];
-      }
     }
     // records in batches; every load of a batch is issued before its math,
     // and the running max is rescaled as in an online softmax
@@ -116,13 +97,13 @@ __device__ void final_merge(const Dims& m, float eps, uint32_t flags,
       }
       M = bm;
     }
-    const float den = (flags & SPLA_FLAG_RLA_NORMALIZE) ? zq - zt : 1.f;
+    const float den = (flags & SPLA_FLAG_RLA_NORMALIZE) ? zt : 1.f;
     float rr[E];
     float ss = 0.f;
 #pragma unroll
     for (int e = 0; e < E; ++e) {
       osp[e] /= l;
-      rr[e] = (rla && !all_sel) ? (ob[e] - ot[e]) / den : 0.f;
+      rr[e] = (rla && !all_sel) ? ot[e] / den : 0.f;
       ss += rr[e] * rr[e];
     }
     ss = wave_sum(ss);
@@ -137,14 +118,23 @@ __device__ void final_merge(const Dims& m, float eps, uint32_t flags,
   }
 }
 
+// ------------------------------------------------ global linear term
+// Rows of S_bar owned by workgroup x of n_wg: row0 .. row0 + nrows - 1.
+__device__ __forceinline__ void lin_rows(int D, int x, int n_wg, int* row0, int* nrows) {
+  const int rw = (D + n_wg - 1) / n_wg;
+  const int r0 = x * rw;
+  *row0 = r0;
+  *nrows = r0 >= D ? 0 : (D - r0 < rw ? D - r0 : rw);
+}
+
 // ------------------------------------------------------------ VALU pass
 template <typename T, int D>
 __global__ __launch_bounds__(256) void sparse_valu_kernel(
     Dims m, float s, float eps, uint32_t flags, const T* __restrict__ kc,
     const T* __restrict__ vc, const T* __restrict__ q, const float* __restrict__ gamma,
+    const float* __restrict__ S, const float* __restrict__ zbar,
     const int32_t* __restrict__ sel, const int32_t* __restrict__ meta, int bps, int stride,
-    float* __restrict__ part, const float* __restrict__ obar_part,
-    const float* __restrict__ zq_part, T* __restrict__ out) {
+    float* __restrict__ part) {
   constexpr int MG = SPLA_MAX_GROUP;
   constexpr int PER = (MG * D + 255) / 256;  // (head, coord) pairs per thread
   __shared__ float sq[MG][D];
@@ -276,20 +266,28 @@ __global__ __launch_bounds__(256) void sparse_valu_kernel(
       __syncthreads();
     }
   }
+  // this workgroup's rows of the global linear term, minus its selected terms
+  int row0, nrows;
+  lin_rows(D, split, gridDim.x, &row0, &nrows);
+  const float* Sb = S + (int64_t)bh * D * D;
   float* rec = part + ((int64_t)bh * gridDim.x + split) * stride;
 #pragma unroll
   for (int r = 0; r < PER; ++r) {
     const int idx = tid + 256 * r;
     if (idx < G * D) {
       const int mm = idx / D, c = idx % D;
+      float ob = 0.f;
+      for (int j = row0; j < row0 + nrows; ++j) ob = fmaf(sphq[mm][j], Sb[j * D + c], ob);
       rec[kPartHead + mm * D + c] = acc[r];
-      rec[kPartHead + (G + mm) * D + c] = accw[r];
+      rec[kPartHead + (G + mm) * D + c] = ob - accw[r];
     }
   }
   if (tid < G) {
+    float zq = 0.f;
+    for (int j = row0; j < row0 + nrows; ++j) zq = fmaf(sphq[tid][j], zbar[(int64_t)bh * D + j], zq);
     rec[tid] = s_m[tid];
     rec[16 + tid] = s_l[tid];
-    rec[32 + tid] = s_zw[tid];
+    rec[32 + tid] = zq - s_zw[tid];
   }
 }
 
@@ -308,13 +306,18 @@ __global__ __launch_bounds__(256) void sparse_valu_kernel(
 template <int D, int BLK>
 __global__ __launch_bounds__(256) void sparse_mfma_kernel(
     Dims m, float s, const bf16_t* __restrict__ kc, const bf16_t* __restrict__ vc,
-    const bf16_t* __restrict__ q, const int32_t* __restrict__ sel,
-    const int32_t* __restrict__ meta, int stride, float* __restrict__ part) {
+    const uint4* __restrict__ qprep, const float* __restrict__ S, const float* __restrict__ zbar,
+    const int32_t* __restrict__ sel, const int32_t* __restrict__ meta, int stride,
+    float* __restrict__ part) {
   constexpr int KS = D / 32;   // k-steps of the first product
   constexpr int MT = D / 16;   // coordinate tiles of the second product
   constexpr int CPB = BLK / 32;  // steps per block
+  constexpr int SPRE = 8;        // S_bar entries per thread loaded up front
   __shared__ float s_o[kSparseWaves][D][17];
   __shared__ float s_m[kSparseWaves][16], s_l[kSparseWaves][16];
+  __shared__ float s_phq[8][D];          // phi(q) of the group's heads
+  __shared__ float s_S[SPRE * 256];      // this workgroup's rows of S_bar
+  __shared__ float s_zb[D];
   const int bh = blockIdx.y;
   const int b = bh / m.hkv, h = bh % m.hkv;
   const int G = m.group;
@@ -329,10 +332,32 @@ __global__ __launch_bounds__(256) void sparse_mfma_kernel(
   // -1), the sequence length and this lane's query slice
   const int blk_sel = p < m.k ? sel[(int64_t)bh * m.k + p] : -1;
   const int L = meta[bh * 4 + 2];
-  const bf16_t* qrow = q + ((int64_t)b * m.hq + h * G + (live ? head : 0)) * D;
-  bf16x8 qraw[KS];
+  // B operands, laid out per lane by the scoring pass: [q | 0] for the
+  // logits, [0 | phi(q)_hi] and [0 | phi(q)_lo] for the linear weights
+  bf16x8 qb[KS], pqh[KS], pql[KS];
+  {
+    const uint4* qp = qprep + (int64_t)bh * 3 * KS * 64 + lane;
 #pragma unroll
-  for (int ks = 0; ks < KS; ++ks) qraw[ks] = *reinterpret_cast<const bf16x8*>(qrow + 32 * ks + 8 * g);
+    for (int ks = 0; ks < KS; ++ks) {
+      qb[ks] = __builtin_bit_cast(bf16x8, qp[(0 * KS + ks) * 64]);
+      pqh[ks] = __builtin_bit_cast(bf16x8, qp[(1 * KS + ks) * 64]);
+      pql[ks] = __builtin_bit_cast(bf16x8, qp[(2 * KS + ks) * 64]);
+    }
+  }
+  // this workgroup's rows of S_bar and z_bar (read here, used in the epilogue)
+  int row0, nrows;
+  lin_rows(D, blockIdx.x, gridDim.x, &row0, &nrows);
+  const bool s_pre = nrows * D <= SPRE * 256;
+  float spre[SPRE];
+  {
+    const float* Sb = S + ((int64_t)bh * D + row0) * D;
+#pragma unroll
+    for (int u = 0; u < SPRE; ++u) {
+      const int e = tid + 256 * u;
+      spre[u] = (s_pre && e < nrows * D) ? Sb[e] : 0.f;
+    }
+  }
+  const float zbv = tid < nrows ? zbar[(int64_t)bh * D + row0 + tid] : 0.f;
   const int nb = (L + BLK - 1) / BLK;
   int n_valid = 0;  // tokens of this step that exist
   bf16x8 ka[2][KS];
@@ -359,52 +384,25 @@ __global__ __launch_bounds__(256) void sparse_mfma_kernel(
 #pragma unroll
   for (int t = 0; t < MT; ++t) acc_o[t] = floatx4{0.f, 0.f, 0.f, 0.f};
   float m_run = -INFINITY, l_run = 0.f;  // exact columns: max / sum; linear columns: sum
+  // wavefront 0 leaves phi(q) (hi + lo) in LDS for the global linear term
+  if (w == 0 && !exact_col && live) {
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        s_phq[head][32 * ks + 8 * g + e] = (float)pqh[ks][e] + (float)pql[ks][e];
+  }
   if (n_valid > 0) {
-    // B operands (while the key / value loads are in flight): [q | 0] for the
-    // logits, [0 | phi(q)_hi] and [0 | phi(q)_lo] for the linear weights
-    bf16x8 qb[KS], pqh[KS], pql[KS];
-    {
-      float x[KS][8];
-      float mx = -INFINITY;
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          x[ks][e] = live ? (float)qraw[ks][e] : 0.f;
-          mx = fmaxf(mx, x[ks][e]);
-        }
-      }
-      mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
-      mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
-      float sum = 0.f;
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) sum += exp2f((x[ks][e] - mx) * kLog2e);
-      sum += __shfl_xor(sum, 16, kWave);
-      sum += __shfl_xor(sum, 32, kWave);
-      const float inv = 1.0f / sum;
-      const __bf16 zero = (__bf16)0.f;
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const float pq = exp2f((x[ks][e] - mx) * kLog2e) * inv;
-          const __bf16 hi = (__bf16)pq;
-          const __bf16 lo = (__bf16)(pq - (float)hi);
-          qb[ks][e] = (exact_col && live) ? (__bf16)x[ks][e] : zero;
-          pqh[ks][e] = (!exact_col && live) ? hi : zero;
-          pql[ks][e] = (!exact_col && live) ? lo : zero;
-        }
-    }
     floatx4 sw[2];
+    float zinv[2];  // 1 / sum exp(k - max k) of this lane's key row, per tile
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt) {
       sw[mt] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks)
         sw[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[mt][ks], qb[ks], sw[mt], 0, 0, 0);
-      // phi(k) of this lane's key row (row i of the tile), spread over lanes i + 16 g'
+      // exp(k - max k) of this lane's key row (row i of the tile), spread over
+      // lanes i + 16 g'; the 1 / sum of phi(k) is applied to the result rows
       float kx[KS][8];
       float mx = -INFINITY;
 #pragma unroll
@@ -422,18 +420,18 @@ __global__ __launch_bounds__(256) void sparse_mfma_kernel(
       for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          kx[ks][e] = exp2f(fmaf(kx[ks][e], kLog2e, -mxl));
+          kx[ks][e] = __builtin_amdgcn_exp2f(fmaf(kx[ks][e], kLog2e, -mxl));
           sum += kx[ks][e];
         }
       sum += __shfl_xor(sum, 16, kWave);
       sum += __shfl_xor(sum, 32, kWave);
-      const float inv = 1.0f / sum;
+      zinv[mt] = 1.0f / sum;
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
         bf16x8 fh, fl;
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          const float f = kx[ks][e] * inv;
+          const float f = kx[ks][e];
           const __bf16 hi = (__bf16)f;
           fh[e] = hi;
           fl[e] = (__bf16)(f - (float)hi);
@@ -444,13 +442,16 @@ __global__ __launch_bounds__(256) void sparse_mfma_kernel(
       }
     }
     // tokens 8g .. 8g+7 of this step: tile 0 rows 4g..4g+3, tile 1 rows 4g..4g+3
+    // (result row 4g + r of tile t is token 8g + 4t + r; its 1 / Z sits in
+    // lane 4g + r)
     float val[8];
     float cmax = -INFINITY;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       const bool ok = 8 * g + e < n_valid;
+      const float zi = __shfl(zinv[e >> 2], 4 * g + (e & 3), kWave);
       const float x = sw[e >> 2][e & 3];
-      val[e] = exact_col ? (ok ? x * s : -INFINITY) : (ok ? x : 0.f);
+      val[e] = exact_col ? (ok ? x * s : -INFINITY) : (ok ? x * zi : 0.f);
       cmax = fmaxf(cmax, val[e]);
     }
     cmax = fmaxf(cmax, __shfl_xor(cmax, 16, kWave));
@@ -459,7 +460,7 @@ __global__ __launch_bounds__(256) void sparse_mfma_kernel(
     bf16x8 bh8, bl8;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      const float pv = exact_col ? exp2f((val[e] - cmax) * kLog2e) : val[e];
+      const float pv = exact_col ? __builtin_amdgcn_exp2f((val[e] - cmax) * kLog2e) : val[e];
       psum += pv;
       const __bf16 hi = (__bf16)pv;
       bh8[e] = hi;
@@ -491,6 +492,9 @@ __global__ __launch_bounds__(256) void sparse_mfma_kernel(
     s_m[w][lane] = m_run;
     s_l[w][lane] = l_run;
   }
+#pragma unroll
+  for (int u = 0; u < SPRE; ++u) s_S[tid + 256 * u] = spre[u];
+  if (tid < D) s_zb[tid] = zbv;
   __syncthreads();
   float* rec = part + ((int64_t)bh * gridDim.x + blockIdx.x) * stride;
   for (int e = tid; e < G * D; e += 256) {
@@ -505,8 +509,15 @@ __global__ __launch_bounds__(256) void sparse_mfma_kernel(
       a = fmaf(s_o[x][c][hh], sc, a);
       aw += s_o[x][c][8 + hh];
     }
+    float ob = 0.f;  // this workgroup's rows of phi(q) S_bar
+    if (s_pre) {
+      for (int r = 0; r < nrows; ++r) ob = fmaf(s_phq[hh][row0 + r], s_S[r * D + c], ob);
+    } else {
+      const float* Sb = S + (int64_t)bh * D * D;
+      for (int r = row0; r < row0 + nrows; ++r) ob = fmaf(s_phq[hh][r], Sb[r * D + c], ob);
+    }
     rec[kPartHead + hh * D + c] = a;
-    rec[kPartHead + (G + hh) * D + c] = aw;
+    rec[kPartHead + (G + hh) * D + c] = ob - aw;
   }
   if (tid < G) {
     float M = -INFINITY;
@@ -518,9 +529,11 @@ __global__ __launch_bounds__(256) void sparse_mfma_kernel(
       l += s_m[x][tid] == -INFINITY ? 0.f : s_l[x][tid] * __expf(s_m[x][tid] - M);
       zw += s_l[x][8 + tid];
     }
+    float zq = 0.f;
+    for (int r = 0; r < nrows; ++r) zq = fmaf(s_phq[tid][row0 + r], s_zb[r], zq);
     rec[tid] = M;
     rec[16 + tid] = l;
-    rec[32 + tid] = zw;
+    rec[32 + tid] = zq - zw;
   }
 }
 
@@ -529,9 +542,9 @@ template <typename T, int D>
 __global__ __launch_bounds__(256) void merge_kernel(
     Dims m, float eps, uint32_t flags, const float* __restrict__ gamma,
     const int32_t* __restrict__ meta, const float* __restrict__ part, int n_rec, int stride,
-    const float* __restrict__ obar_part, const float* __restrict__ zq_part, T* __restrict__ out) {
+    T* __restrict__ out) {
   final_merge<T, D>(m, eps, flags, gamma, meta, part + (int64_t)blockIdx.y * n_rec * stride, n_rec,
-                    stride, obar_part, zq_part, out);
+                    stride, out);
 }
 
 // ------------------------------------------------------------- launchers
@@ -541,17 +554,18 @@ static void valu_td(const Dims& m, const spla_config& cfg, float s, const spla_c
                     hipStream_t st) {
   hipLaunchKernelGGL((sparse_valu_kernel<T, D>), dim3(ws.n_wg, m.bh), dim3(256), 0, st, m, s,
                      cfg.rms_eps, cfg.flags, (const T*)c.k_cache, (const T*)c.v_cache,
-                     (const T*)q, gamma, (const int32_t*)(base + ws.sel),
-                     (const int32_t*)(base + ws.meta), ws.blocks_per_wg, ws.part_stride,
-                     (float*)(base + ws.part), (const float*)(base + ws.obar_part),
-                     (const float*)(base + ws.zq_part), (T*)out);
+                     (const T*)q, gamma, (const float*)c.lin_state, (const float*)c.lin_norm,
+                     (const int32_t*)(base + ws.sel), (const int32_t*)(base + ws.meta),
+                     ws.blocks_per_wg, ws.part_stride, (float*)(base + ws.part));
 }
 
 template <int D, int BLK>
 static void mfma_db(const Dims& m, float s, const spla_cache& c, const void* q,
                     const DecodeWs& ws, char* base, hipStream_t st) {
   hipLaunchKernelGGL((sparse_mfma_kernel<D, BLK>), dim3(ws.n_wg, m.bh), dim3(256), 0, st, m, s,
-                     (const bf16_t*)c.k_cache, (const bf16_t*)c.v_cache, (const bf16_t*)q,
+                     (const bf16_t*)c.k_cache, (const bf16_t*)c.v_cache,
+                     (const uint4*)(base + ws.qprep), (const float*)c.lin_state,
+                     (const float*)c.lin_norm,
                      (const int32_t*)(base + ws.sel), (const int32_t*)(base + ws.meta),
                      ws.part_stride, (float*)(base + ws.part));
 }
@@ -569,9 +583,7 @@ static void merge_td(const Dims& m, const spla_config& cfg, const float* gamma, 
                      const DecodeWs& ws, char* base, hipStream_t st) {
   hipLaunchKernelGGL((merge_kernel<T, D>), dim3(1, m.bh), dim3(256), 0, st, m, cfg.rms_eps,
                      cfg.flags, gamma, (const int32_t*)(base + ws.meta),
-                     (const float*)(base + ws.part), ws.n_wg, ws.part_stride,
-                     (const float*)(base + ws.obar_part), (const float*)(base + ws.zq_part),
-                     (T*)out);
+                     (const float*)(base + ws.part), ws.n_wg, ws.part_stride, (T*)out);
 }
 
 hipError_t launch_sparse(const Dims& m, const spla_config& cfg, const spla_cache& c,

@@ -6,6 +6,23 @@
 
 using spla::Dims;
 
+namespace spla {
+
+int compute_units() {
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) dev = 0;
+  if (cached[dev] == 0) {
+    int v = 0;
+    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v < 1)
+      v = 256;
+    cached[dev] = v;
+  }
+  return cached[dev];
+}
+
+}  // namespace spla
+
 namespace {
 
 int32_t check_cache(const spla_cache* c) {

@@ -8,6 +8,9 @@
 
 namespace spla {
 
+// Compute units of the current device (queried once).
+int compute_units();
+
 // append.hip
 hipError_t launch_append_blocks(const Dims& m, const spla_cache& c, const void* k_new,
                                 const void* v_new, int max_new, const int32_t* n_new,
@@ -21,7 +24,7 @@ hipError_t launch_append_finish(const Dims& m, const spla_cache& c, int max_new,
                                 const int32_t* n_new, hipStream_t st);
 hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t st);
 
-// score.hip: block scoring and the o_bar partials in one launch
+// score.hip: block scoring
 hipError_t launch_score(const Dims& m, const spla_config& cfg, const spla_cache& c,
                         const void* q, const DecodeWs& ws, char* wsbase, hipStream_t st);
 

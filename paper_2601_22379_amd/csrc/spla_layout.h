@@ -68,15 +68,13 @@ SPLA_HD int64_t stats_off4(const Dims& m, int64_t bh, int64_t blk, int part, int
 }
 
 // ---- decode workspace ------------------------------------------------------
-constexpr int kLinRows = 16;      // rows of S_bar per linear-term workgroup
 constexpr int kPartHead = 48;     // per-record header: m[16], l[16], zw[16]
 constexpr int kSparseWaves = 4;   // waves per sparse workgroup
 
 struct DecodeWs {
   int64_t e_vals;     // f32 [bh][G][n_tiles*64]   exp(ell - tile max)
   int64_t tile_part;  // f64 [bh][n_tiles][G][2]   (max, sum) per 64-block tile
-  int64_t obar_part;  // f32 [bh][d/16][G][d]      phi(q) S_bar, per 16-row chunk
-  int64_t zq_part;    // f32 [bh][d/16][G]         <phi(q), z_bar>, per chunk
+  int64_t qprep;      // bf16 [bh][3][d/32][64][8] MFMA B operands: q, phi(q) hi, phi(q) lo
   int64_t sel;        // i32 [bh][k]               selected blocks, ascending
   int64_t meta;       // i32 [bh][4]               (n_selected, all_selected, length, 0)
   int64_t part;       // f32 [bh][n_wg][part_stride]  sparse workgroup partials
@@ -84,7 +82,6 @@ struct DecodeWs {
   int n_wg;           // sparse workgroups per (sequence, kv head)
   int blocks_per_wg;  // selected blocks per VALU-pass workgroup
   int part_stride;    // floats per record: header + acc[G][d] + accw[G][d]
-  int n_lin;          // linear-term workgroups per (sequence, kv head)
 };
 
 // The MFMA sparse pass handles bf16 with G <= 8; everything else uses the
@@ -104,11 +101,9 @@ SPLA_HD DecodeWs decode_ws_layout(const Dims& m) {
   w.blocks_per_wg = 1;
   w.n_wg = use_mfma_sparse(m) ? (int)ceil_div((int64_t)m.k * (m.B / 32), kSparseWaves) : m.k;
   w.part_stride = kPartHead + 2 * m.group * m.d;
-  w.n_lin = m.d / kLinRows;
   w.e_vals = take((int64_t)m.bh * m.group * m.n_tiles * kTileBlocks * 4);
   w.tile_part = take((int64_t)m.bh * m.n_tiles * m.group * 2 * 8);
-  w.obar_part = take((int64_t)m.bh * w.n_lin * m.group * m.d * 4);
-  w.zq_part = take((int64_t)m.bh * w.n_lin * m.group * 4);
+  w.qprep = take((int64_t)m.bh * 3 * m.d * 32 * 2);
   w.sel = take((int64_t)m.bh * m.k * 4);
   w.meta = take((int64_t)m.bh * 4 * 4);
   w.part = take((int64_t)m.bh * w.n_wg * w.part_stride * 4);
