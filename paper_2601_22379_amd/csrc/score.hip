@@ -6,8 +6,9 @@
 // loads are nontemporal (each byte is read once per step). For head m of the
 // group the log block mass is
 //   ell_m(i) = s q_m.mu_i + ln n_i + ln(1 + 1/2 s^2 sum_j q_mj^2 M2_ij / n_i)
-// (Eqs. 8 and 10, diagonal covariance M2/n): four coordinates at a time in
-// fp32, those partial sums accumulated in fp64 and summed over the four
+// (Eqs. 8 and 10, diagonal covariance M2/n): eight coordinates at a time in
+// fp32 (the query coefficients reach the lanes by DPP row broadcasts, not
+// LDS reads), those partial sums accumulated in fp64 and summed over the four
 // quarters with cross-lane shuffles; lane (block, quarter) then finishes
 // heads quarter, quarter+4, ... Each tile yields exp(ell - tile max) per head
 // and block and the (max, sum) of its 64 blocks per head, from which the
@@ -52,10 +53,11 @@ __device__ __forceinline__ void load_tile(const Dims& m, const float* __restrict
   }
 }
 
-// Coefficient tables of sequence x KV head bh: s q and s^2 q^2 / 2 per head,
-// [head][group of 4 coordinates][quarter][4] (the four quarters read
-// adjacent 16-byte words). load_q issues the query loads, write_table fills
-// the tables; clamped entries rewrite the last element's value.
+// Coefficient table of sequence x KV head bh: s q (table 0) and s^2 q^2 / 2
+// (table 1) per head, laid out [quarter][(table * G + head) * 32 + c] for
+// coordinate 32 quarter + c (D = 128; D = 64 uses c < 16). load_q issues the
+// query loads, write_table fills the table; clamped entries rewrite the last
+// element's value.
 template <int G, int D>
 struct QRegs {
   float x[(G * D + 255) / 256];
@@ -74,19 +76,48 @@ __device__ __forceinline__ void load_q(const Dims& m, const T* __restrict__ q, i
 }
 
 template <int G, int D>
-__device__ __forceinline__ void write_table(const QRegs<G, D>& r, double s, float4 (*sq)[D / 16][4],
-                                            float4 (*sq2)[D / 16][4]) {
+__device__ __forceinline__ void write_table(const QRegs<G, D>& r, double s, float (*sco)[2 * G * 32]) {
   constexpr int Q = D / 4;
   constexpr int QE = (G * D + 255) / 256;
 #pragma unroll
   for (int i = 0; i < QE; ++i) {
     const int e = min((int)threadIdx.x + 256 * i, G * D - 1);
     const int mm = e / D, j = e % D;
-    const int qq = j / Q, jj = j % Q;
+    const int qq = j / Q, c = j % Q;
     const double x = (double)r.x[i];
-    reinterpret_cast<float*>(&sq[mm][jj / 4][qq])[jj % 4] = (float)(s * x);
-    reinterpret_cast<float*>(&sq2[mm][jj / 4][qq])[jj % 4] = (float)(0.5 * s * s * x * x);
+    sco[qq][mm * 32 + c] = (float)(s * x);
+    sco[qq][(G + mm) * 32 + c] = (float)(0.5 * s * s * x * x);
   }
+}
+
+// acc (+)= c[lane n of this lane's 16-lane row] * x: the coefficient reaches
+// every lane of the row through a DPP row broadcast, so the products need no
+// LDS traffic. Callers keep at least two other VALU instructions between two
+// updates of one accumulator and never follow a VALU write of c directly.
+#define SPLA_BC_CASE(n, op)                                                                   \
+  case n:                                                                                     \
+    asm volatile(op " %0, %1, %2 row_newbcast:" #n " row_mask:0xf bank_mask:0xf"              \
+                 : "+v"(acc) : "v"(c), "v"(x));                                               \
+    break;
+#define SPLA_BC_SWITCH(op)                                                                    \
+  switch (n) {                                                                                \
+    SPLA_BC_CASE(0, op) SPLA_BC_CASE(1, op) SPLA_BC_CASE(2, op) SPLA_BC_CASE(3, op)            \
+    SPLA_BC_CASE(4, op) SPLA_BC_CASE(5, op) SPLA_BC_CASE(6, op) SPLA_BC_CASE(7, op)            \
+    SPLA_BC_CASE(8, op) SPLA_BC_CASE(9, op) SPLA_BC_CASE(10, op) SPLA_BC_CASE(11, op)          \
+    SPLA_BC_CASE(12, op) SPLA_BC_CASE(13, op) SPLA_BC_CASE(14, op) SPLA_BC_CASE(15, op)        \
+    default: break;                                                                           \
+  }
+__device__ __forceinline__ void mul_row_bcast(float& acc, float c, float x, int n) {
+  SPLA_BC_SWITCH("v_mul_f32_dpp")
+}
+__device__ __forceinline__ void fmac_row_bcast(float& acc, float c, float x, int n) {
+  SPLA_BC_SWITCH("v_fmac_f32_dpp")
+}
+#undef SPLA_BC_SWITCH
+#undef SPLA_BC_CASE
+
+__device__ __forceinline__ float f4_at(const float4& v, int e) {
+  return e == 0 ? v.x : (e == 1 ? v.y : (e == 2 ? v.z : v.w));
 }
 
 // Scores one tile from buf; s_part is this tile's half of the double-buffered
@@ -94,8 +125,7 @@ __device__ __forceinline__ void write_table(const QRegs<G, D>& r, double s, floa
 template <int G, int D>
 __device__ __forceinline__ void score_tile(const Dims& m, const int32_t* __restrict__ seq_lens,
                                            int first_order, int t, const TileBuf<D / 16>& buf,
-                                           const float4 (*sq)[D / 16][4],
-                                           const float4 (*sq2)[D / 16][4],
+                                           const float (*sco)[2 * G * 32],
                                            double (*s_part)[G][2], float* __restrict__ e_vals,
                                            double* __restrict__ tile_part) {
   constexpr int NJ = D / 16;
@@ -106,33 +136,43 @@ __device__ __forceinline__ void score_tile(const Dims& m, const int32_t* __restr
   const int blk = tile * kTileBlocks + kScoreGroup * w + (lane & 15);
   const int L = seq_lens[bh / m.hkv];
   const int nb = (L + m.B - 1) / m.B;
+  // this lane's coefficients: cf[k] holds entry 16 k + (lane % 16) of its
+  // quarter's table, read once per tile
+  constexpr int NK = (2 * G * 32) / 16;
+  float cf[NK];
+#pragma unroll
+  for (int k = 0; k < NK; ++k) cf[k] = sco[qt][16 * k + (lane & 15)];
   double am[G], av[G];
 #pragma unroll
   for (int mm = 0; mm < G; ++mm) am[mm] = av[mm] = 0.0;
-  // four coordinates at a time in fp32, accumulated across groups in fp64
+  // eight coordinates at a time in fp32, those partials added in fp64. The
+  // 2G partials of a step are updated round-robin, so one accumulator's
+  // updates are 2G instructions apart (plus a nop for G = 1).
+  asm volatile("s_nop 4");  // spacing after any earlier EXEC / VGPR write
 #pragma unroll
-  for (int j = 0; j < NJ; ++j) {
+  for (int jp = 0; jp < NJ / 2; ++jp) {
+    float pa[G], pb[G];
 #pragma unroll
-    for (int mm = 0; mm < G; ++mm) {
-      const float4 c = sq[mm][j][qt];
-      float pa = c.x * buf.mu[j].x;
-      pa = fmaf(c.y, buf.mu[j].y, pa);
-      pa = fmaf(c.z, buf.mu[j].z, pa);
-      pa = fmaf(c.w, buf.mu[j].w, pa);
-      am[mm] += (double)pa;
-      asm volatile("" : "+v"(am[mm]));  // add in coordinate order; keeps few partials live
+    for (int e8 = 0; e8 < 8; ++e8) {
+      const int c = 8 * jp + e8;  // coordinate within the quarter
+      const float xm = f4_at(buf.mu[2 * jp + (e8 >> 2)], e8 & 3);
+      const float xv = f4_at(buf.m2[2 * jp + (e8 >> 2)], e8 & 3);
+#pragma unroll
+      for (int mm = 0; mm < G; ++mm) {
+        if (e8 == 0) mul_row_bcast(pa[mm], cf[mm * 2 + (c >> 4)], xm, c & 15);
+        else fmac_row_bcast(pa[mm], cf[mm * 2 + (c >> 4)], xm, c & 15);
+      }
+#pragma unroll
+      for (int mm = 0; mm < G; ++mm) {
+        if (e8 == 0) mul_row_bcast(pb[mm], cf[(G + mm) * 2 + (c >> 4)], xv, c & 15);
+        else fmac_row_bcast(pb[mm], cf[(G + mm) * 2 + (c >> 4)], xv, c & 15);
+      }
+      if (G == 1) asm volatile("s_nop 0");
     }
-    // (also in first-order mode, where the term is discarded: a branch here
-    // would let the compiler sink the second-moment loads into it)
 #pragma unroll
     for (int mm = 0; mm < G; ++mm) {
-      const float4 c = sq2[mm][j][qt];
-      float pb = c.x * buf.m2[j].x;
-      pb = fmaf(c.y, buf.m2[j].y, pb);
-      pb = fmaf(c.z, buf.m2[j].z, pb);
-      pb = fmaf(c.w, buf.m2[j].w, pb);
-      av[mm] += (double)pb;
-      asm volatile("" : "+v"(av[mm]));
+      am[mm] += (double)pa[mm];
+      av[mm] += (double)pb[mm];
     }
   }
 #pragma unroll
@@ -268,8 +308,7 @@ __global__ __launch_bounds__(256) void score_kernel(
     const T* __restrict__ q, double s, int first_order, float* __restrict__ e_vals,
     double* __restrict__ tile_part, uint4* __restrict__ qprep) {
   constexpr int NJ = D / 16;  // float4 loads per lane and statistics part
-  __shared__ float4 sq[G][NJ][4];
-  __shared__ float4 sq2[G][NJ][4];
+  __shared__ float sco[4][2 * G * 32];
   __shared__ double s_part[4][G][2];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int t = blockIdx.x;  // item: sequence x KV head x tile
@@ -289,9 +328,9 @@ __global__ __launch_bounds__(256) void score_kernel(
   TileBuf<NJ> A;
   load_tile<NJ>(m, stats, t, true, first_order, kScoreGroup * w + (lane & 15), lane >> 4, A);
   __builtin_amdgcn_sched_barrier(0);
-  write_table<G, D>(qr, s, sq, sq2);
+  write_table<G, D>(qr, s, sco);
   __syncthreads();
-  score_tile<G, D>(m, seq_lens, first_order, t, A, sq, sq2, s_part, e_vals, tile_part);
+  score_tile<G, D>(m, seq_lens, first_order, t, A, sco, s_part, e_vals, tile_part);
 }
 
 template <int G, typename T, int D>
