@@ -9,8 +9,8 @@
 // (Eqs. 8 and 10, diagonal covariance M2/n): eight coordinates at a time in
 // fp32 (the query coefficients reach the lanes by DPP row broadcasts, not
 // LDS reads), those partial sums accumulated in fp64 and summed over the four
-// quarters with cross-lane shuffles; lane (block, quarter) then finishes
-// heads quarter, quarter+4, ... Each tile yields exp(ell - tile max) per head
+// quarters with a cross-lane reduce-scatter; lane (block, quarter) then
+// finishes heads quarter, quarter+4, ... Each tile yields exp(ell - tile max) per head
 // and block and the (max, sum) of its 64 blocks per head, from which the
 // selection forms each head's normaliser Z (Eq. 9) without another pass over
 // the statistics. For the matrix-core sparse pass, bh trailing workgroups
@@ -175,41 +175,48 @@ __device__ __forceinline__ void score_tile(const Dims& m, const int32_t* __restr
       av[mm] += (double)pb[mm];
     }
   }
+  // reduce-scatter over the four quarters (lanes l ^ 16, l ^ 32): lane
+  // (block, qt) ends with the sums of heads qt + 4u, u < U (zero past G)
+  double ra[U], rv[U];
+  {
+    const bool k1 = (qt & 2) != 0, k0 = (qt & 1) != 0;
 #pragma unroll
-  for (int mm = 0; mm < G; ++mm) {
-    am[mm] += __shfl_xor(am[mm], 16, kWave);
-    am[mm] += __shfl_xor(am[mm], 32, kWave);
-    av[mm] += __shfl_xor(av[mm], 16, kWave);
-    av[mm] += __shfl_xor(av[mm], 32, kWave);
+    for (int u = 0; u < U; ++u) {
+      double ta[2], tv[2];
+#pragma unroll
+      for (int r0 = 0; r0 < 2; ++r0) {
+        const int hl = 4 * u + r0, hh = hl + 2;
+        const double al = hl < G ? am[hl < G ? hl : 0] : 0.0, ah = hh < G ? am[hh < G ? hh : 0] : 0.0;
+        const double vl = hl < G ? av[hl < G ? hl : 0] : 0.0, vh = hh < G ? av[hh < G ? hh : 0] : 0.0;
+        ta[r0] = (k1 ? ah : al) + __shfl_xor(k1 ? al : ah, 32, kWave);
+        tv[r0] = (k1 ? vh : vl) + __shfl_xor(k1 ? vl : vh, 32, kWave);
+      }
+      ra[u] = (k0 ? ta[1] : ta[0]) + __shfl_xor(k0 ? ta[0] : ta[1], 16, kWave);
+      rv[u] = (k0 ? tv[1] : tv[0]) + __shfl_xor(k0 ? tv[0] : tv[1], 16, kWave);
+    }
   }
-  // every lane now holds all G sums of its block; lane (block, qt) finishes
-  // heads qt, qt+4, ...: one fp64 log1p / exp per head and lane
+  // lane (block, qt) finishes heads qt + 4u. ln n and ln(1 + x) are O(1)
+  // and taken in fp32 (absolute error ~1e-7 on ell); ell itself is fp64.
   const bool valid = blk < nb;
   const int n_i = valid ? block_count(L, m.B, blk) : 1;
-  const double ln_n = log((double)n_i);
+  const double ln_n = (double)logf((float)n_i);
   const int nbp = m.n_tiles * kTileBlocks;
   float* ev = e_vals + (int64_t)bh * G * nbp;
   double ell[U];
 #pragma unroll
   for (int u = 0; u < U; ++u) {
     const int mm = qt + 4 * u;
-    double a = 0.0, v = 0.0;
-#pragma unroll
-    for (int c = 0; c < G; ++c)
-      if (c == mm) {
-        a = am[c];
-        v = av[c];
-      }
-    double x = a + ln_n;
-    if (!first_order) x += log1p(v / n_i);
+    double x = ra[u] + ln_n;
+    if (!first_order) x += (double)log1pf((float)(rv[u] / n_i));
     ell[u] = valid ? x : -INFINITY;
-    double mx = ell[u];
-#pragma unroll
-    for (int o = 1; o < 16; o <<= 1) mx = fmax(mx, __shfl_xor(mx, o, kWave));
-    if ((lane & 15) == 0 && mm < G) s_part[w][mm][0] = mx;
+    // the tile offset is the max of the fp32-rounded ell (any common offset
+    // works; this one is exact in both precisions)
+    const float mx = row_max_to15((float)ell[u]);
+    if ((lane & 15) == 15 && mm < G) s_part[w][mm][0] = (double)mx;
   }
   __syncthreads();
-  // exp(ell - tile max): the tile's 64 blocks share one offset per head
+  // exp(ell - tile max): the tile's 64 blocks share one offset per head; the
+  // fp64 difference enters expf as a hi + lo pair
 #pragma unroll
   for (int u = 0; u < U; ++u) {
     const int mm = qt + 4 * u;
@@ -217,12 +224,14 @@ __device__ __forceinline__ void score_tile(const Dims& m, const int32_t* __restr
       double tmx = -INFINITY;
 #pragma unroll
       for (int x = 0; x < 4; ++x) tmx = fmax(tmx, s_part[x][mm][0]);
-      const double e = valid ? exp(ell[u] - tmx) : 0.0;
-      double sum = e;
-#pragma unroll
-      for (int o = 1; o < 16; o <<= 1) sum += __shfl_xor(sum, o, kWave);
-      ev[(int64_t)mm * nbp + blk] = (float)e;
-      if ((lane & 15) == 0) s_part[w][mm][1] = sum;
+      const double d = ell[u] - tmx;
+      const float dh = (float)d;
+      const float dl = (float)(d - (double)dh);
+      const float eh = expf(dh);
+      const float e = valid ? fmaf(eh, dl, eh) : 0.f;
+      ev[(int64_t)mm * nbp + blk] = e;
+      const double sum = row_sum_to15((double)e);
+      if ((lane & 15) == 15) s_part[w][mm][1] = sum;
     }
   }
   __syncthreads();

@@ -112,6 +112,28 @@ __device__ __forceinline__ double wave_max_u(double x) {
   return lane_f64(x, 63);
 }
 
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ float dpp_f32(float old, float v) {
+  return __uint_as_float(dpp_u32<CTRL, ROW_MASK>(__float_as_uint(old), __float_as_uint(v)));
+}
+
+// Max / sum over the 16 lanes of this lane's DPP row (row_shr steps); lane
+// 15 of each row ends with the result.
+__device__ __forceinline__ float row_max_to15(float x) {
+  x = fmaxf(x, dpp_f32<0x111, 0xF>(-INFINITY, x));
+  x = fmaxf(x, dpp_f32<0x112, 0xF>(-INFINITY, x));
+  x = fmaxf(x, dpp_f32<0x114, 0xF>(-INFINITY, x));
+  x = fmaxf(x, dpp_f32<0x118, 0xF>(-INFINITY, x));
+  return x;
+}
+__device__ __forceinline__ double row_sum_to15(double x) {
+  x += dpp_f64<0x111, 0xF>(0.0, x);
+  x += dpp_f64<0x112, 0xF>(0.0, x);
+  x += dpp_f64<0x114, 0xF>(0.0, x);
+  x += dpp_f64<0x118, 0xF>(0.0, x);
+  return x;
+}
+
 // Number of tokens of block i in a sequence of length L.
 __device__ __forceinline__ int block_count(int L, int B, int i) {
   int n = L - i * B;
