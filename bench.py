@@ -32,7 +32,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "SPLA decode-step latency (µs) + achieved HBM GB/s vs peak at 128K ctx"
 PEAK_HBM_GBS = 8000.0
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "score_cfg3_traffic.json")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "score_kernel_traffic.json")
 SCORE_SOURCES = ["paper_2601_22379_amd/csrc/score.hip", "paper_2601_22379_amd/csrc/spla_layout.h",
                  "paper_2601_22379_amd/csrc/spla_device.h"]
 
@@ -132,6 +132,83 @@ def _cpu_model():
     return "unknown"
 
 
+# ---------------------------------------------------------------------------
+# rocprofv3 summaries (CSV output of the passes listed in the summaries)
+
+def _kernel_short(name):
+    return name.split("(")[0].replace("void ", "")
+
+
+def trace_summary(trace_dir, workload, command, out_path):
+    """Per-kernel averages of a `rocprofv3 --kernel-trace --stats` pass."""
+    import csv
+    rows = list(csv.DictReader(open(os.path.join(trace_dir, "run_kernel_stats.csv"))))
+    lines = [f"# SPLA decode, {workload}: kernel trace", "",
+             f"command: `{command}`", "",
+             "| kernel | calls | avg us | min us | max us |", "|---|---|---|---|---|"]
+    for r in rows:
+        n = r["Name"]
+        if "spla" not in n:
+            continue
+        lines.append(f"| {_kernel_short(n)} | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
+                     f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} |")
+    with open(out_path, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
+def traffic_summary(fetch_dir, write_dir, workload, commands, out_md, out_json, score_bytes):
+    """Calibrated HBM bytes per dispatch from FETCH_SIZE / WRITE_SIZE passes.
+
+    Both counters are in KiB per dispatch. Each is scaled by what it reads for
+    the 1 GiB elementwise copy (--copy-calibration: 1 GiB read, 1 GiB written).
+    """
+    import csv
+    import collections
+
+    def per_kernel(d, counter):
+        acc = collections.defaultdict(list)
+        for r in csv.DictReader(open(os.path.join(d, "run_counter_collection.csv"))):
+            if r["Counter_Name"] == counter:
+                acc[r["Kernel_Name"]].append(float(r["Counter_Value"]))
+        return {k: sum(v) / len(v) for k, v in acc.items()}
+
+    fetch, write = per_kernel(fetch_dir, "FETCH_SIZE"), per_kernel(write_dir, "WRITE_SIZE")
+    copy = [k for k in fetch if "AUnaryFunctor" in k or "MulFunctor" in k]
+    assert copy, "no calibration copy kernel in the FETCH_SIZE pass"
+    gib_kib = float(1 << 20)
+    f_scale = gib_kib / fetch[copy[0]]
+    w_scale = gib_kib / write[copy[0]]
+    lines = [f"# SPLA decode, {workload}: HBM traffic per dispatch (rocprofv3 counters)", ""]
+    lines += [f"command: `{c}`" for c in commands]
+    lines += ["", f"calibration (1 GiB read + 1 GiB written by one elementwise kernel): "
+              f"FETCH_SIZE reads {fetch[copy[0]]:.1f} KiB -> scale {f_scale:.4f}; "
+              f"WRITE_SIZE reads {write[copy[0]]:.1f} KiB -> scale {w_scale:.4f}", "",
+              "| kernel | FETCH_SIZE KiB | WRITE_SIZE KiB | calibrated read MB | calibrated write MB |",
+              "|---|---|---|---|---|"]
+    score = None
+    for k in sorted(fetch):
+        if "spla" not in k or "append" in k:
+            continue
+        fr, wr = fetch[k] * f_scale * 1024, write.get(k, 0.0) * w_scale * 1024
+        lines.append(f"| {_kernel_short(k)} | {fetch[k]:.1f} | {write.get(k, 0.0):.1f} | "
+                     f"{fr / 1e6:.3f} | {wr / 1e6:.3f} |")
+        if "score_kernel" in k:
+            score = (fr, wr)
+    assert score is not None, "no score kernel in the counter passes"
+    lines += ["", f"score kernel: algorithmic {score_bytes / 1e6:.3f} MB per dispatch, counted "
+              f"{(score[0] + score[1]) / 1e6:.3f} MB (read {score[0] / 1e6:.3f} + write "
+              f"{score[1] / 1e6:.3f})"]
+    with open(out_md, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    with open(out_json, "w") as f:
+        json.dump({"workload": workload, "source_sha": source_hash(SCORE_SOURCES),
+                   "hbm_bytes_per_launch": int(round(score[0] + score[1])),
+                   "read_bytes": int(round(score[0])), "write_bytes": int(round(score[1])),
+                   "fetch_scale": f_scale, "write_scale": w_scale}, f, indent=1)
+    print("\n".join(lines))
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -144,7 +221,28 @@ def main():
     ap.add_argument("--no-graph", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB copy kernel (for counter scaling)")
+    ap.add_argument("--trace-summary", metavar="DIR",
+                    help="write the profiles/ summary of a kernel-trace pass in DIR and exit")
+    ap.add_argument("--traffic-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="write the profiles/ traffic summary of two counter passes and exit")
+    ap.add_argument("--command", action="append", default=[],
+                    help="profiling command quoted in a summary (repeatable)")
     args = ap.parse_args()
+    if args.trace_summary or args.traffic_summary:
+        import spla_inputs as si
+        w = si.config(args.config)
+        tag = f"decode_{w.name}"
+        if args.trace_summary:
+            trace_summary(args.trace_summary, w.name, " && ".join(args.command),
+                          os.path.join(ROOT, "profiles", f"{tag}_kernel_trace.md"))
+        if args.traffic_summary:
+            ab = si.algorithmic_bytes(w, None)
+            score_bytes = ab["stats"] + w.batch * w.n_q_heads * w.head_dim * (
+                4 if w.dtype == "f32" else 2)
+            traffic_summary(args.traffic_summary[0], args.traffic_summary[1], w.name,
+                            args.command, os.path.join(ROOT, "profiles", f"{tag}_traffic.md"),
+                            TRAFFIC_FILE, score_bytes)
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(f"bench.py: --gpus {args.gpus} (world size {world}) requested; this SPLA decode "
@@ -305,10 +403,18 @@ def main():
             tr = json.load(f)
         if tr.get("source_sha") == source_hash(SCORE_SOURCES) and tr.get("workload") == w.name:
             traffic = tr["hbm_bytes_per_launch"]
+    # the committed kernel-trace summary's average for the same kernel: the
+    # events above also span the kernel's dispatch latency (about 2 us)
+    prof_us = None
+    trace_md = os.path.join(ROOT, "profiles", f"decode_{w.name}_kernel_trace.md")
+    if os.path.exists(trace_md):
+        for ln in open(trace_md):
+            if ln.startswith("| spla::score_kernel"):
+                prof_us = float(ln.split("|")[3])
     roofline = {"kernel": "score", "bound": "hbm", "achieved": round(achieved, 1),
                 "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4),
                 "traffic": traffic, "algorithmic_bytes_per_launch": score_bytes,
-                "avg_launch_us": round(score_us, 3)}
+                "avg_launch_us": round(score_us, 3), "profiled_avg_us": prof_us}
     cpu = None
     if not args.no_cpu_baseline:
         log("timing the CPU oracle")

@@ -132,9 +132,10 @@ enum { SPLA_CACHE_NUM_BUFFERS = 6 };
 /* Kernel phases that spla_decode_ex / spla_step_ex can bracket with events. */
 enum {
   SPLA_PHASE_APPEND = 0, /* single-token append of spla_step */
-  SPLA_PHASE_SCORE = 1,  /* block statistics stream -> per-head block mass; o_bar = phi(q) S_bar */
+  SPLA_PHASE_SCORE = 1,  /* block statistics stream -> per-head block mass */
   SPLA_PHASE_SELECT = 2, /* group score, top-k */
-  SPLA_PHASE_SPARSE = 3, /* fused exact + selected-linear pass over the selected blocks */
+  SPLA_PHASE_SPARSE = 3, /* fused exact + selected-linear pass over the selected blocks,
+                            with the rows of o_bar = phi(q) S_bar split over its workgroups */
   SPLA_PHASE_MERGE = 4,  /* merge of that pass, residual, RMSNorm, output */
   SPLA_NUM_PHASES = 8
 };
