@@ -33,70 +33,93 @@ typedef float floatx4 __attribute__((ext_vector_type(4)));
 constexpr float kLog2e = 1.4426950408889634f;
 
 // ---------------------------------------------------------------- merge
-// Combines the n_rec records of a (sequence, KV head) (blockIdx.y) and
-// writes the output rows of the group's G heads.
+// Combines the n_rec records of a (sequence, KV head) and writes the output
+// rows of the group's G heads: one wavefront per head, lane l owning the E
+// adjacent coordinates E l .. E l + E - 1. The record headers of a batch of
+// 64 records are read one record per lane; every load of a batch (and the
+// gain row) is issued before any arithmetic.
+template <int E>
+__device__ __forceinline__ void load_vec(const float* p, float (&v)[E]) {
+  if constexpr (E == 2) {
+    const float2 x = *reinterpret_cast<const float2*>(p);
+    v[0] = x.x;
+    v[1] = x.y;
+  } else {
+#pragma unroll
+    for (int e = 0; e < E; ++e) v[e] = p[e];
+  }
+}
+
 template <typename T, int D>
-__device__ void final_merge(const Dims& m, float eps, uint32_t flags,
-                            const float* __restrict__ gamma, const int32_t* __restrict__ meta,
-                            const float* __restrict__ rec, int n_rec, int stride,
-                            T* __restrict__ out) {
-  constexpr int E = D / 64;       // coordinates per lane
-  constexpr int NB = 8;           // records loaded per batch
-  const int bh = blockIdx.y;
+__global__ __launch_bounds__(1024) void merge_kernel(
+    Dims m, float eps, uint32_t flags, const float* __restrict__ gamma,
+    const int32_t* __restrict__ meta, const float* __restrict__ part, int n_rec, int stride,
+    T* __restrict__ out) {
+  constexpr int E = D / 64;  // coordinates per lane
+  constexpr int NB = 16;     // record bodies per load batch
+  const int bh = blockIdx.x;
   const int b = bh / m.hkv, h = bh % m.hkv;
   const int G = m.group;
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int g = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int c0 = E * lane;
+  const float* rec = part + (int64_t)bh * n_rec * stride;
+  const int64_t orow = ((int64_t)b * m.hq + h * G + g) * D + c0;
+  const bool rla = !(flags & SPLA_FLAG_NO_RLA);
+  float gm[E];
+  load_vec<E>(gamma + (int64_t)(h * G + g) * D + c0, gm);
   const int all_sel = meta[bh * 4 + 1];
   const int L = meta[bh * 4 + 2];
-  const bool rla = !(flags & SPLA_FLAG_NO_RLA);
-  for (int g = w; g < G; g += 4) {
-    const int64_t orow = ((int64_t)b * m.hq + h * G + g) * D;
-    if (L == 0) {
+  float M = -INFINITY, l = 0.f, zt = 0.f;
+  float osp[E], ot[E];
 #pragma unroll
-      for (int e = 0; e < E; ++e) Elem<T>::store(out, orow + lane + 64 * e, 0.f);
-      continue;
-    }
-    // records in batches; every load of a batch is issued before its math,
-    // and the running max is rescaled as in an online softmax
-    float M = -INFINITY, l = 0.f, zt = 0.f;
-    float osp[E], ot[E];
-#pragma unroll
-    for (int e = 0; e < E; ++e) osp[e] = ot[e] = 0.f;
-    for (int x0 = 0; x0 < n_rec; x0 += NB) {
-      float mx[NB], lx[NB], zx[NB], a[NB][E], aw[NB][E];
+  for (int e = 0; e < E; ++e) osp[e] = ot[e] = 0.f;
+  for (int x0 = 0; x0 < n_rec; x0 += 64) {
+    // headers: lane u holds record x0 + u
+    const bool hv = x0 + lane < n_rec;
+    const float* hr = rec + (int64_t)(hv ? x0 + lane : 0) * stride;
+    const float hm = hv ? hr[g] : -INFINITY;
+    const float hl = hv ? hr[16 + g] : 0.f;
+    const float hz = hv ? hr[32 + g] : 0.f;
+    const int nb_here = n_rec - x0 < 64 ? n_rec - x0 : 64;
+    // bodies, NB at a time (the first batch is issued with the headers)
+    for (int u0 = 0; u0 < nb_here; u0 += NB) {
+      float a[NB][E], aw[NB][E];
 #pragma unroll
       for (int u = 0; u < NB; ++u) {
-        const bool ok = x0 + u < n_rec;
-        const float* r = rec + (int64_t)(ok ? x0 + u : 0) * stride;
-        mx[u] = ok ? r[g] : -INFINITY;
-        lx[u] = ok ? r[16 + g] : 0.f;
-        zx[u] = ok ? r[32 + g] : 0.f;
-#pragma unroll
-        for (int e = 0; e < E; ++e) {
-          a[u][e] = ok ? r[kPartHead + g * D + lane + 64 * e] : 0.f;
-          aw[u][e] = ok ? r[kPartHead + (G + g) * D + lane + 64 * e] : 0.f;
-        }
+        const int x = x0 + u0 + u < n_rec ? x0 + u0 + u : 0;
+        load_vec<E>(rec + (int64_t)x * stride + kPartHead + g * D + c0, a[u]);
+        load_vec<E>(rec + (int64_t)x * stride + kPartHead + (G + g) * D + c0, aw[u]);
       }
-      float bm = M;
+      if (u0 == 0) {  // fold this batch of headers into the running max
+        const float bm = fmaxf(M, wave_max(hm));
+        const float alpha = M == -INFINITY ? 0.f : __expf(M - bm);
+        l *= alpha;
 #pragma unroll
-      for (int u = 0; u < NB; ++u) bm = fmaxf(bm, mx[u]);
-      const float alpha = M == -INFINITY ? 0.f : __expf(M - bm);
-      l *= alpha;
-#pragma unroll
-      for (int e = 0; e < E; ++e) osp[e] *= alpha;
+        for (int e = 0; e < E; ++e) osp[e] *= alpha;
+        M = bm;
+        l += wave_sum(hm == -INFINITY ? 0.f : hl * __expf(hm - M));
+        zt += wave_sum(hz);
+      }
+      const float sc_l = hm == -INFINITY ? 0.f : __expf(hm - M);  // lane u: record x0 + u
 #pragma unroll
       for (int u = 0; u < NB; ++u) {
-        const float sc = mx[u] == -INFINITY ? 0.f : __expf(mx[u] - bm);
-        l = fmaf(lx[u], sc, l);
-        zt += zx[u];
+        const bool ok = u0 + u < nb_here;
+        const float sc = ok ? __shfl(sc_l, u0 + u, 64) : 0.f;
 #pragma unroll
         for (int e = 0; e < E; ++e) {
           osp[e] = fmaf(a[u][e], sc, osp[e]);
-          ot[e] += aw[u][e];
+          ot[e] += ok ? aw[u][e] : 0.f;
         }
       }
-      M = bm;
     }
+  }
+  float o[E];
+  if (L == 0) {
+#pragma unroll
+    for (int e = 0; e < E; ++e) o[e] = 0.f;
+  } else {
+    // residual r = o_bar - o_tilde (over its normaliser with RLA_NORMALIZE),
+    // exactly 0 when every token was selected; out = o_sparse + gamma r / rms(r)
     const float den = (flags & SPLA_FLAG_RLA_NORMALIZE) ? zt : 1.f;
     float rr[E];
     float ss = 0.f;
@@ -109,13 +132,10 @@ __device__ void final_merge(const Dims& m, float eps, uint32_t flags,
     ss = wave_sum(ss);
     const float inv = 1.0f / sqrtf(ss / D + eps);
 #pragma unroll
-    for (int e = 0; e < E; ++e) {
-      const int c = lane + 64 * e;
-      float o = osp[e];
-      if (rla) o = fmaf(gamma[(int64_t)(h * G + g) * D + c] * rr[e], inv, o);
-      Elem<T>::store(out, orow + c, o);
-    }
+    for (int e = 0; e < E; ++e) o[e] = rla ? fmaf(gm[e] * rr[e], inv, osp[e]) : osp[e];
   }
+#pragma unroll
+  for (int e = 0; e < E; ++e) Elem<T>::store(out, orow + e, o[e]);
 }
 
 // ------------------------------------------------ global linear term
@@ -537,16 +557,6 @@ __global__ __launch_bounds__(256) void sparse_mfma_kernel(
   }
 }
 
-// One workgroup per (sequence, KV head): merges the records of the pass.
-template <typename T, int D>
-__global__ __launch_bounds__(256) void merge_kernel(
-    Dims m, float eps, uint32_t flags, const float* __restrict__ gamma,
-    const int32_t* __restrict__ meta, const float* __restrict__ part, int n_rec, int stride,
-    T* __restrict__ out) {
-  final_merge<T, D>(m, eps, flags, gamma, meta, part + (int64_t)blockIdx.y * n_rec * stride, n_rec,
-                    stride, out);
-}
-
 // ------------------------------------------------------------- launchers
 template <typename T, int D>
 static void valu_td(const Dims& m, const spla_config& cfg, float s, const spla_cache& c,
@@ -581,7 +591,7 @@ static void mfma_d(const Dims& m, float s, const spla_cache& c, const void* q,
 template <typename T, int D>
 static void merge_td(const Dims& m, const spla_config& cfg, const float* gamma, void* out,
                      const DecodeWs& ws, char* base, hipStream_t st) {
-  hipLaunchKernelGGL((merge_kernel<T, D>), dim3(1, m.bh), dim3(256), 0, st, m, cfg.rms_eps,
+  hipLaunchKernelGGL((merge_kernel<T, D>), dim3(m.bh), dim3(64 * m.group), 0, st, m, cfg.rms_eps,
                      cfg.flags, gamma, (const int32_t*)(base + ws.meta),
                      (const float*)(base + ws.part), ws.n_wg, ws.part_stride, (T*)out);
 }
