@@ -1,293 +1,22 @@
-// Block selection, one workgroup per (sequence, KV head) (Sec. 2.1 Eq. 3 with
-// Select = TopK; Sec. 2.2 Eq. 6 group score; Sec. 4 forced blocks).
-//
-// 1. Each head's normaliser Z_m (Eq. 9) is the log-sum-exp of the 64-block
-//    tile partials of the score pass (fp64); wavefront m handles head m and
-//    leaves the tile weights exp(M_tile,m - Z_m) in LDS.
-// 2. score(i) = sum_m e_m(i) exp(M_tile(i),m - Z_m), fp64 accumulation,
-//    rounded to an fp32 key (scores are positive, so the bit patterns order
-//    like the values; +1 keeps every candidate above the excluded 0). Thread
-//    t owns the R consecutive blocks t*R .. t*R + R - 1.
-// 3. The kp-th largest key (kp = k - forced blocks) is found digit by digit
-//    (bits 30..20, 19..10, 9..0; bit 31 is clear): one LDS histogram per
-//    digit, each wavefront then reads the whole histogram and finds the digit
-//    itself, so a digit costs one barrier. The search stops as soon as the bin holding
-//    the kp-th key is taken whole.
-// 4. Keys above the threshold, the first `need` keys equal to it (ties go to
-//    the lower block id) and the forced blocks (first n_sink, last n_local)
-//    are written in ascending block order after one block-wide prefix sum.
-#include "spla_device.h"
+// Block selection kernel: one 1024-thread workgroup per (sequence, KV head);
+// the selection itself is select_blocks (spla_select.h).
 #include "spla_kernels.h"
+#include "spla_select.h"
 
 namespace spla {
 
 constexpr int kSelThreads = 1024;
-constexpr int kSelWaves = kSelThreads / 64;
-constexpr int kMaxTiles = SPLA_MAX_BLOCKS / kTileBlocks;  // tiles per sequence
-
-// Block-wide exclusive prefix sum (thread order); one barrier.
-__device__ __forceinline__ uint32_t block_excl_scan_u32(uint32_t v, uint32_t* lds, uint32_t* total) {
-  const int w = threadIdx.x >> 6;
-  const uint32_t x = wave_incl_scan_u32(v);
-  if ((threadIdx.x & 63) == 63) lds[w] = x;
-  __syncthreads();
-  uint32_t base = 0, tot = 0;
-#pragma unroll
-  for (int i = 0; i < kSelWaves; ++i) {
-    const uint32_t t = lds[i];
-    base += i < w ? t : 0u;
-    tot += t;
-  }
-  *total = tot;
-  return base + x - v;
-}
-
-// R consecutive floats from a 4R-byte aligned address (zeros when !ok).
-template <int R>
-__device__ __forceinline__ void load_run(const float* p, bool ok, float (&out)[R]) {
-  if constexpr (R == 1) {
-    out[0] = ok ? p[0] : 0.f;
-  } else if constexpr (R == 2) {
-    const float2 v = ok ? *reinterpret_cast<const float2*>(p) : make_float2(0.f, 0.f);
-    out[0] = v.x;
-    out[1] = v.y;
-  } else {
-#pragma unroll
-    for (int j = 0; j < R / 4; ++j) {
-      const float4 v = ok ? reinterpret_cast<const float4*>(p)[j] : make_float4(0.f, 0.f, 0.f, 0.f);
-      out[4 * j] = v.x;
-      out[4 * j + 1] = v.y;
-      out[4 * j + 2] = v.z;
-      out[4 * j + 3] = v.w;
-    }
-  }
-}
-
-struct RadixPick {
-  uint32_t digit;  // bin holding the need-th largest key
-  uint32_t above;  // keys in higher bins
-  uint32_t cnt;    // keys in that bin
-  uint32_t total;  // keys in the histogram
-};
-
-// Finds, from a histogram of 64 * BPL bins, the bin holding the need-th
-// largest key. Every wavefront computes the same (wave-uniform) answer: lane
-// l first sums bins BPL l .. BPL l + BPL - 1 (reading its run from a rotated
-// start so that the lanes spread over the LDS banks), then the BPL bins of the
-// lane that holds the key are spread one per lane.
-template <int BPL>
-__device__ __forceinline__ RadixPick radix_pick(const uint32_t* hist, uint32_t need) {
-  constexpr int NV = BPL / 4;
-  const int lane = threadIdx.x & 63;
-  uint32_t c = 0u;
-#pragma unroll
-  for (int j = 0; j < NV; ++j) {
-    const int jj = (j + lane) & (NV - 1);
-    const uint4 v = *reinterpret_cast<const uint4*>(hist + BPL * lane + 4 * jj);
-    c += v.x + v.y + v.z + v.w;
-  }
-  const uint32_t pre = wave_incl_scan_u32(c);
-  const uint32_t total = lane_u32(pre, 63);
-  const uint32_t above_l = total - pre;  // keys in the bins of lanes > l
-  const uint64_t here = __ballot(above_l < need && need <= above_l + c);
-  const int src = here ? __ffsll((unsigned long long)here) - 1 : 0;
-  const uint32_t above_src = lane_u32(above_l, src);
-  const uint32_t v = lane < BPL ? hist[BPL * src + lane] : 0u;
-  const uint32_t p2 = wave_incl_scan_u32(v);
-  const uint32_t a2 = above_src + lane_u32(p2, 63) - p2;  // keys in bins above this one
-  const uint64_t here2 = __ballot(lane < BPL && a2 < need && need <= a2 + v);
-  const int d = here2 ? __ffsll((unsigned long long)here2) - 1 : 0;
-  RadixPick p;
-  p.digit = (uint32_t)(BPL * src + d);
-  p.above = lane_u32(a2, d);
-  p.cnt = lane_u32(v, d);
-  p.total = total;
-  return p;
-}
 
 template <int R>
 __global__ __launch_bounds__(kSelThreads) void select_kernel(
     Dims m, const int32_t* __restrict__ seq_lens, const float* __restrict__ e_vals,
     const double* __restrict__ tile_part, int32_t* __restrict__ sel_ws,
     int32_t* __restrict__ sel_out, int32_t* __restrict__ meta) {
-  constexpr int HC = R <= 2 ? 16 / R : (R <= 8 ? 4 : 32 / R);  // heads per load batch
-  constexpr int TJ = R <= 4 ? 1 : R / 4;      // tiles per lane: n_tiles <= 16 R
-  __shared__ float sw[kMaxTiles * SPLA_MAX_GROUP];       // tile weights [tile][head]
-  __shared__ __align__(16) uint32_t hist[4096];  // digit histograms: 2048 + 1024 + 1024 bins
-  __shared__ uint32_t scan_lds[kSelWaves];
+  __shared__ SelectSmem<kSelThreads, kMaxTiles * SPLA_MAX_GROUP> sm;
   const int bh = blockIdx.x;
-  const int b = bh / m.hkv;
-  const int G = m.group, k = m.k;
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int nbp = m.n_tiles * kTileBlocks;
-  const int i0 = tid * R;
-  const int kp = k - m.n_sink - m.n_local;
-  const double* tp = tile_part + (int64_t)bh * m.n_tiles * G * 2;
-  const float* ev = e_vals + (int64_t)bh * G * nbp + i0;
-  int32_t* sel = sel_ws + (int64_t)bh * k;
-  int32_t* so = sel_out ? sel_out + (int64_t)bh * k : nullptr;
-
-  // --- loads that need no sequence length go out first
-  const int L = seq_lens[b];
-  double tm[TJ], ts[TJ];
-#pragma unroll
-  for (int j = 0; j < TJ; ++j) {
-    const int t = lane + 64 * j;
-    const bool ok = w < G && t < m.n_tiles;
-    tm[j] = ok ? tp[(t * G + w) * 2] : -INFINITY;
-    ts[j] = ok ? tp[(t * G + w) * 2 + 1] : 0.0;
-  }
-  float e[HC][R];  // nbp is a multiple of 64 >= R: a thread's run is all in or all out
-#pragma unroll
-  for (int h = 0; h < HC; ++h) load_run<R>(ev + (int64_t)h * nbp, h < G && i0 < nbp, e[h]);
-
-  const int nb = (L + m.B - 1) / m.B;
-  if (nb <= k) {  // L == 0 included: nothing or everything is selected
-    for (int x = tid; x < k; x += kSelThreads) {
-      const int v = x < nb ? x : -1;
-      sel[x] = v;
-      if (so) so[x] = v;
-    }
-    if (tid == 0) {
-      meta[bh * 4 + 0] = nb;
-      meta[bh * 4 + 1] = 1;
-      meta[bh * 4 + 2] = L;
-      meta[bh * 4 + 3] = 0;
-    }
-    return;
-  }
-  const int n_tu = (nb + kTileBlocks - 1) / kTileBlocks;
-  reinterpret_cast<uint4*>(hist)[tid] = make_uint4(0u, 0u, 0u, 0u);
-  // --- 1. Z_m and the tile weights of head m = w
-  if (kp > 0 && w < G) {
-    double mx = -INFINITY;
-#pragma unroll
-    for (int j = 0; j < TJ; ++j)
-      if (lane + 64 * j < n_tu) mx = fmax(mx, tm[j]);
-    mx = wave_max_u(mx);
-    double s = 0.0;
-#pragma unroll
-    for (int j = 0; j < TJ; ++j)
-      if (lane + 64 * j < n_tu && tm[j] > -INFINITY) s += ts[j] * exp(tm[j] - mx);
-    s = wave_sum_u(s);
-    const double Z = mx + log(s);
-#pragma unroll
-    for (int j = 0; j < TJ; ++j) {
-      const int t = lane + 64 * j;
-      if (t < n_tu) sw[t * G + w] = tm[j] > -INFINITY ? (float)exp(tm[j] - Z) : 0.f;
-    }
-  }
-  __syncthreads();
-
-  uint32_t gt = 0xFFFFFFFFu;  // keys above gt are taken
-  uint32_t eqv = 0u;          // of the keys equal to eqv, the first eq_need are taken
-  uint32_t eq_need = 0u;
-  uint32_t key[R];
-#pragma unroll
-  for (int r = 0; r < R; ++r) key[r] = 0u;
-  if (kp > 0) {
-    // --- 2. keys
-    const int t = i0 / kTileBlocks;  // R <= 64: one tile per thread
-    double sc[R];
-#pragma unroll
-    for (int r = 0; r < R; ++r) sc[r] = 0.0;
-    for (int h0 = 0; h0 < G; h0 += HC) {
-      if (h0 > 0) {
-#pragma unroll
-        for (int h = 0; h < HC; ++h)
-          load_run<R>(ev + (int64_t)(h0 + h) * nbp, h0 + h < G && i0 < nbp, e[h]);
-      }
-#pragma unroll
-      for (int h = 0; h < HC; ++h) {
-        if (h0 + h < G) {
-          const double wv = t < n_tu ? (double)sw[t * G + h0 + h] : 0.0;
-#pragma unroll
-          for (int r = 0; r < R; ++r) sc[r] = fma((double)e[h][r], wv, sc[r]);
-        }
-      }
-    }
-#pragma unroll
-    for (int r = 0; r < R; ++r) {
-      const int i = i0 + r;
-      key[r] = (i < nb && i >= m.n_sink && i < nb - m.n_local)
-                   ? __float_as_uint((float)sc[r]) + 1u : 0u;
-    }
-    // --- 3. the kp-th largest key, one digit per barrier
-    uint32_t prefix = 0u, need = (uint32_t)kp;
-#pragma unroll
-    for (int rd = 0; rd < 3; ++rd) {
-      const int sh = 20 - 10 * rd;  // digits: bits 30..20, 19..10, 9..0
-      const uint32_t msk = rd == 0 ? 0x7FFu : 0x3FFu;
-      uint32_t* H = hist + (rd == 0 ? 0 : 1024 + 1024 * rd);
-#pragma unroll
-      for (int r = 0; r < R; ++r)
-        if (key[r] != 0u && (rd == 0 || (key[r] >> (sh + 10)) == prefix))
-          atomicAdd(&H[(key[r] >> sh) & msk], 1u);
-      __syncthreads();
-      const RadixPick p = rd == 0 ? radix_pick<32>(H, need) : radix_pick<16>(H, need);
-      if (rd == 0 && p.total < need) {  // fewer candidates than kp: take all
-        gt = 0u;
-        break;
-      }
-      need -= p.above;
-      prefix = (prefix << 10) | p.digit;
-      if (need == p.cnt) {  // the bin is taken whole
-        const uint32_t lo = prefix << sh;
-        gt = lo == 0u ? 0u : lo - 1u;
-        break;
-      }
-      if (rd == 2) {  // prefix is now the kp-th key itself
-        gt = prefix;
-        eqv = prefix;
-        eq_need = need;
-      }
-    }
-  }
-
-  // --- 4. ascending output: (taken above/forced) | (ties) << 16, one scan
-  uint32_t na = 0u, ne = 0u;
-#pragma unroll
-  for (int r = 0; r < R; ++r) {
-    const int i = i0 + r;
-    const bool forced = i < nb && (i < m.n_sink || i >= nb - m.n_local);
-    const bool g = forced || (key[r] != 0u && key[r] > gt);
-    na += g ? 1u : 0u;
-    ne += (!g && eq_need > 0u && key[r] == eqv) ? 1u : 0u;
-  }
-  uint32_t tot_p;
-  const uint32_t before = block_excl_scan_u32(na | (ne << 16), scan_lds, &tot_p);
-  uint32_t a_run = before & 0xFFFFu, e_run = before >> 16;
-#pragma unroll
-  for (int r = 0; r < R; ++r) {
-    const int i = i0 + r;
-    const bool forced = i < nb && (i < m.n_sink || i >= nb - m.n_local);
-    const bool g = forced || (key[r] != 0u && key[r] > gt);
-    const bool q = !g && eq_need > 0u && key[r] == eqv;
-    int pos = -1;
-    if (g) {
-      pos = (int)(a_run + (e_run < eq_need ? e_run : eq_need));
-      ++a_run;
-    } else if (q) {
-      if (e_run < eq_need) pos = (int)(a_run + e_run);
-      ++e_run;
-    }
-    if (pos >= 0 && pos < k) {
-      sel[pos] = i;
-      if (so) so[pos] = i;
-    }
-  }
-  const uint32_t ta = tot_p & 0xFFFFu, te = tot_p >> 16;
-  const int tot = (int)(ta + (te < eq_need ? te : eq_need));
-  if (tid == 0) {
-    meta[bh * 4 + 0] = tot < k ? tot : k;
-    meta[bh * 4 + 1] = 0;
-    meta[bh * 4 + 2] = L;
-    meta[bh * 4 + 3] = tot;
-  }
-  for (int x = tot + tid; x < k; x += kSelThreads) {
-    sel[x] = -1;
-    if (so) so[x] = -1;
-  }
+  select_blocks<kSelThreads, R, kMaxTiles * SPLA_MAX_GROUP>(
+      m, bh, seq_lens, e_vals, tile_part, sm, sel_ws + (int64_t)bh * m.k, meta + bh * 4,
+      sel_out ? sel_out + (int64_t)bh * m.k : nullptr);
 }
 
 hipError_t launch_select(const Dims& m, const spla_cache& c, const DecodeWs& ws, char* base,

@@ -24,6 +24,7 @@
 // writes the same records.
 #include "spla_device.h"
 #include "spla_kernels.h"
+#include "spla_select.h"
 
 namespace spla {
 
@@ -323,16 +324,28 @@ __global__ __launch_bounds__(256) void sparse_valu_kernel(
 // <phi(q), phi(k)> of the same heads; one accumulator holds both. phi(k) and
 // the probabilities enter the products as bf16 hi + lo pairs (about 16
 // mantissa bits); accumulation is fp32.
-template <int D, int BLK>
+//
+// R > 0: the workgroup first selects the blocks of its (sequence, KV head)
+// itself (select_blocks with 256 threads, R blocks per thread; every
+// workgroup of the pair computes the same selection), so no selection kernel
+// runs; workgroup 0 publishes the selection and the meta words. R = 0: the
+// selection comes from the selection kernel.
+template <int D, int BLK, int R>
 __global__ __launch_bounds__(256) void sparse_mfma_kernel(
     Dims m, float s, const bf16_t* __restrict__ kc, const bf16_t* __restrict__ vc,
     const uint4* __restrict__ qprep, const float* __restrict__ S, const float* __restrict__ zbar,
-    const int32_t* __restrict__ sel, const int32_t* __restrict__ meta, int stride,
-    float* __restrict__ part) {
+    const int32_t* __restrict__ sel, int32_t* __restrict__ meta, int stride,
+    float* __restrict__ part, const int32_t* __restrict__ seq_lens,
+    const float* __restrict__ e_vals, const double* __restrict__ tile_part,
+    int32_t* __restrict__ sel_out) {
   constexpr int KS = D / 32;   // k-steps of the first product
   constexpr int MT = D / 16;   // coordinate tiles of the second product
   constexpr int CPB = BLK / 32;  // steps per block
   constexpr int SPRE = 8;        // S_bar entries per thread loaded up front
+  constexpr int SWN = R > 0 ? kTileBlocks * 8 : 4;  // tile weights: <= 64 tiles x 8 heads
+  __shared__ SelectSmem<256, SWN> ssm;
+  __shared__ int32_t s_sel[R > 0 ? SPLA_MAX_TOP_K : 1];
+  __shared__ int32_t s_meta[4];
   __shared__ float s_o[kSparseWaves][D][17];
   __shared__ float s_m[kSparseWaves][16], s_l[kSparseWaves][16];
   __shared__ float s_phq[8][D];          // phi(q) of the group's heads
@@ -348,10 +361,6 @@ __global__ __launch_bounds__(256) void sparse_mfma_kernel(
   const bool exact_col = j < 8;
   const int head = exact_col ? j : j - 8;
   const bool live = head < G;
-  // independent loads first: the block id (entries past the selection are
-  // -1), the sequence length and this lane's query slice
-  const int blk_sel = p < m.k ? sel[(int64_t)bh * m.k + p] : -1;
-  const int L = meta[bh * 4 + 2];
   // B operands, laid out per lane by the scoring pass: [q | 0] for the
   // logits, [0 | phi(q)_hi] and [0 | phi(q)_lo] for the linear weights
   bf16x8 qb[KS], pqh[KS], pql[KS];
@@ -378,6 +387,20 @@ __global__ __launch_bounds__(256) void sparse_mfma_kernel(
     }
   }
   const float zbv = tid < nrows ? zbar[(int64_t)bh * D + row0 + tid] : 0.f;
+  // this wavefront's block id (entries past the selection are -1) and the
+  // sequence length
+  int blk_sel, L;
+  if constexpr (R > 0) {
+    select_blocks<256, R, SWN>(m, bh, seq_lens, e_vals, tile_part, ssm, s_sel, s_meta,
+                               blockIdx.x == 0 && sel_out ? sel_out + (int64_t)bh * m.k : nullptr);
+    __syncthreads();
+    if (blockIdx.x == 0 && tid < 4) meta[bh * 4 + tid] = s_meta[tid];
+    blk_sel = p < m.k ? s_sel[p] : -1;
+    L = s_meta[2];
+  } else {
+    blk_sel = p < m.k ? sel[(int64_t)bh * m.k + p] : -1;
+    L = meta[bh * 4 + 2];
+  }
   const int nb = (L + BLK - 1) / BLK;
   int n_valid = 0;  // tokens of this step that exist
   bf16x8 ka[2][KS];
@@ -569,23 +592,50 @@ static void valu_td(const Dims& m, const spla_config& cfg, float s, const spla_c
                      ws.blocks_per_wg, ws.part_stride, (float*)(base + ws.part));
 }
 
-template <int D, int BLK>
-static void mfma_db(const Dims& m, float s, const spla_cache& c, const void* q,
-                    const DecodeWs& ws, char* base, hipStream_t st) {
-  hipLaunchKernelGGL((sparse_mfma_kernel<D, BLK>), dim3(ws.n_wg, m.bh), dim3(256), 0, st, m, s,
+// Blocks per thread of the in-workgroup selection (0: use the selection
+// kernel). Every workgroup repeats the selection of its (sequence, KV head),
+// which pays only while the grid is small (about two workgroups per compute
+// unit) and the block count is at most 4096.
+static int sparse_select_r(const Dims& m) {
+  if (!use_mfma_sparse(m) || m.nb_cap > 256 * 16) return 0;
+  const DecodeWs ws = decode_ws_layout(m);
+  if ((int64_t)ws.n_wg * m.bh > 2 * (int64_t)compute_units()) return 0;
+  const int per = (int)ceil_div(m.nb_cap, 256);
+  return per <= 2 ? 2 : (per <= 4 ? 4 : (per <= 8 ? 8 : 16));
+}
+
+bool sparse_selects(const Dims& m) { return sparse_select_r(m) > 0; }
+
+template <int D, int BLK, int R>
+static void mfma_dbr(const Dims& m, float s, const spla_cache& c, int32_t* sel_out,
+                     const DecodeWs& ws, char* base, hipStream_t st) {
+  hipLaunchKernelGGL((sparse_mfma_kernel<D, BLK, R>), dim3(ws.n_wg, m.bh), dim3(256), 0, st, m, s,
                      (const bf16_t*)c.k_cache, (const bf16_t*)c.v_cache,
                      (const uint4*)(base + ws.qprep), (const float*)c.lin_state,
-                     (const float*)c.lin_norm,
-                     (const int32_t*)(base + ws.sel), (const int32_t*)(base + ws.meta),
-                     ws.part_stride, (float*)(base + ws.part));
+                     (const float*)c.lin_norm, (const int32_t*)(base + ws.sel),
+                     (int32_t*)(base + ws.meta), ws.part_stride, (float*)(base + ws.part),
+                     c.seq_lens, (const float*)(base + ws.e_vals),
+                     (const double*)(base + ws.tile_part), sel_out);
+}
+
+template <int D, int BLK>
+static void mfma_db(const Dims& m, float s, const spla_cache& c, int32_t* sel_out,
+                    const DecodeWs& ws, char* base, hipStream_t st) {
+  switch (sparse_select_r(m)) {
+    case 2: mfma_dbr<D, BLK, 2>(m, s, c, sel_out, ws, base, st); break;
+    case 4: mfma_dbr<D, BLK, 4>(m, s, c, sel_out, ws, base, st); break;
+    case 8: mfma_dbr<D, BLK, 8>(m, s, c, sel_out, ws, base, st); break;
+    case 16: mfma_dbr<D, BLK, 16>(m, s, c, sel_out, ws, base, st); break;
+    default: mfma_dbr<D, BLK, 0>(m, s, c, sel_out, ws, base, st); break;
+  }
 }
 
 template <int D>
-static void mfma_d(const Dims& m, float s, const spla_cache& c, const void* q,
+static void mfma_d(const Dims& m, float s, const spla_cache& c, int32_t* sel_out,
                    const DecodeWs& ws, char* base, hipStream_t st) {
-  if (m.B == 32) mfma_db<D, 32>(m, s, c, q, ws, base, st);
-  else if (m.B == 64) mfma_db<D, 64>(m, s, c, q, ws, base, st);
-  else mfma_db<D, 128>(m, s, c, q, ws, base, st);
+  if (m.B == 32) mfma_db<D, 32>(m, s, c, sel_out, ws, base, st);
+  else if (m.B == 64) mfma_db<D, 64>(m, s, c, sel_out, ws, base, st);
+  else mfma_db<D, 128>(m, s, c, sel_out, ws, base, st);
 }
 
 template <typename T, int D>
@@ -597,12 +647,12 @@ static void merge_td(const Dims& m, const spla_config& cfg, const float* gamma, 
 }
 
 hipError_t launch_sparse(const Dims& m, const spla_config& cfg, const spla_cache& c,
-                         const void* q, const float* gamma, void* out, const DecodeWs& ws,
-                         char* base, hipStream_t st) {
+                         const void* q, const float* gamma, void* out, int32_t* sel_out,
+                         const DecodeWs& ws, char* base, hipStream_t st) {
   const float s = cfg.softmax_scale > 0.f ? cfg.softmax_scale : (float)(1.0 / sqrt((double)m.d));
   if (use_mfma_sparse(m)) {
-    if (m.d == 64) mfma_d<64>(m, s, c, q, ws, base, st);
-    else mfma_d<128>(m, s, c, q, ws, base, st);
+    if (m.d == 64) mfma_d<64>(m, s, c, sel_out, ws, base, st);
+    else mfma_d<128>(m, s, c, sel_out, ws, base, st);
   } else if (m.elem == 4) {
     if (m.d == 64) valu_td<float, 64>(m, cfg, s, c, q, gamma, out, ws, base, st);
     else valu_td<float, 128>(m, cfg, s, c, q, gamma, out, ws, base, st);

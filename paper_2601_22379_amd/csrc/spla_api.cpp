@@ -67,13 +67,13 @@ int32_t run_decode(const spla_config* cfg, const spla_cache* cache, const void* 
     PhaseMark pm(ev, st, SPLA_PHASE_SCORE);
     SPLA_TRY(spla::launch_score(m, *cfg, *cache, q, L, base, st));
   }
-  {
+  if (!spla::sparse_selects(m)) {
     PhaseMark pm(ev, st, SPLA_PHASE_SELECT);
     SPLA_TRY(spla::launch_select(m, *cache, L, base, sel_idx, st));
   }
   {
     PhaseMark pm(ev, st, SPLA_PHASE_SPARSE);
-    SPLA_TRY(spla::launch_sparse(m, *cfg, *cache, q, w, out, L, base, st));
+    SPLA_TRY(spla::launch_sparse(m, *cfg, *cache, q, w, out, sel_idx, L, base, st));
   }
   {
     PhaseMark pm(ev, st, SPLA_PHASE_MERGE);

@@ -32,10 +32,13 @@ hipError_t launch_score(const Dims& m, const spla_config& cfg, const spla_cache&
 hipError_t launch_select(const Dims& m, const spla_cache& c, const DecodeWs& ws, char* wsbase,
                          int32_t* sel_out, hipStream_t st);
 
-// sparse.hip: fused pass over the selected blocks (records), then the merge
+// sparse.hip: fused pass over the selected blocks (records), then the merge.
+// When sparse_selects(m), the sparse pass makes the selection itself (and
+// writes sel_out) and launch_select must not be called.
+bool sparse_selects(const Dims& m);
 hipError_t launch_sparse(const Dims& m, const spla_config& cfg, const spla_cache& c,
-                         const void* q, const float* rms_weight, void* out, const DecodeWs& ws,
-                         char* wsbase, hipStream_t st);
+                         const void* q, const float* rms_weight, void* out, int32_t* sel_out,
+                         const DecodeWs& ws, char* wsbase, hipStream_t st);
 hipError_t launch_merge(const Dims& m, const spla_config& cfg, const float* rms_weight, void* out,
                         const DecodeWs& ws, char* wsbase, hipStream_t st);
 
