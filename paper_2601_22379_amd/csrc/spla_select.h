@@ -189,16 +189,25 @@ __device__ void select_blocks(const Dims& m, int bh, const int32_t* __restrict__
     for (int j = 0; j < TJ; ++j)
       if (lane + 64 * j < n_tu) mx = fmax(mx, tm[j]);
     mx = wave_max_u(mx);
+    // the tile terms exp(M - max) <= 1 are taken in fp32 (the dominant terms
+    // have small arguments, so the sum is good to about 1e-7); the sum and
+    // its log stay fp64
     double s = 0.0;
 #pragma unroll
     for (int j = 0; j < TJ; ++j)
-      if (lane + 64 * j < n_tu && tm[j] > -INFINITY) s += ts[j] * exp(tm[j] - mx);
+      if (lane + 64 * j < n_tu && tm[j] > -INFINITY)
+        s += ts[j] * (double)expf((float)(tm[j] - mx));
     s = wave_sum_u(s);
     const double Z = mx + log(s);
 #pragma unroll
     for (int j = 0; j < TJ; ++j) {
       const int t = lane + 64 * j;
-      if (t < n_tu) sw[t * G + mm] = tm[j] > -INFINITY ? (float)exp(tm[j] - Z) : 0.f;
+      if (t < n_tu) {  // exp(M - Z) in fp32 from an fp64 hi + lo argument
+        const double d = tm[j] - Z;
+        const float dh = (float)d, dl = (float)(d - (double)dh);
+        const float eh = expf(dh);
+        sw[t * G + mm] = tm[j] > -INFINITY ? fmaf(eh, dl, eh) : 0.f;
+      }
     }
   }
   __syncthreads();
