@@ -188,11 +188,11 @@ __device__ __forceinline__ void score_tile(const Dims& m, const int32_t* __restr
         const int hl = 4 * u + r0, hh = hl + 2;
         const double al = hl < G ? am[hl < G ? hl : 0] : 0.0, ah = hh < G ? am[hh < G ? hh : 0] : 0.0;
         const double vl = hl < G ? av[hl < G ? hl : 0] : 0.0, vh = hh < G ? av[hh < G ? hh : 0] : 0.0;
-        ta[r0] = (k1 ? ah : al) + __shfl_xor(k1 ? al : ah, 32, kWave);
-        tv[r0] = (k1 ? vh : vl) + __shfl_xor(k1 ? vl : vh, 32, kWave);
+        ta[r0] = (k1 ? ah : al) + xor32(k1 ? al : ah);
+        tv[r0] = (k1 ? vh : vl) + xor32(k1 ? vl : vh);
       }
-      ra[u] = (k0 ? ta[1] : ta[0]) + __shfl_xor(k0 ? ta[0] : ta[1], 16, kWave);
-      rv[u] = (k0 ? tv[1] : tv[0]) + __shfl_xor(k0 ? tv[0] : tv[1], 16, kWave);
+      ra[u] = (k0 ? ta[1] : ta[0]) + xor16(k0 ? ta[0] : ta[1]);
+      rv[u] = (k0 ? tv[1] : tv[0]) + xor16(k0 ? tv[0] : tv[1]);
     }
   }
   // lane (block, qt) finishes heads qt + 4u. ln n and ln(1 + x) are O(1)

@@ -455,8 +455,8 @@ __global__ __launch_bounds__(256) void sparse_mfma_kernel(
           kx[ks][e] = (float)ka[mt][ks][e];
           mx = fmaxf(mx, kx[ks][e]);
         }
-      mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
-      mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+      mx = fmaxf(mx, xor16(mx));
+      mx = fmaxf(mx, xor32(mx));
       const float mxl = mx * kLog2e;
       float sum = 0.f;
 #pragma unroll
@@ -466,8 +466,8 @@ __global__ __launch_bounds__(256) void sparse_mfma_kernel(
           kx[ks][e] = __builtin_amdgcn_exp2f(fmaf(kx[ks][e], kLog2e, -mxl));
           sum += kx[ks][e];
         }
-      sum += __shfl_xor(sum, 16, kWave);
-      sum += __shfl_xor(sum, 32, kWave);
+      sum += xor16(sum);
+      sum += xor32(sum);
       zinv[mt] = 1.0f / sum;
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
@@ -497,8 +497,8 @@ __global__ __launch_bounds__(256) void sparse_mfma_kernel(
       val[e] = exact_col ? (ok ? x * s : -INFINITY) : (ok ? x * zi : 0.f);
       cmax = fmaxf(cmax, val[e]);
     }
-    cmax = fmaxf(cmax, __shfl_xor(cmax, 16, kWave));
-    cmax = fmaxf(cmax, __shfl_xor(cmax, 32, kWave));
+    cmax = fmaxf(cmax, xor16(cmax));
+    cmax = fmaxf(cmax, xor32(cmax));
     float psum = 0.f;
     bf16x8 bh8, bl8;
 #pragma unroll
@@ -509,8 +509,8 @@ __global__ __launch_bounds__(256) void sparse_mfma_kernel(
       bh8[e] = hi;
       bl8[e] = (__bf16)(pv - (float)hi);
     }
-    psum += __shfl_xor(psum, 16, kWave);
-    psum += __shfl_xor(psum, 32, kWave);
+    psum += xor16(psum);
+    psum += xor32(psum);
     m_run = exact_col ? cmax : -INFINITY;
     l_run = psum;
     if (n_valid < 32) {  // rows past the sequence end may hold anything: zero them

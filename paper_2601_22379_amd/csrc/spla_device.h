@@ -41,20 +41,54 @@ template <> struct Elem<bf16_t> {
   }
 };
 
-template <typename T>
-__device__ __forceinline__ T wave_sum(T v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
-  return v;
+// ---- lane exchanges without LDS: lane l receives lane l ^ 32 / l ^ 16 (the
+// gfx950 permlane swaps; 1-D workgroups, so lane = threadIdx.x % 64).
+__device__ __forceinline__ uint32_t lane_xor32(uint32_t x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+  return (threadIdx.x & 32) ? r[0] : r[1];
+}
+__device__ __forceinline__ uint32_t lane_xor16(uint32_t x) {
+  const auto r = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+  return (threadIdx.x & 16) ? r[0] : r[1];
+}
+__device__ __forceinline__ float xor32(float x) { return __uint_as_float(lane_xor32(__float_as_uint(x))); }
+__device__ __forceinline__ float xor16(float x) { return __uint_as_float(lane_xor16(__float_as_uint(x))); }
+__device__ __forceinline__ double xor32(double x) {
+  const uint64_t u = __double_as_longlong(x);
+  const uint64_t lo = lane_xor32((uint32_t)u), hi = lane_xor32((uint32_t)(u >> 32));
+  return __longlong_as_double((long long)((hi << 32) | lo));
+}
+__device__ __forceinline__ double xor16(double x) {
+  const uint64_t u = __double_as_longlong(x);
+  const uint64_t lo = lane_xor16((uint32_t)u), hi = lane_xor16((uint32_t)(u >> 32));
+  return __longlong_as_double((long long)((hi << 32) | lo));
 }
 
-template <typename T>
-__device__ __forceinline__ T wave_max(T v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    T u = __shfl_xor(v, o, kWave);
-    v = u > v ? u : v;
-  }
+// Rotations inside 16-lane rows and quad permutes (DPP).
+template <int CTRL>
+__device__ __forceinline__ float dpp_rot(float x) {
+  return __uint_as_float((uint32_t)__builtin_amdgcn_update_dpp(0, (int)__float_as_uint(x), CTRL,
+                                                               0xF, 0xF, false));
+}
+
+// Sum / max over the wavefront; every lane gets the same bits (each step
+// combines a value with its partner's, and + / max commute).
+__device__ __forceinline__ float wave_sum(float v) {
+  v += xor32(v);
+  v += xor16(v);
+  v += dpp_rot<0x128>(v);  // row_ror:8
+  v += dpp_rot<0x124>(v);  // row_ror:4
+  v += dpp_rot<0x4E>(v);   // quad_perm [2,3,0,1]
+  v += dpp_rot<0xB1>(v);   // quad_perm [1,0,3,2]
+  return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+  v = fmaxf(v, xor32(v));
+  v = fmaxf(v, xor16(v));
+  v = fmaxf(v, dpp_rot<0x128>(v));
+  v = fmaxf(v, dpp_rot<0x124>(v));
+  v = fmaxf(v, dpp_rot<0x4E>(v));
+  v = fmaxf(v, dpp_rot<0xB1>(v));
   return v;
 }
 
