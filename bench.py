@@ -32,9 +32,23 @@ sys.path.insert(0, ROOT)
 
 METRIC = "SPLA decode-step latency (µs) + achieved HBM GB/s vs peak at 128K ctx"
 PEAK_HBM_GBS = 8000.0
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "score_kernel_traffic.json")
-SCORE_SOURCES = ["paper_2601_22379_amd/csrc/score.hip", "paper_2601_22379_amd/csrc/spla_layout.h",
-                 "paper_2601_22379_amd/csrc/spla_device.h"]
+KERNEL_SOURCES = sorted("paper_2601_22379_amd/csrc/" + f
+                        for f in os.listdir(os.path.join(ROOT, "paper_2601_22379_amd", "csrc"))
+                        if f.endswith((".hip", ".h")))
+
+
+def traffic_file(kernel):
+    return os.path.join(ROOT, "profiles", f"{kernel}_kernel_traffic.json")
+
+
+def dominant_bytes(w, ab, kernel):
+    """Algorithmic bytes one launch of the dominant kernel moves: the whole
+    decode (everything but the append) for the single-launch kernel, the
+    statistics plus the queries for the scoring kernel."""
+    if kernel == "decode":
+        return ab["total"] - ab["append"]
+    return ab["stats"] + w.batch * w.n_q_heads * w.head_dim * (4 if w.dtype == "f32" else 2)
+
 
 
 def log(msg):
@@ -157,11 +171,13 @@ def trace_summary(trace_dir, workload, command, out_path):
     print("\n".join(lines))
 
 
-def traffic_summary(fetch_dir, write_dir, workload, commands, out_md, out_json, score_bytes):
+def traffic_summary(fetch_dir, write_dir, workload, commands, out_md, kernel, kernel_bytes):
     """Calibrated HBM bytes per dispatch from FETCH_SIZE / WRITE_SIZE passes.
 
     Both counters are in KiB per dispatch. Each is scaled by what it reads for
     the 1 GiB elementwise copy (--copy-calibration: 1 GiB read, 1 GiB written).
+    The figures of `kernel` (the dominant kernel) also go to its JSON file,
+    which bench.py reports while the kernel sources are unchanged.
     """
     import csv
     import collections
@@ -186,25 +202,26 @@ def traffic_summary(fetch_dir, write_dir, workload, commands, out_md, out_json, 
               f"WRITE_SIZE reads {write[copy[0]]:.1f} KiB -> scale {w_scale:.4f}", "",
               "| kernel | FETCH_SIZE KiB | WRITE_SIZE KiB | calibrated read MB | calibrated write MB |",
               "|---|---|---|---|---|"]
-    score = None
+    dom = None
     for k in sorted(fetch):
         if "spla" not in k or "append" in k:
             continue
         fr, wr = fetch[k] * f_scale * 1024, write.get(k, 0.0) * w_scale * 1024
         lines.append(f"| {_kernel_short(k)} | {fetch[k]:.1f} | {write.get(k, 0.0):.1f} | "
                      f"{fr / 1e6:.3f} | {wr / 1e6:.3f} |")
-        if "score_kernel" in k:
-            score = (fr, wr)
-    assert score is not None, "no score kernel in the counter passes"
-    lines += ["", f"score kernel: algorithmic {score_bytes / 1e6:.3f} MB per dispatch, counted "
-              f"{(score[0] + score[1]) / 1e6:.3f} MB (read {score[0] / 1e6:.3f} + write "
-              f"{score[1] / 1e6:.3f})"]
+        if f"{kernel}_kernel" in k:
+            dom = (fr, wr)
+    assert dom is not None, f"no {kernel} kernel in the counter passes"
+    lines += ["", f"{kernel} kernel: algorithmic {kernel_bytes / 1e6:.3f} MB per dispatch, counted "
+              f"{(dom[0] + dom[1]) / 1e6:.3f} MB (read {dom[0] / 1e6:.3f} + write "
+              f"{dom[1] / 1e6:.3f})"]
     with open(out_md, "w") as f:
         f.write("\n".join(lines) + "\n")
-    with open(out_json, "w") as f:
-        json.dump({"workload": workload, "source_sha": source_hash(SCORE_SOURCES),
-                   "hbm_bytes_per_launch": int(round(score[0] + score[1])),
-                   "read_bytes": int(round(score[0])), "write_bytes": int(round(score[1])),
+    with open(traffic_file(kernel), "w") as f:
+        json.dump({"workload": workload, "kernel": kernel,
+                   "source_sha": source_hash(KERNEL_SOURCES),
+                   "hbm_bytes_per_launch": int(round(dom[0] + dom[1])),
+                   "read_bytes": int(round(dom[0])), "write_bytes": int(round(dom[1])),
                    "fetch_scale": f_scale, "write_scale": w_scale}, f, indent=1)
     print("\n".join(lines))
 
@@ -225,6 +242,8 @@ def main():
                     help="write the profiles/ summary of a kernel-trace pass in DIR and exit")
     ap.add_argument("--traffic-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="write the profiles/ traffic summary of two counter passes and exit")
+    ap.add_argument("--kernel", default="decode", choices=["decode", "score"],
+                    help="dominant kernel of a --traffic-summary")
     ap.add_argument("--command", action="append", default=[],
                     help="profiling command quoted in a summary (repeatable)")
     args = ap.parse_args()
@@ -237,11 +256,9 @@ def main():
                           os.path.join(ROOT, "profiles", f"{tag}_kernel_trace.md"))
         if args.traffic_summary:
             ab = si.algorithmic_bytes(w, None)
-            score_bytes = ab["stats"] + w.batch * w.n_q_heads * w.head_dim * (
-                4 if w.dtype == "f32" else 2)
             traffic_summary(args.traffic_summary[0], args.traffic_summary[1], w.name,
                             args.command, os.path.join(ROOT, "profiles", f"{tag}_traffic.md"),
-                            TRAFFIC_FILE, score_bytes)
+                            args.kernel, dominant_bytes(w, ab, args.kernel))
         return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -295,7 +312,10 @@ def main():
             return caches[r].step(kn_d[s], vn_d[s], q, gamma, outs[r], sels[r], events)
         return caches[r].decode(q, gamma, outs[r], sels[r], events)
 
-    phase_names = ["append", "score", "select", "sparse", "merge"]
+    # the dominant kernel: the single-launch decode kernel where the shape has
+    # one, else the statistics scan of the separate-kernel path
+    launched = spla.decode_phases(cfg)
+    dom = "decode" if launched == ["decode"] else "score"
     for s in range(W):
         one(s)
     torch.cuda.synchronize()
@@ -313,32 +333,50 @@ def main():
     wall = time.perf_counter() - wall0
     ms_per_step = t_a.elapsed_time(t_b) / K
 
-    # the same K steps with HIP events around the dominant kernel only (the
-    # statistics scan), recorded by the library on the stream it launches on
-    ev = [spla.make_events(["score"]) for _ in range(K)]
+    # the same K steps with HIP events around the dominant kernel only,
+    # recorded by the library on the stream it launches on
+    ev = [spla.make_events([dom]) for _ in range(K)]
     torch.cuda.synchronize()
     t_a.record()
     for s in range(K):
         one(W + K + s, ev[s][0])
     t_b.record()
     torch.cuda.synchronize()
-    ms_per_step_score_events = t_a.elapsed_time(t_b) / K
-    score_us = float(np.mean([e[1]["score"][0].elapsed_time(e[1]["score"][1]) for e in ev])) * 1e3
+    ms_per_step_dom_events = t_a.elapsed_time(t_b) / K
+    dom_us = float(np.mean([e[1][dom][0].elapsed_time(e[1][dom][1]) for e in ev])) * 1e3
 
-    # per-phase breakdown (every phase bracketed; the extra event records
-    # lengthen the step, so this loop only apportions time between kernels)
-    evp = [spla.make_events(phase_names) for _ in range(K)]
-    torch.cuda.synchronize()
-    for s in range(K):
-        one(W + 2 * K + s, evp[s][0])
-    torch.cuda.synchronize()
+    # per-phase breakdown of the separate-kernel path (every phase bracketed;
+    # the extra event records lengthen the step, so this loop only apportions
+    # time between kernels), and that path's plain step latency
+    sep_names = ["score", "select", "sparse", "merge"] + (["append"] if appending else [])
+    for c in caches:
+        c.cfg.flags |= spla.FLAG_SEPARATE_KERNELS
+    sep_launched = set(spla.decode_phases(caches[0].cfg)) | {"append"}
+    try:
+        for s in range(W):
+            one(s)
+        torch.cuda.synchronize()
+        t_a.record()
+        for s in range(K):
+            one(W + s)
+        t_b.record()
+        torch.cuda.synchronize()
+        sep_ms = t_a.elapsed_time(t_b) / K
+        evp = [spla.make_events(sep_names) for _ in range(K)]
+        torch.cuda.synchronize()
+        for s in range(K):
+            one(W + 2 * K + s, evp[s][0])
+        torch.cuda.synchronize()
+    finally:
+        for c in caches:
+            c.cfg.flags &= ~spla.FLAG_SEPARATE_KERNELS
     phases = {}
-    for name in phase_names:
-        if appending or name != "append":
+    for name in sep_names:
+        if name in sep_launched:
             phases[name] = float(np.mean([e[1][name][0].elapsed_time(e[1][name][1])
                                           for e in evp])) * 1e3
     log(f"timed {K} steps: {ms_per_step * 1e3:.2f} us/step (wall {wall / K * 1e6:.2f} us/step); "
-        f"score kernel {score_us:.2f} us; phases us: "
+        f"{dom} kernel {dom_us:.2f} us; separate kernels {sep_ms * 1e3:.2f} us/step, phases us: "
         + ", ".join(f"{k}={v:.2f}" for k, v in phases.items()))
 
     graph_us = None
@@ -395,26 +433,27 @@ def main():
     ab = si.algorithmic_bytes(w, sel_counts)
     total = ab["total"]
     value = total / (ms_per_step * 1e-3) / 1e9
-    score_bytes = ab["stats"] + w.batch * w.n_q_heads * w.head_dim * (4 if w.dtype == "f32" else 2)
-    achieved = score_bytes / (score_us * 1e-6) / 1e9
+    dom_bytes = dominant_bytes(w, ab, dom)
+    achieved = dom_bytes / (dom_us * 1e-6) / 1e9
     traffic = None
-    if os.path.exists(TRAFFIC_FILE):
-        with open(TRAFFIC_FILE) as f:
+    tfile = traffic_file(dom)
+    if os.path.exists(tfile):
+        with open(tfile) as f:
             tr = json.load(f)
-        if tr.get("source_sha") == source_hash(SCORE_SOURCES) and tr.get("workload") == w.name:
+        if tr.get("source_sha") == source_hash(KERNEL_SOURCES) and tr.get("workload") == w.name:
             traffic = tr["hbm_bytes_per_launch"]
     # the committed kernel-trace summary's average for the same kernel: the
-    # events above also span the kernel's dispatch latency (about 2 us)
+    # events above also span the kernel's dispatch latency
     prof_us = None
     trace_md = os.path.join(ROOT, "profiles", f"decode_{w.name}_kernel_trace.md")
     if os.path.exists(trace_md):
         for ln in open(trace_md):
-            if ln.startswith("| spla::score_kernel"):
+            if ln.startswith(f"| spla::{dom}_kernel"):
                 prof_us = float(ln.split("|")[3])
-    roofline = {"kernel": "score", "bound": "hbm", "achieved": round(achieved, 1),
+    roofline = {"kernel": dom, "bound": "hbm", "achieved": round(achieved, 1),
                 "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4),
-                "traffic": traffic, "algorithmic_bytes_per_launch": score_bytes,
-                "avg_launch_us": round(score_us, 3), "profiled_avg_us": prof_us}
+                "traffic": traffic, "algorithmic_bytes_per_launch": dom_bytes,
+                "avg_launch_us": round(dom_us, 3), "profiled_avg_us": prof_us}
     cpu = None
     if not args.no_cpu_baseline:
         log("timing the CPU oracle")
@@ -438,11 +477,12 @@ def main():
                    "top_k": w.top_k, "n_sink": w.n_sink, "n_local": w.n_local,
                    "cache_replicas": R, "appends_per_step": w.appends_per_step},
         "latency_us": round(ms_per_step * 1e3, 3),
-        "latency_us_with_score_events": round(ms_per_step_score_events * 1e3, 3),
+        "latency_us_with_kernel_events": round(ms_per_step_dom_events * 1e3, 3),
+        "latency_us_separate_kernels": round(sep_ms * 1e3, 3),
         "latency_us_hip_graph": None if graph_us is None else round(graph_us, 3),
         "frac_of_peak_hbm": round(value / PEAK_HBM_GBS, 4),
         "algorithmic_bytes": ab,
-        "phases_us": {k: round(v, 3) for k, v in phases.items()},
+        "phases_us_separate_kernels": {k: round(v, 3) for k, v in phases.items()},
         "roofline": roofline,
         "cpu_baseline": cpu,
     }

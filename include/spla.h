@@ -61,11 +61,20 @@ typedef enum spla_dtype { SPLA_F32 = 0, SPLA_BF16 = 1 } spla_dtype;
 enum {
   SPLA_FLAG_NO_RLA = 1u,        /* SPA: output = exact sparse branch only */
   SPLA_FLAG_FIRST_ORDER = 2u,   /* block score with Eq. 11 (mean only) instead of Eq. 10 */
-  SPLA_FLAG_RLA_NORMALIZE = 4u  /* divide the residual by <phi(q), z_bar - z_selected> */
+  SPLA_FLAG_RLA_NORMALIZE = 4u, /* divide the residual by <phi(q), z_bar - z_selected> */
+  SPLA_FLAG_SEPARATE_KERNELS = 8u /* run the decode as separate score / select / sparse /
+                                     merge launches instead of the single-launch kernel
+                                     (same arithmetic, bit-identical results; for
+                                     per-phase timing) */
 };
 
 /* err_flags bits written by the device */
-enum { SPLA_DEVERR_CAPACITY = 1 };
+enum {
+  SPLA_DEVERR_CAPACITY = 1, /* an append was clipped at max_seq_len */
+  SPLA_DEVERR_SYNC = 2      /* the single-launch decode found its workspace counters not
+                               zero at launch, or gave up a bounded wait: the output of
+                               that call is undefined; spla_workspace_init repairs it */
+};
 
 /* Library limits of this build. */
 enum {
@@ -137,12 +146,14 @@ enum {
   SPLA_PHASE_SPARSE = 3, /* fused exact + selected-linear pass over the selected blocks,
                             with the rows of o_bar = phi(q) S_bar split over its workgroups */
   SPLA_PHASE_MERGE = 4,  /* merge of that pass, residual, RMSNorm, output */
+  SPLA_PHASE_DECODE = 5, /* the single-launch decode kernel (all of phases 1-4) */
   SPLA_NUM_PHASES = 8
 };
 
 /* Optional timing hooks: each non-NULL start[p] / stop[p] (a hipEvent_t) is
  * recorded on the call's stream right before / after the launch(es) of phase
- * p. A phase the library does not launch separately records nothing. */
+ * p. The phases a call records are given by spla_decode_phase_mask (plus
+ * SPLA_PHASE_APPEND for spla_step_ex); the others record nothing. */
 typedef struct spla_events {
   void* start[SPLA_NUM_PHASES];
   void* stop[SPLA_NUM_PHASES];
@@ -163,14 +174,33 @@ int32_t spla_validate(const spla_config* cfg);
  * in the order listed at spla_cache. Host only. */
 int32_t spla_cache_bytes(const spla_config* cfg, size_t* out_bytes);
 
-/* Device workspace that spla_decode / spla_step need (host-only query). */
+/* Device workspace that spla_decode / spla_step need (host-only query). The
+ * workspace holds scratch (block masses, the selection, per-workgroup
+ * records) and, in its last words, the counters of the single-launch decode,
+ * which must be zero when a call starts: zero the workspace once with
+ * spla_workspace_init (or any zero fill) before its first use; every call
+ * leaves the counters zero again. */
 int32_t spla_workspace_bytes(const spla_config* cfg, size_t* out_bytes);
+
+/* The phases whose events spla_decode_ex records for cfg, as bits
+ * 1 << SPLA_PHASE_*: (1 << SPLA_PHASE_DECODE) when the decode runs as one
+ * launch, otherwise the separate score, select, sparse and merge phases (the
+ * select phase is folded into the sparse launch on grids of at most two
+ * workgroups per compute unit; its two events are then recorded back to
+ * back). Host only. */
+int32_t spla_decode_phase_mask(const spla_config* cfg, uint32_t* out_mask);
 
 /* Device workspace that spla_append needs for up to max_new tokens per
  * sequence (host-only query). */
 int32_t spla_append_workspace_bytes(const spla_config* cfg, int32_t max_new, size_t* out_bytes);
 
 /* ---------------------------------------------------------- device calls */
+
+/* Zero-fills a decode workspace of workspace_bytes bytes (at least
+ * spla_workspace_bytes(cfg), 256-byte aligned) with a fill kernel on
+ * `stream`. Needed once per workspace before its first decode. */
+int32_t spla_workspace_init(const spla_config* cfg, void* workspace, size_t workspace_bytes,
+                            void* stream);
 
 /* Empties the cache: zero-fills blk_stats, lin_state, lin_norm and seq_lens
  * (K/V rows are left as they are; they are never read past seq_lens). */
@@ -203,7 +233,11 @@ int32_t spla_append(const spla_config* cfg, const spla_cache* cache,
  *  sel_idx:    device int32 [batch][Hkv][top_k] or NULL: the selected block
  *              ids of each KV head in ascending order, padded with -1 when a
  *              sequence has fewer than top_k blocks.
- *  workspace:  device, at least spla_workspace_bytes(cfg), 256-byte aligned.
+ *  workspace:  device, at least spla_workspace_bytes(cfg), 256-byte aligned,
+ *              prepared once by spla_workspace_init.
+ * Bf16 shapes with d = 128, G <= 8 and at most 8192 blocks per sequence run
+ * as one kernel launch (unless SPLA_FLAG_SEPARATE_KERNELS); the others as
+ * separate score, select, sparse and merge launches.
  * For each sequence with L = seq_lens[b] tokens, nb = ceil(L / B) blocks:
  * if nb <= top_k every block is selected and the output is exact attention;
  * otherwise the sink and local blocks plus the top-scored remaining blocks

@@ -1,0 +1,230 @@
+// Single-launch decode step: block scoring, selection, the fused pass over
+// the selected blocks and the merge of every (sequence, KV head) in one
+// kernel, so that selections and the reads of the selected keys and values of
+// the heads scored first overlap the statistics stream of the others.
+//
+// One workgroup per item, in workgroup-index order:
+//   score items   kTilesPerItem 64-block statistics tiles of one (sequence,
+//                 KV head) (score_items), in (sequence, KV head) order. The
+//                 workgroup that finishes a head's last item runs the head's
+//                 selection (select_blocks), which publishes every selected
+//                 block as its own word (block + 2, never 0).
+//   sparse items  one per share x of the fused pass (sparse_body) of each
+//                 (sequence, KV head), in the same order: each wavefront polls
+//                 the word of the block it reads, and the workgroup clears
+//                 those words once read. The workgroup that writes a head's
+//                 last record merges the head's records into its output rows.
+// Only sparse items wait (for their head's selection), and only for score
+// items, which have smaller indices and never wait; workgroups start in index
+// order on each XCD, so every score item starts, and every wait ends. Waits
+// are bounded all the same (kSpinLimit polls); a wait that gives up sets
+// SPLA_DEVERR_SYNC.
+//
+// Data published by one workgroup and read by another (e_vals, tile_part,
+// the selection words, the records) is written and read with
+// device-coherent accesses (Mem<true>: agent-scope atomic loads and stores,
+// which bypass the per-XCD L2 caches); the producer waits for its stores to
+// complete before the word that announces them is updated. No cache-wide
+// writeback or invalidation (agent-scope fences) is used: on this GPU they
+// act on a whole L2 and cost far more than the kilobytes moved. The counters
+// and words are agent-scope atomics, each alone in a 128-byte line
+// (sync_layout). Each call leaves them all at zero: a head's selecting
+// workgroup resets its item counter, its sparse workgroups their selection
+// words, and its merging workgroup its record counter.
+#include "spla_kernels.h"
+#include "spla_score.h"
+#include "spla_select.h"
+#include "spla_sparse.h"
+
+namespace spla {
+
+constexpr int kSpinLimit = 1 << 20;  // polls of a wait (about a second)
+#ifndef SPLA_TILES_PER_ITEM
+#define SPLA_TILES_PER_ITEM 1
+#endif
+constexpr int kTilesPerItem = SPLA_TILES_PER_ITEM;  // statistics tiles per score item
+
+struct FusedArgs {
+  Dims m;
+  const float* stats;
+  const int32_t* seq_lens;
+  const bf16_t* q;
+  const bf16_t* kc;
+  const bf16_t* vc;
+  const float* S;
+  const float* zbar;
+  const float* gamma;
+  bf16_t* out;
+  int32_t* sel_out;    // caller's selection output or NULL
+  int32_t* err_flags;  // caller's error word or NULL
+  float* e_vals;
+  double* tile_part;
+  int32_t* sel;
+  int32_t* meta;
+  float* part;
+  int32_t* sync;
+  SyncLayout y;
+  double s_score;
+  float s;
+  float eps;
+  uint32_t flags;
+  int first_order;
+  int n_si;     // score items per (sequence, KV head)
+  int n_wg;     // sparse items per (sequence, KV head)
+  int stride;   // floats per record
+};
+
+__device__ __forceinline__ int atomic_add_agent(int32_t* p, int v) {
+  return __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ int load_agent(const int32_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void store_agent(int32_t* p, int v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ void report_sync_error(const FusedArgs& a) {
+  atomic_add_agent(a.sync + a.y.err, 1);
+  if (a.err_flags) atomicOr(a.err_flags, (int)SPLA_DEVERR_SYNC);
+}
+
+// Every thread: waits until its stores (Mem<true>, so device-coherent once
+// complete) have completed, then the workgroup counts itself in *ctr. True in
+// every thread of the workgroup that arrived as the n-th; that workgroup reads
+// what the others published with Mem<true> loads.
+__device__ __forceinline__ bool arrive_last(int32_t* ctr, int n, int* s_flag) {
+  wait_memory();
+  __syncthreads();
+  if (threadIdx.x == 0) *s_flag = atomic_add_agent(ctr, 1) == n - 1;
+  __syncthreads();
+  return *s_flag != 0;
+}
+
+// R: blocks per thread of the selection (256 R >= blocks per sequence).
+template <int G, int BLK, int R>
+__global__ __launch_bounds__(256) void decode_kernel(FusedArgs a) {
+  constexpr int D = 128;
+  constexpr int SWN = 4 * R * G;  // tile weights: n_tiles <= 4 R
+  __shared__ union {
+    ScoreSmem<G> sc;
+    SelectSmem<256, SWN> se;
+    SparseSmem<D> sp;
+  } sm;
+  __shared__ int s_flag;
+  const Dims& m = a.m;
+  const SyncLayout& y = a.y;
+  int32_t* sy = a.sync;
+  const int tid = threadIdx.x;
+  const int n_score = m.bh * a.n_si;
+  if ((int)blockIdx.x < n_score) {
+    // ---------------------------------------------------------- score item
+    const int t = (int)blockIdx.x;
+    const int bh = t / a.n_si, i = t % a.n_si;
+    score_items<G, bf16_t, D, true, kTilesPerItem>(
+        m, a.stats, a.seq_lens, a.q, a.s_score, a.first_order,
+        bh * m.n_tiles + i * kTilesPerItem, a.e_vals, a.tile_part, sm.sc);
+    int32_t* done = sy + y.items_done + (int64_t)bh * kSyncLine;
+    if (!arrive_last(done, a.n_si, &s_flag)) return;
+    if (tid == 0) store_agent(done, 0);
+    select_blocks<256, R, SWN, true, 2>(m, bh, a.seq_lens, a.e_vals, a.tile_part, sm.se,
+                                        sy + y.sel_ready + (int64_t)bh * m.k, nullptr,
+                                        a.sel_out ? a.sel_out + (int64_t)bh * m.k : nullptr);
+    return;
+  }
+  // ------------------------------------------------------------ sparse item
+  const int j = (int)blockIdx.x - n_score;
+  const int bh = j / a.n_wg, x = j % a.n_wg;
+  SparseRegs<D> r;
+  sparse_prologue<D>(m, a.q, a.S, a.zbar, bh, x, a.n_wg, r);
+  // this wavefront's block: poll its selection word (lane 0), then share it
+  const int step = sparse_step_entry<BLK>(x);
+  int32_t* word = sy + y.sel_ready + (int64_t)bh * m.k + step;
+  int v = 1;
+  if (step < m.k && (tid & 63) == 0) {
+    v = load_agent(word);
+    for (int n = 0; v == 0 && n < kSpinLimit; ++n) {
+      __builtin_amdgcn_s_sleep(4);
+      v = load_agent(word);
+    }
+    if (v == 0) report_sync_error(a);
+  }
+  const int blk_sel = __builtin_amdgcn_readfirstlane(v) - 2;
+  const int L = min(max(a.seq_lens[bh / m.hkv], 0), m.cap);
+  sparse_body<D, BLK, true>(m, a.s, a.kc, a.vc, a.S, blk_sel, L, bh, x, a.n_wg, r, sm.sp, a.part,
+                            a.stride);
+  if (step < m.k && (tid & 63) == 0) store_agent(word, 0);  // read by this workgroup only
+  int32_t* recs = sy + y.recs_done + (int64_t)bh * kSyncLine;
+  if (!arrive_last(recs, a.n_wg, &s_flag)) return;
+  if (tid == 0) store_agent(recs, 0);
+  const int nb = (L + BLK - 1) / BLK;
+  const int all_sel = nb <= m.k;
+  const float* rec = a.part + (int64_t)bh * a.n_wg * a.stride;
+  for (int g = tid >> 6; g < G; g += 4)
+    merge_head<bf16_t, D, true>(m, a.eps, a.flags, a.gamma, all_sel, L, rec, a.n_wg, a.stride,
+                                a.out, bh, g);
+}
+
+template <int G, int BLK, int R>
+static void decode_gbr(const FusedArgs& a, hipStream_t st) {
+  const int grid = a.m.bh * (a.n_si + a.n_wg);
+  hipLaunchKernelGGL((decode_kernel<G, BLK, R>), dim3((unsigned)grid), dim3(256), 0, st, a);
+}
+
+template <int G, int R>
+static void decode_gr(const FusedArgs& a, hipStream_t st) {
+  if (a.m.B == 32) decode_gbr<G, 32, R>(a, st);
+  else if (a.m.B == 64) decode_gbr<G, 64, R>(a, st);
+  else decode_gbr<G, 128, R>(a, st);
+}
+
+template <int G>
+static void decode_g(const FusedArgs& a, hipStream_t st) {
+  if (a.m.nb_cap <= 256 * 8) decode_gr<G, 8>(a, st);
+  else decode_gr<G, 32>(a, st);
+}
+
+hipError_t launch_decode_fused(const Dims& m, const spla_config& cfg, const spla_cache& c,
+                               const void* q, const float* gamma, void* out, int32_t* sel_out,
+                               const DecodeWs& ws, char* base, hipStream_t st) {
+  FusedArgs a;
+  a.m = m;
+  a.stats = c.blk_stats;
+  a.seq_lens = c.seq_lens;
+  a.q = (const bf16_t*)q;
+  a.kc = (const bf16_t*)c.k_cache;
+  a.vc = (const bf16_t*)c.v_cache;
+  a.S = c.lin_state;
+  a.zbar = c.lin_norm;
+  a.gamma = gamma;
+  a.out = (bf16_t*)out;
+  a.sel_out = sel_out;
+  a.err_flags = c.err_flags;
+  a.e_vals = (float*)(base + ws.e_vals);
+  a.tile_part = (double*)(base + ws.tile_part);
+  a.sel = (int32_t*)(base + ws.sel);
+  a.meta = (int32_t*)(base + ws.meta);
+  a.part = (float*)(base + ws.part);
+  a.sync = (int32_t*)(base + ws.sync);
+  a.y = sync_layout(m);
+  a.s_score = cfg.softmax_scale > 0.f ? (double)cfg.softmax_scale : 1.0 / sqrt((double)m.d);
+  a.s = cfg.softmax_scale > 0.f ? cfg.softmax_scale : (float)(1.0 / sqrt((double)m.d));
+  a.eps = cfg.rms_eps;
+  a.flags = cfg.flags;
+  a.first_order = (cfg.flags & SPLA_FLAG_FIRST_ORDER) != 0;
+  a.n_si = (int)ceil_div(m.n_tiles, kTilesPerItem);
+  a.n_wg = ws.n_wg;
+  a.stride = ws.part_stride;
+  switch (m.group) {
+    case 1: decode_g<1>(a, st); break;
+    case 2: decode_g<2>(a, st); break;
+    case 3: decode_g<3>(a, st); break;
+    case 4: decode_g<4>(a, st); break;
+    case 5: decode_g<5>(a, st); break;
+    case 6: decode_g<6>(a, st); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace spla

@@ -1,357 +1,29 @@
-// Block scoring (Sec. 3.1), one workgroup per (sequence, KV head, tile of 64
-// blocks) item; every item's loads are in flight from the start. Within a
-// tile each wavefront takes 16 blocks, lane =
-// (block, quarter of the head dimension); every 16-byte load of the
-// tile-interleaved statistics is a contiguous 256 B run per 16 lanes, and the
-// loads are nontemporal (each byte is read once per step). For head m of the
-// group the log block mass is
-//   ell_m(i) = s q_m.mu_i + ln n_i + ln(1 + 1/2 s^2 sum_j q_mj^2 M2_ij / n_i)
-// (Eqs. 8 and 10, diagonal covariance M2/n): eight coordinates at a time in
-// fp32 (the query coefficients reach the lanes by DPP row broadcasts, not
-// LDS reads), those partial sums accumulated in fp64 and summed over the four
-// quarters with a cross-lane reduce-scatter; lane (block, quarter) then
-// finishes heads quarter, quarter+4, ... Each tile yields exp(ell - tile max) per head
-// and block and the (max, sum) of its 64 blocks per head, from which the
-// selection forms each head's normaliser Z (Eq. 9) without another pass over
-// the statistics. For the matrix-core sparse pass, bh trailing workgroups
-// also lay out the query operands of its products.
-#include "spla_device.h"
+// Block scoring kernel (Sec. 3.1): one workgroup per (sequence, KV head,
+// tile of 64 blocks) item; every item's loads are in flight from the start.
+// The per-tile arithmetic is score_items (spla_score.h).
 #include "spla_kernels.h"
+#include "spla_score.h"
 
 namespace spla {
-
-constexpr int kScoreGroup = 16;  // blocks per wavefront
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-
-template <int NJ>
-struct TileBuf {
-  float4 mu[NJ], m2[NJ];
-};
-
-// Issues the statistics loads of item t (sequence x KV head x tile) for this
-// lane; an item past the run (valid = false) re-reads the first 16 bytes of
-// the buffer, so every path issues the same loads and no wait depends on the
-// branch taken.
-template <int NJ>
-__device__ __forceinline__ void load_tile(const Dims& m, const float* __restrict__ stats, int t,
-                                          bool valid, int first_order, int bi, int qt,
-                                          TileBuf<NJ>& buf) {
-  const int bh = t / m.n_tiles, tile = t % m.n_tiles;
-  const int64_t blk = (int64_t)tile * kTileBlocks + bi;
-  // first order: the second-moment loads re-read the means (same lines)
-  const f32x4* pm = reinterpret_cast<const f32x4*>(
-      valid ? stats + stats_off4(m, bh, blk, 0, qt * NJ) : stats);
-  const f32x4* pv = reinterpret_cast<const f32x4*>(
-      valid ? stats + stats_off4(m, bh, blk, first_order ? 0 : 1, qt * NJ) : stats);
-  const int stride = valid ? kTileBlocks : 0;
-#pragma unroll
-  for (int j = 0; j < NJ; ++j) {  // interleaved: group j is usable once its two loads land
-    const f32x4 x = __builtin_nontemporal_load(pm + j * stride);
-    const f32x4 y = __builtin_nontemporal_load(pv + j * stride);
-    buf.mu[j] = make_float4(x[0], x[1], x[2], x[3]);
-    buf.m2[j] = make_float4(y[0], y[1], y[2], y[3]);
-  }
-}
-
-// Coefficient table of sequence x KV head bh: s q (table 0) and s^2 q^2 / 2
-// (table 1) per head, laid out [quarter][(table * G + head) * 32 + c] for
-// coordinate 32 quarter + c (D = 128; D = 64 uses c < 16). load_q issues the
-// query loads, write_table fills the table; clamped entries rewrite the last
-// element's value.
-template <int G, int D>
-struct QRegs {
-  float x[(G * D + 255) / 256];
-};
-
-template <int G, typename T, int D>
-__device__ __forceinline__ void load_q(const Dims& m, const T* __restrict__ q, int bh,
-                                       QRegs<G, D>& r) {
-  constexpr int QE = (G * D + 255) / 256;
-  const int b = bh / m.hkv, h = bh % m.hkv;
-#pragma unroll
-  for (int i = 0; i < QE; ++i) {
-    const int e = min((int)threadIdx.x + 256 * i, G * D - 1);
-    r.x[i] = Elem<T>::load(q, ((int64_t)b * m.hq + h * G + e / D) * D + e % D);
-  }
-}
-
-template <int G, int D>
-__device__ __forceinline__ void write_table(const QRegs<G, D>& r, double s, float (*sco)[2 * G * 32]) {
-  constexpr int Q = D / 4;
-  constexpr int QE = (G * D + 255) / 256;
-#pragma unroll
-  for (int i = 0; i < QE; ++i) {
-    const int e = min((int)threadIdx.x + 256 * i, G * D - 1);
-    const int mm = e / D, j = e % D;
-    const int qq = j / Q, c = j % Q;
-    const double x = (double)r.x[i];
-    sco[qq][mm * 32 + c] = (float)(s * x);
-    sco[qq][(G + mm) * 32 + c] = (float)(0.5 * s * s * x * x);
-  }
-}
-
-// acc (+)= c[lane n of this lane's 16-lane row] * x: the coefficient reaches
-// every lane of the row through a DPP row broadcast, so the products need no
-// LDS traffic. Callers keep at least two other VALU instructions between two
-// updates of one accumulator and never follow a VALU write of c directly.
-#define SPLA_BC_CASE(n, op)                                                                   \
-  case n:                                                                                     \
-    asm volatile(op " %0, %1, %2 row_newbcast:" #n " row_mask:0xf bank_mask:0xf"              \
-                 : "+v"(acc) : "v"(c), "v"(x));                                               \
-    break;
-#define SPLA_BC_SWITCH(op)                                                                    \
-  switch (n) {                                                                                \
-    SPLA_BC_CASE(0, op) SPLA_BC_CASE(1, op) SPLA_BC_CASE(2, op) SPLA_BC_CASE(3, op)            \
-    SPLA_BC_CASE(4, op) SPLA_BC_CASE(5, op) SPLA_BC_CASE(6, op) SPLA_BC_CASE(7, op)            \
-    SPLA_BC_CASE(8, op) SPLA_BC_CASE(9, op) SPLA_BC_CASE(10, op) SPLA_BC_CASE(11, op)          \
-    SPLA_BC_CASE(12, op) SPLA_BC_CASE(13, op) SPLA_BC_CASE(14, op) SPLA_BC_CASE(15, op)        \
-    default: break;                                                                           \
-  }
-__device__ __forceinline__ void mul_row_bcast(float& acc, float c, float x, int n) {
-  SPLA_BC_SWITCH("v_mul_f32_dpp")
-}
-__device__ __forceinline__ void fmac_row_bcast(float& acc, float c, float x, int n) {
-  SPLA_BC_SWITCH("v_fmac_f32_dpp")
-}
-#undef SPLA_BC_SWITCH
-#undef SPLA_BC_CASE
-
-__device__ __forceinline__ float f4_at(const float4& v, int e) {
-  return e == 0 ? v.x : (e == 1 ? v.y : (e == 2 ? v.z : v.w));
-}
-
-// Scores one tile from buf; s_part is this tile's half of the double-buffered
-// cross-wavefront scratch.
-template <int G, int D>
-__device__ __forceinline__ void score_tile(const Dims& m, const int32_t* __restrict__ seq_lens,
-                                           int first_order, int t, const TileBuf<D / 16>& buf,
-                                           const float (*sco)[2 * G * 32],
-                                           double (*s_part)[G][2], float* __restrict__ e_vals,
-                                           double* __restrict__ tile_part) {
-  constexpr int NJ = D / 16;
-  constexpr int U = (G + 3) / 4;
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int qt = lane >> 4;
-  const int bh = t / m.n_tiles, tile = t % m.n_tiles;
-  const int blk = tile * kTileBlocks + kScoreGroup * w + (lane & 15);
-  const int L = seq_lens[bh / m.hkv];
-  const int nb = (L + m.B - 1) / m.B;
-  // this lane's coefficients: cf[k] holds entry 16 k + (lane % 16) of its
-  // quarter's table, read once per tile
-  constexpr int NK = (2 * G * 32) / 16;
-  float cf[NK];
-#pragma unroll
-  for (int k = 0; k < NK; ++k) cf[k] = sco[qt][16 * k + (lane & 15)];
-  double am[G], av[G];
-#pragma unroll
-  for (int mm = 0; mm < G; ++mm) am[mm] = av[mm] = 0.0;
-  // eight coordinates at a time in fp32, those partials added in fp64. The
-  // 2G partials of a step are updated round-robin, so one accumulator's
-  // updates are 2G instructions apart (plus a nop for G = 1).
-  asm volatile("s_nop 4");  // spacing after any earlier EXEC / VGPR write
-#pragma unroll
-  for (int jp = 0; jp < NJ / 2; ++jp) {
-    float pa[G], pb[G];
-#pragma unroll
-    for (int e8 = 0; e8 < 8; ++e8) {
-      const int c = 8 * jp + e8;  // coordinate within the quarter
-      const float xm = f4_at(buf.mu[2 * jp + (e8 >> 2)], e8 & 3);
-      const float xv = f4_at(buf.m2[2 * jp + (e8 >> 2)], e8 & 3);
-#pragma unroll
-      for (int mm = 0; mm < G; ++mm) {
-        if (e8 == 0) mul_row_bcast(pa[mm], cf[mm * 2 + (c >> 4)], xm, c & 15);
-        else fmac_row_bcast(pa[mm], cf[mm * 2 + (c >> 4)], xm, c & 15);
-      }
-#pragma unroll
-      for (int mm = 0; mm < G; ++mm) {
-        if (e8 == 0) mul_row_bcast(pb[mm], cf[(G + mm) * 2 + (c >> 4)], xv, c & 15);
-        else fmac_row_bcast(pb[mm], cf[(G + mm) * 2 + (c >> 4)], xv, c & 15);
-      }
-      if (G == 1) asm volatile("s_nop 0");
-    }
-#pragma unroll
-    for (int mm = 0; mm < G; ++mm) {
-      am[mm] += (double)pa[mm];
-      av[mm] += (double)pb[mm];
-    }
-  }
-  // reduce-scatter over the four quarters (lanes l ^ 16, l ^ 32): lane
-  // (block, qt) ends with the sums of heads qt + 4u, u < U (zero past G)
-  double ra[U], rv[U];
-  {
-    const bool k1 = (qt & 2) != 0, k0 = (qt & 1) != 0;
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      double ta[2], tv[2];
-#pragma unroll
-      for (int r0 = 0; r0 < 2; ++r0) {
-        const int hl = 4 * u + r0, hh = hl + 2;
-        const double al = hl < G ? am[hl < G ? hl : 0] : 0.0, ah = hh < G ? am[hh < G ? hh : 0] : 0.0;
-        const double vl = hl < G ? av[hl < G ? hl : 0] : 0.0, vh = hh < G ? av[hh < G ? hh : 0] : 0.0;
-        ta[r0] = (k1 ? ah : al) + xor32(k1 ? al : ah);
-        tv[r0] = (k1 ? vh : vl) + xor32(k1 ? vl : vh);
-      }
-      ra[u] = (k0 ? ta[1] : ta[0]) + xor16(k0 ? ta[0] : ta[1]);
-      rv[u] = (k0 ? tv[1] : tv[0]) + xor16(k0 ? tv[0] : tv[1]);
-    }
-  }
-  // lane (block, qt) finishes heads qt + 4u. ln n and ln(1 + x) are O(1)
-  // and taken in fp32 (absolute error ~1e-7 on ell); ell itself is fp64.
-  const bool valid = blk < nb;
-  const int n_i = valid ? block_count(L, m.B, blk) : 1;
-  const double ln_n = (double)logf((float)n_i);
-  const int nbp = m.n_tiles * kTileBlocks;
-  float* ev = e_vals + (int64_t)bh * G * nbp;
-  double ell[U];
-#pragma unroll
-  for (int u = 0; u < U; ++u) {
-    const int mm = qt + 4 * u;
-    double x = ra[u] + ln_n;
-    if (!first_order) x += (double)log1pf((float)(rv[u] / n_i));
-    ell[u] = valid ? x : -INFINITY;
-    // the tile offset is the max of the fp32-rounded ell (any common offset
-    // works; this one is exact in both precisions)
-    const float mx = row_max_to15((float)ell[u]);
-    if ((lane & 15) == 15 && mm < G) s_part[w][mm][0] = (double)mx;
-  }
-  __syncthreads();
-  // exp(ell - tile max): the tile's 64 blocks share one offset per head; the
-  // fp64 difference enters expf as a hi + lo pair
-#pragma unroll
-  for (int u = 0; u < U; ++u) {
-    const int mm = qt + 4 * u;
-    if (mm < G) {
-      double tmx = -INFINITY;
-#pragma unroll
-      for (int x = 0; x < 4; ++x) tmx = fmax(tmx, s_part[x][mm][0]);
-      const double d = ell[u] - tmx;
-      const float dh = (float)d;
-      const float dl = (float)(d - (double)dh);
-      const float eh = expf(dh);
-      const float e = valid ? fmaf(eh, dl, eh) : 0.f;
-      ev[(int64_t)mm * nbp + blk] = e;
-      const double sum = row_sum_to15((double)e);
-      if ((lane & 15) == 15) s_part[w][mm][1] = sum;
-    }
-  }
-  __syncthreads();
-  if (tid < G) {
-    double mx = -INFINITY, sum = 0.0;
-#pragma unroll
-    for (int x = 0; x < 4; ++x) {
-      mx = fmax(mx, s_part[x][tid][0]);
-      sum += s_part[x][tid][1];
-    }
-    double* tp = tile_part + (((int64_t)bh * m.n_tiles + tile) * G + tid) * 2;
-    tp[0] = mx;
-    tp[1] = sum;
-  }
-}
-
-// Query operands of the sparse pass's matrix products for one sequence x KV
-// head, in the per-lane order the pass loads them (16 bytes per lane and
-// k-step): lane l = (g = l / 16, column j = l % 16) holds coordinates
-// 32 ks + 8 g .. +7 of head j (columns 0..7: q itself, the exact-branch
-// logits) or of head j - 8 (columns 8..15: phi(q) as a bf16 hi + lo pair,
-// the linear weights); absent heads are zero. phi is the softmax over the
-// feature dimension (Sec. 3.2).
-template <int G, int D>
-__device__ void prep_q_operands(const Dims& m, const bf16_t* __restrict__ q, int bh,
-                                uint4* __restrict__ qprep, float (*sphi)[D]) {
-  constexpr int KS = D / 32;
-  const int b = bh / m.hkv, h = bh % m.hkv;
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  for (int mm = w; mm < G; mm += 4) {
-    float x[D / 64];
-    float mx = -INFINITY;
-#pragma unroll
-    for (int e = 0; e < D / 64; ++e) {
-      x[e] = Elem<bf16_t>::load(q, ((int64_t)b * m.hq + h * G + mm) * D + lane + 64 * e);
-      mx = fmaxf(mx, x[e]);
-    }
-    mx = wave_max(mx);
-    float sum = 0.f;
-#pragma unroll
-    for (int e = 0; e < D / 64; ++e) {
-      x[e] = __expf(x[e] - mx);
-      sum += x[e];
-    }
-    sum = wave_sum(sum);
-    const float inv = 1.0f / sum;
-#pragma unroll
-    for (int e = 0; e < D / 64; ++e) sphi[mm][lane + 64 * e] = x[e] * inv;
-  }
-  __syncthreads();
-  for (int c = tid; c < 3 * KS * 64; c += 256) {
-    const int kind = c / (KS * 64), ks = (c / 64) % KS, l = c % 64;
-    const int g = l >> 4, j = l & 15;
-    const bool exact = j < 8;
-    const int head = exact ? j : j - 8;
-    const bool live = head < G && (kind == 0) == exact;
-    uint16_t v[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int coord = 32 * ks + 8 * g + e;
-      uint16_t bits = 0;
-      if (live) {
-        if (kind == 0) {
-          bits = q[((int64_t)b * m.hq + h * G + head) * D + coord].bits;
-        } else {
-          const float pq = sphi[head][coord];
-          const __bf16 hi = (__bf16)pq;
-          const __bf16 val = kind == 1 ? hi : (__bf16)(pq - (float)hi);
-          bits = __builtin_bit_cast(uint16_t, val);
-        }
-      }
-      v[e] = bits;
-    }
-    qprep[((int64_t)bh * 3 * KS + kind * KS + ks) * 64 + l] =
-        make_uint4(v[0] | ((uint32_t)v[1] << 16), v[2] | ((uint32_t)v[3] << 16),
-                   v[4] | ((uint32_t)v[5] << 16), v[6] | ((uint32_t)v[7] << 16));
-  }
-}
 
 template <int G, typename T, int D>
 __global__ __launch_bounds__(256) void score_kernel(
     Dims m, const float* __restrict__ stats, const int32_t* __restrict__ seq_lens,
     const T* __restrict__ q, double s, int first_order, float* __restrict__ e_vals,
-    double* __restrict__ tile_part, uint4* __restrict__ qprep) {
-  constexpr int NJ = D / 16;  // float4 loads per lane and statistics part
-  __shared__ float sco[4][2 * G * 32];
-  __shared__ double s_part[4][G][2];
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int t = blockIdx.x;  // item: sequence x KV head x tile
-  if (t >= m.bh * m.n_tiles) {  // trailing workgroups: query operands of the sparse pass
-    if constexpr (G <= 8 && sizeof(T) == 2) {
-      __shared__ float sphi[G][D];
-      prep_q_operands<G, D>(m, q, t - m.bh * m.n_tiles, qprep, sphi);
-    }
-    return;
-  }
-  // load order: the query elements of the coefficient table, then the
-  // statistics (16 x 16 B per lane); the table is built while the statistics
-  // are in flight. Items past the sequence end are scored and masked: an
-  // early exit would let the compiler sink the loads below the barrier.
-  QRegs<G, D> qr;
-  load_q<G, T, D>(m, q, t / m.n_tiles, qr);
-  TileBuf<NJ> A;
-  load_tile<NJ>(m, stats, t, true, first_order, kScoreGroup * w + (lane & 15), lane >> 4, A);
-  __builtin_amdgcn_sched_barrier(0);
-  write_table<G, D>(qr, s, sco);
-  __syncthreads();
-  score_tile<G, D>(m, seq_lens, first_order, t, A, sco, s_part, e_vals, tile_part);
+    double* __restrict__ tile_part) {
+  __shared__ ScoreSmem<G> sm;
+  score_items<G, T, D, false, 1>(m, stats, seq_lens, q, s, first_order, (int)blockIdx.x, e_vals,
+                               tile_part, sm);
 }
 
 template <int G, typename T, int D>
 static void score_gtd(const Dims& m, const spla_config& cfg, const spla_cache& c, const void* q,
                       const DecodeWs& ws, char* base, hipStream_t st) {
   const double s = cfg.softmax_scale > 0.f ? (double)cfg.softmax_scale : 1.0 / sqrt((double)m.d);
-  const int n_prep = use_mfma_sparse(m) ? m.bh : 0;
-  hipLaunchKernelGGL((score_kernel<G, T, D>), dim3((unsigned)(m.bh * m.n_tiles + n_prep)),
-                     dim3(256), 0, st, m, (const float*)c.blk_stats, (const int32_t*)c.seq_lens,
-                     (const T*)q, s, (int)((cfg.flags & SPLA_FLAG_FIRST_ORDER) != 0),
-                     (float*)(base + ws.e_vals), (double*)(base + ws.tile_part),
-                     (uint4*)(base + ws.qprep));
+  hipLaunchKernelGGL((score_kernel<G, T, D>), dim3((unsigned)(m.bh * m.n_tiles)), dim3(256), 0,
+                     st, m, (const float*)c.blk_stats, (const int32_t*)c.seq_lens, (const T*)q, s,
+                     (int)((cfg.flags & SPLA_FLAG_FIRST_ORDER) != 0),
+                     (float*)(base + ws.e_vals), (double*)(base + ws.tile_part));
 }
 
 template <typename T, int D>

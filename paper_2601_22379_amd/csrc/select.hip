@@ -14,7 +14,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
     int32_t* __restrict__ sel_out, int32_t* __restrict__ meta) {
   __shared__ SelectSmem<kSelThreads, kMaxTiles * SPLA_MAX_GROUP> sm;
   const int bh = blockIdx.x;
-  select_blocks<kSelThreads, R, kMaxTiles * SPLA_MAX_GROUP>(
+  select_blocks<kSelThreads, R, kMaxTiles * SPLA_MAX_GROUP, false>(
       m, bh, seq_lens, e_vals, tile_part, sm, sel_ws + (int64_t)bh * m.k, meta + bh * 4,
       sel_out ? sel_out + (int64_t)bh * m.k : nullptr);
 }

@@ -63,6 +63,11 @@ int32_t run_decode(const spla_config* cfg, const spla_cache* cache, const void* 
   const Dims m = spla::make_dims(*cfg);
   const spla::DecodeWs L = spla::decode_ws_layout(m);
   char* base = static_cast<char*>(ws);
+  if (spla::use_fused_decode(m) && !(cfg->flags & SPLA_FLAG_SEPARATE_KERNELS)) {
+    PhaseMark pm(ev, st, SPLA_PHASE_DECODE);
+    SPLA_TRY(spla::launch_decode_fused(m, *cfg, *cache, q, w, out, sel_idx, L, base, st));
+    return SPLA_OK;
+  }
   {
     PhaseMark pm(ev, st, SPLA_PHASE_SCORE);
     SPLA_TRY(spla::launch_score(m, *cfg, *cache, q, L, base, st));
@@ -70,6 +75,8 @@ int32_t run_decode(const spla_config* cfg, const spla_cache* cache, const void* 
   if (!spla::sparse_selects(m)) {
     PhaseMark pm(ev, st, SPLA_PHASE_SELECT);
     SPLA_TRY(spla::launch_select(m, *cache, L, base, sel_idx, st));
+  } else {
+    PhaseMark pm(ev, st, SPLA_PHASE_SELECT);  // folded into the sparse launch: empty
   }
   {
     PhaseMark pm(ev, st, SPLA_PHASE_SPARSE);
@@ -107,6 +114,17 @@ extern "C" int32_t spla_reset(const spla_config* cfg, const spla_cache* cache, v
   SPLA_TRY(spla::launch_fill_zero(cache->lin_state, b[3], st));
   SPLA_TRY(spla::launch_fill_zero(cache->lin_norm, b[4], st));
   SPLA_TRY(spla::launch_fill_zero(cache->seq_lens, b[5], st));
+  return SPLA_OK;
+}
+
+extern "C" int32_t spla_workspace_init(const spla_config* cfg, void* ws, size_t ws_bytes,
+                                       void* stream) {
+  int32_t s = spla_validate(cfg);
+  if (s != SPLA_OK) return s;
+  size_t need = 0;
+  spla_workspace_bytes(cfg, &need);
+  if ((s = check_ws(ws, ws_bytes, need)) != SPLA_OK) return s;
+  SPLA_TRY(spla::launch_fill_zero(ws, need, static_cast<hipStream_t>(stream)));
   return SPLA_OK;
 }
 

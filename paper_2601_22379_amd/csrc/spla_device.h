@@ -168,6 +168,53 @@ __device__ __forceinline__ double row_sum_to15(double x) {
   return x;
 }
 
+// ---- memory access policy of data that one workgroup hands to another
+// within a launch. Mem<false>: ordinary loads and stores (the data crosses a
+// kernel boundary). Mem<true>: agent-scope atomic loads and stores, which
+// the compiler emits with the device-coherence bit (sc1): they write through
+// and read past the per-XCD L2 caches, so no cache-wide writeback or
+// invalidation is needed between producer and consumer.
+template <bool CO>
+struct Mem;
+template <>
+struct Mem<false> {
+  template <typename T>
+  static __device__ __forceinline__ T ld(const T* p) { return *p; }
+  template <typename T>
+  static __device__ __forceinline__ void st(T* p, T v) { *p = v; }
+  static __device__ __forceinline__ float2 ld2(const float* p) {
+    return *reinterpret_cast<const float2*>(p);
+  }
+  static __device__ __forceinline__ float4 ld4(const float* p) {
+    return *reinterpret_cast<const float4*>(p);
+  }
+};
+template <>
+struct Mem<true> {
+  template <typename T>
+  static __device__ __forceinline__ T ld(const T* p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  template <typename T>
+  static __device__ __forceinline__ void st(T* p, T v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  static __device__ __forceinline__ float2 ld2(const float* p) {  // 8-byte aligned
+    const uint64_t u = __hip_atomic_load(reinterpret_cast<const uint64_t*>(p), __ATOMIC_RELAXED,
+                                         __HIP_MEMORY_SCOPE_AGENT);
+    return make_float2(__uint_as_float((uint32_t)u), __uint_as_float((uint32_t)(u >> 32)));
+  }
+  static __device__ __forceinline__ float4 ld4(const float* p) {  // 16-byte aligned
+    const float2 a = ld2(p), b = ld2(p + 2);
+    return make_float4(a.x, a.y, b.x, b.y);
+  }
+};
+
+// Waits until every memory operation this wavefront issued has completed
+// (for the coherent stores of Mem<true>: reached the device-coherent level).
+// The memory clobber keeps the compiler from moving accesses across it.
+__device__ __forceinline__ void wait_memory() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
 // Number of tokens of block i in a sequence of length L.
 __device__ __forceinline__ int block_count(int L, int B, int i) {
   int n = L - i * B;

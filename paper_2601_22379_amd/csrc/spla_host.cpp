@@ -27,6 +27,7 @@ extern "C" const char* spla_phase_name(int32_t p) {
     case SPLA_PHASE_SELECT: return "select";
     case SPLA_PHASE_SPARSE: return "sparse";
     case SPLA_PHASE_MERGE: return "merge";
+    case SPLA_PHASE_DECODE: return "decode";
     default: return nullptr;
   }
 }
@@ -49,7 +50,8 @@ extern "C" int32_t spla_validate(const spla_config* c) {
   if (c->dtype != SPLA_F32 && c->dtype != SPLA_BF16) return SPLA_ERR_INVALID_ARG;
   if (!isfinite(c->softmax_scale)) return SPLA_ERR_INVALID_ARG;
   if (!isfinite(c->rms_eps) || c->rms_eps < 0.0f) return SPLA_ERR_INVALID_ARG;
-  const uint32_t known = SPLA_FLAG_NO_RLA | SPLA_FLAG_FIRST_ORDER | SPLA_FLAG_RLA_NORMALIZE;
+  const uint32_t known = SPLA_FLAG_NO_RLA | SPLA_FLAG_FIRST_ORDER | SPLA_FLAG_RLA_NORMALIZE |
+                         SPLA_FLAG_SEPARATE_KERNELS;
   if (c->flags & ~known) return SPLA_ERR_INVALID_ARG;
   // every derived byte count must fit comfortably in 63 bits
   const Dims m = spla::make_dims(*c);
@@ -87,5 +89,17 @@ extern "C" int32_t spla_append_workspace_bytes(const spla_config* c, int32_t max
   if (max_new < 0) return SPLA_ERR_INVALID_ARG;
   if (max_new > c->max_seq_len) return SPLA_ERR_CAPACITY;
   *out = (size_t)spla::append_ws_layout(spla::make_dims(*c), max_new).total;
+  return SPLA_OK;
+}
+
+extern "C" int32_t spla_decode_phase_mask(const spla_config* c, uint32_t* out) {
+  if (!out) return SPLA_ERR_INVALID_ARG;
+  int32_t st = spla_validate(c);
+  if (st != SPLA_OK) return st;
+  if (spla::use_fused_decode(spla::make_dims(*c)) && !(c->flags & SPLA_FLAG_SEPARATE_KERNELS))
+    *out = 1u << SPLA_PHASE_DECODE;
+  else
+    *out = (1u << SPLA_PHASE_SCORE) | (1u << SPLA_PHASE_SELECT) | (1u << SPLA_PHASE_SPARSE) |
+           (1u << SPLA_PHASE_MERGE);
   return SPLA_OK;
 }

@@ -42,4 +42,10 @@ hipError_t launch_sparse(const Dims& m, const spla_config& cfg, const spla_cache
 hipError_t launch_merge(const Dims& m, const spla_config& cfg, const float* rms_weight, void* out,
                         const DecodeWs& ws, char* wsbase, hipStream_t st);
 
+// decode.hip: the single-launch decode (use_fused_decode shapes)
+hipError_t launch_decode_fused(const Dims& m, const spla_config& cfg, const spla_cache& c,
+                               const void* q, const float* rms_weight, void* out,
+                               int32_t* sel_out, const DecodeWs& ws, char* wsbase,
+                               hipStream_t st);
+
 }  // namespace spla

@@ -74,10 +74,11 @@ constexpr int kSparseWaves = 4;   // waves per sparse workgroup
 struct DecodeWs {
   int64_t e_vals;     // f32 [bh][G][n_tiles*64]   exp(ell - tile max)
   int64_t tile_part;  // f64 [bh][n_tiles][G][2]   (max, sum) per 64-block tile
-  int64_t qprep;      // bf16 [bh][3][d/32][64][8] MFMA B operands: q, phi(q) hi, phi(q) lo
   int64_t sel;        // i32 [bh][k]               selected blocks, ascending
   int64_t meta;       // i32 [bh][4]               (n_selected, all_selected, length, 0)
   int64_t part;       // f32 [bh][n_wg][part_stride]  sparse workgroup partials
+  int64_t sync;       // i32 [sync_layout(m).words]  counters of the single-launch decode;
+                      //   zero between calls
   int64_t total;
   int n_wg;           // sparse workgroups per (sequence, kv head)
   int blocks_per_wg;  // selected blocks per VALU-pass workgroup
@@ -87,6 +88,40 @@ struct DecodeWs {
 // The MFMA sparse pass handles bf16 with G <= 8; everything else uses the
 // VALU pass. Both write records in the same format.
 SPLA_HD bool use_mfma_sparse(const Dims& m) { return m.elem == 2 && m.group <= 8; }
+
+// The single-launch decode covers the matrix-core shapes with d = 128,
+// G <= 6 (larger groups exceed its register budget) and at most 8192 blocks
+// per sequence (its selection runs in one 256-thread workgroup, at most 32
+// blocks per thread).
+constexpr int kFusedMaxBlocks = 256 * 32;
+constexpr int kFusedMaxGroup = 6;
+SPLA_HD bool use_fused_decode(const Dims& m) {
+  return use_mfma_sparse(m) && m.d == 128 && m.group <= kFusedMaxGroup &&
+         m.nb_cap <= kFusedMaxBlocks;
+}
+
+// The decode workspace's synchronisation area (int32 words). Every counter
+// that many workgroups update sits alone in its 128-byte line (counters that
+// share a line serialise their atomics).
+constexpr int kSyncLine = 32;  // int32 words per line
+struct SyncLayout {
+  int64_t err;         // error word (bad waits)
+  int64_t items_done;  // [bh], line stride: score items finished
+  int64_t recs_done;   // [bh], line stride: sparse records written
+  int64_t sel_ready;   // [bh][k]: selected block + 2 (1: none), 0 until the selection
+                       //   of that (sequence, KV head) is published
+  int64_t words;
+};
+SPLA_HD SyncLayout sync_layout(const Dims& m) {
+  SyncLayout y;
+  const int64_t per = (int64_t)m.bh * kSyncLine;
+  y.err = 0;
+  y.items_done = kSyncLine;
+  y.recs_done = y.items_done + per;
+  y.sel_ready = y.recs_done + per;
+  y.words = y.sel_ready + align_up((int64_t)m.bh * m.k, kSyncLine);
+  return y;
+}
 
 SPLA_HD DecodeWs decode_ws_layout(const Dims& m) {
   DecodeWs w;
@@ -103,10 +138,10 @@ SPLA_HD DecodeWs decode_ws_layout(const Dims& m) {
   w.part_stride = kPartHead + 2 * m.group * m.d;
   w.e_vals = take((int64_t)m.bh * m.group * m.n_tiles * kTileBlocks * 4);
   w.tile_part = take((int64_t)m.bh * m.n_tiles * m.group * 2 * 8);
-  w.qprep = take((int64_t)m.bh * 3 * m.d * 32 * 2);
   w.sel = take((int64_t)m.bh * m.k * 4);
   w.meta = take((int64_t)m.bh * 4 * 4);
   w.part = take((int64_t)m.bh * w.n_wg * w.part_stride * 4);
+  w.sync = take(sync_layout(m).words * 4);
   w.total = off;
   return w;
 }

@@ -5,8 +5,9 @@
 // (256 threads) when the block count is small enough, which saves a launch.
 //
 // 1. Each head's normaliser Z_m (Eq. 9) is the log-sum-exp of the 64-block
-//    tile partials of the score pass (fp64); wavefront w handles heads w,
-//    w + NW, ... and leaves the tile weights exp(M_tile,m - Z_m) in LDS.
+//    tile partials of the score pass; wavefront w handles heads w, w + NW, ...
+//    and leaves the tile weights exp(M_tile,m - Z_m) in LDS (computed as
+//    exp(M_tile,m - max) / sum, fp64 sum).
 // 2. score(i) = sum_m e_m(i) exp(M_tile(i),m - Z_m), fp64 accumulation,
 //    rounded to an fp32 key (scores are positive, so the bit patterns order
 //    like the values; +1 keeps every candidate above the excluded 0). Thread
@@ -18,7 +19,10 @@
 //    bin holding the kp-th key is taken whole.
 // 4. Keys above the threshold, the first `need` keys equal to it (ties go to
 //    the lower block id) and the forced blocks (first n_sink, last n_local)
-//    are written in ascending block order after one block-wide prefix sum.
+//    are placed in ascending block order by one block-wide prefix sum,
+//    staged in LDS and written out by the first k threads.
+// The per-key logic is written with bitwise tests and selects: with one
+// wavefront per SIMD, branch and exec-mask bookkeeping would dominate.
 #pragma once
 
 #include "spla_device.h"
@@ -46,18 +50,18 @@ __device__ __forceinline__ uint32_t block_excl_scan_u32(uint32_t v, uint32_t* ld
 }
 
 // R consecutive floats from a 4R-byte aligned address (zeros when !ok).
-template <int R>
+template <int R, bool CO>
 __device__ __forceinline__ void load_run(const float* p, bool ok, float (&out)[R]) {
   if constexpr (R == 1) {
-    out[0] = ok ? p[0] : 0.f;
+    out[0] = ok ? Mem<CO>::ld(p) : 0.f;
   } else if constexpr (R == 2) {
-    const float2 v = ok ? *reinterpret_cast<const float2*>(p) : make_float2(0.f, 0.f);
+    const float2 v = ok ? Mem<CO>::ld2(p) : make_float2(0.f, 0.f);
     out[0] = v.x;
     out[1] = v.y;
   } else {
 #pragma unroll
     for (int j = 0; j < R / 4; ++j) {
-      const float4 v = ok ? reinterpret_cast<const float4*>(p)[j] : make_float4(0.f, 0.f, 0.f, 0.f);
+      const float4 v = ok ? Mem<CO>::ld4(p + 4 * j) : make_float4(0.f, 0.f, 0.f, 0.f);
       out[4 * j] = v.x;
       out[4 * j + 1] = v.y;
       out[4 * j + 2] = v.z;
@@ -109,12 +113,14 @@ __device__ __forceinline__ RadixPick radix_pick(const uint32_t* hist, uint32_t n
 }
 
 // LDS of one selection: tile weights [tile][head] (SWN >= n_tiles * G), the
-// digit histograms (2048 + 1024 + 1024 bins) and the scan totals.
+// digit histograms (2048 + 1024 + 1024 bins), the scan totals and the
+// staging of the output (k slots, then one spare slot per thread).
 template <int NT, int SWN>
 struct SelectSmem {
   float sw[SWN];
   __align__(16) uint32_t hist[4096];
   uint32_t scan[NT / 64];
+  int32_t out[SPLA_MAX_TOP_K + NT];
 };
 
 // The selection of sequence x KV head bh by the NT threads of a workgroup,
@@ -122,8 +128,12 @@ struct SelectSmem {
 // Writes sel[0 .. k) (ascending block ids, -1 padded), meta4 = (selected,
 // all selected, length, candidates) and, if so is not NULL, the ids to so as
 // well. sel, meta4 and so may point to global memory or to LDS; the caller
-// synchronises before reading them.
-template <int NT, int R, int SWN>
+// synchronises before reading them. CO: e_vals and tile_part are read, and
+// sel and meta4 (then global) written, with Mem<true> (another workgroup of
+// the same launch produced / consumes them). SEL_OFF is added to every id
+// written to sel (not to so): with SEL_OFF = 2 an entry is never 0, so a
+// consumer can poll sel itself for the selection (meta4 may then be NULL).
+template <int NT, int R, int SWN, bool CO, int SEL_OFF = 0>
 __device__ void select_blocks(const Dims& m, int bh, const int32_t* __restrict__ seq_lens,
                               const float* __restrict__ e_vals,
                               const double* __restrict__ tile_part, SelectSmem<NT, SWN>& sm,
@@ -143,31 +153,31 @@ __device__ void select_blocks(const Dims& m, int bh, const int32_t* __restrict__
   const float* ev = e_vals + (int64_t)bh * G * nbp + i0;
 
   // --- loads that need no sequence length go out first
-  const int L = seq_lens[b];
+  const int L = min(max(seq_lens[b], 0), m.cap);  // a length past the capacity is clipped
   double tm[TJ], ts[TJ];
 #pragma unroll
   for (int j = 0; j < TJ; ++j) {
     const int t = lane + 64 * j;
     const bool ok = w < G && t < m.n_tiles;
-    tm[j] = ok ? tp[(t * G + w) * 2] : -INFINITY;
-    ts[j] = ok ? tp[(t * G + w) * 2 + 1] : 0.0;
+    tm[j] = ok ? Mem<CO>::ld(tp + (t * G + w) * 2) : -INFINITY;
+    ts[j] = ok ? Mem<CO>::ld(tp + (t * G + w) * 2 + 1) : 0.0;
   }
   float e[HC][R];  // nbp is a multiple of 64 >= R: a thread's run is all in or all out
 #pragma unroll
-  for (int h = 0; h < HC; ++h) load_run<R>(ev + (int64_t)h * nbp, h < G && i0 < nbp, e[h]);
+  for (int h = 0; h < HC; ++h) load_run<R, CO>(ev + (int64_t)h * nbp, h < G && i0 < nbp, e[h]);
 
   const int nb = (L + m.B - 1) / m.B;
   if (nb <= k) {  // L == 0 included: nothing or everything is selected
     for (int x = tid; x < k; x += NT) {
       const int v = x < nb ? x : -1;
-      sel[x] = v;
+      Mem<CO>::st(sel + x, v + SEL_OFF);
       if (so) so[x] = v;
     }
-    if (tid == 0) {
-      meta4[0] = nb;
-      meta4[1] = 1;
-      meta4[2] = L;
-      meta4[3] = 0;
+    if (tid == 0 && meta4) {
+      Mem<CO>::st(meta4 + 0, nb);
+      Mem<CO>::st(meta4 + 1, 1);
+      Mem<CO>::st(meta4 + 2, L);
+      Mem<CO>::st(meta4 + 3, 0);
     }
     return;
   }
@@ -180,8 +190,8 @@ __device__ void select_blocks(const Dims& m, int bh, const int32_t* __restrict__
       for (int j = 0; j < TJ; ++j) {
         const int t = lane + 64 * j;
         const bool ok = t < m.n_tiles;
-        tm[j] = ok ? tp[(t * G + mm) * 2] : -INFINITY;
-        ts[j] = ok ? tp[(t * G + mm) * 2 + 1] : 0.0;
+        tm[j] = ok ? Mem<CO>::ld(tp + (t * G + mm) * 2) : -INFINITY;
+        ts[j] = ok ? Mem<CO>::ld(tp + (t * G + mm) * 2 + 1) : 0.0;
       }
     }
     double mx = -INFINITY;
@@ -189,25 +199,27 @@ __device__ void select_blocks(const Dims& m, int bh, const int32_t* __restrict__
     for (int j = 0; j < TJ; ++j)
       if (lane + 64 * j < n_tu) mx = fmax(mx, tm[j]);
     mx = wave_max_u(mx);
-    // the tile terms exp(M - max) <= 1 are taken in fp32 (the dominant terms
-    // have small arguments, so the sum is good to about 1e-7); the sum and
-    // its log stay fp64
+    // tile weight exp(M - Z) = exp(M - max) / sum_t S_t exp(M_t - max), S_t
+    // being tile t's sum of exp(ell - M_t) (Eq. 9 with Z = max + log sum: no
+    // logarithm is needed). exp(M - max) <= 1 is taken in fp32 from an fp64
+    // hi + lo argument; the sum and the division stay fp64.
+    float et[TJ];
     double s = 0.0;
 #pragma unroll
-    for (int j = 0; j < TJ; ++j)
-      if (lane + 64 * j < n_tu && tm[j] > -INFINITY)
-        s += ts[j] * (double)expf((float)(tm[j] - mx));
+    for (int j = 0; j < TJ; ++j) {
+      const bool on = lane + 64 * j < n_tu && tm[j] > -INFINITY;
+      const double d = on ? tm[j] - mx : 0.0;
+      const float dh = (float)d, dl = (float)(d - (double)dh);
+      const float eh = expf(dh);
+      et[j] = on ? fmaf(eh, dl, eh) : 0.f;
+      s += ts[j] * (double)et[j];
+    }
     s = wave_sum_u(s);
-    const double Z = mx + log(s);
+    const double inv = 1.0 / s;
 #pragma unroll
     for (int j = 0; j < TJ; ++j) {
       const int t = lane + 64 * j;
-      if (t < n_tu) {  // exp(M - Z) in fp32 from an fp64 hi + lo argument
-        const double d = tm[j] - Z;
-        const float dh = (float)d, dl = (float)(d - (double)dh);
-        const float eh = expf(dh);
-        sw[t * G + mm] = tm[j] > -INFINITY ? fmaf(eh, dl, eh) : 0.f;
-      }
+      if (t < n_tu) sw[t * G + mm] = (float)((double)et[j] * inv);
     }
   }
   __syncthreads();
@@ -228,7 +240,7 @@ __device__ void select_blocks(const Dims& m, int bh, const int32_t* __restrict__
       if (h0 > 0) {
 #pragma unroll
         for (int h = 0; h < HC; ++h)
-          load_run<R>(ev + (int64_t)(h0 + h) * nbp, h0 + h < G && i0 < nbp, e[h]);
+          load_run<R, CO>(ev + (int64_t)(h0 + h) * nbp, h0 + h < G && i0 < nbp, e[h]);
       }
 #pragma unroll
       for (int h = 0; h < HC; ++h) {
@@ -239,13 +251,17 @@ __device__ void select_blocks(const Dims& m, int bh, const int32_t* __restrict__
         }
       }
     }
+    // candidates: real blocks that are not forced (bitwise tests: no branches)
 #pragma unroll
     for (int r = 0; r < R; ++r) {
       const int i = i0 + r;
-      key[r] = (i < nb && i >= m.n_sink && i < nb - m.n_local)
-                   ? __float_as_uint((float)sc[r]) + 1u : 0u;
+      const bool cand = (i < nb) & (i >= m.n_sink) & (i < nb - m.n_local);
+      key[r] = cand ? __float_as_uint((float)sc[r]) + 1u : 0u;
     }
-    // --- 3. the kp-th largest key, one digit per barrier
+    // --- 3. the kp-th largest key, one digit per barrier. Every key is added
+    // to its digit's bin (adding 0 when it is not in the running), so the
+    // atomics need no per-lane branches; a wavefront none of whose keys is in
+    // the running skips them.
     uint32_t prefix = 0u, need = (uint32_t)kp;
 #pragma unroll
     for (int rd = 0; rd < 3; ++rd) {
@@ -253,9 +269,10 @@ __device__ void select_blocks(const Dims& m, int bh, const int32_t* __restrict__
       const uint32_t msk = rd == 0 ? 0x7FFu : 0x3FFu;
       uint32_t* H = hist + (rd == 0 ? 0 : 1024 + 1024 * rd);
 #pragma unroll
-      for (int r = 0; r < R; ++r)
-        if (key[r] != 0u && (rd == 0 || (key[r] >> (sh + 10)) == prefix))
-          atomicAdd(&H[(key[r] >> sh) & msk], 1u);
+      for (int r = 0; r < R; ++r) {
+        const bool in = (key[r] != 0u) & ((rd == 0) | ((key[r] >> (sh + 10)) == prefix));
+        if (__ballot(in) != 0ull) atomicAdd(&H[(key[r] >> sh) & msk], in ? 1u : 0u);
+      }
       __syncthreads();
       const RadixPick p = rd == 0 ? radix_pick<32>(H, need) : radix_pick<16>(H, need);
       if (rd == 0 && p.total < need) {  // fewer candidates than kp: take all
@@ -277,49 +294,45 @@ __device__ void select_blocks(const Dims& m, int bh, const int32_t* __restrict__
     }
   }
 
-  // --- 4. ascending output: (taken above/forced) | (ties) << 16, one scan
+  // --- 4. ascending output: (taken above/forced) | (ties) << 16, one scan;
+  // every thread writes its taken ids to their slots in LDS (ids not taken go
+  // to the thread's spare slot), then the first k threads copy the k slots out
+  bool tk[R], tq[R];
   uint32_t na = 0u, ne = 0u;
 #pragma unroll
   for (int r = 0; r < R; ++r) {
     const int i = i0 + r;
-    const bool forced = i < nb && (i < m.n_sink || i >= nb - m.n_local);
-    const bool g = forced || (key[r] != 0u && key[r] > gt);
-    na += g ? 1u : 0u;
-    ne += (!g && eq_need > 0u && key[r] == eqv) ? 1u : 0u;
+    const bool forced = (i < nb) & ((i < m.n_sink) | (i >= nb - m.n_local));
+    tk[r] = forced | ((key[r] != 0u) & (key[r] > gt));
+    tq[r] = !tk[r] & (eq_need > 0u) & (key[r] == eqv);
+    na += tk[r] ? 1u : 0u;
+    ne += tq[r] ? 1u : 0u;
   }
   uint32_t tot_p;
   const uint32_t before = block_excl_scan_u32<NW>(na | (ne << 16), sm.scan, &tot_p);
   uint32_t a_run = before & 0xFFFFu, e_run = before >> 16;
 #pragma unroll
   for (int r = 0; r < R; ++r) {
-    const int i = i0 + r;
-    const bool forced = i < nb && (i < m.n_sink || i >= nb - m.n_local);
-    const bool g = forced || (key[r] != 0u && key[r] > gt);
-    const bool q = !g && eq_need > 0u && key[r] == eqv;
-    int pos = -1;
-    if (g) {
-      pos = (int)(a_run + (e_run < eq_need ? e_run : eq_need));
-      ++a_run;
-    } else if (q) {
-      if (e_run < eq_need) pos = (int)(a_run + e_run);
-      ++e_run;
-    }
-    if (pos >= 0 && pos < k) {
-      sel[pos] = i;
-      if (so) so[pos] = i;
-    }
+    const uint32_t pg = a_run + (e_run < eq_need ? e_run : eq_need);
+    const uint32_t pq = e_run < eq_need ? a_run + e_run : 0xFFFFFFFFu;
+    const uint32_t pos = tk[r] ? pg : (tq[r] ? pq : 0xFFFFFFFFu);
+    a_run += tk[r] ? 1u : 0u;
+    e_run += tq[r] ? 1u : 0u;
+    sm.out[pos < (uint32_t)k ? (int)pos : SPLA_MAX_TOP_K + tid] = i0 + r;
   }
   const uint32_t ta = tot_p & 0xFFFFu, te = tot_p >> 16;
   const int tot = (int)(ta + (te < eq_need ? te : eq_need));
-  if (tid == 0) {
-    meta4[0] = tot < k ? tot : k;
-    meta4[1] = 0;
-    meta4[2] = L;
-    meta4[3] = tot;
+  __syncthreads();
+  for (int x = tid; x < k; x += NT) {
+    const int v = x < tot ? sm.out[x] : -1;
+    Mem<CO>::st(sel + x, v + SEL_OFF);
+    if (so) so[x] = v;
   }
-  for (int x = tot + tid; x < k; x += NT) {
-    sel[x] = -1;
-    if (so) so[x] = -1;
+  if (tid == 0 && meta4) {
+    Mem<CO>::st(meta4 + 0, tot < k ? tot : k);
+    Mem<CO>::st(meta4 + 1, 0);
+    Mem<CO>::st(meta4 + 2, L);
+    Mem<CO>::st(meta4 + 3, tot);
   }
 }
 

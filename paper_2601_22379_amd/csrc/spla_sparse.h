@@ -1,0 +1,468 @@
+// The fused pass over the selected blocks and the merge (Secs. 2.2, 3.2,
+// 3.3), as device functions shared by the separate sparse / merge kernels and
+// the single-launch decode kernel.
+//
+// Every selected block is read from HBM once. From that read the pass
+// accumulates, for each of the G query heads of the KV head,
+//   - the exact branch of Eq. (5): online max m, normaliser l and
+//     acc = sum_t exp(s q.k_t - m) v_t over the selected tokens, and
+//   - the selected-token linear term of Eq. (16):
+//     accw = sum_t <phi(q), phi(k_t)> v_t and zw = sum_t <phi(q), phi(k_t)>,
+//     phi being the softmax over the feature dimension.
+// The global linear term o_bar = phi(q) S_bar and <phi(q), z_bar> (Eq. 15) is
+// split over the same workgroups by rows of S_bar: workgroup x of the n_wg of
+// a (sequence, KV head) owns rows x*RW .. x*RW + RW - 1 (RW = ceil(d / n_wg)),
+// loads them at its start next to the key / value loads, and subtracts its
+// selected-token terms from its share, so each record carries
+// (m, l, zq_x - zw, acc, obar_x - accw). The merge combines the records: the
+// sum of the last fields is the residual numerator o_bar - o_tilde of
+// Eq. (14) (and its normaliser <phi(q), z_bar> - z_tilde); the residual is
+// exactly 0 when every token is selected. It writes
+// out = o_sparse + gamma * r / sqrt(mean(r^2) + eps) (Sec. 3.3).
+//
+// The matrix-core pass (bf16, G <= 8) runs one 32-token step of one selected
+// block per wavefront on v_mfma_f32_16x16x32_bf16; the workgroup's four
+// wavefronts take consecutive steps.
+#pragma once
+
+#include "spla_device.h"
+
+namespace spla {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+constexpr float kLog2e = 1.4426950408889634f;
+
+// Rows of S_bar owned by workgroup x of n_wg: row0 .. row0 + nrows - 1.
+__device__ __forceinline__ void lin_rows(int D, int x, int n_wg, int* row0, int* nrows) {
+  const int rw = (D + n_wg - 1) / n_wg;
+  const int r0 = x * rw;
+  *row0 = r0;
+  *nrows = r0 >= D ? 0 : (D - r0 < rw ? D - r0 : rw);
+}
+
+// ------------------------------------------------------------------ merge
+template <int E, bool CO>
+__device__ __forceinline__ void load_vec(const float* p, float (&v)[E]) {
+  if constexpr (E == 2) {
+    const float2 x = Mem<CO>::ld2(p);
+    v[0] = x.x;
+    v[1] = x.y;
+  } else {
+#pragma unroll
+    for (int e = 0; e < E; ++e) v[e] = Mem<CO>::ld(p + e);
+  }
+}
+
+// Combines the n_rec records `rec` of sequence x KV head bh for query head g
+// of the group and writes its output row; one wavefront, lane l owning the E
+// adjacent coordinates E l .. E l + E - 1. The record headers of a batch of
+// 64 records are read one record per lane; every load of a batch (and the
+// gain row) is issued before any arithmetic. CO: the records are read with
+// Mem<true> (written by other workgroups of the same launch).
+template <typename T, int D, bool CO>
+__device__ __forceinline__ void merge_head(const Dims& m, float eps, uint32_t flags,
+                                           const float* __restrict__ gamma, int all_sel, int L,
+                                           const float* rec, int n_rec, int stride,
+                                           T* __restrict__ out, int bh, int g) {
+  constexpr int E = D / 64;  // coordinates per lane
+  constexpr int NB = 16;     // record bodies per load batch
+  const int b = bh / m.hkv, h = bh % m.hkv;
+  const int G = m.group;
+  const int lane = threadIdx.x & 63;
+  const int c0 = E * lane;
+  const int64_t orow = ((int64_t)b * m.hq + h * G + g) * D + c0;
+  const bool rla = !(flags & SPLA_FLAG_NO_RLA);
+  float gm[E];
+  load_vec<E, false>(gamma + (int64_t)(h * G + g) * D + c0, gm);
+  float M = -INFINITY, l = 0.f, zt = 0.f;
+  float osp[E], ot[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) osp[e] = ot[e] = 0.f;
+  for (int x0 = 0; x0 < n_rec; x0 += 64) {
+    // headers: lane u holds record x0 + u
+    const bool hv = x0 + lane < n_rec;
+    const float* hr = rec + (int64_t)(hv ? x0 + lane : 0) * stride;
+    const float hm = hv ? Mem<CO>::ld(hr + g) : -INFINITY;
+    const float hl = hv ? Mem<CO>::ld(hr + 16 + g) : 0.f;
+    const float hz = hv ? Mem<CO>::ld(hr + 32 + g) : 0.f;
+    const int nb_here = n_rec - x0 < 64 ? n_rec - x0 : 64;
+    // bodies, NB at a time (the first batch is issued with the headers)
+    for (int u0 = 0; u0 < nb_here; u0 += NB) {
+      float a[NB][E], aw[NB][E];
+#pragma unroll
+      for (int u = 0; u < NB; ++u) {
+        const int x = x0 + u0 + u < n_rec ? x0 + u0 + u : 0;
+        load_vec<E, CO>(rec + (int64_t)x * stride + kPartHead + g * D + c0, a[u]);
+        load_vec<E, CO>(rec + (int64_t)x * stride + kPartHead + (G + g) * D + c0, aw[u]);
+      }
+      if (u0 == 0) {  // fold this batch of headers into the running max
+        const float bm = fmaxf(M, wave_max(hm));
+        const float alpha = M == -INFINITY ? 0.f : __expf(M - bm);
+        l *= alpha;
+#pragma unroll
+        for (int e = 0; e < E; ++e) osp[e] *= alpha;
+        M = bm;
+        l += wave_sum(hm == -INFINITY ? 0.f : hl * __expf(hm - M));
+        zt += wave_sum(hz);
+      }
+      const float sc_l = hm == -INFINITY ? 0.f : __expf(hm - M);  // lane u: record x0 + u
+#pragma unroll
+      for (int u = 0; u < NB; ++u) {
+        const bool ok = u0 + u < nb_here;
+        const float sc = ok ? __shfl(sc_l, u0 + u, 64) : 0.f;
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          osp[e] = fmaf(a[u][e], sc, osp[e]);
+          ot[e] += ok ? aw[u][e] : 0.f;
+        }
+      }
+    }
+  }
+  float o[E];
+  if (L == 0) {
+#pragma unroll
+    for (int e = 0; e < E; ++e) o[e] = 0.f;
+  } else {
+    // residual r = o_bar - o_tilde (over its normaliser with RLA_NORMALIZE),
+    // exactly 0 when every token was selected; out = o_sparse + gamma r / rms(r)
+    const float den = (flags & SPLA_FLAG_RLA_NORMALIZE) ? zt : 1.f;
+    float rr[E];
+    float ss = 0.f;
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      osp[e] /= l;
+      rr[e] = (rla && !all_sel) ? ot[e] / den : 0.f;
+      ss += rr[e] * rr[e];
+    }
+    ss = wave_sum(ss);
+    const float inv = 1.0f / sqrtf(ss / D + eps);
+#pragma unroll
+    for (int e = 0; e < E; ++e) o[e] = rla ? fmaf(gm[e] * rr[e], inv, osp[e]) : osp[e];
+  }
+#pragma unroll
+  for (int e = 0; e < E; ++e) Elem<T>::store(out, orow + e, o[e]);
+}
+
+// ------------------------------------------------------ matrix-core pass
+constexpr int kSparsePre = 8;  // S_bar entries per thread loaded up front
+
+// LDS of one sparse workgroup.
+template <int D>
+struct SparseSmem {
+  float o[kSparseWaves][D][17];
+  float m[kSparseWaves][16], l[kSparseWaves][16];
+  float phq[8][D];                 // phi(q) of the group's heads
+  float S[kSparsePre * 256];       // this workgroup's rows of S_bar
+  float zb[D];
+};
+
+// What a workgroup loads before it knows its blocks: the B operands of its
+// products and its rows of S_bar and z_bar.
+template <int D>
+struct SparseRegs {
+  bf16x8 qb[D / 32], pqh[D / 32], pql[D / 32];
+  float spre[kSparsePre];
+  float zbv;
+  int row0, nrows;
+};
+
+// With g = lane / 16 and j = lane % 16 (the MFMA column), the B operands of
+// the first product hold coordinates 32 ks + 8 g .. +7 of head j (columns
+// 0..7: q itself, for the exact-branch logits) or of head j - 8 (columns
+// 8..15: phi(q) as a bf16 hi + lo pair, for the linear weights); absent heads
+// are zero. The four lanes of a column (g = 0..3) hold all d coordinates of
+// its head, so the softmax of phi(q) needs only the two lane swaps. Also
+// issues the loads of this workgroup's rows of S_bar and z_bar (x of n_wg).
+template <int D>
+__device__ __forceinline__ void sparse_prologue(const Dims& m, const bf16_t* __restrict__ q,
+                                                const float* __restrict__ S,
+                                                const float* __restrict__ zbar, int bh, int x,
+                                                int n_wg, SparseRegs<D>& r) {
+  constexpr int KS = D / 32;
+  const int b = bh / m.hkv, h = bh % m.hkv;
+  const int G = m.group;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int j = lane & 15, g = lane >> 4;
+  const bool exact_col = j < 8;
+  const int head = exact_col ? j : j - 8;
+  const bool live = head < G;
+  const bf16_t* qrow = q + ((int64_t)b * m.hq + h * G + (live ? head : 0)) * D + 8 * g;
+  uint4 raw[KS];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) raw[ks] = *reinterpret_cast<const uint4*>(qrow + 32 * ks);
+  lin_rows(D, x, n_wg, &r.row0, &r.nrows);
+  {
+    const bool s_pre = r.nrows * D <= kSparsePre * 256;
+    const float* Sb = S + ((int64_t)bh * D + r.row0) * D;
+#pragma unroll
+    for (int u = 0; u < kSparsePre; ++u) {
+      const int e = tid + 256 * u;
+      r.spre[u] = (s_pre && e < r.nrows * D) ? Sb[e] : 0.f;
+    }
+  }
+  r.zbv = tid < r.nrows ? zbar[(int64_t)bh * D + r.row0 + tid] : 0.f;
+  // phi(q) of this lane's head (every lane computes it; columns 0..7 discard it)
+  float xv[KS][8];
+  float mx = -INFINITY;
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) {
+    const bf16x8 v = __builtin_bit_cast(bf16x8, raw[ks]);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      xv[ks][e] = (float)v[e];
+      mx = fmaxf(mx, xv[ks][e]);
+    }
+  }
+  mx = fmaxf(mx, xor16(mx));
+  mx = fmaxf(mx, xor32(mx));
+  float sum = 0.f;
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      xv[ks][e] = __expf(xv[ks][e] - mx);
+      sum += xv[ks][e];
+    }
+  sum += xor16(sum);
+  sum += xor32(sum);
+  const float inv = 1.0f / sum;
+  const bf16x8 zero = __builtin_bit_cast(bf16x8, make_uint4(0u, 0u, 0u, 0u));
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) {
+    bf16x8 hi8, lo8;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float pq = xv[ks][e] * inv;
+      const __bf16 hi = (__bf16)pq;
+      hi8[e] = hi;
+      lo8[e] = (__bf16)(pq - (float)hi);
+    }
+    r.qb[ks] = (exact_col && live) ? __builtin_bit_cast(bf16x8, raw[ks]) : zero;
+    r.pqh[ks] = (!exact_col && live) ? hi8 : zero;
+    r.pql[ks] = (!exact_col && live) ? lo8 : zero;
+  }
+}
+
+// Selected block of this wavefront's step: entry p of the selection, where
+// workgroup x's wavefront w takes step 4 x + w and a block has BLK / 32 steps.
+template <int BLK>
+__device__ __forceinline__ int sparse_step_entry(int x) {
+  return (x * kSparseWaves + (int)(threadIdx.x >> 6)) / (BLK / 32);
+}
+
+// One 32-token step of one selected block per wavefront, then the record of
+// workgroup x (of n_wg) of sequence x KV head bh. blk_sel: this wavefront's
+// block (entry sparse_step_entry of the selection; -1 for none); L: the
+// sequence length. For the two 16-row tiles of a step the key row loaded by
+// lane l is token 8 (i / 4) + 4 tile + (i % 4), i = l % 16, so that after
+// S = K [Q | phi(Q)]^T the accumulator rows held by lane l are exactly the
+// tokens 8 g .. 8 g + 7 of the step, in order - the layout the second product
+// needs for its B operand. Columns 0..7 carry the exact-branch logits of heads
+// 0..G-1, columns 8..15 the linear weights <phi(q), phi(k)> of the same heads;
+// one accumulator holds both. phi(k) and the probabilities enter the products
+// as bf16 hi + lo pairs (about 16 mantissa bits); accumulation is fp32. CO:
+// the record is written with Mem<true> (merged by another workgroup of the
+// same launch).
+template <int D, int BLK, bool CO>
+__device__ __forceinline__ void sparse_body(const Dims& m, float s,
+                                            const bf16_t* __restrict__ kc,
+                                            const bf16_t* __restrict__ vc,
+                                            const float* __restrict__ S, int blk_sel, int L,
+                                            int bh, int x, int n_wg,
+                                            const SparseRegs<D>& r, SparseSmem<D>& sm,
+                                            float* __restrict__ part, int stride) {
+  constexpr int KS = D / 32;     // k-steps of the first product
+  constexpr int MT = D / 16;     // coordinate tiles of the second product
+  constexpr int CPB = BLK / 32;  // steps per block
+  const int G = m.group;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int j = lane & 15, g = lane >> 4, i = lane & 15;
+  const int ch = (x * kSparseWaves + w) % CPB;
+  const bool exact_col = j < 8;
+  const int head = exact_col ? j : j - 8;
+  const bool live = head < G;
+  L = min(max(L, 0), m.cap);
+  const int nb = (L + BLK - 1) / BLK;
+  int n_valid = 0;  // tokens of this step that exist
+  bf16x8 ka[2][KS];
+  bf16x8 va[MT];
+  if (blk_sel >= 0 && nb > 0) {
+    const int blk = blk_sel >= nb ? nb - 1 : blk_sel;
+    n_valid = min(32, block_count(L, BLK, blk) - ch * 32);
+    if (n_valid > 0) {
+      const bf16_t* kblk = kc + ((int64_t)bh * m.cap + (int64_t)blk * BLK + ch * 32) * D;
+      const bf16_t* vblk = vc + ((int64_t)bh * m.nb_cap + blk) * D * BLK + ch * 32;
+#pragma unroll
+      for (int mt = 0; mt < 2; ++mt) {
+        const int row = 8 * (i >> 2) + 4 * mt + (i & 3);
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+          ka[mt][ks] = *reinterpret_cast<const bf16x8*>(kblk + (int64_t)row * D + 32 * ks + 8 * g);
+      }
+#pragma unroll
+      for (int t = 0; t < MT; ++t)
+        va[t] = *reinterpret_cast<const bf16x8*>(vblk + (int64_t)(16 * t + i) * BLK + 8 * g);
+    }
+  }
+  floatx4 acc_o[MT];
+#pragma unroll
+  for (int t = 0; t < MT; ++t) acc_o[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+  float m_run = -INFINITY, l_run = 0.f;  // exact columns: max / sum; linear columns: sum
+  // wavefront 0 leaves phi(q) (hi + lo) in LDS for the global linear term
+  if (w == 0 && !exact_col && live) {
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        sm.phq[head][32 * ks + 8 * g + e] = (float)r.pqh[ks][e] + (float)r.pql[ks][e];
+  }
+  if (n_valid > 0) {
+    floatx4 sw[2];
+    float zinv[2];  // 1 / sum exp(k - max k) of this lane's key row, per tile
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt) {
+      sw[mt] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks)
+        sw[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[mt][ks], r.qb[ks], sw[mt], 0, 0, 0);
+      // exp(k - max k) of this lane's key row (row i of the tile), spread over
+      // lanes i + 16 g'; the 1 / sum of phi(k) is applied to the result rows
+      float kx[KS][8];
+      float mx = -INFINITY;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          kx[ks][e] = (float)ka[mt][ks][e];
+          mx = fmaxf(mx, kx[ks][e]);
+        }
+      mx = fmaxf(mx, xor16(mx));
+      mx = fmaxf(mx, xor32(mx));
+      const float mxl = mx * kLog2e;
+      float sum = 0.f;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          kx[ks][e] = __builtin_amdgcn_exp2f(fmaf(kx[ks][e], kLog2e, -mxl));
+          sum += kx[ks][e];
+        }
+      sum += xor16(sum);
+      sum += xor32(sum);
+      zinv[mt] = 1.0f / sum;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        bf16x8 fh, fl;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float f = kx[ks][e];
+          const __bf16 hi = (__bf16)f;
+          fh[e] = hi;
+          fl[e] = (__bf16)(f - (float)hi);
+        }
+        sw[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fh, r.pqh[ks], sw[mt], 0, 0, 0);
+        sw[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fh, r.pql[ks], sw[mt], 0, 0, 0);
+        sw[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fl, r.pqh[ks], sw[mt], 0, 0, 0);
+      }
+    }
+    // tokens 8g .. 8g+7 of this step: tile 0 rows 4g..4g+3, tile 1 rows 4g..4g+3
+    // (result row 4g + r of tile t is token 8g + 4t + r; its 1 / Z sits in
+    // lane 4g + r)
+    float val[8];
+    float cmax = -INFINITY;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const bool ok = 8 * g + e < n_valid;
+      const float zi = __shfl(zinv[e >> 2], 4 * g + (e & 3), kWave);
+      const float xx = sw[e >> 2][e & 3];
+      val[e] = exact_col ? (ok ? xx * s : -INFINITY) : (ok ? xx * zi : 0.f);
+      cmax = fmaxf(cmax, val[e]);
+    }
+    cmax = fmaxf(cmax, xor16(cmax));
+    cmax = fmaxf(cmax, xor32(cmax));
+    float psum = 0.f;
+    bf16x8 bh8, bl8;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float pv = exact_col ? __builtin_amdgcn_exp2f((val[e] - cmax) * kLog2e) : val[e];
+      psum += pv;
+      const __bf16 hi = (__bf16)pv;
+      bh8[e] = hi;
+      bl8[e] = (__bf16)(pv - (float)hi);
+    }
+    psum += xor16(psum);
+    psum += xor32(psum);
+    m_run = exact_col ? cmax : -INFINITY;
+    l_run = psum;
+    if (n_valid < 32) {  // rows past the sequence end may hold anything: zero them
+#pragma unroll
+      for (int t = 0; t < MT; ++t)
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if (8 * g + e >= n_valid) va[t][e] = (__bf16)0.f;
+    }
+#pragma unroll
+    for (int t = 0; t < MT; ++t) {
+      acc_o[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va[t], bh8, acc_o[t], 0, 0, 0);
+      acc_o[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va[t], bl8, acc_o[t], 0, 0, 0);
+    }
+  }
+  // ---- merge the four wavefronts of the workgroup into one record
+#pragma unroll
+  for (int t = 0; t < MT; ++t)
+#pragma unroll
+    for (int rr = 0; rr < 4; ++rr) sm.o[w][16 * t + 4 * g + rr][j] = acc_o[t][rr];
+  if (lane < 16) {
+    sm.m[w][lane] = m_run;
+    sm.l[w][lane] = l_run;
+  }
+#pragma unroll
+  for (int u = 0; u < kSparsePre; ++u) sm.S[tid + 256 * u] = r.spre[u];
+  if (tid < D) sm.zb[tid] = r.zbv;
+  __syncthreads();
+  const int row0 = r.row0, nrows = r.nrows;
+  const bool s_pre = nrows * D <= kSparsePre * 256;
+  float* rec = part + ((int64_t)bh * n_wg + x) * stride;
+  for (int e = tid; e < G * D; e += 256) {
+    const int hh = e / D, c = e % D;
+    float M = -INFINITY;
+#pragma unroll
+    for (int xx = 0; xx < kSparseWaves; ++xx) M = fmaxf(M, sm.m[xx][hh]);
+    float a = 0.f, aw = 0.f;
+#pragma unroll
+    for (int xx = 0; xx < kSparseWaves; ++xx) {
+      const float sc = sm.m[xx][hh] == -INFINITY ? 0.f : __expf(sm.m[xx][hh] - M);
+      a = fmaf(sm.o[xx][c][hh], sc, a);
+      aw += sm.o[xx][c][8 + hh];
+    }
+    float ob = 0.f;  // this workgroup's rows of phi(q) S_bar
+    if (s_pre) {
+      for (int rr = 0; rr < nrows; ++rr) ob = fmaf(sm.phq[hh][row0 + rr], sm.S[rr * D + c], ob);
+    } else {
+      const float* Sb = S + (int64_t)bh * D * D;
+      for (int rr = row0; rr < row0 + nrows; ++rr) ob = fmaf(sm.phq[hh][rr], Sb[rr * D + c], ob);
+    }
+    Mem<CO>::st(rec + kPartHead + hh * D + c, a);
+    Mem<CO>::st(rec + kPartHead + (G + hh) * D + c, ob - aw);
+  }
+  if (tid < G) {
+    float M = -INFINITY;
+#pragma unroll
+    for (int xx = 0; xx < kSparseWaves; ++xx) M = fmaxf(M, sm.m[xx][tid]);
+    float l = 0.f, zw = 0.f;
+#pragma unroll
+    for (int xx = 0; xx < kSparseWaves; ++xx) {
+      l += sm.m[xx][tid] == -INFINITY ? 0.f : sm.l[xx][tid] * __expf(sm.m[xx][tid] - M);
+      zw += sm.l[xx][8 + tid];
+    }
+    float zq = 0.f;
+    for (int rr = 0; rr < nrows; ++rr) zq = fmaf(sm.phq[tid][row0 + rr], sm.zb[rr], zq);
+    Mem<CO>::st(rec + tid, M);
+    Mem<CO>::st(rec + 16 + tid, l);
+    Mem<CO>::st(rec + 32 + tid, zq - zw);
+  }
+}
+
+}  // namespace spla

@@ -20,10 +20,10 @@ LIB_PATH = os.path.join(_HERE, "libspla.so")
 HOST_LIB_PATH = os.path.join(_HERE, "libspla_host.so")
 
 F32, BF16 = 0, 1
-FLAG_NO_RLA, FLAG_FIRST_ORDER, FLAG_RLA_NORMALIZE = 1, 2, 4
-DEVERR_CAPACITY = 1
+FLAG_NO_RLA, FLAG_FIRST_ORDER, FLAG_RLA_NORMALIZE, FLAG_SEPARATE_KERNELS = 1, 2, 4, 8
+DEVERR_CAPACITY, DEVERR_SYNC = 1, 2
 MAX_GROUP, MAX_TOP_K, MAX_BLOCKS, WORKSPACE_ALIGN = 16, 256, 32768, 256
-PHASES = {"append": 0, "score": 1, "select": 2, "sparse": 3, "merge": 4}
+PHASES = {"append": 0, "score": 1, "select": 2, "sparse": 3, "merge": 4, "decode": 5}
 NUM_PHASES = 8
 STATUS = {0: "ok", -1: "invalid argument", -2: "unsupported shape",
           -3: "capacity or library limit exceeded", -4: "workspace missing, too small or misaligned",
@@ -31,9 +31,10 @@ STATUS = {0: "ok", -1: "invalid argument", -2: "unsupported shape",
 
 # every symbol include/spla.h declares
 EXPORTS = ["spla_status_string", "spla_phase_name", "spla_validate", "spla_cache_bytes",
-           "spla_workspace_bytes", "spla_append_workspace_bytes", "spla_reset", "spla_append",
+           "spla_workspace_bytes", "spla_append_workspace_bytes", "spla_decode_phase_mask",
+           "spla_workspace_init", "spla_reset", "spla_append",
            "spla_decode", "spla_decode_ex", "spla_step", "spla_step_ex"]
-HOST_EXPORTS = EXPORTS[:6]
+HOST_EXPORTS = EXPORTS[:7]
 
 
 class SplaError(RuntimeError):
@@ -75,8 +76,12 @@ def _declare(lib, host_only=False):
     lib.spla_workspace_bytes.argtypes = [cfgp, POINTER(c_size_t)]
     lib.spla_append_workspace_bytes.restype = c_int32
     lib.spla_append_workspace_bytes.argtypes = [cfgp, c_int32, POINTER(c_size_t)]
+    lib.spla_decode_phase_mask.restype = c_int32
+    lib.spla_decode_phase_mask.argtypes = [cfgp, POINTER(c_uint32)]
     if host_only:
         return lib
+    lib.spla_workspace_init.restype = c_int32
+    lib.spla_workspace_init.argtypes = [cfgp, c_void_p, c_size_t, c_void_p]
     lib.spla_reset.restype = c_int32
     lib.spla_reset.argtypes = [cfgp, cachep, c_void_p]
     lib.spla_append.restype = c_int32
@@ -161,6 +166,14 @@ def append_workspace_bytes(cfg: SplaConfig, max_new: int, library=None) -> int:
     return int(n.value)
 
 
+def decode_phases(cfg: SplaConfig, library=None) -> list:
+    """Names of the phases whose events spla_decode_ex records for cfg."""
+    mask = c_uint32(0)
+    _check((library or lib()).spla_decode_phase_mask(ctypes.byref(cfg), ctypes.byref(mask)),
+           "spla_decode_phase_mask")
+    return [n for n, p in PHASES.items() if mask.value >> p & 1]
+
+
 def torch_dtype(cfg: SplaConfig):
     return torch.float32 if cfg.dtype == F32 else torch.bfloat16
 
@@ -198,6 +211,9 @@ class SplaCache:
         self.seq_lens = torch.zeros(cfg.batch, dtype=torch.int32, device=self.device)
         self.err = torch.zeros(1, dtype=torch.int32, device=self.device)
         self.workspace = _aligned_workspace(workspace_bytes(cfg), self.device)
+        _check(lib().spla_workspace_init(ctypes.byref(cfg), _ptr(self.workspace),
+                                         self.workspace.numel(), _stream(self.device)),
+               "spla_workspace_init")
         self._append_ws = None
         self._struct = SplaCacheStruct(self.k.data_ptr(), self.v.data_ptr(),
                                        self.stats.data_ptr(), self.state.data_ptr(),
@@ -294,7 +310,8 @@ class SplaCache:
                 self.norm.view(c.batch, c.n_kv_heads, c.head_dim))
 
 
-def make_events(phases: Sequence[str] = ("score", "select", "sparse", "merge", "append")):
+def make_events(phases: Sequence[str] = ("score", "select", "sparse", "merge", "decode",
+                                        "append")):
     """torch.cuda.Event pairs for the given phases, and the SplaEvents that
     points at their HIP events. Returns (events_struct, {phase: (start, stop)})."""
     ev = SplaEvents()

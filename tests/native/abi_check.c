@@ -36,7 +36,8 @@ int main(void) {
   c = base(); c.max_seq_len = 64 * 32769; EXPECT(spla_validate(&c), SPLA_ERR_CAPACITY);
   c = base(); c.dtype = 7; EXPECT(spla_validate(&c), SPLA_ERR_INVALID_ARG);
   c = base(); c.rms_eps = -1.0f; EXPECT(spla_validate(&c), SPLA_ERR_INVALID_ARG);
-  c = base(); c.flags = 8; EXPECT(spla_validate(&c), SPLA_ERR_INVALID_ARG);
+  c = base(); c.flags = 16; EXPECT(spla_validate(&c), SPLA_ERR_INVALID_ARG);
+  c = base(); c.flags = SPLA_FLAG_SEPARATE_KERNELS; EXPECT(spla_validate(&c), SPLA_OK);
   c = base(); c.n_sink_blocks = -1; EXPECT(spla_validate(&c), SPLA_ERR_INVALID_ARG);
   c = base(); c.batch = 0; EXPECT(spla_validate(&c), SPLA_ERR_INVALID_ARG);
   c = base();

@@ -136,3 +136,22 @@ def test_header_and_host_code_under_sanitizers(tmp_path):
                          os.path.join(ROOT, "tests", "native", "abi_check.c")],
                         capture_output=True, text=True)
     assert r2.returncode == 0, r2.stderr
+
+
+@pytest.mark.parametrize("libname", ["hip", "host"])
+@pytest.mark.parametrize("kw,single", [
+    ({}, True),                                              # the 128K benchmark shape
+    (dict(n_q_heads=40, n_kv_heads=8), True),                # G = 5
+    (dict(block_size=128, max_seq_len=65536), True),
+    (dict(max_seq_len=64 * 8192), True),                     # largest single-launch block count
+    (dict(max_seq_len=64 * 8193), False),
+    (dict(n_q_heads=64, n_kv_heads=8), False),               # G = 8
+    (dict(head_dim=64), False),
+    (dict(dtype="f32"), False),
+    (dict(flags=spla.FLAG_SEPARATE_KERNELS), False),
+])
+def test_decode_phase_mask(libname, kw, single):
+    lib = spla.lib() if libname == "hip" else spla.host_lib()
+    got = spla.decode_phases(_cfg(**kw), lib)
+    assert got == (["decode"] if single else ["score", "select", "sparse", "merge"])
+
