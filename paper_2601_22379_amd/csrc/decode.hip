@@ -101,15 +101,21 @@ __device__ __forceinline__ bool arrive_last(int32_t* ctr, int n, int* s_flag) {
   return *s_flag != 0;
 }
 
+// Built for three waves per SIMD (at most 168 registers per lane; measured
+// faster than two, and than four with its 128-register budget).
+constexpr int kDecodeWaves = 3;
+
 // R: blocks per thread of the selection (256 R >= blocks per sequence).
 template <int G, int BLK, int R>
-__global__ __launch_bounds__(256) void decode_kernel(FusedArgs a) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(kDecodeWaves, kDecodeWaves)))
+void decode_kernel(FusedArgs a) {
   constexpr int D = 128;
   constexpr int SWN = 4 * R * G;  // tile weights: n_tiles <= 4 R
+  constexpr int GC = G <= 4 ? 4 : (G <= 6 ? 6 : 8);  // accumulator columns per kind
   __shared__ union {
     ScoreSmem<G> sc;
     SelectSmem<256, SWN> se;
-    SparseSmem<D> sp;
+    SparseSmem<D, GC> sp;
   } sm;
   __shared__ int s_flag;
   const Dims& m = a.m;
@@ -135,8 +141,9 @@ __global__ __launch_bounds__(256) void decode_kernel(FusedArgs a) {
   // ------------------------------------------------------------ sparse item
   const int j = (int)blockIdx.x - n_score;
   const int bh = j / a.n_wg, x = j % a.n_wg;
-  SparseRegs<D> r;
-  sparse_prologue<D>(m, a.q, a.S, a.zbar, bh, x, a.n_wg, r);
+  SparseRegs r;
+  sparse_prologue<D, GC>(m, a.q, a.S, a.zbar, bh, x, a.n_wg, r, sm.sp);
+  const int L = min(max(a.seq_lens[bh / m.hkv], 0), m.cap);  // before the wait: not produced here
   // this wavefront's block: poll its selection word (lane 0), then share it
   const int step = sparse_step_entry<BLK>(x);
   int32_t* word = sy + y.sel_ready + (int64_t)bh * m.k + step;
@@ -150,8 +157,7 @@ __global__ __launch_bounds__(256) void decode_kernel(FusedArgs a) {
     if (v == 0) report_sync_error(a);
   }
   const int blk_sel = __builtin_amdgcn_readfirstlane(v) - 2;
-  const int L = min(max(a.seq_lens[bh / m.hkv], 0), m.cap);
-  sparse_body<D, BLK, true>(m, a.s, a.kc, a.vc, a.S, blk_sel, L, bh, x, a.n_wg, r, sm.sp, a.part,
+  sparse_body<D, BLK, true, GC>(m, a.s, a.kc, a.vc, a.S, blk_sel, L, bh, x, a.n_wg, r, sm.sp, a.part,
                             a.stride);
   if (step < m.k && (tid & 63) == 0) store_agent(word, 0);  // read by this workgroup only
   int32_t* recs = sy + y.recs_done + (int64_t)bh * kSyncLine;

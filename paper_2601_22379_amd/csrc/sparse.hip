@@ -206,21 +206,21 @@ __global__ __launch_bounds__(256) void sparse_mfma_kernel(
   __shared__ SelectSmem<256, SWN> ssm;
   __shared__ int32_t s_sel[R > 0 ? SPLA_MAX_TOP_K : 1];
   __shared__ int32_t s_meta[4];
-  __shared__ SparseSmem<D> sm;
+  __shared__ SparseSmem<D, 8> sm;
   const int bh = blockIdx.y;
-  SparseRegs<D> r;
-  sparse_prologue<D>(m, q, S, zbar, bh, (int)blockIdx.x, (int)gridDim.x, r);
+  SparseRegs r;
+  sparse_prologue<D, 8>(m, q, S, zbar, bh, (int)blockIdx.x, (int)gridDim.x, r, sm);
   if constexpr (R > 0) {
     select_blocks<256, R, SWN, false>(m, bh, seq_lens, e_vals, tile_part, ssm, s_sel, s_meta,
                                blockIdx.x == 0 && sel_out ? sel_out + (int64_t)bh * m.k : nullptr);
     __syncthreads();
     if (blockIdx.x == 0 && threadIdx.x < 4) meta[bh * 4 + threadIdx.x] = s_meta[threadIdx.x];
     const int e = sparse_step_entry<BLK>((int)blockIdx.x);
-    sparse_body<D, BLK, false>(m, s, kc, vc, S, e < m.k ? s_sel[e] : -1, s_meta[2], bh, (int)blockIdx.x,
+    sparse_body<D, BLK, false, 8>(m, s, kc, vc, S, e < m.k ? s_sel[e] : -1, s_meta[2], bh, (int)blockIdx.x,
                         (int)gridDim.x, r, sm, part, stride);
   } else {
     const int e = sparse_step_entry<BLK>((int)blockIdx.x);
-    sparse_body<D, BLK, false>(m, s, kc, vc, S, e < m.k ? sel[(int64_t)bh * m.k + e] : -1,
+    sparse_body<D, BLK, false, 8>(m, s, kc, vc, S, e < m.k ? sel[(int64_t)bh * m.k + e] : -1,
                         meta[bh * 4 + 2], bh, (int)blockIdx.x, (int)gridDim.x, r, sm, part,
                         stride);
   }

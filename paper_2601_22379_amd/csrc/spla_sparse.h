@@ -146,23 +146,25 @@ __device__ __forceinline__ void merge_head(const Dims& m, float eps, uint32_t fl
 }
 
 // ------------------------------------------------------ matrix-core pass
-constexpr int kSparsePre = 8;  // S_bar entries per thread loaded up front
+constexpr int kSparsePre = 4;  // S_bar entries per thread loaded up front
 
-// LDS of one sparse workgroup.
-template <int D>
+// LDS of one sparse workgroup for groups of at most GC heads: the B
+// operands of the first products (q, phi(q) hi, phi(q) lo per k-step, in
+// lane order), the four wavefronts' accumulators (exact columns 0 .. GC-1,
+// linear columns GC .. 2 GC-1), phi(q) and this workgroup's rows of S_bar.
+template <int D, int GC>
 struct SparseSmem {
-  float o[kSparseWaves][D][17];
+  uint4 qops[3][D / 32][64];
+  float o[kSparseWaves][D][2 * GC + 1];
   float m[kSparseWaves][16], l[kSparseWaves][16];
-  float phq[8][D];                 // phi(q) of the group's heads
-  float S[kSparsePre * 256];       // this workgroup's rows of S_bar
+  float phq[GC][D];
+  float S[kSparsePre * 256];
   float zb[D];
 };
 
-// What a workgroup loads before it knows its blocks: the B operands of its
-// products and its rows of S_bar and z_bar.
-template <int D>
+// What a workgroup loads before it knows its blocks: its rows of S_bar and
+// z_bar (the query operands go to LDS).
 struct SparseRegs {
-  bf16x8 qb[D / 32], pqh[D / 32], pql[D / 32];
   float spre[kSparsePre];
   float zbv;
   int row0, nrows;
@@ -175,11 +177,11 @@ struct SparseRegs {
 // are zero. The four lanes of a column (g = 0..3) hold all d coordinates of
 // its head, so the softmax of phi(q) needs only the two lane swaps. Also
 // issues the loads of this workgroup's rows of S_bar and z_bar (x of n_wg).
-template <int D>
+template <int D, int GC>
 __device__ __forceinline__ void sparse_prologue(const Dims& m, const bf16_t* __restrict__ q,
                                                 const float* __restrict__ S,
                                                 const float* __restrict__ zbar, int bh, int x,
-                                                int n_wg, SparseRegs<D>& r) {
+                                                int n_wg, SparseRegs& r, SparseSmem<D, GC>& sm) {
   constexpr int KS = D / 32;
   const int b = bh / m.hkv, h = bh % m.hkv;
   const int G = m.group;
@@ -228,20 +230,34 @@ __device__ __forceinline__ void sparse_prologue(const Dims& m, const bf16_t* __r
   sum += xor16(sum);
   sum += xor32(sum);
   const float inv = 1.0f / sum;
-  const bf16x8 zero = __builtin_bit_cast(bf16x8, make_uint4(0u, 0u, 0u, 0u));
+  // wavefront 0 leaves the operands and phi(q) (hi + lo) in LDS; absent
+  // operands are masked to zero (bit masks, not selects between arrays)
+  const bool lin = !exact_col && live;
+  const uint32_t mq = (exact_col && live) ? 0xFFFFFFFFu : 0u, ml = lin ? 0xFFFFFFFFu : 0u;
+  auto masked = [](uint4 v, uint32_t k) { return make_uint4(v.x & k, v.y & k, v.z & k, v.w & k); };
+  if ((tid >> 6) == 0) {
 #pragma unroll
-  for (int ks = 0; ks < KS; ++ks) {
-    bf16x8 hi8, lo8;
+    for (int ks = 0; ks < KS; ++ks) {
+      bf16x8 hi8, lo8;
+      float ph[8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const float pq = xv[ks][e] * inv;
-      const __bf16 hi = (__bf16)pq;
-      hi8[e] = hi;
-      lo8[e] = (__bf16)(pq - (float)hi);
+      for (int e = 0; e < 8; ++e) {
+        const float pq = xv[ks][e] * inv;
+        const __bf16 hi = (__bf16)pq;
+        const __bf16 lo = (__bf16)(pq - (float)hi);
+        hi8[e] = hi;
+        lo8[e] = lo;
+        ph[e] = (float)hi + (float)lo;
+      }
+      sm.qops[0][ks][lane] = masked(raw[ks], mq);
+      sm.qops[1][ks][lane] = masked(__builtin_bit_cast(uint4, hi8), ml);
+      sm.qops[2][ks][lane] = masked(__builtin_bit_cast(uint4, lo8), ml);
+      if (lin) {
+        float4* dst = reinterpret_cast<float4*>(&sm.phq[head][32 * ks + 8 * g]);
+        dst[0] = make_float4(ph[0], ph[1], ph[2], ph[3]);
+        dst[1] = make_float4(ph[4], ph[5], ph[6], ph[7]);
+      }
     }
-    r.qb[ks] = (exact_col && live) ? __builtin_bit_cast(bf16x8, raw[ks]) : zero;
-    r.pqh[ks] = (!exact_col && live) ? hi8 : zero;
-    r.pql[ks] = (!exact_col && live) ? lo8 : zero;
   }
 }
 
@@ -265,14 +281,14 @@ __device__ __forceinline__ int sparse_step_entry(int x) {
 // as bf16 hi + lo pairs (about 16 mantissa bits); accumulation is fp32. CO:
 // the record is written with Mem<true> (merged by another workgroup of the
 // same launch).
-template <int D, int BLK, bool CO>
+template <int D, int BLK, bool CO, int GC>
 __device__ __forceinline__ void sparse_body(const Dims& m, float s,
                                             const bf16_t* __restrict__ kc,
                                             const bf16_t* __restrict__ vc,
                                             const float* __restrict__ S, int blk_sel, int L,
-                                            int bh, int x, int n_wg,
-                                            const SparseRegs<D>& r, SparseSmem<D>& sm,
-                                            float* __restrict__ part, int stride) {
+                                            int bh, int x, int n_wg, const SparseRegs& r,
+                                            SparseSmem<D, GC>& sm, float* __restrict__ part,
+                                            int stride) {
   constexpr int KS = D / 32;     // k-steps of the first product
   constexpr int MT = D / 16;     // coordinate tiles of the second product
   constexpr int CPB = BLK / 32;  // steps per block
@@ -310,14 +326,7 @@ __device__ __forceinline__ void sparse_body(const Dims& m, float s,
 #pragma unroll
   for (int t = 0; t < MT; ++t) acc_o[t] = floatx4{0.f, 0.f, 0.f, 0.f};
   float m_run = -INFINITY, l_run = 0.f;  // exact columns: max / sum; linear columns: sum
-  // wavefront 0 leaves phi(q) (hi + lo) in LDS for the global linear term
-  if (w == 0 && !exact_col && live) {
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
-#pragma unroll
-      for (int e = 0; e < 8; ++e)
-        sm.phq[head][32 * ks + 8 * g + e] = (float)r.pqh[ks][e] + (float)r.pql[ks][e];
-  }
+  __syncthreads();  // the query operands of the prologue are in LDS
   if (n_valid > 0) {
     floatx4 sw[2];
     float zinv[2];  // 1 / sum exp(k - max k) of this lane's key row, per tile
@@ -326,46 +335,40 @@ __device__ __forceinline__ void sparse_body(const Dims& m, float s,
       sw[mt] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks)
-        sw[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[mt][ks], r.qb[ks], sw[mt], 0, 0, 0);
+        sw[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+            ka[mt][ks], __builtin_bit_cast(bf16x8, sm.qops[0][ks][lane]), sw[mt], 0, 0, 0);
       // exp(k - max k) of this lane's key row (row i of the tile), spread over
       // lanes i + 16 g'; the 1 / sum of phi(k) is applied to the result rows
-      float kx[KS][8];
       float mx = -INFINITY;
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          kx[ks][e] = (float)ka[mt][ks][e];
-          mx = fmaxf(mx, kx[ks][e]);
-        }
+        for (int e = 0; e < 8; ++e) mx = fmaxf(mx, (float)ka[mt][ks][e]);
       mx = fmaxf(mx, xor16(mx));
       mx = fmaxf(mx, xor32(mx));
       const float mxl = mx * kLog2e;
+      // exp(k - max k) k-step by k-step, each step straight into its products
       float sum = 0.f;
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          kx[ks][e] = __builtin_amdgcn_exp2f(fmaf(kx[ks][e], kLog2e, -mxl));
-          sum += kx[ks][e];
-        }
-      sum += xor16(sum);
-      sum += xor32(sum);
-      zinv[mt] = 1.0f / sum;
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
         bf16x8 fh, fl;
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          const float f = kx[ks][e];
+          const float f = __builtin_amdgcn_exp2f(fmaf((float)ka[mt][ks][e], kLog2e, -mxl));
+          sum += f;
           const __bf16 hi = (__bf16)f;
           fh[e] = hi;
           fl[e] = (__bf16)(f - (float)hi);
         }
-        sw[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fh, r.pqh[ks], sw[mt], 0, 0, 0);
-        sw[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fh, r.pql[ks], sw[mt], 0, 0, 0);
-        sw[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fl, r.pqh[ks], sw[mt], 0, 0, 0);
+        const bf16x8 ph = __builtin_bit_cast(bf16x8, sm.qops[1][ks][lane]);
+        const bf16x8 pl = __builtin_bit_cast(bf16x8, sm.qops[2][ks][lane]);
+        sw[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fh, ph, sw[mt], 0, 0, 0);
+        sw[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fh, pl, sw[mt], 0, 0, 0);
+        sw[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fl, ph, sw[mt], 0, 0, 0);
       }
+      sum += xor16(sum);
+      sum += xor32(sum);
+      zinv[mt] = 1.0f / sum;
     }
     // tokens 8g .. 8g+7 of this step: tile 0 rows 4g..4g+3, tile 1 rows 4g..4g+3
     // (result row 4g + r of tile t is token 8g + 4t + r; its 1 / Z sits in
@@ -410,10 +413,13 @@ __device__ __forceinline__ void sparse_body(const Dims& m, float s,
     }
   }
   // ---- merge the four wavefronts of the workgroup into one record
+  if (live) {  // only the live columns: exact heads to 0 .., linear heads to GC ..
+    const int cj = exact_col ? head : GC + head;
 #pragma unroll
-  for (int t = 0; t < MT; ++t)
+    for (int t = 0; t < MT; ++t)
 #pragma unroll
-    for (int rr = 0; rr < 4; ++rr) sm.o[w][16 * t + 4 * g + rr][j] = acc_o[t][rr];
+      for (int rr = 0; rr < 4; ++rr) sm.o[w][16 * t + 4 * g + rr][cj] = acc_o[t][rr];
+  }
   if (lane < 16) {
     sm.m[w][lane] = m_run;
     sm.l[w][lane] = l_run;
@@ -435,7 +441,7 @@ __device__ __forceinline__ void sparse_body(const Dims& m, float s,
     for (int xx = 0; xx < kSparseWaves; ++xx) {
       const float sc = sm.m[xx][hh] == -INFINITY ? 0.f : __expf(sm.m[xx][hh] - M);
       a = fmaf(sm.o[xx][c][hh], sc, a);
-      aw += sm.o[xx][c][8 + hh];
+      aw += sm.o[xx][c][GC + hh];
     }
     float ob = 0.f;  // this workgroup's rows of phi(q) S_bar
     if (s_pre) {
