@@ -285,15 +285,19 @@ def main():
     n_q = 3 * K + W + 2 * R + 1
     if appending:
         # per-step inputs generated before timing: token rows and queries
+        # step s appends position lengths[b] - 1 + s // R of each sequence
+        # (each replica advances on its own); one generator call per
+        # (sequence, KV head) covers every step
         kn = np.zeros((n_q, w.batch, w.n_kv_heads, w.head_dim), np.float32)
         vn = np.zeros_like(kn)
-        for s in range(n_q):
-            r = s % R
-            for b in range(w.batch):
-                pos = w.lengths[b] - 1 + s // R
-                for h in range(w.n_kv_heads):
-                    kk, vv = si.gen_kv(w, b, h, pos, pos + 1)
-                    kn[s, b, h], vn[s, b, h] = kk[0], vv[0]
+        n_pos = (n_q - 1) // R + 1
+        steps = np.arange(n_q)
+        for b in range(w.batch):
+            p0 = w.lengths[b] - 1
+            for h in range(w.n_kv_heads):
+                kk, vv = si.gen_kv(w, b, h, p0, p0 + n_pos)
+                kn[:, b, h], vn[:, b, h] = kk[steps // R], vv[steps // R]
+        log(f"generated the tokens of {n_q} appending steps")
         kn_d = torch.from_numpy(kn).to(dt).to(dev)
         vn_d = torch.from_numpy(vn).to(dt).to(dev)
         qs = torch.from_numpy(np.stack([si.gen_q_batch(w, s) for s in range(min(n_q, 64))])).to(

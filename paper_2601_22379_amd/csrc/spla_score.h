@@ -90,34 +90,41 @@ __device__ __forceinline__ void write_table(const QRegs<G, D>& r, double s, floa
   }
 }
 
-// acc (+)= c[lane n of this lane's 16-lane row] * x: the coefficient reaches
+// acc (+)= c[lane N of this lane's 16-lane row] * x: the coefficient reaches
 // every lane of the row through a DPP row broadcast, so the products need no
 // LDS traffic. Callers keep at least two other VALU instructions between two
 // updates of one accumulator and never follow a VALU write of c directly.
-#define SPLA_BC_CASE(n, op)                                                                   \
-  case n:                                                                                     \
-    asm volatile(op " %0, %1, %2 row_newbcast:" #n " row_mask:0xf bank_mask:0xf"              \
-                 : "+v"(acc) : "v"(c), "v"(x));                                               \
-    break;
-#define SPLA_BC_SWITCH(op)                                                                    \
-  switch (n) {                                                                                \
-    SPLA_BC_CASE(0, op) SPLA_BC_CASE(1, op) SPLA_BC_CASE(2, op) SPLA_BC_CASE(3, op)            \
-    SPLA_BC_CASE(4, op) SPLA_BC_CASE(5, op) SPLA_BC_CASE(6, op) SPLA_BC_CASE(7, op)            \
-    SPLA_BC_CASE(8, op) SPLA_BC_CASE(9, op) SPLA_BC_CASE(10, op) SPLA_BC_CASE(11, op)          \
-    SPLA_BC_CASE(12, op) SPLA_BC_CASE(13, op) SPLA_BC_CASE(14, op) SPLA_BC_CASE(15, op)        \
-    default: break;                                                                           \
-  }
-__device__ __forceinline__ void mul_row_bcast(float& acc, float c, float x, int n) {
-  SPLA_BC_SWITCH("v_mul_f32_dpp")
+template <bool FIRST, int N>
+__device__ __forceinline__ void row_bcast_fma(float& acc, float c, float x) {
+  if constexpr (FIRST)
+    asm volatile("v_mul_f32_dpp %0, %1, %2 row_newbcast:%3 row_mask:0xf bank_mask:0xf"
+                 : "=v"(acc) : "v"(c), "v"(x), "i"(N));
+  else
+    asm volatile("v_fmac_f32_dpp %0, %1, %2 row_newbcast:%3 row_mask:0xf bank_mask:0xf"
+                 : "+v"(acc) : "v"(c), "v"(x), "i"(N));
 }
-__device__ __forceinline__ void fmac_row_bcast(float& acc, float c, float x, int n) {
-  SPLA_BC_SWITCH("v_fmac_f32_dpp")
-}
-#undef SPLA_BC_SWITCH
-#undef SPLA_BC_CASE
 
-__device__ __forceinline__ float f4_at(const float4& v, int e) {
-  return e == 0 ? v.x : (e == 1 ? v.y : (e == 2 ? v.z : v.w));
+template <int E>
+__device__ __forceinline__ float f4_at(const float4& v) {
+  static_assert(E >= 0 && E < 4, "float4 element");
+  if constexpr (E == 0) return v.x;
+  else if constexpr (E == 1) return v.y;
+  else if constexpr (E == 2) return v.z;
+  else return v.w;
+}
+
+// f(Idx<I>{}) for I = B, ..., E - 1: the index is a constant expression in
+// every call, whatever the size of the body.
+template <int I>
+struct Idx {
+  static constexpr int v = I;
+};
+template <int B, int E, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (B < E) {
+    f(Idx<B>{});
+    static_for<B + 1, E>(f);
+  }
 }
 
 // Scores one tile from buf; s_part is this tile's half of the double-buffered
@@ -149,32 +156,30 @@ __device__ __forceinline__ void score_tile(const Dims& m, const int32_t* __restr
   // 2G partials of a step are updated round-robin, so one accumulator's
   // updates are 2G instructions apart (plus a nop for G = 1).
   asm volatile("s_nop 4");  // spacing after any earlier EXEC / VGPR write
-#pragma unroll
-  for (int jp = 0; jp < NJ / 2; ++jp) {
+  static_for<0, NJ / 2>([&](auto jpi) {
+    constexpr int jp = decltype(jpi)::v;
     float pa[G], pb[G];
-#pragma unroll
-    for (int e8 = 0; e8 < 8; ++e8) {
-      const int c = 8 * jp + e8;  // coordinate within the quarter
-      const float xm = f4_at(buf.mu[2 * jp + (e8 >> 2)], e8 & 3);
-      const float xv = f4_at(buf.m2[2 * jp + (e8 >> 2)], e8 & 3);
-#pragma unroll
-      for (int mm = 0; mm < G; ++mm) {
-        if (e8 == 0) mul_row_bcast(pa[mm], cf[mm * 2 + (c >> 4)], xm, c & 15);
-        else fmac_row_bcast(pa[mm], cf[mm * 2 + (c >> 4)], xm, c & 15);
-      }
-#pragma unroll
-      for (int mm = 0; mm < G; ++mm) {
-        if (e8 == 0) mul_row_bcast(pb[mm], cf[(G + mm) * 2 + (c >> 4)], xv, c & 15);
-        else fmac_row_bcast(pb[mm], cf[(G + mm) * 2 + (c >> 4)], xv, c & 15);
-      }
-      if (G == 1) asm volatile("s_nop 0");
-    }
+    static_for<0, 8>([&](auto ei) {
+      constexpr int e8 = decltype(ei)::v;
+      constexpr int c = 8 * jp + e8;  // coordinate within the quarter
+      const float xm = f4_at<e8 & 3>(buf.mu[2 * jp + (e8 >> 2)]);
+      const float xv = f4_at<e8 & 3>(buf.m2[2 * jp + (e8 >> 2)]);
+      static_for<0, G>([&](auto mi) {
+        constexpr int mm = decltype(mi)::v;
+        row_bcast_fma<e8 == 0, c & 15>(pa[mm], cf[mm * 2 + (c >> 4)], xm);
+      });
+      static_for<0, G>([&](auto mi) {
+        constexpr int mm = decltype(mi)::v;
+        row_bcast_fma<e8 == 0, c & 15>(pb[mm], cf[(G + mm) * 2 + (c >> 4)], xv);
+      });
+      if constexpr (G == 1) asm volatile("s_nop 0");
+    });
 #pragma unroll
     for (int mm = 0; mm < G; ++mm) {
       am[mm] += (double)pa[mm];
       av[mm] += (double)pb[mm];
     }
-  }
+  });
   // reduce-scatter over the four quarters (lanes l ^ 16, l ^ 32): lane
   // (block, qt) ends with the sums of heads qt + 4u, u < U (zero past G)
   double ra[U], rv[U];

@@ -111,7 +111,8 @@ __device__ __forceinline__ void merge_head(const Dims& m, float eps, uint32_t fl
 #pragma unroll
       for (int u = 0; u < NB; ++u) {
         const bool ok = u0 + u < nb_here;
-        const float sc = ok ? __shfl(sc_l, u0 + u, 64) : 0.f;
+        const float sc =
+            ok ? __int_as_float(__builtin_amdgcn_readlane(__float_as_int(sc_l), u0 + u)) : 0.f;
 #pragma unroll
         for (int e = 0; e < E; ++e) {
           osp[e] = fmaf(a[u][e], sc, osp[e]);
@@ -326,7 +327,34 @@ __device__ __forceinline__ void sparse_body(const Dims& m, float s,
 #pragma unroll
   for (int t = 0; t < MT; ++t) acc_o[t] = floatx4{0.f, 0.f, 0.f, 0.f};
   float m_run = -INFINITY, l_run = 0.f;  // exact columns: max / sum; linear columns: sum
-  __syncthreads();  // the query operands of the prologue are in LDS
+  // while the K/V loads fly: this workgroup's rows of phi(q) S_bar and of
+  // <phi(q), z_bar> (they do not depend on the selection)
+  constexpr int NO = (GC * D + 255) / 256;  // outputs (head, coordinate) per thread
+  const int row0 = r.row0, nrows = r.nrows;
+  const bool s_pre = nrows * D <= kSparsePre * 256;
+#pragma unroll
+  for (int u = 0; u < kSparsePre; ++u) sm.S[tid + 256 * u] = r.spre[u];
+  if (tid < D) sm.zb[tid] = r.zbv;
+  __syncthreads();  // the query operands, phi(q) and the S_bar rows are in LDS
+  float ob[NO];
+#pragma unroll
+  for (int i = 0; i < NO; ++i) {
+    const int e = tid + 256 * i;
+    const int hh = e / D, c = e % D;
+    float acc = 0.f;
+    if (e < G * D) {
+      if (s_pre) {
+        for (int rr = 0; rr < nrows; ++rr) acc = fmaf(sm.phq[hh][row0 + rr], sm.S[rr * D + c], acc);
+      } else {
+        const float* Sb = S + (int64_t)bh * D * D;
+        for (int rr = row0; rr < row0 + nrows; ++rr) acc = fmaf(sm.phq[hh][rr], Sb[rr * D + c], acc);
+      }
+    }
+    ob[i] = acc;
+  }
+  float zq = 0.f;
+  if (tid < G)
+    for (int rr = 0; rr < nrows; ++rr) zq = fmaf(sm.phq[tid][row0 + rr], sm.zb[rr], zq);
   if (n_valid > 0) {
     floatx4 sw[2];
     float zinv[2];  // 1 / sum exp(k - max k) of this lane's key row, per tile
@@ -424,14 +452,12 @@ __device__ __forceinline__ void sparse_body(const Dims& m, float s,
     sm.m[w][lane] = m_run;
     sm.l[w][lane] = l_run;
   }
-#pragma unroll
-  for (int u = 0; u < kSparsePre; ++u) sm.S[tid + 256 * u] = r.spre[u];
-  if (tid < D) sm.zb[tid] = r.zbv;
   __syncthreads();
-  const int row0 = r.row0, nrows = r.nrows;
-  const bool s_pre = nrows * D <= kSparsePre * 256;
   float* rec = part + ((int64_t)bh * n_wg + x) * stride;
-  for (int e = tid; e < G * D; e += 256) {
+#pragma unroll
+  for (int i = 0; i < NO; ++i) {
+    const int e = tid + 256 * i;
+    if (e >= G * D) break;
     const int hh = e / D, c = e % D;
     float M = -INFINITY;
 #pragma unroll
@@ -443,15 +469,8 @@ __device__ __forceinline__ void sparse_body(const Dims& m, float s,
       a = fmaf(sm.o[xx][c][hh], sc, a);
       aw += sm.o[xx][c][GC + hh];
     }
-    float ob = 0.f;  // this workgroup's rows of phi(q) S_bar
-    if (s_pre) {
-      for (int rr = 0; rr < nrows; ++rr) ob = fmaf(sm.phq[hh][row0 + rr], sm.S[rr * D + c], ob);
-    } else {
-      const float* Sb = S + (int64_t)bh * D * D;
-      for (int rr = row0; rr < row0 + nrows; ++rr) ob = fmaf(sm.phq[hh][rr], Sb[rr * D + c], ob);
-    }
     Mem<CO>::st(rec + kPartHead + hh * D + c, a);
-    Mem<CO>::st(rec + kPartHead + (G + hh) * D + c, ob - aw);
+    Mem<CO>::st(rec + kPartHead + (G + hh) * D + c, ob[i] - aw);
   }
   if (tid < G) {
     float M = -INFINITY;
@@ -463,8 +482,6 @@ __device__ __forceinline__ void sparse_body(const Dims& m, float s,
       l += sm.m[xx][tid] == -INFINITY ? 0.f : sm.l[xx][tid] * __expf(sm.m[xx][tid] - M);
       zw += sm.l[xx][8 + tid];
     }
-    float zq = 0.f;
-    for (int rr = 0; rr < nrows; ++rr) zq = fmaf(sm.phq[tid][row0 + rr], sm.zb[rr], zq);
     Mem<CO>::st(rec + tid, M);
     Mem<CO>::st(rec + 16 + tid, l);
     Mem<CO>::st(rec + 32 + tid, zq - zw);
