@@ -127,15 +127,18 @@ void decode_kernel(FusedArgs a) {
     // ---------------------------------------------------------- score item
     const int t = (int)blockIdx.x;
     const int bh = t / a.n_si, i = t % a.n_si;
+    const int L = a.seq_lens[bh / m.hkv];  // for the selection; loaded long before it is used
     score_items<G, bf16_t, D, true, kTilesPerItem>(
         m, a.stats, a.seq_lens, a.q, a.s_score, a.first_order,
         bh * m.n_tiles + i * kTilesPerItem, a.e_vals, a.tile_part, sm.sc);
     int32_t* done = sy + y.items_done + (int64_t)bh * kSyncLine;
     if (!arrive_last(done, a.n_si, &s_flag)) return;
-    if (tid == 0) store_agent(done, 0);
-    select_blocks<256, R, SWN, true, 2>(m, bh, a.seq_lens, a.e_vals, a.tile_part, sm.se,
+    select_blocks<256, R, SWN, true, 2>(m, bh, L, a.e_vals, a.tile_part, sm.se,
                                         sy + y.sel_ready + (int64_t)bh * m.k, nullptr,
                                         a.sel_out ? a.sel_out + (int64_t)bh * m.k : nullptr);
+    // reset last: vmcnt counts stores, so an earlier store would hold up
+    // every wait on the selection's loads until it completed
+    if (tid == 0) store_agent(done, 0);
     return;
   }
   // ------------------------------------------------------------ sparse item
@@ -143,6 +146,7 @@ void decode_kernel(FusedArgs a) {
   const int bh = j / a.n_wg, x = j % a.n_wg;
   SparseRegs r;
   sparse_prologue<D, GC>(m, a.q, a.S, a.zbar, bh, x, a.n_wg, r, sm.sp);
+  sparse_linear<D, GC>(m, a.S, bh, r, sm.sp);
   const int L = min(max(a.seq_lens[bh / m.hkv], 0), m.cap);  // before the wait: not produced here
   // this wavefront's block: poll its selection word (lane 0), then share it
   const int step = sparse_step_entry<BLK>(x);
@@ -157,18 +161,18 @@ void decode_kernel(FusedArgs a) {
     if (v == 0) report_sync_error(a);
   }
   const int blk_sel = __builtin_amdgcn_readfirstlane(v) - 2;
-  sparse_body<D, BLK, true, GC>(m, a.s, a.kc, a.vc, a.S, blk_sel, L, bh, x, a.n_wg, r, sm.sp, a.part,
-                            a.stride);
+  sparse_body<D, BLK, true, GC>(m, a.s, a.kc, a.vc, blk_sel, L, bh, x, a.n_wg, r, sm.sp, a.part,
+                                a.stride);
   if (step < m.k && (tid & 63) == 0) store_agent(word, 0);  // read by this workgroup only
   int32_t* recs = sy + y.recs_done + (int64_t)bh * kSyncLine;
   if (!arrive_last(recs, a.n_wg, &s_flag)) return;
-  if (tid == 0) store_agent(recs, 0);
   const int nb = (L + BLK - 1) / BLK;
   const int all_sel = nb <= m.k;
   const float* rec = a.part + (int64_t)bh * a.n_wg * a.stride;
   for (int g = tid >> 6; g < G; g += 4)
     merge_head<bf16_t, D, true>(m, a.eps, a.flags, a.gamma, all_sel, L, rec, a.n_wg, a.stride,
                                 a.out, bh, g);
+  if (tid == 0) store_agent(recs, 0);  // last, as for the item counter
 }
 
 template <int G, int BLK, int R>

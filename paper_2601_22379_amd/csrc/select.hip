@@ -15,8 +15,8 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
   __shared__ SelectSmem<kSelThreads, kMaxTiles * SPLA_MAX_GROUP> sm;
   const int bh = blockIdx.x;
   select_blocks<kSelThreads, R, kMaxTiles * SPLA_MAX_GROUP, false>(
-      m, bh, seq_lens, e_vals, tile_part, sm, sel_ws + (int64_t)bh * m.k, meta + bh * 4,
-      sel_out ? sel_out + (int64_t)bh * m.k : nullptr);
+      m, bh, seq_lens[bh / m.hkv], e_vals, tile_part, sm, sel_ws + (int64_t)bh * m.k,
+      meta + bh * 4, sel_out ? sel_out + (int64_t)bh * m.k : nullptr);
 }
 
 hipError_t launch_select(const Dims& m, const spla_cache& c, const DecodeWs& ws, char* base,

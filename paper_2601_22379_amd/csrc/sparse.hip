@@ -210,19 +210,22 @@ __global__ __launch_bounds__(256) void sparse_mfma_kernel(
   const int bh = blockIdx.y;
   SparseRegs r;
   sparse_prologue<D, 8>(m, q, S, zbar, bh, (int)blockIdx.x, (int)gridDim.x, r, sm);
+  sparse_linear<D, 8>(m, S, bh, r, sm);
   if constexpr (R > 0) {
-    select_blocks<256, R, SWN, false>(m, bh, seq_lens, e_vals, tile_part, ssm, s_sel, s_meta,
-                               blockIdx.x == 0 && sel_out ? sel_out + (int64_t)bh * m.k : nullptr);
+    select_blocks<256, R, SWN, false>(m, bh, seq_lens[bh / m.hkv], e_vals, tile_part, ssm, s_sel,
+                                      s_meta,
+                                      blockIdx.x == 0 && sel_out ? sel_out + (int64_t)bh * m.k
+                                                                 : nullptr);
     __syncthreads();
     if (blockIdx.x == 0 && threadIdx.x < 4) meta[bh * 4 + threadIdx.x] = s_meta[threadIdx.x];
     const int e = sparse_step_entry<BLK>((int)blockIdx.x);
-    sparse_body<D, BLK, false, 8>(m, s, kc, vc, S, e < m.k ? s_sel[e] : -1, s_meta[2], bh, (int)blockIdx.x,
-                        (int)gridDim.x, r, sm, part, stride);
+    sparse_body<D, BLK, false, 8>(m, s, kc, vc, e < m.k ? s_sel[e] : -1, s_meta[2], bh,
+                                  (int)blockIdx.x, (int)gridDim.x, r, sm, part, stride);
   } else {
     const int e = sparse_step_entry<BLK>((int)blockIdx.x);
-    sparse_body<D, BLK, false, 8>(m, s, kc, vc, S, e < m.k ? sel[(int64_t)bh * m.k + e] : -1,
-                        meta[bh * 4 + 2], bh, (int)blockIdx.x, (int)gridDim.x, r, sm, part,
-                        stride);
+    sparse_body<D, BLK, false, 8>(m, s, kc, vc, e < m.k ? sel[(int64_t)bh * m.k + e] : -1,
+                                  meta[bh * 4 + 2], bh, (int)blockIdx.x, (int)gridDim.x, r, sm,
+                                  part, stride);
   }
 }
 

@@ -123,8 +123,10 @@ struct SelectSmem {
   int32_t out[SPLA_MAX_TOP_K + NT];
 };
 
-// The selection of sequence x KV head bh by the NT threads of a workgroup,
-// thread t owning blocks t R .. t R + R - 1 (NT R >= blocks of the capacity).
+// The selection of sequence x KV head bh (length seq_len, clipped to the
+// capacity) by the NT threads of a workgroup, thread t owning blocks
+// t R .. t R + R - 1 (NT R >= blocks of the capacity). The length is an
+// argument so that no load of it sits in front of the first loads here.
 // Writes sel[0 .. k) (ascending block ids, -1 padded), meta4 = (selected,
 // all selected, length, candidates) and, if so is not NULL, the ids to so as
 // well. sel, meta4 and so may point to global memory or to LDS; the caller
@@ -134,7 +136,7 @@ struct SelectSmem {
 // written to sel (not to so): with SEL_OFF = 2 an entry is never 0, so a
 // consumer can poll sel itself for the selection (meta4 may then be NULL).
 template <int NT, int R, int SWN, bool CO, int SEL_OFF = 0>
-__device__ void select_blocks(const Dims& m, int bh, const int32_t* __restrict__ seq_lens,
+__device__ void select_blocks(const Dims& m, int bh, int seq_len,
                               const float* __restrict__ e_vals,
                               const double* __restrict__ tile_part, SelectSmem<NT, SWN>& sm,
                               int32_t* sel, int32_t* meta4, int32_t* so) {
@@ -143,7 +145,6 @@ __device__ void select_blocks(const Dims& m, int bh, const int32_t* __restrict__
   constexpr int TJ = (NT * R + 4095) / 4096;  // tiles per lane: n_tiles <= NT R / 64
   float* sw = sm.sw;
   uint32_t* hist = sm.hist;
-  const int b = bh / m.hkv;
   const int G = m.group, k = m.k;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int nbp = m.n_tiles * kTileBlocks;
@@ -152,8 +153,7 @@ __device__ void select_blocks(const Dims& m, int bh, const int32_t* __restrict__
   const double* tp = tile_part + (int64_t)bh * m.n_tiles * G * 2;
   const float* ev = e_vals + (int64_t)bh * G * nbp + i0;
 
-  // --- loads that need no sequence length go out first
-  const int L = min(max(seq_lens[b], 0), m.cap);  // a length past the capacity is clipped
+  const int L = min(max(seq_len, 0), m.cap);  // a length past the capacity is clipped
   double tm[TJ], ts[TJ];
 #pragma unroll
   for (int j = 0; j < TJ; ++j) {

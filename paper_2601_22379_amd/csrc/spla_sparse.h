@@ -163,12 +163,16 @@ struct SparseSmem {
   float zb[D];
 };
 
-// What a workgroup loads before it knows its blocks: its rows of S_bar and
-// z_bar (the query operands go to LDS).
+// What a workgroup loads and computes before it knows its blocks: its rows
+// of S_bar and z_bar (the query operands go to LDS), then its share of
+// phi(q) S_bar (ob: output e = tid + 256 i is head e / D, coordinate e % D)
+// and of <phi(q), z_bar> (zq, thread g < G for head g).
 struct SparseRegs {
   float spre[kSparsePre];
   float zbv;
   int row0, nrows;
+  float ob[4];
+  float zq;
 };
 
 // With g = lane / 16 and j = lane % 16 (the MFMA column), the B operands of
@@ -262,6 +266,52 @@ __device__ __forceinline__ void sparse_prologue(const Dims& m, const bf16_t* __r
   }
 }
 
+// This workgroup's rows x of the global linear term (Eq. 15): ob and zq of r,
+// from the S_bar rows of r and phi(q) (LDS). Needs nothing from the
+// selection, so it runs while the workgroup would otherwise wait for it.
+template <int D, int GC>
+__device__ __forceinline__ void sparse_linear(const Dims& m, const float* __restrict__ S, int bh,
+                                              SparseRegs& r, SparseSmem<D, GC>& sm) {
+  constexpr int NO = (GC * D + 255) / 256;  // outputs (head, coordinate) per thread
+  constexpr int RMAX = kSparsePre * 256 / D;  // rows held in LDS
+  static_assert(NO <= 4, "ob holds four outputs");
+  const int G = m.group, tid = threadIdx.x;
+  const int row0 = r.row0, nrows = r.nrows;
+  const bool s_pre = nrows <= RMAX;
+#pragma unroll
+  for (int u = 0; u < kSparsePre; ++u) sm.S[tid + 256 * u] = r.spre[u];
+  if (tid < D) sm.zb[tid] = r.zbv;
+  __syncthreads();  // the query operands, phi(q) and the S_bar rows are in LDS
+  // rows past nrows are zero in LDS; their phi(q) index is clamped
+#pragma unroll
+  for (int i = 0; i < NO; ++i) {
+    const int e = tid + 256 * i;
+    const int hh = e / D, c = e % D;
+    float acc = 0.f;
+    if (e < G * D) {
+      if (s_pre) {
+#pragma unroll
+        for (int rr = 0; rr < RMAX; ++rr)
+          acc = fmaf(sm.phq[hh][min(row0 + rr, D - 1)], sm.S[rr * D + c], acc);
+      } else {
+        const float* Sb = S + (int64_t)bh * D * D;
+        for (int rr = row0; rr < row0 + nrows; ++rr) acc = fmaf(sm.phq[hh][rr], Sb[rr * D + c], acc);
+      }
+    }
+    r.ob[i] = acc;
+  }
+  float zq = 0.f;
+  if (tid < G) {
+    if (s_pre) {
+#pragma unroll
+      for (int rr = 0; rr < RMAX; ++rr) zq = fmaf(sm.phq[tid][min(row0 + rr, D - 1)], sm.zb[rr], zq);
+    } else {
+      for (int rr = 0; rr < nrows; ++rr) zq = fmaf(sm.phq[tid][row0 + rr], sm.zb[rr], zq);
+    }
+  }
+  r.zq = zq;
+}
+
 // Selected block of this wavefront's step: entry p of the selection, where
 // workgroup x's wavefront w takes step 4 x + w and a block has BLK / 32 steps.
 template <int BLK>
@@ -286,7 +336,7 @@ template <int D, int BLK, bool CO, int GC>
 __device__ __forceinline__ void sparse_body(const Dims& m, float s,
                                             const bf16_t* __restrict__ kc,
                                             const bf16_t* __restrict__ vc,
-                                            const float* __restrict__ S, int blk_sel, int L,
+                                            int blk_sel, int L,
                                             int bh, int x, int n_wg, const SparseRegs& r,
                                             SparseSmem<D, GC>& sm, float* __restrict__ part,
                                             int stride) {
@@ -327,34 +377,7 @@ __device__ __forceinline__ void sparse_body(const Dims& m, float s,
 #pragma unroll
   for (int t = 0; t < MT; ++t) acc_o[t] = floatx4{0.f, 0.f, 0.f, 0.f};
   float m_run = -INFINITY, l_run = 0.f;  // exact columns: max / sum; linear columns: sum
-  // while the K/V loads fly: this workgroup's rows of phi(q) S_bar and of
-  // <phi(q), z_bar> (they do not depend on the selection)
   constexpr int NO = (GC * D + 255) / 256;  // outputs (head, coordinate) per thread
-  const int row0 = r.row0, nrows = r.nrows;
-  const bool s_pre = nrows * D <= kSparsePre * 256;
-#pragma unroll
-  for (int u = 0; u < kSparsePre; ++u) sm.S[tid + 256 * u] = r.spre[u];
-  if (tid < D) sm.zb[tid] = r.zbv;
-  __syncthreads();  // the query operands, phi(q) and the S_bar rows are in LDS
-  float ob[NO];
-#pragma unroll
-  for (int i = 0; i < NO; ++i) {
-    const int e = tid + 256 * i;
-    const int hh = e / D, c = e % D;
-    float acc = 0.f;
-    if (e < G * D) {
-      if (s_pre) {
-        for (int rr = 0; rr < nrows; ++rr) acc = fmaf(sm.phq[hh][row0 + rr], sm.S[rr * D + c], acc);
-      } else {
-        const float* Sb = S + (int64_t)bh * D * D;
-        for (int rr = row0; rr < row0 + nrows; ++rr) acc = fmaf(sm.phq[hh][rr], Sb[rr * D + c], acc);
-      }
-    }
-    ob[i] = acc;
-  }
-  float zq = 0.f;
-  if (tid < G)
-    for (int rr = 0; rr < nrows; ++rr) zq = fmaf(sm.phq[tid][row0 + rr], sm.zb[rr], zq);
   if (n_valid > 0) {
     floatx4 sw[2];
     float zinv[2];  // 1 / sum exp(k - max k) of this lane's key row, per tile
@@ -470,7 +493,7 @@ __device__ __forceinline__ void sparse_body(const Dims& m, float s,
       aw += sm.o[xx][c][GC + hh];
     }
     Mem<CO>::st(rec + kPartHead + hh * D + c, a);
-    Mem<CO>::st(rec + kPartHead + (G + hh) * D + c, ob[i] - aw);
+    Mem<CO>::st(rec + kPartHead + (G + hh) * D + c, r.ob[i] - aw);
   }
   if (tid < G) {
     float M = -INFINITY;
@@ -484,7 +507,7 @@ __device__ __forceinline__ void sparse_body(const Dims& m, float s,
     }
     Mem<CO>::st(rec + tid, M);
     Mem<CO>::st(rec + 16 + tid, l);
-    Mem<CO>::st(rec + 32 + tid, zq - zw);
+    Mem<CO>::st(rec + 32 + tid, r.zq - zw);
   }
 }
 
