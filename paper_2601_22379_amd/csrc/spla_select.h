@@ -49,25 +49,32 @@ __device__ __forceinline__ uint32_t block_excl_scan_u32(uint32_t v, uint32_t* ld
   return base + x - v;
 }
 
-// R consecutive floats from a 4R-byte aligned address (zeros when !ok).
+// R consecutive floats at base + off (4R-byte aligned; zeros when !ok). The
+// loads are issued whether or not ok (from base when not): a load under a
+// branch makes the compiler wait for it inside the branch, before the loads
+// after it are issued.
 template <int R, bool CO>
-__device__ __forceinline__ void load_run(const float* p, bool ok, float (&out)[R]) {
+__device__ __forceinline__ void load_run(const float* base, int64_t off, bool ok,
+                                         float (&out)[R]) {
+  const float* p = base + (ok ? off : 0);
   if constexpr (R == 1) {
-    out[0] = ok ? Mem<CO>::ld(p) : 0.f;
+    out[0] = Mem<CO>::ld(p);
   } else if constexpr (R == 2) {
-    const float2 v = ok ? Mem<CO>::ld2(p) : make_float2(0.f, 0.f);
+    const float2 v = Mem<CO>::ld2(p);
     out[0] = v.x;
     out[1] = v.y;
   } else {
 #pragma unroll
     for (int j = 0; j < R / 4; ++j) {
-      const float4 v = ok ? Mem<CO>::ld4(p + 4 * j) : make_float4(0.f, 0.f, 0.f, 0.f);
+      const float4 v = Mem<CO>::ld4(p + 4 * j);
       out[4 * j] = v.x;
       out[4 * j + 1] = v.y;
       out[4 * j + 2] = v.z;
       out[4 * j + 3] = v.w;
     }
   }
+#pragma unroll
+  for (int r = 0; r < R; ++r) out[r] = ok ? out[r] : 0.f;
 }
 
 struct RadixPick {
@@ -151,20 +158,23 @@ __device__ void select_blocks(const Dims& m, int bh, int seq_len,
   const int i0 = tid * R;
   const int kp = k - m.n_sink - m.n_local;
   const double* tp = tile_part + (int64_t)bh * m.n_tiles * G * 2;
-  const float* ev = e_vals + (int64_t)bh * G * nbp + i0;
+  const float* ev = e_vals + (int64_t)bh * G * nbp;  // this thread's run: + h nbp + i0
 
   const int L = min(max(seq_len, 0), m.cap);  // a length past the capacity is clipped
   double tm[TJ], ts[TJ];
 #pragma unroll
-  for (int j = 0; j < TJ; ++j) {
+  for (int j = 0; j < TJ; ++j) {  // unconditional loads (from tp itself when not ok)
     const int t = lane + 64 * j;
     const bool ok = w < G && t < m.n_tiles;
-    tm[j] = ok ? Mem<CO>::ld(tp + (t * G + w) * 2) : -INFINITY;
-    ts[j] = ok ? Mem<CO>::ld(tp + (t * G + w) * 2 + 1) : 0.0;
+    const double* p = tp + (ok ? (t * G + w) * 2 : 0);
+    const double a0 = Mem<CO>::ld(p), a1 = Mem<CO>::ld(p + 1);
+    tm[j] = ok ? a0 : -INFINITY;
+    ts[j] = ok ? a1 : 0.0;
   }
   float e[HC][R];  // nbp is a multiple of 64 >= R: a thread's run is all in or all out
 #pragma unroll
-  for (int h = 0; h < HC; ++h) load_run<R, CO>(ev + (int64_t)h * nbp, h < G && i0 < nbp, e[h]);
+  for (int h = 0; h < HC; ++h)
+    load_run<R, CO>(ev, (int64_t)h * nbp + i0, h < G && i0 < nbp, e[h]);
 
   const int nb = (L + m.B - 1) / m.B;
   if (nb <= k) {  // L == 0 included: nothing or everything is selected
@@ -190,8 +200,10 @@ __device__ void select_blocks(const Dims& m, int bh, int seq_len,
       for (int j = 0; j < TJ; ++j) {
         const int t = lane + 64 * j;
         const bool ok = t < m.n_tiles;
-        tm[j] = ok ? Mem<CO>::ld(tp + (t * G + mm) * 2) : -INFINITY;
-        ts[j] = ok ? Mem<CO>::ld(tp + (t * G + mm) * 2 + 1) : 0.0;
+        const double* p = tp + (ok ? (t * G + mm) * 2 : 0);
+        const double a0 = Mem<CO>::ld(p), a1 = Mem<CO>::ld(p + 1);
+        tm[j] = ok ? a0 : -INFINITY;
+        ts[j] = ok ? a1 : 0.0;
       }
     }
     double mx = -INFINITY;
@@ -240,7 +252,7 @@ __device__ void select_blocks(const Dims& m, int bh, int seq_len,
       if (h0 > 0) {
 #pragma unroll
         for (int h = 0; h < HC; ++h)
-          load_run<R, CO>(ev + (int64_t)(h0 + h) * nbp, h0 + h < G && i0 < nbp, e[h]);
+          load_run<R, CO>(ev, (int64_t)(h0 + h) * nbp + i0, h0 + h < G && i0 < nbp, e[h]);
       }
 #pragma unroll
       for (int h = 0; h < HC; ++h) {

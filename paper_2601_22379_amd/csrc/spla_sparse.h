@@ -84,10 +84,12 @@ __device__ __forceinline__ void merge_head(const Dims& m, float eps, uint32_t fl
     // headers: lane u holds record x0 + u
     const bool hv = x0 + lane < n_rec;
     const float* hr = rec + (int64_t)(hv ? x0 + lane : 0) * stride;
-    const float hm = hv ? Mem<CO>::ld(hr + g) : -INFINITY;
-    const float hl = hv ? Mem<CO>::ld(hr + 16 + g) : 0.f;
-    const float hz = hv ? Mem<CO>::ld(hr + 32 + g) : 0.f;
+    // loaded whether or not hv (no branch), selected after the first bodies
+    // are issued, so that no wait for them comes before those loads
+    const float hm0 = Mem<CO>::ld(hr + g), hl0 = Mem<CO>::ld(hr + 16 + g);
+    const float hz0 = Mem<CO>::ld(hr + 32 + g);
     const int nb_here = n_rec - x0 < 64 ? n_rec - x0 : 64;
+    float sc_l = 0.f;  // lane u: weight exp(m - M) of record x0 + u
     // bodies, NB at a time (the first batch is issued with the headers)
     for (int u0 = 0; u0 < nb_here; u0 += NB) {
       float a[NB][E], aw[NB][E];
@@ -97,7 +99,9 @@ __device__ __forceinline__ void merge_head(const Dims& m, float eps, uint32_t fl
         load_vec<E, CO>(rec + (int64_t)x * stride + kPartHead + g * D + c0, a[u]);
         load_vec<E, CO>(rec + (int64_t)x * stride + kPartHead + (G + g) * D + c0, aw[u]);
       }
+      __builtin_amdgcn_sched_barrier(0);
       if (u0 == 0) {  // fold this batch of headers into the running max
+        const float hm = hv ? hm0 : -INFINITY, hl = hv ? hl0 : 0.f, hz = hv ? hz0 : 0.f;
         const float bm = fmaxf(M, wave_max(hm));
         const float alpha = M == -INFINITY ? 0.f : __expf(M - bm);
         l *= alpha;
@@ -106,8 +110,8 @@ __device__ __forceinline__ void merge_head(const Dims& m, float eps, uint32_t fl
         M = bm;
         l += wave_sum(hm == -INFINITY ? 0.f : hl * __expf(hm - M));
         zt += wave_sum(hz);
+        sc_l = hm == -INFINITY ? 0.f : __expf(hm - M);
       }
-      const float sc_l = hm == -INFINITY ? 0.f : __expf(hm - M);  // lane u: record x0 + u
 #pragma unroll
       for (int u = 0; u < NB; ++u) {
         const bool ok = u0 + u < nb_here;
@@ -201,15 +205,22 @@ __device__ __forceinline__ void sparse_prologue(const Dims& m, const bf16_t* __r
   for (int ks = 0; ks < KS; ++ks) raw[ks] = *reinterpret_cast<const uint4*>(qrow + 32 * ks);
   lin_rows(D, x, n_wg, &r.row0, &r.nrows);
   {
+    // loads issued whether or not in range (from row 0 when not): no branch
     const bool s_pre = r.nrows * D <= kSparsePre * 256;
-    const float* Sb = S + ((int64_t)bh * D + r.row0) * D;
+    const float* Sh = S + (int64_t)bh * D * D;
 #pragma unroll
     for (int u = 0; u < kSparsePre; ++u) {
       const int e = tid + 256 * u;
-      r.spre[u] = (s_pre && e < r.nrows * D) ? Sb[e] : 0.f;
+      const bool ok = s_pre && e < r.nrows * D;
+      const float v = Sh[ok ? r.row0 * D + e : 0];
+      r.spre[u] = ok ? v : 0.f;
     }
   }
-  r.zbv = tid < r.nrows ? zbar[(int64_t)bh * D + r.row0 + tid] : 0.f;
+  {
+    const bool ok = tid < r.nrows;
+    const float v = zbar[(int64_t)bh * D + (ok ? r.row0 + tid : 0)];
+    r.zbv = ok ? v : 0.f;
+  }
   // phi(q) of this lane's head (every lane computes it; columns 0..7 discard it)
   float xv[KS][8];
   float mx = -INFINITY;
