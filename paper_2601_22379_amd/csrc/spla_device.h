@@ -176,8 +176,15 @@ __device__ __forceinline__ double row_sum_to15(double x) {
 // invalidation is needed between producer and consumer.
 template <bool CO>
 struct Mem;
+constexpr int kCacheSc1 = 16;  // cache-policy operand of the buffer intrinsics: sc1
+// ld16(base, off): the 16 bytes at byte offset off (16-byte aligned) of a
+// wave-uniform base. Mem<true> issues it as one buffer load with the sc1
+// bit (agent-scope atomics are at most 8 bytes wide).
 template <>
 struct Mem<false> {
+  static __device__ __forceinline__ uint4 ld16(const void* base, uint32_t off) {
+    return *reinterpret_cast<const uint4*>(static_cast<const char*>(base) + off);
+  }
   template <typename T>
   static __device__ __forceinline__ T ld(const T* p) { return *p; }
   template <typename T>
@@ -191,6 +198,14 @@ struct Mem<false> {
 };
 template <>
 struct Mem<true> {
+  static __device__ __forceinline__ uint4 ld16(const void* base, uint32_t off) {
+    // raw buffer over the 4 GiB above base (dword 3: the gfx9 data format)
+    const __amdgpu_buffer_rsrc_t r =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, -1, 0x00020000);
+    typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+    const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kCacheSc1);
+    return make_uint4(v[0], v[1], v[2], v[3]);
+  }
   template <typename T>
   static __device__ __forceinline__ T ld(const T* p) {
     return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);

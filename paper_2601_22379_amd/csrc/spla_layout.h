@@ -73,7 +73,7 @@ constexpr int kSparseWaves = 4;   // waves per sparse workgroup
 
 struct DecodeWs {
   int64_t e_vals;     // f32 [bh][G][n_tiles*64]   exp(ell - tile max)
-  int64_t tile_part;  // f64 [bh][n_tiles][G][2]   (max, sum) per 64-block tile
+  int64_t tile_part;  // f64 [bh][G][n_tiles][2]   (max, sum) per 64-block tile
   int64_t sel;        // i32 [bh][k]               selected blocks, ascending
   int64_t meta;       // i32 [bh][4]               (n_selected, all_selected, length, 0)
   int64_t part;       // f32 [bh][n_wg][part_stride]  sparse workgroup partials

@@ -247,7 +247,7 @@ __device__ __forceinline__ void score_tile(const Dims& m, const int32_t* __restr
       mx = fmax(mx, s_part[x][tid][0]);
       sum += s_part[x][tid][1];
     }
-    double* tp = tile_part + (((int64_t)bh * m.n_tiles + tile) * G + tid) * 2;
+    double* tp = tile_part + (((int64_t)bh * G + tid) * m.n_tiles + tile) * 2;
     Mem<CO>::st(tp, mx);
     Mem<CO>::st(tp + 1, sum);
   }

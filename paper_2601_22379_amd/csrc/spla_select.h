@@ -49,32 +49,43 @@ __device__ __forceinline__ uint32_t block_excl_scan_u32(uint32_t v, uint32_t* ld
   return base + x - v;
 }
 
-// R consecutive floats at base + off (4R-byte aligned; zeros when !ok). The
-// loads are issued whether or not ok (from base when not): a load under a
-// branch makes the compiler wait for it inside the branch, before the loads
-// after it are issued.
+// R consecutive floats at base + off (4R-byte aligned; zeros when !ok); base
+// is wave-uniform. The loads are issued whether or not ok (from base when
+// not): a load under a branch makes the compiler wait for it inside the
+// branch, before the loads after it are issued.
 template <int R, bool CO>
 __device__ __forceinline__ void load_run(const float* base, int64_t off, bool ok,
                                          float (&out)[R]) {
-  const float* p = base + (ok ? off : 0);
+  const int64_t o = ok ? off : 0;
   if constexpr (R == 1) {
-    out[0] = Mem<CO>::ld(p);
+    out[0] = Mem<CO>::ld(base + o);
   } else if constexpr (R == 2) {
-    const float2 v = Mem<CO>::ld2(p);
+    const float2 v = Mem<CO>::ld2(base + o);
     out[0] = v.x;
     out[1] = v.y;
   } else {
 #pragma unroll
     for (int j = 0; j < R / 4; ++j) {
-      const float4 v = Mem<CO>::ld4(p + 4 * j);
-      out[4 * j] = v.x;
-      out[4 * j + 1] = v.y;
-      out[4 * j + 2] = v.z;
-      out[4 * j + 3] = v.w;
+      const uint4 v = Mem<CO>::ld16(base, (uint32_t)(o + 4 * j) * 4u);
+      out[4 * j] = __uint_as_float(v.x);
+      out[4 * j + 1] = __uint_as_float(v.y);
+      out[4 * j + 2] = __uint_as_float(v.z);
+      out[4 * j + 3] = __uint_as_float(v.w);
     }
   }
 #pragma unroll
   for (int r = 0; r < R; ++r) out[r] = ok ? out[r] : 0.f;
+}
+
+// The (max, sum) partial of tile t of the head whose partials start at tp
+// (wave-uniform), as one 16-byte load; (-inf, 0) when !ok.
+template <bool CO>
+__device__ __forceinline__ void load_tile_part(const double* tp, int t, bool ok, double& mx,
+                                               double& sum) {
+  const uint4 v = Mem<CO>::ld16(tp, (uint32_t)(ok ? t : 0) * 16u);
+  const double a = __hiloint2double((int)v.y, (int)v.x), b = __hiloint2double((int)v.w, (int)v.z);
+  mx = ok ? a : -INFINITY;
+  sum = ok ? b : 0.0;
 }
 
 struct RadixPick {
@@ -163,13 +174,10 @@ __device__ void select_blocks(const Dims& m, int bh, int seq_len,
   const int L = min(max(seq_len, 0), m.cap);  // a length past the capacity is clipped
   double tm[TJ], ts[TJ];
 #pragma unroll
-  for (int j = 0; j < TJ; ++j) {  // unconditional loads (from tp itself when not ok)
+  for (int j = 0; j < TJ; ++j) {
     const int t = lane + 64 * j;
-    const bool ok = w < G && t < m.n_tiles;
-    const double* p = tp + (ok ? (t * G + w) * 2 : 0);
-    const double a0 = Mem<CO>::ld(p), a1 = Mem<CO>::ld(p + 1);
-    tm[j] = ok ? a0 : -INFINITY;
-    ts[j] = ok ? a1 : 0.0;
+    load_tile_part<CO>(tp + (int64_t)(w < G ? w : 0) * m.n_tiles * 2, t, w < G && t < m.n_tiles,
+                       tm[j], ts[j]);
   }
   float e[HC][R];  // nbp is a multiple of 64 >= R: a thread's run is all in or all out
 #pragma unroll
@@ -199,11 +207,7 @@ __device__ void select_blocks(const Dims& m, int bh, int seq_len,
 #pragma unroll
       for (int j = 0; j < TJ; ++j) {
         const int t = lane + 64 * j;
-        const bool ok = t < m.n_tiles;
-        const double* p = tp + (ok ? (t * G + mm) * 2 : 0);
-        const double a0 = Mem<CO>::ld(p), a1 = Mem<CO>::ld(p + 1);
-        tm[j] = ok ? a0 : -INFINITY;
-        ts[j] = ok ? a1 : 0.0;
+        load_tile_part<CO>(tp + (int64_t)mm * m.n_tiles * 2, t, t < m.n_tiles, tm[j], ts[j]);
       }
     }
     double mx = -INFINITY;
