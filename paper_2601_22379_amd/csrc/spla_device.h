@@ -120,6 +120,9 @@ __device__ __forceinline__ uint32_t wave_incl_scan_u32(uint32_t x) {
 __device__ __forceinline__ uint32_t lane_u32(uint32_t v, int lane) {
   return (uint32_t)__builtin_amdgcn_readlane((int)v, lane);
 }
+__device__ __forceinline__ float lane_f32(float v, int lane) {
+  return __uint_as_float(lane_u32(__float_as_uint(v), lane));
+}
 __device__ __forceinline__ double lane_f64(double v, int lane) {
   const uint64_t x = __double_as_longlong(v);
   const uint32_t lo = lane_u32((uint32_t)x, lane), hi = lane_u32((uint32_t)(x >> 32), lane);

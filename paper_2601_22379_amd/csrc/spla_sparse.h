@@ -43,39 +43,48 @@ __device__ __forceinline__ void lin_rows(int D, int x, int n_wg, int* row0, int*
 }
 
 // ------------------------------------------------------------------ merge
+// E consecutive floats at byte offset off of the wave-uniform base.
 template <int E, bool CO>
-__device__ __forceinline__ void load_vec(const float* p, float (&v)[E]) {
-  if constexpr (E == 2) {
-    const float2 x = Mem<CO>::ld2(p);
+__device__ __forceinline__ void load_vec(const float* base, uint32_t off, float (&v)[E]) {
+  static_assert(E == 2 || E == 4, "two or four floats per lane");
+  if constexpr (E == 4) {
+    const uint4 x = Mem<CO>::ld16(base, off);
+    v[0] = __uint_as_float(x.x);
+    v[1] = __uint_as_float(x.y);
+    v[2] = __uint_as_float(x.z);
+    v[3] = __uint_as_float(x.w);
+  } else {
+    const float2 x = Mem<CO>::ld2(base + off / 4);
     v[0] = x.x;
     v[1] = x.y;
-  } else {
-#pragma unroll
-    for (int e = 0; e < E; ++e) v[e] = Mem<CO>::ld(p + e);
   }
 }
 
-// Combines the n_rec records `rec` of sequence x KV head bh for query head g
-// of the group and writes its output row; one wavefront, lane l owning the E
-// adjacent coordinates E l .. E l + E - 1. The record headers of a batch of
-// 64 records are read one record per lane; every load of a batch (and the
-// gain row) is issued before any arithmetic. CO: the records are read with
-// Mem<true> (written by other workgroups of the same launch).
+// Combines the n_rec records `rec` (wave-uniform) of sequence x KV head bh
+// for query head g of the group and writes its output row; one wavefront.
+// Each half-wavefront takes every other record, lane l owning the E = D / 32
+// adjacent coordinates E (l % 32) .. +E-1, so that one load instruction
+// fetches two record rows (16 bytes per lane for D = 128); the halves are
+// added at the end. The record headers of a batch of 64 records are read
+// one record per lane; every load of a batch (and the gain row) is issued
+// before any arithmetic. CO: the records are read with Mem<true> (written
+// by other workgroups of the same launch).
 template <typename T, int D, bool CO>
 __device__ __forceinline__ void merge_head(const Dims& m, float eps, uint32_t flags,
                                            const float* __restrict__ gamma, int all_sel, int L,
                                            const float* rec, int n_rec, int stride,
                                            T* __restrict__ out, int bh, int g) {
-  constexpr int E = D / 64;  // coordinates per lane
-  constexpr int NB = 16;     // record bodies per load batch
+  constexpr int E = D / 32;  // coordinates per lane
+  constexpr int NP = 8;      // record pairs per load batch
   const int b = bh / m.hkv, h = bh % m.hkv;
   const int G = m.group;
-  const int lane = threadIdx.x & 63;
-  const int c0 = E * lane;
+  const int lane = threadIdx.x & 63, hf = lane >> 5;
+  const int c0 = E * (lane & 31);
   const int64_t orow = ((int64_t)b * m.hq + h * G + g) * D + c0;
   const bool rla = !(flags & SPLA_FLAG_NO_RLA);
   float gm[E];
-  load_vec<E, false>(gamma + (int64_t)(h * G + g) * D + c0, gm);
+#pragma unroll
+  for (int e = 0; e < E; ++e) gm[e] = gamma[(int64_t)(h * G + g) * D + c0 + e];
   float M = -INFINITY, l = 0.f, zt = 0.f;
   float osp[E], ot[E];
 #pragma unroll
@@ -90,14 +99,15 @@ __device__ __forceinline__ void merge_head(const Dims& m, float eps, uint32_t fl
     const float hz0 = Mem<CO>::ld(hr + 32 + g);
     const int nb_here = n_rec - x0 < 64 ? n_rec - x0 : 64;
     float sc_l = 0.f;  // lane u: weight exp(m - M) of record x0 + u
-    // bodies, NB at a time (the first batch is issued with the headers)
-    for (int u0 = 0; u0 < nb_here; u0 += NB) {
-      float a[NB][E], aw[NB][E];
+    // bodies, NP pairs at a time (the first batch is issued with the headers)
+    for (int u0 = 0; u0 < nb_here; u0 += 2 * NP) {
+      float a[NP][E], aw[NP][E];
 #pragma unroll
-      for (int u = 0; u < NB; ++u) {
-        const int x = x0 + u0 + u < n_rec ? x0 + u0 + u : 0;
-        load_vec<E, CO>(rec + (int64_t)x * stride + kPartHead + g * D + c0, a[u]);
-        load_vec<E, CO>(rec + (int64_t)x * stride + kPartHead + (G + g) * D + c0, aw[u]);
+      for (int u = 0; u < NP; ++u) {
+        const int xr = x0 + u0 + 2 * u + hf;
+        const uint32_t o = (uint32_t)((int64_t)(xr < n_rec ? xr : 0) * stride + kPartHead + c0) * 4u;
+        load_vec<E, CO>(rec, o + (uint32_t)(g * D) * 4u, a[u]);
+        load_vec<E, CO>(rec, o + (uint32_t)((G + g) * D) * 4u, aw[u]);
       }
       __builtin_amdgcn_sched_barrier(0);
       if (u0 == 0) {  // fold this batch of headers into the running max
@@ -113,10 +123,12 @@ __device__ __forceinline__ void merge_head(const Dims& m, float eps, uint32_t fl
         sc_l = hm == -INFINITY ? 0.f : __expf(hm - M);
       }
 #pragma unroll
-      for (int u = 0; u < NB; ++u) {
-        const bool ok = u0 + u < nb_here;
-        const float sc =
-            ok ? __int_as_float(__builtin_amdgcn_readlane(__float_as_int(sc_l), u0 + u)) : 0.f;
+      for (int u = 0; u < NP; ++u) {
+        const int r0 = u0 + 2 * u;  // this pair's records within the batch: r0, r0 + 1
+        const float s0 = r0 < nb_here ? lane_f32(sc_l, r0) : 0.f;
+        const float s1 = r0 + 1 < nb_here ? lane_f32(sc_l, r0 + 1) : 0.f;
+        const bool ok = r0 + hf < nb_here;
+        const float sc = hf ? s1 : s0;
 #pragma unroll
         for (int e = 0; e < E; ++e) {
           osp[e] = fmaf(a[u][e], sc, osp[e]);
@@ -124,6 +136,11 @@ __device__ __forceinline__ void merge_head(const Dims& m, float eps, uint32_t fl
         }
       }
     }
+  }
+#pragma unroll
+  for (int e = 0; e < E; ++e) {  // the two halves' records
+    osp[e] += xor32(osp[e]);
+    ot[e] += xor32(ot[e]);
   }
   float o[E];
   if (L == 0) {
@@ -141,13 +158,15 @@ __device__ __forceinline__ void merge_head(const Dims& m, float eps, uint32_t fl
       rr[e] = (rla && !all_sel) ? ot[e] / den : 0.f;
       ss += rr[e] * rr[e];
     }
-    ss = wave_sum(ss);
+    ss = wave_sum(hf ? 0.f : ss);  // each coordinate once
     const float inv = 1.0f / sqrtf(ss / D + eps);
 #pragma unroll
     for (int e = 0; e < E; ++e) o[e] = rla ? fmaf(gm[e] * rr[e], inv, osp[e]) : osp[e];
   }
+  if (hf == 0) {
 #pragma unroll
-  for (int e = 0; e < E; ++e) Elem<T>::store(out, orow + e, o[e]);
+    for (int e = 0; e < E; ++e) Elem<T>::store(out, orow + e, o[e]);
+  }
 }
 
 // ------------------------------------------------------ matrix-core pass
