@@ -109,10 +109,18 @@ typedef struct spla_config {
  * Caller-owned device buffers that persist across calls. Sizes in bytes are
  * given by spla_cache_bytes (index in brackets). Let nb_cap = max_seq_len / B
  * and n_tiles = ceil(nb_cap / 64).
- *  [0] k_cache   dtype [batch][Hkv][max_seq_len][d]       token-major keys
- *  [1] v_cache   dtype [batch][Hkv][nb_cap][d][B]         values, transposed
- *                inside each block: element (token t, coord c) is at
- *                [t / B][c][t % B]
+ *  [0] k_cache   dtype [batch][Hkv][max_seq_len * d]      keys
+ *  [1] v_cache   dtype [batch][Hkv][max_seq_len * d]      values
+ *                fp32: keys token-major ([t][c]), values transposed inside
+ *                each block ([t / B][c][t % B]).
+ *                bf16: both in 32-token steps of 32 d elements, each step
+ *                stored in the order the matrix-core pass loads it, as
+ *                16-byte chunks of 8 elements (chunk q at element q * 8 of
+ *                step t / 32). With tt = t % 32, key (t, c) is element c % 8
+ *                of chunk ((tt / 4) % 2 * (d / 32) + c / 32) * 64
+ *                + (c / 8) % 4 * 16 + 4 * (tt / 8) + tt % 4, and value
+ *                (t, c) is element tt % 8 of chunk (c / 16) * 64
+ *                + (tt / 8) * 16 + c % 16.
  *  [2] blk_stats fp32  [batch][Hkv][n_tiles][2][d/4][64][4]
  *                part 0 the block key mean, part 1 the block's sum of
  *                squared deviations from it (M2; variance = M2 / n_i). Block

@@ -52,13 +52,26 @@ SPLA_HD Dims make_dims(const spla_config& c) {
 }
 
 // ---- cache buffers (element offsets) ---------------------------------------
-// k_cache [bh][cap][d]
+// fp32 caches: k_cache [bh][cap][d] (token-major), v_cache [bh][nb_cap][d][B]
+// (transposed inside each block). bf16 caches: both [bh][cap / 32][32 d],
+// each 32-token step stored as the 16-byte chunks (8 elements) that lane l
+// of the matrix-core pass loads, chunk q of a step at q * 8 elements:
+//   keys    chunk (mt * d/32 + ks) * 64 + l holds token 8 (i / 4) + 4 mt +
+//           i % 4, coordinates 32 ks + 8 g .. +7   (l = 16 g + i)
+//   values  chunk t * 64 + l holds coordinate 16 t + i, tokens 8 g .. 8 g + 7
+// so that each load instruction of a wavefront reads 1 KiB in one piece.
 SPLA_HD int64_t k_off(const Dims& m, int64_t bh, int64_t t, int j) {
-  return (bh * m.cap + t) * m.d + j;
+  if (m.elem == 4) return (bh * m.cap + t) * m.d + j;
+  const int tt = (int)(t & 31);
+  const int mt = (tt >> 2) & 1, i = 4 * (tt >> 3) + (tt & 3);
+  const int q = (mt * (m.d >> 5) + (j >> 5)) * 64 + ((j >> 3) & 3) * 16 + i;
+  return (bh * m.cap + (t & ~(int64_t)31)) * m.d + q * 8 + (j & 7);
 }
-// v_cache [bh][nb_cap][d][B]
 SPLA_HD int64_t v_off(const Dims& m, int64_t bh, int64_t t, int c) {
-  return ((bh * m.nb_cap + t / m.B) * m.d + c) * m.B + (t % m.B);
+  if (m.elem == 4) return ((bh * m.nb_cap + t / m.B) * m.d + c) * m.B + (t % m.B);
+  const int tt = (int)(t & 31);
+  const int q = (c >> 4) * 64 + (tt >> 3) * 16 + (c & 15);
+  return (bh * m.cap + (t & ~(int64_t)31)) * m.d + q * 8 + (tt & 7);
 }
 // blk_stats [bh][n_tiles][2][d/4][64][4]; returns the offset of the float4
 // holding coordinates 4*j4 .. 4*j4+3 of block `blk`, part 0 (mean) or 1 (M2).

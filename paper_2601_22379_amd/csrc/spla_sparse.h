@@ -353,7 +353,8 @@ __device__ __forceinline__ int sparse_step_entry(int x) {
 // workgroup x (of n_wg) of sequence x KV head bh. blk_sel: this wavefront's
 // block (entry sparse_step_entry of the selection; -1 for none); L: the
 // sequence length. For the two 16-row tiles of a step the key row loaded by
-// lane l is token 8 (i / 4) + 4 tile + (i % 4), i = l % 16, so that after
+// lane l is token 8 (i / 4) + 4 tile + (i % 4), i = l % 16 (the bf16 cache
+// stores each step in exactly this order: k_off, v_off), so that after
 // S = K [Q | phi(Q)]^T the accumulator rows held by lane l are exactly the
 // tokens 8 g .. 8 g + 7 of the step, in order - the layout the second product
 // needs for its B operand. Columns 0..7 carry the exact-branch logits of heads
@@ -389,18 +390,17 @@ __device__ __forceinline__ void sparse_body(const Dims& m, float s,
     const int blk = blk_sel >= nb ? nb - 1 : blk_sel;
     n_valid = min(32, block_count(L, BLK, blk) - ch * 32);
     if (n_valid > 0) {
-      const bf16_t* kblk = kc + ((int64_t)bh * m.cap + (int64_t)blk * BLK + ch * 32) * D;
-      const bf16_t* vblk = vc + ((int64_t)bh * m.nb_cap + blk) * D * BLK + ch * 32;
+      // the step's keys and values, stored in load order (k_off, v_off):
+      // chunk (mt KS + ks) 64 + lane and t 64 + lane
+      const int64_t step0 = ((int64_t)bh * m.cap + (int64_t)blk * BLK + ch * 32) * D;
+      const bf16x8* kst = reinterpret_cast<const bf16x8*>(kc + step0) + lane;
+      const bf16x8* vst = reinterpret_cast<const bf16x8*>(vc + step0) + lane;
 #pragma unroll
-      for (int mt = 0; mt < 2; ++mt) {
-        const int row = 8 * (i >> 2) + 4 * mt + (i & 3);
+      for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks)
-          ka[mt][ks] = *reinterpret_cast<const bf16x8*>(kblk + (int64_t)row * D + 32 * ks + 8 * g);
-      }
+        for (int ks = 0; ks < KS; ++ks) ka[mt][ks] = kst[(mt * KS + ks) * 64];
 #pragma unroll
-      for (int t = 0; t < MT; ++t)
-        va[t] = *reinterpret_cast<const bf16x8*>(vblk + (int64_t)(16 * t + i) * BLK + 8 * g);
+      for (int t = 0; t < MT; ++t) va[t] = vst[t * 64];
     }
   }
   floatx4 acc_o[MT];

@@ -295,14 +295,26 @@ class SplaCache:
         return s[:, :, 0, :nb], s[:, :, 1, :nb]
 
     def k_logical(self):
+        """Keys as [batch][Hkv][max_seq_len][d] (undoing the bf16 step order)."""
         c = self.cfg
-        return self.k.view(c.batch, c.n_kv_heads, c.max_seq_len, c.head_dim)
+        B, H, T, d = c.batch, c.n_kv_heads, c.max_seq_len, c.head_dim
+        if c.dtype == F32:
+            return self.k.view(B, H, T, d)
+        # step chunk (mt, ks, g, a, b) holds token 8a + 4mt + b, coordinates 32ks + 8g ..
+        k = self.k.view(B, H, T // 32, 2, d // 32, 4, 4, 4, 8)
+        return k.permute(0, 1, 2, 6, 3, 7, 4, 5, 8).reshape(B, H, T, d)
 
     def v_logical(self):
+        """Values as [batch][Hkv][max_seq_len][d] (undoing the block transpose
+        of fp32 caches and the step order of bf16 ones)."""
         c = self.cfg
-        nb = c.max_seq_len // c.block_size
-        v = self.v.view(c.batch, c.n_kv_heads, nb, c.head_dim, c.block_size)
-        return v.permute(0, 1, 2, 4, 3).reshape(c.batch, c.n_kv_heads, c.max_seq_len, c.head_dim)
+        B, H, T, d = c.batch, c.n_kv_heads, c.max_seq_len, c.head_dim
+        if c.dtype == F32:
+            v = self.v.view(B, H, T // c.block_size, d, c.block_size)
+            return v.permute(0, 1, 2, 4, 3).reshape(B, H, T, d)
+        # step chunk (t, g, i) holds coordinate 16t + i, tokens 8g .. 8g + 7
+        v = self.v.view(B, H, T // 32, d // 16, 4, 16, 8)
+        return v.permute(0, 1, 2, 4, 6, 3, 5).reshape(B, H, T, d)
 
     def state_logical(self):
         c = self.cfg
