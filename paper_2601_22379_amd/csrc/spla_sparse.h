@@ -383,32 +383,30 @@ __device__ __forceinline__ void sparse_body(const Dims& m, float s,
   const bool live = head < G;
   L = min(max(L, 0), m.cap);
   const int nb = (L + BLK - 1) / BLK;
-  int n_valid = 0;  // tokens of this step that exist
-  bf16x8 ka[2][KS];
-  bf16x8 va[MT];
-  if (blk_sel >= 0 && nb > 0) {
-    const int blk = blk_sel >= nb ? nb - 1 : blk_sel;
-    n_valid = min(32, block_count(L, BLK, blk) - ch * 32);
-    if (n_valid > 0) {
-      // the step's keys and values, stored in load order (k_off, v_off):
-      // chunk (mt KS + ks) 64 + lane and t 64 + lane
-      const int64_t step0 = ((int64_t)bh * m.cap + (int64_t)blk * BLK + ch * 32) * D;
-      const bf16x8* kst = reinterpret_cast<const bf16x8*>(kc + step0) + lane;
-      const bf16x8* vst = reinterpret_cast<const bf16x8*>(vc + step0) + lane;
-#pragma unroll
-      for (int mt = 0; mt < 2; ++mt)
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) ka[mt][ks] = kst[(mt * KS + ks) * 64];
-#pragma unroll
-      for (int t = 0; t < MT; ++t) va[t] = vst[t * 64];
-    }
-  }
+  const int blk = blk_sel >= nb ? nb - 1 : blk_sel;
+  const int n_valid = (blk_sel >= 0 && nb > 0) ? min(32, block_count(L, BLK, blk) - ch * 32) : 0;
   floatx4 acc_o[MT];
 #pragma unroll
   for (int t = 0; t < MT; ++t) acc_o[t] = floatx4{0.f, 0.f, 0.f, 0.f};
   float m_run = -INFINITY, l_run = 0.f;  // exact columns: max / sum; linear columns: sum
   constexpr int NO = (GC * D + 255) / 256;  // outputs (head, coordinate) per thread
+  // loads and their use in one branch: a load issued in one branch and used
+  // in another leaves the compiler assuming it may still be in flight after
+  // them, and it then waits for every store before the record's next ones
   if (n_valid > 0) {
+    // the step's keys and values, stored in load order (k_off, v_off):
+    // chunk (mt KS + ks) 64 + lane and t 64 + lane
+    bf16x8 ka[2][KS];
+    bf16x8 va[MT];
+    const int64_t step0 = ((int64_t)bh * m.cap + (int64_t)blk * BLK + ch * 32) * D;
+    const bf16x8* kst = reinterpret_cast<const bf16x8*>(kc + step0) + lane;
+    const bf16x8* vst = reinterpret_cast<const bf16x8*>(vc + step0) + lane;
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) ka[mt][ks] = kst[(mt * KS + ks) * 64];
+#pragma unroll
+    for (int t = 0; t < MT; ++t) va[t] = vst[t * 64];
     floatx4 sw[2];
     float zinv[2];  // 1 / sum exp(k - max k) of this lane's key row, per tile
 #pragma unroll
