@@ -144,16 +144,19 @@ void decode_kernel(FusedArgs a) {
   // ------------------------------------------------------------ sparse item
   const int j = (int)blockIdx.x - n_score;
   const int bh = j / a.n_wg, x = j % a.n_wg;
+  // this wavefront's block: lane 0 polls its selection word, the first
+  // time before the prologue's loads, so that a workgroup that starts after
+  // its selection has it when the prologue is done
+  const int step = sparse_step_entry<BLK>(x);
+  int32_t* word = sy + y.sel_ready + (int64_t)bh * m.k + step;
+  const bool poller = step < m.k && (tid & 63) == 0;
+  int v = 1;
+  if (poller) v = load_agent(word);
+  const int L = min(max(a.seq_lens[bh / m.hkv], 0), m.cap);  // not produced in this launch
   SparseRegs r;
   sparse_prologue<D, GC>(m, a.q, a.S, a.zbar, bh, x, a.n_wg, r, sm.sp);
   sparse_linear<D, GC>(m, a.S, bh, r, sm.sp);
-  const int L = min(max(a.seq_lens[bh / m.hkv], 0), m.cap);  // before the wait: not produced here
-  // this wavefront's block: poll its selection word (lane 0), then share it
-  const int step = sparse_step_entry<BLK>(x);
-  int32_t* word = sy + y.sel_ready + (int64_t)bh * m.k + step;
-  int v = 1;
-  if (step < m.k && (tid & 63) == 0) {
-    v = load_agent(word);
+  if (poller) {
     for (int n = 0; v == 0 && n < kSpinLimit; ++n) {
       __builtin_amdgcn_s_sleep(4);
       v = load_agent(word);
@@ -163,7 +166,7 @@ void decode_kernel(FusedArgs a) {
   const int blk_sel = __builtin_amdgcn_readfirstlane(v) - 2;
   sparse_body<D, BLK, true, GC>(m, a.s, a.kc, a.vc, blk_sel, L, bh, x, a.n_wg, r, sm.sp, a.part,
                                 a.stride);
-  if (step < m.k && (tid & 63) == 0) store_agent(word, 0);  // read by this workgroup only
+  if (poller) store_agent(word, 0);  // read by this workgroup only
   int32_t* recs = sy + y.recs_done + (int64_t)bh * kSyncLine;
   if (!arrive_last(recs, a.n_wg, &s_flag)) return;
   const int nb = (L + BLK - 1) / BLK;
