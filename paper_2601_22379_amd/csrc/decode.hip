@@ -133,6 +133,9 @@ void decode_kernel(FusedArgs a) {
         bh * m.n_tiles + i * kTilesPerItem, a.e_vals, a.tile_part, sm.sc);
     int32_t* done = sy + y.items_done + (int64_t)bh * kSyncLine;
     if (!arrive_last(done, a.n_si, &s_flag)) return;
+    // the selection is on the path to the head's output: its wavefronts go
+    // ahead of the score items that share their SIMDs
+    __builtin_amdgcn_s_setprio(3);
     select_blocks<256, R, SWN, true, 2>(m, bh, L, a.e_vals, a.tile_part, sm.se,
                                         sy + y.sel_ready + (int64_t)bh * m.k, nullptr,
                                         a.sel_out ? a.sel_out + (int64_t)bh * m.k : nullptr);

@@ -28,9 +28,13 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
 }
 
 template <typename T> struct Elem;
+// store4: elements i .. i + 3 in one store (i a multiple of 4).
 template <> struct Elem<float> {
   static __device__ __forceinline__ float load(const float* p, int64_t i) { return p[i]; }
   static __device__ __forceinline__ void store(float* p, int64_t i, float v) { p[i] = v; }
+  static __device__ __forceinline__ void store4(float* p, int64_t i, const float (&v)[4]) {
+    *reinterpret_cast<float4*>(p + i) = make_float4(v[0], v[1], v[2], v[3]);
+  }
 };
 template <> struct Elem<bf16_t> {
   static __device__ __forceinline__ float load(const bf16_t* p, int64_t i) {
@@ -38,6 +42,11 @@ template <> struct Elem<bf16_t> {
   }
   static __device__ __forceinline__ void store(bf16_t* p, int64_t i, float v) {
     p[i].bits = f32_to_bf16(v);
+  }
+  static __device__ __forceinline__ void store4(bf16_t* p, int64_t i, const float (&v)[4]) {
+    const uint32_t a = f32_to_bf16(v[0]) | ((uint32_t)f32_to_bf16(v[1]) << 16);
+    const uint32_t b = f32_to_bf16(v[2]) | ((uint32_t)f32_to_bf16(v[3]) << 16);
+    *reinterpret_cast<uint2*>(p + i) = make_uint2(a, b);
   }
 };
 

@@ -164,8 +164,12 @@ __device__ __forceinline__ void merge_head(const Dims& m, float eps, uint32_t fl
     for (int e = 0; e < E; ++e) o[e] = rla ? fmaf(gm[e] * rr[e], inv, osp[e]) : osp[e];
   }
   if (hf == 0) {
+    if constexpr (E == 4) {
+      Elem<T>::store4(out, orow, o);
+    } else {
 #pragma unroll
-    for (int e = 0; e < E; ++e) Elem<T>::store(out, orow + e, o[e]);
+      for (int e = 0; e < E; ++e) Elem<T>::store(out, orow + e, o[e]);
+    }
   }
 }
 
