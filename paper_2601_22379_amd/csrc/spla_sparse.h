@@ -34,6 +34,27 @@ typedef float floatx4 __attribute__((ext_vector_type(4)));
 
 constexpr float kLog2e = 1.4426950408889634f;
 
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
+// x = hi + lo as bf16 pairs (about 16 mantissa bits): hi = bf16(x), lo =
+// bf16(x - hi), both rounded to nearest. Each pair of hi is converted once
+// and read back from the packed bits (element 0 in the low half).
+__device__ __forceinline__ void split_bf16x8(const float (&x)[8], bf16x8& hi, bf16x8& lo) {
+  uint32_t hp[4], lp[4];
+#pragma unroll
+  for (int p = 0; p < 4; ++p) {
+    const uint32_t u =
+        __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{x[2 * p], x[2 * p + 1]}, bf16x2));
+    const float h0 = __uint_as_float(u << 16), h1 = __uint_as_float(u & 0xFFFF0000u);
+    hp[p] = u;
+    lp[p] = __builtin_bit_cast(
+        uint32_t, __builtin_convertvector(f32x2{x[2 * p] - h0, x[2 * p + 1] - h1}, bf16x2));
+  }
+  hi = __builtin_bit_cast(bf16x8, make_uint4(hp[0], hp[1], hp[2], hp[3]));
+  lo = __builtin_bit_cast(bf16x8, make_uint4(lp[0], lp[1], lp[2], lp[3]));
+}
+
 // Rows of S_bar owned by workgroup x of n_wg: row0 .. row0 + nrows - 1.
 __device__ __forceinline__ void lin_rows(int D, int x, int n_wg, int* row0, int* nrows) {
   const int rw = (D + n_wg - 1) / n_wg;
@@ -435,14 +456,13 @@ __device__ __forceinline__ void sparse_body(const Dims& m, float s,
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
         bf16x8 fh, fl;
+        float f[8];
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          const float f = __builtin_amdgcn_exp2f(fmaf((float)ka[mt][ks][e], kLog2e, -mxl));
-          sum += f;
-          const __bf16 hi = (__bf16)f;
-          fh[e] = hi;
-          fl[e] = (__bf16)(f - (float)hi);
+          f[e] = __builtin_amdgcn_exp2f(fmaf((float)ka[mt][ks][e], kLog2e, -mxl));
+          sum += f[e];
         }
+        split_bf16x8(f, fh, fl);
         const bf16x8 ph = __builtin_bit_cast(bf16x8, sm.qops[1][ks][lane]);
         const bf16x8 pl = __builtin_bit_cast(bf16x8, sm.qops[2][ks][lane]);
         sw[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fh, ph, sw[mt], 0, 0, 0);
@@ -470,14 +490,13 @@ __device__ __forceinline__ void sparse_body(const Dims& m, float s,
     cmax = fmaxf(cmax, xor32(cmax));
     float psum = 0.f;
     bf16x8 bh8, bl8;
+    float pv[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      const float pv = exact_col ? __builtin_amdgcn_exp2f((val[e] - cmax) * kLog2e) : val[e];
-      psum += pv;
-      const __bf16 hi = (__bf16)pv;
-      bh8[e] = hi;
-      bl8[e] = (__bf16)(pv - (float)hi);
+      pv[e] = exact_col ? __builtin_amdgcn_exp2f((val[e] - cmax) * kLog2e) : val[e];
+      psum += pv[e];
     }
+    split_bf16x8(pv, bh8, bl8);
     psum += xor16(psum);
     psum += xor32(psum);
     m_run = exact_col ? cmax : -INFINITY;
