@@ -159,10 +159,26 @@ void decode_kernel(FusedArgs a) {
   SparseRegs r;
   sparse_prologue<D, GC>(m, a.q, a.S, a.zbar, bh, x, a.n_wg, r, sm.sp);
   sparse_linear<D, GC>(m, a.S, bh, r, sm.sp);
-  if (poller) {
-    for (int n = 0; v == 0 && n < kSpinLimit; ++n) {
-      __builtin_amdgcn_s_sleep(4);
-      v = load_agent(word);
+  if (poller && v == 0) {
+    // three polls in flight: each turn issues one and takes the oldest, so
+    // a published word is seen about one memory round trip after it lands
+    // (one poll at a time would add up to another round trip)
+    // (unrolled by three so that no register of a poll in flight is copied:
+    // a copy would wait for it)
+    int p1 = load_agent(word);
+    __builtin_amdgcn_s_sleep(2);
+    int p2 = load_agent(word);
+    int p3;
+    for (int n = 0; n < kSpinLimit; n += 3) {
+      __builtin_amdgcn_s_sleep(2);
+      p3 = load_agent(word);
+      if ((v = p1) != 0) break;
+      __builtin_amdgcn_s_sleep(2);
+      p1 = load_agent(word);
+      if ((v = p2) != 0) break;
+      __builtin_amdgcn_s_sleep(2);
+      p2 = load_agent(word);
+      if ((v = p3) != 0) break;
     }
     if (v == 0) report_sync_error(a);
   }
