@@ -10,9 +10,9 @@
 //                 selection (select_blocks), which publishes every selected
 //                 block as its own word (block + 2, never 0).
 //   sparse items  one per share x of the fused pass (sparse_body) of each
-//                 (sequence, KV head), in the same order: each wavefront polls
-//                 the word of the block it reads, and the workgroup clears
-//                 those words once read. The workgroup that writes a head's
+//                 (sequence, KV head), in the same order: one lane polls the
+//                 words of the workgroup's blocks (one 16-byte chunk), and
+//                 clears them once read. The workgroup that writes a head's
 //                 last record merges the head's records into its output rows.
 // Only sparse items wait (for their head's selection), and only for score
 // items, which have smaller indices and never wait; workgroups start in index
@@ -23,12 +23,12 @@
 // Data published by one workgroup and read by another (e_vals, tile_part,
 // the selection words, the records) is written and read with
 // device-coherent accesses (Mem<true>: agent-scope atomic loads and stores,
-// which bypass the per-XCD L2 caches); the producer waits for its stores to
-// complete before the word that announces them is updated. No cache-wide
-// writeback or invalidation (agent-scope fences) is used: on this GPU they
-// act on a whole L2 and cost far more than the kilobytes moved. The counters
-// and words are agent-scope atomics, each alone in a 128-byte line
-// (sync_layout). Each call leaves them all at zero: a head's selecting
+// and sc1 buffer loads, which bypass the per-XCD L2 caches); the producer
+// waits for its stores to complete before the word that announces them is
+// updated. No cache-wide writeback or invalidation (agent-scope fences) is
+// used: on this GPU they act on a whole L2 and cost far more than the
+// kilobytes moved. The counters are agent-scope atomics, each alone in a
+// 128-byte line; the selection words of a head share lines (sync_layout). Each call leaves them all at zero: a head's selecting
 // workgroup resets its item counter, its sparse workgroups their selection
 // words, and its merging workgroup its record counter.
 #include "spla_kernels.h"
@@ -118,6 +118,7 @@ void decode_kernel(FusedArgs a) {
     SparseSmem<D, GC> sp;
   } sm;
   __shared__ int s_flag;
+  __shared__ int s_words[4];
   const Dims& m = a.m;
   const SyncLayout& y = a.y;
   int32_t* sy = a.sync;
@@ -147,45 +148,77 @@ void decode_kernel(FusedArgs a) {
   // ------------------------------------------------------------ sparse item
   const int j = (int)blockIdx.x - n_score;
   const int bh = j / a.n_wg, x = j % a.n_wg;
-  // this wavefront's block: lane 0 polls its selection word, the first
-  // time before the prologue's loads, so that a workgroup that starts after
-  // its selection has it when the prologue is done
-  const int step = sparse_step_entry<BLK>(x);
-  int32_t* word = sy + y.sel_ready + (int64_t)bh * m.k + step;
-  const bool poller = step < m.k && (tid & 63) == 0;
-  int v = 1;
-  if (poller) v = load_agent(word);
+  // the workgroup's selection entries (one per step: 4x / (BLK/32) .. of its
+  // four steps, 4 / (BLK/32) of them) are polled by lane 0 of wavefront 0
+  // alone, as the 16-byte chunk holding them, the first time before the
+  // prologue's loads (a workgroup that starts after its selection then has
+  // them when the prologue is done); one poller per workgroup keeps the
+  // polling traffic on the line the selection writes low
+  constexpr int CPB = BLK / 32;
+  constexpr int NE = CPB >= 4 ? 1 : 4 / CPB;  // entries of one workgroup
+  const int e0 = (x * kSparseWaves) / CPB;
+  const int32_t* words = sy + y.sel_ready + (int64_t)bh * m.k;
+  const uint32_t chunk = (uint32_t)(e0 / 4) * 16u;  // the area is padded for the last row
+  const bool poller = tid == 0;
+  auto ready = [&](const uint4& c) {
+    bool ok = true;
+#pragma unroll
+    for (int i = 0; i < NE; ++i) {
+      const int e = e0 + i, c4 = e & 3;
+      const uint32_t v = c4 == 0 ? c.x : (c4 == 1 ? c.y : (c4 == 2 ? c.z : c.w));
+      ok = ok && (e >= m.k || v != 0u);
+    }
+    return ok;
+  };
+  uint4 cv = make_uint4(1u, 1u, 1u, 1u);
+  if (poller) cv = Mem<true>::ld16(words, chunk);
   const int L = min(max(a.seq_lens[bh / m.hkv], 0), m.cap);  // not produced in this launch
   SparseRegs r;
   sparse_prologue<D, GC>(m, a.q, a.S, a.zbar, bh, x, a.n_wg, r, sm.sp);
   sparse_linear<D, GC>(m, a.S, bh, r, sm.sp);
-  if (poller && v == 0) {
+  if (poller && !ready(cv)) {
     // three polls in flight: each turn issues one and takes the oldest, so
     // a published word is seen about one memory round trip after it lands
-    // (one poll at a time would add up to another round trip)
-    // (unrolled by three so that no register of a poll in flight is copied:
-    // a copy would wait for it)
-    int p1 = load_agent(word);
+    // (one poll at a time would add up to another round trip); unrolled by
+    // three so that no register of a poll in flight is copied (a copy
+    // would wait for it)
+    uint4 p1 = Mem<true>::ld16(words, chunk);
     __builtin_amdgcn_s_sleep(2);
-    int p2 = load_agent(word);
-    int p3;
+    uint4 p2 = Mem<true>::ld16(words, chunk);
+    uint4 p3;
+    bool ok = false;
     for (int n = 0; n < kSpinLimit; n += 3) {
       __builtin_amdgcn_s_sleep(2);
-      p3 = load_agent(word);
-      if ((v = p1) != 0) break;
+      p3 = Mem<true>::ld16(words, chunk);
+      if (ready(p1)) { cv = p1; ok = true; break; }
       __builtin_amdgcn_s_sleep(2);
-      p1 = load_agent(word);
-      if ((v = p2) != 0) break;
+      p1 = Mem<true>::ld16(words, chunk);
+      if (ready(p2)) { cv = p2; ok = true; break; }
       __builtin_amdgcn_s_sleep(2);
-      p2 = load_agent(word);
-      if ((v = p3) != 0) break;
+      p2 = Mem<true>::ld16(words, chunk);
+      if (ready(p3)) { cv = p3; ok = true; break; }
     }
-    if (v == 0) report_sync_error(a);
+    if (!ok) {
+      report_sync_error(a);
+      cv = make_uint4(0u, 0u, 0u, 0u);  // entries of a wait that gave up: no block
+    }
   }
+  if (poller) {
+    const uint32_t vals[4] = {cv.x, cv.y, cv.z, cv.w};
+#pragma unroll
+    for (int w = 0; w < kSparseWaves; ++w) s_words[w] = (int)vals[((x * kSparseWaves + w) / CPB) & 3];
+  }
+  __syncthreads();
+  const int step = sparse_step_entry<BLK>(x);
+  const int v = step < m.k ? s_words[tid >> 6] : 1;  // 0 only after a wait that gave up
   const int blk_sel = __builtin_amdgcn_readfirstlane(v) - 2;
   sparse_body<D, BLK, true, GC>(m, a.s, a.kc, a.vc, blk_sel, L, bh, x, a.n_wg, r, sm.sp, a.part,
                                 a.stride);
-  if (poller) store_agent(word, 0);  // read by this workgroup only
+  if (poller) {  // the workgroup's entries, read by it only
+#pragma unroll
+    for (int i = 0; i < NE; ++i)
+      if (e0 + i < m.k) store_agent(const_cast<int32_t*>(words) + e0 + i, 0);
+  }
   int32_t* recs = sy + y.recs_done + (int64_t)bh * kSyncLine;
   if (!arrive_last(recs, a.n_wg, &s_flag)) return;
   const int nb = (L + BLK - 1) / BLK;

@@ -132,7 +132,9 @@ SPLA_HD SyncLayout sync_layout(const Dims& m) {
   y.items_done = kSyncLine;
   y.recs_done = y.items_done + per;
   y.sel_ready = y.recs_done + per;
-  y.words = y.sel_ready + align_up((int64_t)m.bh * m.k, kSyncLine);
+  // (+4: a workgroup reads its entries as the 16-byte chunk holding them,
+  // which may reach 3 words past the last row)
+  y.words = y.sel_ready + align_up((int64_t)m.bh * m.k + 4, kSyncLine);
   return y;
 }
 

@@ -36,11 +36,12 @@ SYNC_LINE = 32  # int32 words per counter line
 def sync_area(cfg, cache):
     """The synchronisation area at the end of the decode workspace: a line
     with the error word, then per (sequence, KV head) a score-item counter
-    line and a record counter line, then the selection words ([bh][k]).
-    Returns the words and the offset of the score-item counters."""
+    line and a record counter line, then the selection words ([bh][k], then
+    4 words of padding, rounded up to whole lines). Returns the words and
+    the offset of the score-item counters."""
     bh = cfg.batch * cfg.n_kv_heads
     items_done = SYNC_LINE
-    n = items_done + 2 * bh * SYNC_LINE + -(-bh * cfg.top_k // SYNC_LINE) * SYNC_LINE
+    n = items_done + 2 * bh * SYNC_LINE + -(-(bh * cfg.top_k + 4) // SYNC_LINE) * SYNC_LINE
     span = -(-n * 4 // spla.WORKSPACE_ALIGN) * spla.WORKSPACE_ALIGN
     total = spla.workspace_bytes(cfg)
     return cache.workspace[total - span:total - span + 4 * n].view(torch.int32), items_done
