@@ -201,10 +201,14 @@ __device__ __forceinline__ void score_tile(const Dims& m, const int32_t* __restr
     }
   }
   // lane (block, qt) finishes heads qt + 4u. ln n and ln(1 + x) are O(1)
-  // and taken in fp32 (absolute error ~1e-7 on ell); ell itself is fp64.
+  // and taken in fp32 from the hardware log2 (about one ulp of log2, so an
+  // absolute error ~1e-7 on ell; ln n is the same for every full block);
+  // x = rv / n uses the hardware reciprocal. ell itself is fp64.
+  constexpr float kLn2f = 0.69314718055994531f;
   const bool valid = blk < nb;
   const int n_i = valid ? block_count(L, m.B, blk) : 1;
-  const double ln_n = (double)logf((float)n_i);
+  const float rcp_n = __builtin_amdgcn_rcpf((float)n_i);
+  const double ln_n = (double)(__builtin_amdgcn_logf((float)n_i) * kLn2f);
   const int nbp = m.n_tiles * kTileBlocks;
   float* ev = e_vals + (int64_t)bh * G * nbp;
   double ell[U];
@@ -212,7 +216,8 @@ __device__ __forceinline__ void score_tile(const Dims& m, const int32_t* __restr
   for (int u = 0; u < U; ++u) {
     const int mm = qt + 4 * u;
     double x = ra[u] + ln_n;
-    if (!first_order) x += (double)log1pf((float)(rv[u] / n_i));
+    if (!first_order)
+      x += (double)(__builtin_amdgcn_logf(1.0f + (float)rv[u] * rcp_n) * kLn2f);
     ell[u] = valid ? x : -INFINITY;
     // the tile offset is the max of the fp32-rounded ell (any common offset
     // works; this one is exact in both precisions)
@@ -220,8 +225,9 @@ __device__ __forceinline__ void score_tile(const Dims& m, const int32_t* __restr
     if ((lane & 15) == 15 && mm < G) s_part[w][mm][0] = (double)mx;
   }
   __syncthreads();
-  // exp(ell - tile max): the tile's 64 blocks share one offset per head; the
-  // fp64 difference enters expf as a hi + lo pair
+  // exp(ell - tile max) = 2^t, t = (ell - tile max) log2(e) in fp64: the
+  // tile's 64 blocks share one offset per head; 2^t is the hardware exp2 of
+  // t's fp32 head times 1 + (the rest of t) ln 2
 #pragma unroll
   for (int u = 0; u < U; ++u) {
     const int mm = qt + 4 * u;
@@ -229,11 +235,11 @@ __device__ __forceinline__ void score_tile(const Dims& m, const int32_t* __restr
       double tmx = -INFINITY;
 #pragma unroll
       for (int x = 0; x < 4; ++x) tmx = fmax(tmx, s_part[x][mm][0]);
-      const double d = ell[u] - tmx;
-      const float dh = (float)d;
-      const float dl = (float)(d - (double)dh);
-      const float eh = expf(dh);
-      const float e = valid ? fmaf(eh, dl, eh) : 0.f;
+      const double t = (ell[u] - tmx) * 1.4426950408889634;
+      const float th = (float)t;
+      const float tl = (float)(t - (double)th);
+      const float eh = __builtin_amdgcn_exp2f(th);
+      const float e = valid ? fmaf(eh, tl * kLn2f, eh) : 0.f;
       Mem<CO>::st(ev + (int64_t)mm * nbp + blk, e);
       const double sum = row_sum_to15((double)e);
       if ((lane & 15) == 15) s_part[w][mm][1] = sum;
