@@ -61,6 +61,28 @@ __device__ __forceinline__ uint32_t lane_xor16(uint32_t x) {
   return (threadIdx.x & 16) ? r[0] : r[1];
 }
 __device__ __forceinline__ float xor32(float x) { return __uint_as_float(lane_xor32(__float_as_uint(x))); }
+// Reduce-scatter steps with one swap and no selects. half_sum(a, b): lanes
+// 0..31 get a(l) + a(l + 32), lanes 32..63 get b(l - 32) + b(l);
+// row_pair_sum(a, b): lanes of even 16-lane rows get a(l) + a(l + 16),
+// lanes of odd rows b(l - 16) + b(l). The permlane swaps exchange exactly
+// the halves (rows) that the other side needs.
+__device__ __forceinline__ double half_sum(double a, double b) {
+  const uint64_t ua = __double_as_longlong(a), ub = __double_as_longlong(b);
+  const auto lo = __builtin_amdgcn_permlane32_swap((uint32_t)ua, (uint32_t)ub, false, false);
+  const auto hi =
+      __builtin_amdgcn_permlane32_swap((uint32_t)(ua >> 32), (uint32_t)(ub >> 32), false, false);
+  return __longlong_as_double((long long)(((uint64_t)hi[0] << 32) | lo[0])) +
+         __longlong_as_double((long long)(((uint64_t)hi[1] << 32) | lo[1]));
+}
+__device__ __forceinline__ double row_pair_sum(double a, double b) {
+  const uint64_t ua = __double_as_longlong(a), ub = __double_as_longlong(b);
+  const auto lo = __builtin_amdgcn_permlane16_swap((uint32_t)ua, (uint32_t)ub, false, false);
+  const auto hi =
+      __builtin_amdgcn_permlane16_swap((uint32_t)(ua >> 32), (uint32_t)(ub >> 32), false, false);
+  return __longlong_as_double((long long)(((uint64_t)hi[0] << 32) | lo[0])) +
+         __longlong_as_double((long long)(((uint64_t)hi[1] << 32) | lo[1]));
+}
+
 __device__ __forceinline__ float xor16(float x) { return __uint_as_float(lane_xor16(__float_as_uint(x))); }
 __device__ __forceinline__ double xor32(double x) {
   const uint64_t u = __double_as_longlong(x);

@@ -180,25 +180,25 @@ __device__ __forceinline__ void score_tile(const Dims& m, const int32_t* __restr
       av[mm] += (double)pb[mm];
     }
   });
-  // reduce-scatter over the four quarters (lanes l ^ 16, l ^ 32): lane
-  // (block, qt) ends with the sums of heads qt + 4u, u < U (zero past G)
+  // reduce-scatter over the four quarters (qt = lane / 16): lane (block, qt)
+  // ends with the sums of heads qt + 4u, u < U (zero past G). Quarters 0, 1
+  // keep heads 4u, 4u + 1 and quarters 2, 3 heads 4u + 2, 4u + 3 (half_sum),
+  // then even quarters keep the first of those, odd ones the second
+  // (row_pair_sum).
   double ra[U], rv[U];
-  {
-    const bool k1 = (qt & 2) != 0, k0 = (qt & 1) != 0;
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      double ta[2], tv[2];
+  for (int u = 0; u < U; ++u) {
+    double ta[2], tv[2];
 #pragma unroll
-      for (int r0 = 0; r0 < 2; ++r0) {
-        const int hl = 4 * u + r0, hh = hl + 2;
-        const double al = hl < G ? am[hl < G ? hl : 0] : 0.0, ah = hh < G ? am[hh < G ? hh : 0] : 0.0;
-        const double vl = hl < G ? av[hl < G ? hl : 0] : 0.0, vh = hh < G ? av[hh < G ? hh : 0] : 0.0;
-        ta[r0] = (k1 ? ah : al) + xor32(k1 ? al : ah);
-        tv[r0] = (k1 ? vh : vl) + xor32(k1 ? vl : vh);
-      }
-      ra[u] = (k0 ? ta[1] : ta[0]) + xor16(k0 ? ta[0] : ta[1]);
-      rv[u] = (k0 ? tv[1] : tv[0]) + xor16(k0 ? tv[0] : tv[1]);
+    for (int r0 = 0; r0 < 2; ++r0) {
+      const int hl = 4 * u + r0, hh = hl + 2;
+      const double al = hl < G ? am[hl < G ? hl : 0] : 0.0, ah = hh < G ? am[hh < G ? hh : 0] : 0.0;
+      const double vl = hl < G ? av[hl < G ? hl : 0] : 0.0, vh = hh < G ? av[hh < G ? hh : 0] : 0.0;
+      ta[r0] = half_sum(al, ah);
+      tv[r0] = half_sum(vl, vh);
     }
+    ra[u] = row_pair_sum(ta[0], ta[1]);
+    rv[u] = row_pair_sum(tv[0], tv[1]);
   }
   // lane (block, qt) finishes heads qt + 4u. ln n and ln(1 + x) are O(1)
   // and taken in fp32 from the hardware log2 (about one ulp of log2, so an
