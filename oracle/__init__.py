@@ -15,6 +15,9 @@ from .spla_oracle import (  # noqa: F401
     DecodeResult,
     block_ranges,
     block_stats,
+    window_ranges,
+    window_stats,
+    pool_windows_to_blocks,
     feature_map,
     global_state,
     log_block_mass,

@@ -38,6 +38,14 @@ step it affects):
   weight gamma, eps 1e-6) of the residual to the exact output, with no gate
   beyond gamma (Sec. 3.3).
 * an empty sequence (L = 0) decodes to a zero output with no selection.
+* strided block selection (Sec. 3.1, "Strided Block Selection"; optional):
+  window w covers tokens [w s, min(w s + C, L)), one window per start below
+  L, so the last windows may be partial and use their real counts. Each
+  window gets the Taylor mass of its own keys; the per-head normaliser Z sums
+  the masses of all windows; the group score of a window is Eq. (6) over
+  windows; a block's relevance is the maximum group score over every window
+  that shares a token with the block. With C = s = B the windows are the
+  blocks and nothing changes.
 """
 
 from __future__ import annotations
@@ -72,18 +80,31 @@ class SplaParams:
     first_order: bool = False
     no_rla: bool = False
     rla_normalize: bool = False
+    window: Optional[int] = None
+    stride: Optional[int] = None
 
     def scale(self, d: int) -> float:
         return (1.0 / math.sqrt(d)) if self.softmax_scale is None else float(self.softmax_scale)
+
+    def windows(self):
+        """(C, s) of the selection windows; one window per block (C = s = B)
+        unless window and stride are given (the paper's runs: C = 32, s = 16)."""
+        C = self.block_size if self.window is None else int(self.window)
+        st = self.block_size if self.stride is None else int(self.stride)
+        if not 1 <= st <= C:
+            raise ValueError("selection windows need 1 <= stride <= window")
+        return C, st
 
 
 @dataclass
 class KVState:
     """What the append step maintains for one KV head (Sec. 3.1 and Eq. 15).
 
-    mean, var: [nb, d] per-block key mean and diagonal population variance;
-    counts: [nb] tokens per block; s_bar: [d, d] global linear-attention
-    state; z_bar: [d] sum of phi(k) (kept for the optional normaliser).
+    mean, var: [n, d] key mean and diagonal population variance of each
+    scoring unit; counts: [n] tokens per unit; s_bar: [d, d] global
+    linear-attention state; z_bar: [d] sum of phi(k) (kept for the optional
+    normaliser). The units are the blocks when window is None, else the
+    selection windows of size window and stride stride.
     """
 
     mean: np.ndarray
@@ -92,6 +113,8 @@ class KVState:
     s_bar: np.ndarray
     z_bar: np.ndarray
     length: int
+    window: Optional[int] = None
+    stride: Optional[int] = None
 
 
 @dataclass
@@ -99,9 +122,11 @@ class DecodeResult:
     """Everything the decode step produces for one KV head group.
 
     out [G, d]; sel: selected block ids ascending (length <= k); score [nb];
-    ell [G, nb] per-head log block mass; o_sparse [G, d]; r [G, d] residual
-    (zero when nothing is unselected or the RLA branch is off); o_bar and
-    o_tilde [G, d]; n_forced: number of forced blocks (0 when nb <= k).
+    ell [G, n] per-head log mass of the n scoring units (the blocks, or the
+    selection windows, whose group scores are then extras["window_score"]);
+    o_sparse [G, d]; r [G, d] residual (zero when nothing is unselected or
+    the RLA branch is off); o_bar and o_tilde [G, d]; n_forced: number of
+    forced blocks (0 when nb <= k).
     """
 
     out: np.ndarray
@@ -149,6 +174,46 @@ def block_stats(K: np.ndarray, L: int, B: int):
         var[i] = ((blk - mean[i]) ** 2).mean(axis=0)
         counts[i] = b - a
     return mean, var, counts
+
+
+def window_ranges(L: int, C: int, s: int) -> list:
+    """Token ranges of the strided selection windows (Sec. 3.1, "Strided
+    Block Selection": windows of C tokens every s tokens). 0-based: window w
+    holds tokens [ws, min(ws + C, L)) for every start ws < L, so the last
+    windows may be partial."""
+    nw = -(-L // s)
+    return [(w * s, min(w * s + C, L)) for w in range(nw)]
+
+
+def window_stats(K: np.ndarray, L: int, C: int, s: int):
+    """Key mean and diagonal population covariance of every selection window
+    (the block statistics of Sec. 3.1 taken over a window's tokens).
+    Returns mean [nw, d], var [nw, d], counts [nw]."""
+    K = np.asarray(K, dtype=f64)
+    ranges = window_ranges(L, C, s)
+    d = K.shape[-1]
+    mean = np.zeros((len(ranges), d), dtype=f64)
+    var = np.zeros((len(ranges), d), dtype=f64)
+    counts = np.zeros(len(ranges), dtype=np.int64)
+    for w, (a, b) in enumerate(ranges):
+        win = K[a:b]
+        mean[w] = win.mean(axis=0)
+        var[w] = ((win - mean[w]) ** 2).mean(axis=0)
+        counts[w] = b - a
+    return mean, var, counts
+
+
+def pool_windows_to_blocks(wscore: np.ndarray, L: int, B: int, C: int, s: int) -> np.ndarray:
+    """Block relevance by max-pooling window scores (Sec. 3.1, "Strided
+    Block Selection"). Reading: block i takes the largest score among the
+    windows that share at least one token with it. Returns score [nb]."""
+    wscore = np.asarray(wscore, dtype=f64)
+    wr = np.array(window_ranges(L, C, s), dtype=np.int64).reshape(-1, 2)
+    out = np.zeros(-(-L // B), dtype=f64)
+    for i, (a, b) in enumerate(block_ranges(L, B)):
+        touching = (wr[:, 0] < b) & (wr[:, 1] > a)
+        out[i] = wscore[touching].max()
+    return out
 
 
 # ---------------------------------------------------------- O3 feature map
@@ -308,26 +373,44 @@ def combine(o_sparse: np.ndarray, r: np.ndarray, gamma: np.ndarray, eps: float) 
 
 
 # ------------------------------------------------------ state and decode
-def build_state(K: np.ndarray, V: np.ndarray, L: int, B: int) -> KVState:
-    """State of one KV head after its first L tokens were appended."""
-    mean, var, counts = block_stats(K, L, B)
+def build_state(K: np.ndarray, V: np.ndarray, L: int, B: int,
+                window: Optional[int] = None, stride: Optional[int] = None) -> KVState:
+    """State of one KV head after its first L tokens were appended; the
+    statistics are per block, or per selection window when window and
+    stride are given (C = s = B is the block path)."""
+    if (window, stride) == (B, B):
+        window = stride = None
+    if window is None and stride is None:
+        mean, var, counts = block_stats(K, L, B)
+    else:
+        mean, var, counts = window_stats(K, L, window, stride)
     s_bar, z_bar = global_state(K, V, L)
-    return KVState(mean, var, counts, s_bar, z_bar, L)
+    return KVState(mean, var, counts, s_bar, z_bar, L, window, stride)
 
 
 def append_state(state: Optional[KVState], k_new: np.ndarray, v_new: np.ndarray, B: int,
-                 d: Optional[int] = None) -> KVState:
+                 d: Optional[int] = None, window: Optional[int] = None,
+                 stride: Optional[int] = None) -> KVState:
     """Streaming append of tokens, one at a time (Eq. 15 for the state; the
-    block statistics updated with Welford's recurrence for the mean and the
-    sum of squared deviations). A decode issued after an append sees the
-    appended tokens (the query at position N attends to 1..N, Sec. 2)."""
+    statistics of every unit that holds the token updated with Welford's
+    recurrence for the mean and the sum of squared deviations). The units are
+    the blocks, or the selection windows when window and stride are given: a
+    token at position t lies in the windows whose start ws satisfies
+    ws <= t < ws + C. A decode issued after an append sees the appended tokens
+    (the query at position N attends to 1..N, Sec. 2)."""
     k_new = np.asarray(k_new, dtype=f64)
     v_new = np.asarray(v_new, dtype=f64)
+    if (window, stride) == (B, B):
+        window = stride = None
     if d is None:
         d = k_new.shape[-1]
     if state is None:
         state = KVState(np.zeros((0, d)), np.zeros((0, d)), np.zeros(0, dtype=np.int64),
-                        np.zeros((d, d)), np.zeros(d), 0)
+                        np.zeros((d, d)), np.zeros(d), 0, window, stride)
+    elif (state.window, state.stride) != (window, stride):
+        raise ValueError("append with other selection windows than the state holds")
+    C = B if window is None else window
+    st = B if stride is None else stride
     mean = [row.copy() for row in state.mean]
     m2 = [state.var[i] * state.counts[i] for i in range(len(state.counts))]
     counts = [int(c) for c in state.counts]
@@ -335,22 +418,24 @@ def append_state(state: Optional[KVState], k_new: np.ndarray, v_new: np.ndarray,
     z_bar = state.z_bar.copy()
     L = state.length
     for k, v in zip(k_new, v_new):
-        i = L // B
-        if i == len(counts):
+        if L % st == 0:  # token L opens unit L / s
             mean.append(np.zeros(d))
             m2.append(np.zeros(d))
             counts.append(0)
-        counts[i] += 1
-        delta = k - mean[i]
-        mean[i] = mean[i] + delta / counts[i]
-        m2[i] = m2[i] + delta * (k - mean[i])
+        for i in range(max(0, len(counts) - C // st - 2), len(counts)):
+            if not i * st <= L < i * st + C:
+                continue
+            counts[i] += 1
+            delta = k - mean[i]
+            mean[i] = mean[i] + delta / counts[i]
+            m2[i] = m2[i] + delta * (k - mean[i])
         phik = feature_map(k)
         s_bar += np.outer(phik, v)
         z_bar += phik
         L += 1
     cnt = np.array(counts, dtype=np.int64)
     var = np.array([m2[i] / counts[i] for i in range(len(counts))]).reshape(-1, d)
-    return KVState(np.array(mean).reshape(-1, d), var, cnt, s_bar, z_bar, L)
+    return KVState(np.array(mean).reshape(-1, d), var, cnt, s_bar, z_bar, L, window, stride)
 
 
 def decode_kv_head(q: np.ndarray, state: KVState, K: np.ndarray, V: np.ndarray,
@@ -371,8 +456,17 @@ def decode_kv_head(q: np.ndarray, state: KVState, K: np.ndarray, V: np.ndarray,
         return DecodeResult(z.copy(), np.zeros(0, dtype=np.int64), np.zeros(0), np.zeros((G, 0)),
                             z.copy(), z.copy(), z.copy(), z.copy(), 0)
     s = p.scale(d)
+    C, st = p.windows()
+    strided = (C, st) != (B, B)
+    if (state.window, state.stride) != ((C, st) if strided else (None, None)):
+        raise ValueError("the state's statistics are not over the selection windows of p")
+    # per-unit (block, or window) log mass and Eq. (6) group score over units
     ell = log_block_mass(q, state.mean, state.var, state.counts, s, p.first_order)
     score = group_block_scores(ell)
+    extras = {}
+    if strided:
+        extras["window_score"] = score
+        score = pool_windows_to_blocks(score, L, B, C, st)
     nb = len(score)
     if force_selection is None:
         sel = select_blocks(score, k, p.n_sink, p.n_local)
@@ -384,11 +478,11 @@ def decode_kv_head(q: np.ndarray, state: KVState, K: np.ndarray, V: np.ndarray,
     if p.no_rla:
         z = np.zeros_like(o_sparse)
         return DecodeResult(o_sparse.copy(), sel, score, ell, o_sparse, z, z.copy(), z.copy(),
-                            n_forced)
+                            n_forced, extras)
     r, o_bar, o_tilde = residual_linear_attention(q, state.s_bar, state.z_bar, K, V, tok, L,
                                                   p.rla_normalize)
     out = combine(o_sparse, r, gamma, p.rms_eps)
-    return DecodeResult(out, sel, score, ell, o_sparse, r, o_bar, o_tilde, n_forced)
+    return DecodeResult(out, sel, score, ell, o_sparse, r, o_bar, o_tilde, n_forced, extras)
 
 
 def decode_from_state(q: np.ndarray, states: Sequence[KVState], K: np.ndarray, V: np.ndarray,
@@ -412,5 +506,7 @@ def decode_from_state(q: np.ndarray, states: Sequence[KVState], K: np.ndarray, V
 def decode_sequence(q: np.ndarray, K: np.ndarray, V: np.ndarray, L: int, gamma: np.ndarray,
                     p: SplaParams, force_selection=None):
     """Append the first L tokens of every KV head, then decode q."""
-    states = [build_state(K[h], V[h], L, p.block_size) for h in range(K.shape[0])]
+    C, st = p.windows()
+    win = (None, None) if (C, st) == (p.block_size, p.block_size) else (C, st)
+    states = [build_state(K[h], V[h], L, p.block_size, *win) for h in range(K.shape[0])]
     return decode_from_state(q, states, K, V, gamma, p, force_selection)

@@ -13,6 +13,7 @@ import pytest
 import oracle as O
 import oracle.spla_oracle as OS
 import test_oracle_pins as P
+import test_oracle_windows as W
 
 
 def _patch(monkeypatch, name, fn):
@@ -166,3 +167,37 @@ def test_forced_blocks_dropped(monkeypatch, flip):
         return orig(nb, k, n_sink, 0)
     _patch(monkeypatch, "forced_blocks", bad)
     _expect_failure((P.test_forced_blocks_always_selected_even_with_lowest_scores, ()))
+
+
+def _pool(rule):
+    def f(wscore, L, B, C, s):
+        wscore = np.asarray(wscore, dtype=float)
+        out = np.zeros(-(-L // B))
+        for i, (a, b) in enumerate(OS.block_ranges(L, B)):
+            ws = [w for w in range(len(wscore))
+                  if (rule == "start" and a <= w * s < b)
+                  or (rule == "inside" and a <= w * s and min(w * s + C, L) <= b)]
+            out[i] = max(wscore[w] for w in ws) if ws else 0.0
+        return out
+    return f
+
+
+@pytest.mark.parametrize("rule", ["start", "inside"])
+def test_pooling_over_the_wrong_windows(monkeypatch, rule):
+    """Blocks pooling only the windows that start in them, or only those
+    inside them, in place of every window that touches them."""
+    _patch(monkeypatch, "pool_windows_to_blocks", _pool(rule))
+    _expect_failure((W.test_x17_pooling_matches_token_set_overlap, (117, 32, 32, 16)),
+                    (W.test_x18_planted_tokens_at_a_block_end_select_both_blocks, ()))
+
+
+@pytest.mark.parametrize("mistake", ["no_partial", "short"])
+def test_wrong_window_ranges(monkeypatch, mistake):
+    """Partial windows at the end dropped, or every window a token short."""
+    def bad(L, C, s):
+        if mistake == "no_partial":
+            return [(w * s, w * s + C) for w in range(L // s) if w * s + C <= L]
+        return [(w * s, min(w * s + C - 1, L)) for w in range(-(-L // s))]
+    _patch(monkeypatch, "window_ranges", bad)
+    _expect_failure((W.test_x15_constant_keys_window_and_block_scores_closed_form, ()),
+                    (W.test_x16_window_mass_matches_token_sum, (32, 16)))
