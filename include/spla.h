@@ -103,12 +103,21 @@ typedef struct spla_config {
                              logits and the query inside the block score */
   float rms_eps;          /* epsilon of the RMSNorm on the residual, >= 0 (1e-6) */
   uint32_t flags;         /* SPLA_FLAG_* */
+  int32_t sel_window;     /* strided block selection (Sec. 3.1): the block score is
+                             the largest group score of the windows of sel_window
+                             tokens, one starting every sel_stride tokens, that
+                             share a token with the block (the paper: 32 and 16).
+                             Both 0: one window per block. Otherwise sel_stride
+                             divides block_size, sel_window is 1 to 4 times
+                             sel_stride, max_seq_len / sel_stride <= 16384, and
+                             the decode runs as separate launches */
+  int32_t sel_stride;
 } spla_config;
 
 /* ------------------------------------------------------------------- cache
  * Caller-owned device buffers that persist across calls. Sizes in bytes are
  * given by spla_cache_bytes (index in brackets). Let nb_cap = max_seq_len / B
- * and n_tiles = ceil(nb_cap / 64).
+ * and n_tiles = ceil(nb_cap / 64) (see [2] for strided selection).
  *  [0] k_cache   dtype [batch][Hkv][max_seq_len * d]      keys
  *  [1] v_cache   dtype [batch][Hkv][max_seq_len * d]      values
  *                fp32: keys token-major ([t][c]), values transposed inside
@@ -126,7 +135,9 @@ typedef struct spla_config {
  *                squared deviations from it (M2; variance = M2 / n_i). Block
  *                i of a sequence is entry i % 64 of tile i / 64: for each
  *                group of four coordinates, 64 consecutive blocks are stored
- *                side by side
+ *                side by side. With strided selection the entries are the
+ *                windows (window w: tokens w * sel_stride .. + sel_window - 1)
+ *                and n_tiles = ceil(max_seq_len / sel_stride / 64)
  *  [3] lin_state fp32  [batch][Hkv][d][d]  S_bar[j][c] = sum_t phi(k_t)_j v_t,c (Eq. 15)
  *  [4] lin_norm  fp32  [batch][Hkv][d]     z_bar = sum_t phi(k_t)
  *  [5] seq_lens  int32 [batch]             tokens held by each sequence

@@ -19,10 +19,12 @@ __device__ __forceinline__ int appended_count(const Dims& m, int L0, int max_new
   return n < room ? n : room;
 }
 
-// One workgroup per touched block: copies the new rows of that block into
-// the caches and merges the block's statistics. The new tokens' mean and M2
-// are computed two-pass in fp64 and combined with the stored ones by Chan's
-// formula, then rounded to fp32.
+// One workgroup per touched statistics unit (a block, or a strided selection
+// window: unit u holds tokens u us .. u us + ul - 1): merges the new tokens
+// of the unit into its statistics and copies the rows t with
+// u us <= t < (u + 1) us into the caches, so that each row is copied by
+// exactly one unit. The new tokens' mean and M2 are computed two-pass in fp64
+// and combined with the stored ones by Chan's formula, then rounded to fp32.
 template <typename T>
 __global__ __launch_bounds__(128) void append_blocks_kernel(
     Dims m, T* __restrict__ kc, T* __restrict__ vc, float* __restrict__ stats,
@@ -35,9 +37,12 @@ __global__ __launch_bounds__(128) void append_blocks_kernel(
   const int ne = appended_count(m, L0, max_new, n_new, b, &clipped);
   if (clipped && err && blockIdx.x == 0 && bh % m.hkv == 0 && threadIdx.x == 0)
     atomicOr(err, (int)SPLA_DEVERR_CAPACITY);
-  const int i = L0 / m.B + (int)blockIdx.x;
-  const int t_lo = max(L0, i * m.B);
-  const int t_hi = min(L0 + ne, (i + 1) * m.B);
+  // first unit holding token L0: u us + ul > L0
+  const int first = L0 >= m.ul ? (L0 - m.ul) / m.us + 1 : 0;
+  const int i = first + (int)blockIdx.x;
+  const int t_lo = max(L0, i * m.us);
+  const int t_hi = min(L0 + ne, i * m.us + m.ul);
+  const int t_own = min(t_hi, (i + 1) * m.us);  // rows this unit copies: t_lo .. t_own - 1
   const int j = threadIdx.x;
   if (t_hi <= t_lo || j >= m.d) return;
   const int64_t src0 = ((int64_t)bh * max_new - L0) * m.d + j;  // row t at src0 + t*d
@@ -45,8 +50,10 @@ __global__ __launch_bounds__(128) void append_blocks_kernel(
   double sum = 0.0;
   for (int t = t_lo; t < t_hi; ++t) {
     const T kv = k_new[src0 + (int64_t)t * m.d];
-    kc[k_off(m, bh, t, j)] = kv;
-    vc[v_off(m, bh, t, j)] = v_new[src0 + (int64_t)t * m.d];
+    if (t < t_own) {
+      kc[k_off(m, bh, t, j)] = kv;
+      vc[v_off(m, bh, t, j)] = v_new[src0 + (int64_t)t * m.d];
+    }
     sum += (double)Elem<T>::load(&kv, 0);
   }
   const int nc = t_hi - t_lo;
@@ -56,7 +63,7 @@ __global__ __launch_bounds__(128) void append_blocks_kernel(
     const double x = (double)Elem<T>::load(k_new, src0 + (int64_t)t * m.d) - mean_c;
     m2_c += x * x;
   }
-  const int na = t_lo - i * m.B;
+  const int na = t_lo - i * m.us;
   const int64_t o_mean = stats_off4(m, bh, i, 0, j / 4) + (j & 3);
   const int64_t o_m2 = stats_off4(m, bh, i, 1, j / 4) + (j & 3);
   double mean = mean_c, m2 = m2_c;
@@ -239,7 +246,9 @@ __global__ void fill_zero_kernel(uint32_t* __restrict__ p, int64_t n) {
 hipError_t launch_append_blocks(const Dims& m, const spla_cache& c, const void* k_new,
                                 const void* v_new, int max_new, const int32_t* n_new,
                                 hipStream_t st) {
-  dim3 grid((unsigned)(ceil_div(max_new, m.B) + 1), (unsigned)m.bh);
+  // units touched by max_new tokens from any L0 (idle workgroups return)
+  const int64_t nx = windowed(m) ? ceil_div(max_new + m.ul, m.us) + 2 : ceil_div(max_new, m.B) + 1;
+  dim3 grid((unsigned)nx, (unsigned)m.bh);
   if (m.elem == 4)
     hipLaunchKernelGGL(append_blocks_kernel<float>, grid, dim3(128), 0, st, m, (float*)c.k_cache,
                        (float*)c.v_cache, c.blk_stats, c.seq_lens, c.err_flags,

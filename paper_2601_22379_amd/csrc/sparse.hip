@@ -246,7 +246,7 @@ static void valu_td(const Dims& m, const spla_config& cfg, float s, const spla_c
 // which pays only while the grid is small (about two workgroups per compute
 // unit) and the block count is at most 4096.
 static int sparse_select_r(const Dims& m) {
-  if (!use_mfma_sparse(m) || m.nb_cap > 256 * 16) return 0;
+  if (!use_mfma_sparse(m) || m.nb_cap > 256 * 16 || windowed(m)) return 0;
   const DecodeWs ws = decode_ws_layout(m);
   if ((int64_t)ws.n_wg * m.bh > 2 * (int64_t)compute_units()) return 0;
   const int per = (int)ceil_div(m.nb_cap, 256);

@@ -53,6 +53,13 @@ extern "C" int32_t spla_validate(const spla_config* c) {
   const uint32_t known = SPLA_FLAG_NO_RLA | SPLA_FLAG_FIRST_ORDER | SPLA_FLAG_RLA_NORMALIZE |
                          SPLA_FLAG_SEPARATE_KERNELS;
   if (c->flags & ~known) return SPLA_ERR_INVALID_ARG;
+  if (c->sel_window != 0 || c->sel_stride != 0) {  // strided selection windows
+    if (c->sel_stride < 1 || c->sel_window < c->sel_stride) return SPLA_ERR_INVALID_ARG;
+    if (c->block_size % c->sel_stride != 0 || c->sel_window % c->sel_stride != 0 ||
+        c->sel_window > 4 * c->sel_stride)
+      return SPLA_ERR_UNSUPPORTED;
+    if (c->max_seq_len / c->sel_stride > spla::kMaxWindows) return SPLA_ERR_CAPACITY;
+  }
   // every derived byte count must fit comfortably in 63 bits
   const Dims m = spla::make_dims(*c);
   const double kv = (double)m.bh * m.cap * m.d * 4.0;

@@ -19,6 +19,7 @@ namespace spla {
 constexpr int kTileBlocks = 64;   // blocks per statistics tile (one wavefront)
 constexpr int kSubTokens = 32;    // tokens per sparse-pass sub-tile
 constexpr int kAppendChunkTarget = 2048;  // append state-partial workgroups to aim for
+constexpr int kMaxWindows = 16384;  // strided selection windows per sequence at capacity
 
 SPLA_HD int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 SPLA_HD int64_t align_up(int64_t a, int64_t b) { return ceil_div(a, b) * b; }
@@ -27,7 +28,10 @@ SPLA_HD int64_t align_up(int64_t a, int64_t b) { return ceil_div(a, b) * b; }
 struct Dims {
   int batch, hq, hkv, group, d, B, k, n_sink, n_local, cap;
   int nb_cap;    // blocks per sequence at capacity
-  int n_tiles;   // statistics tiles per (sequence, kv head)
+  int us, ul;    // scoring units: unit u holds tokens u us .. u us + ul - 1 (the
+                 // blocks, us = ul = B, or the strided selection windows)
+  int nu_cap;    // units per sequence at capacity
+  int n_tiles;   // statistics tiles (64 units) per (sequence, kv head)
   int bh;        // batch * hkv
   int elem;      // bytes per q / K / V / out element
 };
@@ -45,7 +49,11 @@ SPLA_HD Dims make_dims(const spla_config& c) {
   m.n_local = c.n_local_blocks;
   m.cap = c.max_seq_len;
   m.nb_cap = c.max_seq_len / c.block_size;
-  m.n_tiles = (int)ceil_div(m.nb_cap, kTileBlocks);
+  const bool win = c.sel_window != 0 || c.sel_stride != 0;
+  m.us = win ? c.sel_stride : c.block_size;
+  m.ul = win ? c.sel_window : c.block_size;
+  m.nu_cap = c.max_seq_len / m.us;
+  m.n_tiles = (int)ceil_div(m.nu_cap, kTileBlocks);
   m.bh = c.batch * c.n_kv_heads;
   m.elem = c.dtype == SPLA_F32 ? 4 : 2;
   return m;
@@ -73,8 +81,11 @@ SPLA_HD int64_t v_off(const Dims& m, int64_t bh, int64_t t, int c) {
   const int q = (c >> 4) * 64 + (tt >> 3) * 16 + (c & 15);
   return (bh * m.cap + (t & ~(int64_t)31)) * m.d + q * 8 + (tt & 7);
 }
+// Whether the scoring units are strided selection windows rather than blocks.
+SPLA_HD bool windowed(const Dims& m) { return m.us != m.B || m.ul != m.B; }
+
 // blk_stats [bh][n_tiles][2][d/4][64][4]; returns the offset of the float4
-// holding coordinates 4*j4 .. 4*j4+3 of block `blk`, part 0 (mean) or 1 (M2).
+// holding coordinates 4*j4 .. 4*j4+3 of unit `blk`, part 0 (mean) or 1 (M2).
 SPLA_HD int64_t stats_off4(const Dims& m, int64_t bh, int64_t blk, int part, int j4) {
   return ((((bh * m.n_tiles + blk / kTileBlocks) * 2 + part) * (m.d / 4) + j4) * kTileBlocks +
           blk % kTileBlocks) * 4;
@@ -85,8 +96,8 @@ constexpr int kPartHead = 48;     // per-record header: m[16], l[16], zw[16]
 constexpr int kSparseWaves = 4;   // waves per sparse workgroup
 
 struct DecodeWs {
-  int64_t e_vals;     // f32 [bh][G][n_tiles*64]   exp(ell - tile max)
-  int64_t tile_part;  // f64 [bh][G][n_tiles][2]   (max, sum) per 64-block tile
+  int64_t e_vals;     // f32 [bh][G][n_tiles*64]   exp(ell - tile max), per unit
+  int64_t tile_part;  // f64 [bh][G][n_tiles][2]   (max, sum) per 64-unit tile
   int64_t sel;        // i32 [bh][k]               selected blocks, ascending
   int64_t meta;       // i32 [bh][4]               (n_selected, all_selected, length, 0)
   int64_t part;       // f32 [bh][n_wg][part_stride]  sparse workgroup partials
@@ -110,7 +121,7 @@ constexpr int kFusedMaxBlocks = 256 * 32;
 constexpr int kFusedMaxGroup = 6;
 SPLA_HD bool use_fused_decode(const Dims& m) {
   return use_mfma_sparse(m) && m.d == 128 && m.group <= kFusedMaxGroup &&
-         m.nb_cap <= kFusedMaxBlocks;
+         m.nb_cap <= kFusedMaxBlocks && !windowed(m);
 }
 
 // The decode workspace's synchronisation area (int32 words). Every counter

@@ -142,7 +142,7 @@ __device__ __forceinline__ void score_tile(const Dims& m, const int32_t* __restr
   const int bh = t / m.n_tiles, tile = t % m.n_tiles;
   const int blk = tile * kTileBlocks + kScoreGroup * w + (lane & 15);
   const int L = seq_lens[bh / m.hkv];
-  const int nb = (L + m.B - 1) / m.B;
+  const int nb = (L + m.us - 1) / m.us;  // units (blocks or windows) present
   // this lane's coefficients: cf[k] holds entry 16 k + (lane % 16) of its
   // quarter's table, read once per tile
   constexpr int NK = (2 * G * 32) / 16;
@@ -206,7 +206,7 @@ __device__ __forceinline__ void score_tile(const Dims& m, const int32_t* __restr
   // x = rv / n uses the hardware reciprocal. ell itself is fp64.
   constexpr float kLn2f = 0.69314718055994531f;
   const bool valid = blk < nb;
-  const int n_i = valid ? block_count(L, m.B, blk) : 1;
+  const int n_i = valid ? min(m.ul, L - blk * m.us) : 1;  // tokens of the unit
   const float rcp_n = __builtin_amdgcn_rcpf((float)n_i);
   const double ln_n = (double)(__builtin_amdgcn_logf((float)n_i) * kLn2f);
   const int nbp = m.n_tiles * kTileBlocks;

@@ -153,14 +153,18 @@ struct SelectSmem {
 // the same launch produced / consumes them). SEL_OFF is added to every id
 // written to sel (not to so): with SEL_OFF = 2 an entry is never 0, so a
 // consumer can poll sel itself for the selection (meta4 may then be NULL).
-template <int NT, int R, int SWN, bool CO, int SEL_OFF = 0>
+// WIN: the scoring units are strided selection windows (unit u: tokens
+// u us .. u us + ul - 1, Sec. 3.1) and a block's score is the largest group
+// score among the windows that share a token with it (max-pooling).
+template <int NT, int R, int SWN, bool CO, int SEL_OFF = 0, bool WIN = false>
 __device__ void select_blocks(const Dims& m, int bh, int seq_len,
                               const float* __restrict__ e_vals,
                               const double* __restrict__ tile_part, SelectSmem<NT, SWN>& sm,
                               int32_t* sel, int32_t* meta4, int32_t* so) {
   constexpr int NW = NT / 64;
   constexpr int HC = R <= 2 ? 16 / R : (R <= 8 ? 4 : 32 / R);  // heads per load batch
-  constexpr int TJ = (NT * R + 4095) / 4096;  // tiles per lane: n_tiles <= NT R / 64
+  // tiles per lane: n_tiles <= NT R / 64 blocks, or <= kMaxWindows / 64 windows
+  constexpr int TJ = WIN ? kMaxWindows / 4096 : (NT * R + 4095) / 4096;
   float* sw = sm.sw;
   uint32_t* hist = sm.hist;
   const int G = m.group, k = m.k;
@@ -180,9 +184,11 @@ __device__ void select_blocks(const Dims& m, int bh, int seq_len,
                        tm[j], ts[j]);
   }
   float e[HC][R];  // nbp is a multiple of 64 >= R: a thread's run is all in or all out
+  if constexpr (!WIN) {
 #pragma unroll
-  for (int h = 0; h < HC; ++h)
-    load_run<R, CO>(ev, (int64_t)h * nbp + i0, h < G && i0 < nbp, e[h]);
+    for (int h = 0; h < HC; ++h)
+      load_run<R, CO>(ev, (int64_t)h * nbp + i0, h < G && i0 < nbp, e[h]);
+  }
 
   const int nb = (L + m.B - 1) / m.B;
   if (nb <= k) {  // L == 0 included: nothing or everything is selected
@@ -199,7 +205,8 @@ __device__ void select_blocks(const Dims& m, int bh, int seq_len,
     }
     return;
   }
-  const int n_tu = (nb + kTileBlocks - 1) / kTileBlocks;
+  const int nu = WIN ? (L + m.us - 1) / m.us : nb;  // units present
+  const int n_tu = (nu + kTileBlocks - 1) / kTileBlocks;
   for (int x = tid; x < 1024; x += NT) reinterpret_cast<uint4*>(hist)[x] = make_uint4(0u, 0u, 0u, 0u);
   // --- 1. Z_m and the tile weights of heads m = w, w + NW, ...
   for (int mm = w; kp > 0 && mm < G; mm += NW) {
@@ -248,6 +255,31 @@ __device__ void select_blocks(const Dims& m, int bh, int seq_len,
   for (int r = 0; r < R; ++r) key[r] = 0u;
   if (kp > 0) {
     // --- 2. keys
+    float best[R];  // the block's score, rounded to fp32
+    if constexpr (WIN) {
+      // windows u_lo .. u_lo + nv - 1 touch this thread's blocks; each
+      // window's group score (fp64 sum over the heads) is rounded to fp32 and
+      // pooled into every one of the thread's blocks it shares a token with
+      const int bpw = m.B / m.us, wpb = m.ul / m.us;
+      const int u_lo = i0 * bpw - (wpb - 1), nv = R * bpw + wpb - 1;
+#pragma unroll
+      for (int r = 0; r < R; ++r) best[r] = 0.f;
+      for (int v = 0; v < nv; ++v) {
+        const int u = u_lo + v;
+        if (u < 0 || u >= nu) continue;
+        const int tu = u / kTileBlocks;
+        double g = 0.0;
+        for (int h = 0; h < G; ++h)
+          g = fma((double)Mem<CO>::ld(ev + (int64_t)h * nbp + u), (double)sw[tu * G + h], g);
+        const float f = (float)g;
+        const int64_t a = (int64_t)u * m.us, b = a + m.ul;
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+          const int64_t lo = (int64_t)(i0 + r) * m.B;
+          if (a < lo + m.B && b > lo) best[r] = fmaxf(best[r], f);
+        }
+      }
+    } else {
     const int t = i0 / kTileBlocks;  // R <= 64: one tile per thread
     double sc[R];
 #pragma unroll
@@ -267,12 +299,15 @@ __device__ void select_blocks(const Dims& m, int bh, int seq_len,
         }
       }
     }
+#pragma unroll
+    for (int r = 0; r < R; ++r) best[r] = (float)sc[r];
+    }
     // candidates: real blocks that are not forced (bitwise tests: no branches)
 #pragma unroll
     for (int r = 0; r < R; ++r) {
       const int i = i0 + r;
       const bool cand = (i < nb) & (i >= m.n_sink) & (i < nb - m.n_local);
-      key[r] = cand ? __float_as_uint((float)sc[r]) + 1u : 0u;
+      key[r] = cand ? __float_as_uint(best[r]) + 1u : 0u;
     }
     // --- 3. the kp-th largest key, one digit per barrier. Every key is added
     // to its digit's bin (adding 0 when it is not in the running), so the

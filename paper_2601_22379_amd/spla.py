@@ -48,7 +48,8 @@ class SplaConfig(ctypes.Structure):
                 ("head_dim", c_int32), ("block_size", c_int32), ("top_k", c_int32),
                 ("n_sink_blocks", c_int32), ("n_local_blocks", c_int32),
                 ("max_seq_len", c_int32), ("dtype", c_int32), ("softmax_scale", c_float),
-                ("rms_eps", c_float), ("flags", c_uint32)]
+                ("rms_eps", c_float), ("flags", c_uint32), ("sel_window", c_int32),
+                ("sel_stride", c_int32)]
 
 
 class SplaCacheStruct(ctypes.Structure):
@@ -135,10 +136,11 @@ def _check(status: int, where: str):
 
 def make_config(batch, n_q_heads, n_kv_heads, head_dim, block_size, top_k, max_seq_len,
                 dtype="bf16", n_sink=1, n_local=4, softmax_scale=0.0, rms_eps=1e-6,
-                flags=0) -> SplaConfig:
+                flags=0, sel_window=0, sel_stride=0) -> SplaConfig:
     dt = {"f32": F32, "fp32": F32, "float32": F32, "bf16": BF16, "bfloat16": BF16}.get(dtype, dtype)
     return SplaConfig(batch, n_q_heads, n_kv_heads, head_dim, block_size, top_k, n_sink, n_local,
-                      max_seq_len, int(dt), float(softmax_scale), float(rms_eps), int(flags))
+                      max_seq_len, int(dt), float(softmax_scale), float(rms_eps), int(flags),
+                      int(sel_window), int(sel_stride))
 
 
 def validate(cfg: SplaConfig, library=None) -> int:
@@ -286,9 +288,10 @@ class SplaCache:
 
     # ---- layout views (for checks; pure indexing) ----
     def stats_logical(self):
-        """(mean, M2) as [batch, Hkv, nb_cap, d] fp32 tensors."""
+        """(mean, M2) as [batch, Hkv, n_units, d] fp32 tensors: one unit per
+        block, or per selection window with strided selection."""
         c = self.cfg
-        nb = c.max_seq_len // c.block_size
+        nb = c.max_seq_len // (c.sel_stride if c.sel_stride else c.block_size)
         nt = -(-nb // 64)
         s = self.stats.view(c.batch, c.n_kv_heads, nt, 2, c.head_dim // 4, 64, 4)
         s = s.permute(0, 1, 3, 2, 5, 4, 6).reshape(c.batch, c.n_kv_heads, 2, nt * 64, c.head_dim)

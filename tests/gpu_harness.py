@@ -27,10 +27,12 @@ def params_of(w: si.Workload, **kw) -> O.SplaParams:
                         n_local=w.n_local, **kw)
 
 
-def config_of(w: si.Workload, flags=0, rms_eps=1e-6, softmax_scale=0.0):
+def config_of(w: si.Workload, flags=0, rms_eps=1e-6, softmax_scale=0.0, sel_window=0,
+              sel_stride=0):
     return spla.make_config(w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, w.block_size,
                             w.top_k, w.capacity, w.dtype, n_sink=w.n_sink, n_local=w.n_local,
-                            softmax_scale=softmax_scale, rms_eps=rms_eps, flags=flags)
+                            softmax_scale=softmax_scale, rms_eps=rms_eps, flags=flags,
+                            sel_window=sel_window, sel_stride=sel_stride)
 
 
 def to_dev(x: np.ndarray, w: si.Workload, device):
@@ -63,7 +65,7 @@ def oracle_kv_head(w: si.Workload, b: int, h: int, gamma: np.ndarray, q: np.ndar
     L = int(w.lengths[b]) if L is None else L
     K, V = si.gen_kv(w, b, h, 0, L, threads=16)
     if state is None:
-        state = O.build_state(K, V, L, w.block_size)
+        state = O.build_state(K, V, L, w.block_size, p.window, p.stride)
     G = w.group
     res = O.decode_kv_head(q[h * G:(h + 1) * G], state, K, V, gamma[h * G:(h + 1) * G], p, force)
     return res, state, K, V

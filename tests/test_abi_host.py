@@ -67,6 +67,15 @@ def _cfg(**kw):
     (dict(flags=16), -1),
     (dict(n_sink=0, n_local=0, top_k=1), 0),
     (dict(n_q_heads=40, n_kv_heads=8), 0),
+    (dict(sel_window=32, sel_stride=16), 0),                   # the paper's windows
+    (dict(sel_window=64, sel_stride=32), 0),
+    (dict(sel_window=16, sel_stride=16), 0),
+    (dict(sel_window=32, sel_stride=0), -1),
+    (dict(sel_window=8, sel_stride=16), -1),
+    (dict(sel_window=48, sel_stride=24), -2),                  # stride does not divide B
+    (dict(sel_window=40, sel_stride=16), -2),                  # window not a multiple
+    (dict(sel_window=80, sel_stride=16), -2),                  # more than 4 strides
+    (dict(sel_window=32, sel_stride=16, max_seq_len=16 * 16385 // 64 * 64 + 64), -3),
 ])
 def test_validate_codes(libname, kw, want):
     lib = spla.lib() if libname == "hip" else spla.host_lib()
@@ -82,6 +91,10 @@ def test_sizes_follow_documented_layout():
     assert b[3] == 4 * 8 * 128 * 128 * 4 and b[4] == 4 * 8 * 128 * 4 and b[5] == 16
     assert spla.workspace_bytes(c) % 256 == 0
     assert spla.append_workspace_bytes(c, 1) > 0
+    # strided selection: one statistics entry per window (131072 / 16 = 8192)
+    w = spla.cache_bytes(_cfg(sel_window=32, sel_stride=16))
+    assert w[2] == 4 * 8 * 128 * 2 * 32 * 64 * 4 * 4
+    assert w[:2] == b[:2] and w[3:] == b[3:]
 
 
 def test_device_calls_reject_bad_arguments_before_launch():
@@ -149,6 +162,7 @@ def test_header_and_host_code_under_sanitizers(tmp_path):
     (dict(head_dim=64), False),
     (dict(dtype="f32"), False),
     (dict(flags=spla.FLAG_SEPARATE_KERNELS), False),
+    (dict(sel_window=32, sel_stride=16), False),             # strided selection
 ])
 def test_decode_phase_mask(libname, kw, single):
     lib = spla.lib() if libname == "hip" else spla.host_lib()
