@@ -64,14 +64,15 @@ def source_hash(paths):
     return h.hexdigest()[:16]
 
 
-def build_workload(w, replicas, dev):
+def build_workload(w, replicas, dev, sel_window=0, sel_stride=0):
     import torch
 
     from paper_2601_22379_amd import spla
     import spla_inputs as si
 
     cfg = spla.make_config(w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, w.block_size,
-                           w.top_k, w.capacity, w.dtype, n_sink=w.n_sink, n_local=w.n_local)
+                           w.top_k, w.capacity, w.dtype, n_sink=w.n_sink, n_local=w.n_local,
+                           sel_window=sel_window, sel_stride=sel_stride)
     first = spla.SplaCache(cfg, dev)
     dt = torch.float32 if w.dtype == "f32" else torch.bfloat16
     lens = [w.prefill_length(b) for b in range(w.batch)]
@@ -92,6 +93,68 @@ def build_workload(w, replicas, dev):
         caches.append(c)
     torch.cuda.synchronize()
     return cfg, caches
+
+
+def strided_leg(w, R, dev, qs, gamma, outs, sels, K, W, C=32, s=16):
+    """The same decode with strided selection windows (C tokens every s,
+    max-pooled into blocks; the paper's C = 32, s = 16): a cache of its own
+    (one statistics entry per window), K timed steps, then the same steps
+    with every phase bracketed by HIP events. Returns a dict for the JSON
+    line; the scoring kernel, which streams the window statistics, is the
+    dominant one."""
+    import numpy as np
+    import torch
+
+    from paper_2601_22379_amd import spla
+    import spla_inputs as si
+
+    cfg, caches = build_workload(w, R, dev, C, s)
+
+    def one(i, events=None):
+        r = i % R
+        return caches[r].decode(qs[i % qs.shape[0]], gamma, outs[r], sels[r], events)
+
+    for i in range(W):
+        one(i)
+    t_a = torch.cuda.Event(enable_timing=True)
+    t_b = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_a.record()
+    for i in range(K):
+        one(W + i)
+    t_b.record()
+    torch.cuda.synchronize()
+    lat_us = t_a.elapsed_time(t_b) / K * 1e3
+    names = spla.decode_phases(cfg)
+    ev = [spla.make_events(names) for _ in range(K)]
+    for i in range(K):
+        one(W + K + i, ev[i][0])
+    torch.cuda.synchronize()
+    phases = {n: float(np.mean([e[1][n][0].elapsed_time(e[1][n][1]) for e in ev])) * 1e3
+              for n in names}
+    lens = caches[0].seq_lens.cpu().numpy()
+    sel_np = sels[0].cpu().numpy()
+    sel_counts = [[sum(min(w.block_size, int(lens[b]) - int(i) * w.block_size)
+                       for i in sel_np[b, h] if i >= 0) for h in range(w.n_kv_heads)]
+                  for b in range(w.batch)]
+    ab = si.algorithmic_bytes(w, sel_counts)
+    ab["stats"] = sum(-(-int(L) // s) for L in lens) * w.n_kv_heads * 2 * w.head_dim * 4
+    ab["total"] = ab["q_out"] + ab["stats"] + ab["selected_kv"] + ab["state"] + ab["append"]
+    sb = dominant_bytes(w, ab, "score")
+    del caches
+    torch.cuda.synchronize()
+    log(f"strided selection (C={C}, s={s}): {lat_us:.2f} us/step, phases us: "
+        + ", ".join(f"{k}={v:.2f}" for k, v in phases.items()))
+    return {"window": C, "stride": s, "latency_us": round(lat_us, 3),
+            "value": round(ab["total"] / (lat_us * 1e-6) / 1e9, 1), "unit": "GB/s",
+            "algorithmic_bytes": ab, "phases_us": {k: round(v, 3) for k, v in phases.items()},
+            "roofline": {"kernel": "score", "bound": "hbm",
+                         "achieved": round(sb / (phases["score"] * 1e-6) / 1e9, 1),
+                         "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                         "frac": round(sb / (phases["score"] * 1e-6) / 1e9 / PEAK_HBM_GBS, 4),
+                         "algorithmic_bytes_per_launch": sb,
+                         "avg_launch_us": round(phases["score"], 3),
+                         "avg_launch_method": "per-launch events"}}
 
 
 def cpu_baseline(w, seconds, n_units=2):
@@ -236,6 +299,10 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-graph", action="store_true")
+    ap.add_argument("--no-strided", action="store_true",
+                    help="skip the strided-selection leg (C = 32, s = 16)")
+    ap.add_argument("--strided-only", action="store_true",
+                    help="run only the strided-selection leg and print its JSON (profiling)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB copy kernel (for counter scaling)")
     ap.add_argument("--trace-summary", metavar="DIR",
@@ -250,9 +317,11 @@ def main():
     if args.trace_summary or args.traffic_summary:
         import spla_inputs as si
         w = si.config(args.config)
-        tag = f"decode_{w.name}"
+        tag = f"decode_{w.name}" + ("_strided_c32_s16" if args.strided_only else "")
         if args.trace_summary:
-            trace_summary(args.trace_summary, w.name, " && ".join(args.command),
+            label = w.name + (", strided selection windows C = 32, s = 16"
+                              if args.strided_only else "")
+            trace_summary(args.trace_summary, label, " && ".join(args.command),
                           os.path.join(ROOT, "profiles", f"{tag}_kernel_trace.md"))
         if args.traffic_summary:
             ab = si.algorithmic_bytes(w, None)
@@ -277,6 +346,17 @@ def main():
     dev = torch.device("cuda:0")
     w = si.config(args.config)
     R = max(1, args.replicas)
+    if args.strided_only:
+        dt = torch.float32 if w.dtype == "f32" else torch.bfloat16
+        qs = torch.from_numpy(si.gen_q_batch(w)[None]).to(dt).to(dev)
+        gamma = torch.from_numpy(si.gen_gamma(w)).to(dev)
+        outs = [torch.empty((w.batch, w.n_q_heads, w.head_dim), dtype=dt, device=dev)
+                for _ in range(R)]
+        sels = [torch.empty((w.batch, w.n_kv_heads, w.top_k), dtype=torch.int32, device=dev)
+                for _ in range(R)]
+        print(json.dumps(strided_leg(w, R, dev, qs, gamma, outs, sels, args.steps,
+                                     args.warmup)), flush=True)
+        return
     cfg, caches = build_workload(w, R, dev)
     dt = torch.float32 if w.dtype == "f32" else torch.bfloat16
     K, W = args.steps, args.warmup
@@ -468,6 +548,9 @@ def main():
                 "avg_launch_us": round(dom_us, 3), "avg_launch_method": dom_method,
                 "avg_launch_us_per_launch_events": round(dom_us_events, 3),
                 "profiled_avg_us": prof_us}
+    strided = None
+    if not appending and not args.no_strided:
+        strided = strided_leg(w, R, dev, qs, gamma, outs, sels, K, W)
     cpu = None
     if not args.no_cpu_baseline:
         log("timing the CPU oracle")
@@ -499,6 +582,7 @@ def main():
         "phases_us_separate_kernels": {k: round(v, 3) for k, v in phases.items()},
         "roofline": roofline,
         "cpu_baseline": cpu,
+        "strided_selection": strided,
     }
     print(json.dumps(line), flush=True)
 

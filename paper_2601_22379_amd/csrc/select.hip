@@ -13,10 +13,11 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
     const double* __restrict__ tile_part, int32_t* __restrict__ sel_ws,
     int32_t* __restrict__ sel_out, int32_t* __restrict__ meta) {
   __shared__ SelectSmem<kSelThreads, kMaxTiles * SPLA_MAX_GROUP> sm;
+  __shared__ float wsc[WIN ? kMaxWindows : 1];  // window scores (strided selection)
   const int bh = blockIdx.x;
   select_blocks<kSelThreads, R, kMaxTiles * SPLA_MAX_GROUP, false, 0, WIN>(
       m, bh, seq_lens[bh / m.hkv], e_vals, tile_part, sm, sel_ws + (int64_t)bh * m.k,
-      meta + bh * 4, sel_out ? sel_out + (int64_t)bh * m.k : nullptr);
+      meta + bh * 4, sel_out ? sel_out + (int64_t)bh * m.k : nullptr, wsc);
 }
 
 hipError_t launch_select(const Dims& m, const spla_cache& c, const DecodeWs& ws, char* base,

@@ -155,12 +155,14 @@ struct SelectSmem {
 // consumer can poll sel itself for the selection (meta4 may then be NULL).
 // WIN: the scoring units are strided selection windows (unit u: tokens
 // u us .. u us + ul - 1, Sec. 3.1) and a block's score is the largest group
-// score among the windows that share a token with it (max-pooling).
+// score among the windows that share a token with it (max-pooling); wsc is
+// LDS for kMaxWindows window scores.
 template <int NT, int R, int SWN, bool CO, int SEL_OFF = 0, bool WIN = false>
 __device__ void select_blocks(const Dims& m, int bh, int seq_len,
                               const float* __restrict__ e_vals,
                               const double* __restrict__ tile_part, SelectSmem<NT, SWN>& sm,
-                              int32_t* sel, int32_t* meta4, int32_t* so) {
+                              int32_t* sel, int32_t* meta4, int32_t* so,
+                              float* wsc = nullptr) {
   constexpr int NW = NT / 64;
   constexpr int HC = R <= 2 ? 16 / R : (R <= 8 ? 4 : 32 / R);  // heads per load batch
   // tiles per lane: n_tiles <= NT R / 64 blocks, or <= kMaxWindows / 64 windows
@@ -257,8 +259,53 @@ __device__ void select_blocks(const Dims& m, int bh, int seq_len,
     // --- 2. keys
     float best[R];  // the block's score, rounded to fp32
     if constexpr (WIN) {
-      // windows u_lo .. u_lo + nv - 1 touch this thread's blocks; each
-      // window's group score (fp64 sum over the heads) is rounded to fp32 and
+      // every window's group score (fp64 sum over the heads, rounded to
+      // fp32) into LDS: thread t takes the runs of four windows starting at
+      // 4 (t + j NT); the loads of four heads are issued together, as
+      // 16-byte loads (a run never leaves the 64-window tile, and a run
+      // holding a window below nu lies inside the row)
+      constexpr int J4 = kMaxWindows / (4 * NT);
+      static_assert(kMaxWindows % (4 * NT) == 0, "window staging");
+      double g[J4][4];
+#pragma unroll
+      for (int j = 0; j < J4; ++j)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) g[j][c] = 0.0;
+      for (int h0 = 0; h0 < G; h0 += 4) {
+        uint4 v[4][J4];
+#pragma unroll
+        for (int hh = 0; hh < 4; ++hh) {
+          const int h = min(h0 + hh, G - 1);
+#pragma unroll
+          for (int j = 0; j < J4; ++j) {
+            const int u = 4 * (tid + j * NT);
+            v[hh][j] = Mem<CO>::ld16(ev + (int64_t)h * nbp, (uint32_t)(u < nu ? u : 0) * 4u);
+          }
+        }
+#pragma unroll
+        for (int hh = 0; hh < 4; ++hh) {
+          if (h0 + hh < G) {
+#pragma unroll
+            for (int j = 0; j < J4; ++j) {
+              const int u = 4 * (tid + j * NT);
+              const double wv = (double)sw[((u < nu ? u : 0) / kTileBlocks) * G + h0 + hh];
+              g[j][0] = fma((double)__uint_as_float(v[hh][j].x), wv, g[j][0]);
+              g[j][1] = fma((double)__uint_as_float(v[hh][j].y), wv, g[j][1]);
+              g[j][2] = fma((double)__uint_as_float(v[hh][j].z), wv, g[j][2]);
+              g[j][3] = fma((double)__uint_as_float(v[hh][j].w), wv, g[j][3]);
+            }
+          }
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < J4; ++j)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          const int u = 4 * (tid + j * NT) + c;
+          if (u < nu) wsc[u] = (float)g[j][c];
+        }
+      __syncthreads();
+      // windows u_lo .. u_lo + nv - 1 touch this thread's blocks; each is
       // pooled into every one of the thread's blocks it shares a token with
       const int bpw = m.B / m.us, wpb = m.ul / m.us;
       const int u_lo = i0 * bpw - (wpb - 1), nv = R * bpw + wpb - 1;
@@ -267,11 +314,7 @@ __device__ void select_blocks(const Dims& m, int bh, int seq_len,
       for (int v = 0; v < nv; ++v) {
         const int u = u_lo + v;
         if (u < 0 || u >= nu) continue;
-        const int tu = u / kTileBlocks;
-        double g = 0.0;
-        for (int h = 0; h < G; ++h)
-          g = fma((double)Mem<CO>::ld(ev + (int64_t)h * nbp + u), (double)sw[tu * G + h], g);
-        const float f = (float)g;
+        const float f = wsc[u];
         const int64_t a = (int64_t)u * m.us, b = a + m.ul;
 #pragma unroll
         for (int r = 0; r < R; ++r) {

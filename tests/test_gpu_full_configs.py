@@ -106,3 +106,26 @@ def test_full_size_config4_steps(dev):
                  for b, h in pairs]
         H.log(f"config 4 step {step}: worst rel err {max(i['rel_err'] for i in infos):.3e}, "
               f"swaps {sum(i['n_swapped'] for i in infos)}")
+
+
+@pytest.mark.timeout(900)
+def test_full_size_strided_selection(dev):
+    """The 128K workload with the paper's strided selection windows (C = 32,
+    s = 16, max-pooled into B = 64 blocks): 8192 windows per sequence."""
+    w = si.config("3")
+    C, s = 32, 16
+    cache = spla.SplaCache(H.config_of(w, sel_window=C, sel_stride=s), dev)
+    H.fill_cache(w, cache, device=dev)
+    q = si.gen_q_batch(w)
+    gamma = si.gen_gamma(w)
+    out, sel = cache.decode(H.to_dev(q, w, dev), torch.from_numpy(gamma).to(dev))
+    torch.cuda.synchronize()
+    out = out.float().cpu().numpy()
+    sel = sel.cpu().numpy()
+    check_properties(w, sel, out, w.lengths)
+    p = H.params_of(w, window=C, stride=s)
+    pairs = sample_pairs(w, 2, 1)
+    H.log(f"strided config 3: oracle on {pairs}")
+    infos = [H.check_kv_head(w, b, h, out[b], sel[b, h], q[b], gamma, p) for b, h in pairs]
+    H.log(f"strided config 3: worst rel err {max(i['rel_err'] for i in infos):.3e}, "
+          f"swaps {sum(i['n_swapped'] for i in infos)}")
