@@ -71,9 +71,11 @@ enum {
 /* err_flags bits written by the device */
 enum {
   SPLA_DEVERR_CAPACITY = 1, /* an append was clipped at max_seq_len */
-  SPLA_DEVERR_SYNC = 2      /* the single-launch decode found its workspace counters not
+  SPLA_DEVERR_SYNC = 2,     /* the single-launch decode found its workspace counters not
                                zero at launch, or gave up a bounded wait: the output of
                                that call is undefined; spla_workspace_init repairs it */
+  SPLA_DEVERR_PAGE = 4      /* an append met a block_table entry outside [0, kv_pages):
+                               its rows were not written */
 };
 
 /* Library limits of this build. */
@@ -112,6 +114,11 @@ typedef struct spla_config {
                              sel_stride, max_seq_len / sel_stride <= 16384, and
                              the decode runs as separate launches */
   int32_t sel_stride;
+  int32_t kv_pages;       /* paged KV cache (PagedAttention-style, one page = one block
+                             of B tokens, as in Sec. 2.1): 0 keeps k_cache / v_cache
+                             per sequence as laid out below; > 0 makes them pools of
+                             kv_pages pages addressed through spla_cache.block_table,
+                             and the decode runs as separate launches */
 } spla_config;
 
 /* ------------------------------------------------------------------- cache
@@ -143,6 +150,15 @@ typedef struct spla_config {
  *  [5] seq_lens  int32 [batch]             tokens held by each sequence
  * err_flags: int32 [1] or NULL; SPLA_DEVERR_* bits are OR-ed in, never cleared
  * by the library.
+ * Paged caches (kv_pages > 0): [0] and [1] are pools of kv_pages pages, page p
+ * holding for every KV head h the B rows of one block in the layout above
+ * (element offset (p * Hkv + h) * B * d of the pool); block_table is int32
+ * [batch][max_seq_len / B], caller-owned, read-only to the library, entry
+ * [b][i] naming the page of block i of sequence b. Every block a sequence
+ * holds or will receive by an append must name a page in [0, kv_pages), and
+ * no two live blocks may share one; an append skips rows whose entry is out
+ * of range (SPLA_DEVERR_PAGE), and a decode reads page 0 for such an entry
+ * (its output is then undefined). NULL when kv_pages is 0.
  * A zero-filled cache (spla_reset) is the empty cache.
  */
 typedef struct spla_cache {
@@ -153,6 +169,7 @@ typedef struct spla_cache {
   float* lin_norm;
   int32_t* seq_lens;
   int32_t* err_flags;
+  const int32_t* block_table;
 } spla_cache;
 
 enum { SPLA_CACHE_NUM_BUFFERS = 6 };

@@ -29,7 +29,8 @@ template <typename T>
 __global__ __launch_bounds__(128) void append_blocks_kernel(
     Dims m, T* __restrict__ kc, T* __restrict__ vc, float* __restrict__ stats,
     const int32_t* __restrict__ seq_lens, int32_t* __restrict__ err, const T* __restrict__ k_new,
-    const T* __restrict__ v_new, int max_new, const int32_t* __restrict__ n_new) {
+    const T* __restrict__ v_new, int max_new, const int32_t* __restrict__ n_new,
+    const int32_t* __restrict__ table) {
   const int bh = blockIdx.y;
   const int b = bh / m.hkv;
   const int L0 = seq_lens[b];
@@ -47,12 +48,26 @@ __global__ __launch_bounds__(128) void append_blocks_kernel(
   if (t_hi <= t_lo || j >= m.d) return;
   const int64_t src0 = ((int64_t)bh * max_new - L0) * m.d + j;  // row t at src0 + t*d
 
+  // the slot of the block that holds the rows this unit copies (they all lie
+  // in one block: a unit's first us tokens, us dividing B); -1: a paged
+  // table entry out of range, the rows are not written
+  int64_t slot = -1;
+  if (t_own > t_lo) {
+    const int blk = t_lo / m.B;
+    if (!table) {
+      slot = (int64_t)bh * m.nb_cap + blk;
+    } else {
+      const int p = block_page(m, table, bh, blk);
+      slot = p < 0 ? -1 : (int64_t)p * m.hkv + bh % m.hkv;
+      if (p < 0 && err && j == 0) atomicOr(err, (int)SPLA_DEVERR_PAGE);
+    }
+  }
   double sum = 0.0;
   for (int t = t_lo; t < t_hi; ++t) {
     const T kv = k_new[src0 + (int64_t)t * m.d];
-    if (t < t_own) {
-      kc[k_off(m, bh, t, j)] = kv;
-      vc[v_off(m, bh, t, j)] = v_new[src0 + (int64_t)t * m.d];
+    if (t < t_own && slot >= 0) {
+      kc[k_off_slot(m, slot, t % m.B, j)] = kv;
+      vc[v_off_slot(m, slot, t % m.B, j)] = v_new[src0 + (int64_t)t * m.d];
     }
     sum += (double)Elem<T>::load(&kv, 0);
   }
@@ -252,11 +267,13 @@ hipError_t launch_append_blocks(const Dims& m, const spla_cache& c, const void* 
   if (m.elem == 4)
     hipLaunchKernelGGL(append_blocks_kernel<float>, grid, dim3(128), 0, st, m, (float*)c.k_cache,
                        (float*)c.v_cache, c.blk_stats, c.seq_lens, c.err_flags,
-                       (const float*)k_new, (const float*)v_new, max_new, n_new);
+                       (const float*)k_new, (const float*)v_new, max_new, n_new,
+                       m.pages > 0 ? c.block_table : nullptr);
   else
     hipLaunchKernelGGL(append_blocks_kernel<bf16_t>, grid, dim3(128), 0, st, m,
                        (bf16_t*)c.k_cache, (bf16_t*)c.v_cache, c.blk_stats, c.seq_lens,
-                       c.err_flags, (const bf16_t*)k_new, (const bf16_t*)v_new, max_new, n_new);
+                       c.err_flags, (const bf16_t*)k_new, (const bf16_t*)v_new, max_new, n_new,
+                       m.pages > 0 ? c.block_table : nullptr);
   return hipGetLastError();
 }
 

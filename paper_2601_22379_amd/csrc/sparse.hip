@@ -31,7 +31,7 @@ __global__ __launch_bounds__(256) void sparse_valu_kernel(
     const T* __restrict__ vc, const T* __restrict__ q, const float* __restrict__ gamma,
     const float* __restrict__ S, const float* __restrict__ zbar,
     const int32_t* __restrict__ sel, const int32_t* __restrict__ meta, int bps, int stride,
-    float* __restrict__ part) {
+    float* __restrict__ part, const int32_t* __restrict__ table) {
   constexpr int MG = SPLA_MAX_GROUP;
   constexpr int PER = (MG * D + 255) / 256;  // (head, coord) pairs per thread
   __shared__ float sq[MG][D];
@@ -85,14 +85,21 @@ __global__ __launch_bounds__(256) void sparse_valu_kernel(
     int blk = sel[(int64_t)bh * m.k + p];
     blk = blk < 0 ? 0 : (blk >= nb ? nb - 1 : blk);
     const int n_i = block_count(L, m.B, blk);
+    // the block's slot: per-sequence cache, or its page of a paged pool (an
+    // entry out of range reads page 0)
+    int64_t slot = (int64_t)bh * m.nb_cap + blk;
+    if (table) {
+      const int pg = block_page(m, table, bh, blk);
+      slot = (int64_t)(pg < 0 ? 0 : pg) * m.hkv + h;
+    }
     for (int sub = 0; sub * kSubTokens < n_i; ++sub) {
-      const int t0 = blk * m.B + sub * kSubTokens;
+      const int tb0 = sub * kSubTokens;
       const int nt = min(kSubTokens, n_i - sub * kSubTokens);
       for (int e = tid; e < kSubTokens * D; e += 256) {
         const int row = e / D, col = e % D;
-        sK[row][col] = row < nt ? Elem<T>::load(kc, k_off(m, bh, t0 + row, col)) : 0.f;
+        sK[row][col] = row < nt ? Elem<T>::load(kc, k_off_slot(m, slot, tb0 + row, col)) : 0.f;
         const int c2 = e / kSubTokens, r2 = e % kSubTokens;
-        sV[c2][r2] = r2 < nt ? Elem<T>::load(vc, v_off(m, bh, t0 + r2, c2)) : 0.f;
+        sV[c2][r2] = r2 < nt ? Elem<T>::load(vc, v_off_slot(m, slot, tb0 + r2, c2)) : 0.f;
       }
       __syncthreads();
       for (int r = 0; r < kSubTokens / 4; ++r) {  // phi(k) rows
@@ -201,7 +208,7 @@ __global__ __launch_bounds__(256) void sparse_mfma_kernel(
     const int32_t* __restrict__ sel, int32_t* __restrict__ meta, int stride,
     float* __restrict__ part, const int32_t* __restrict__ seq_lens,
     const float* __restrict__ e_vals, const double* __restrict__ tile_part,
-    int32_t* __restrict__ sel_out) {
+    int32_t* __restrict__ sel_out, const int32_t* __restrict__ table) {
   constexpr int SWN = R > 0 ? kTileBlocks * 8 : 4;  // tile weights: <= 64 tiles x 8 heads
   __shared__ SelectSmem<256, SWN> ssm;
   __shared__ int32_t s_sel[R > 0 ? SPLA_MAX_TOP_K : 1];
@@ -220,12 +227,12 @@ __global__ __launch_bounds__(256) void sparse_mfma_kernel(
     if (blockIdx.x == 0 && threadIdx.x < 4) meta[bh * 4 + threadIdx.x] = s_meta[threadIdx.x];
     const int e = sparse_step_entry<BLK>((int)blockIdx.x);
     sparse_body<D, BLK, false, 8>(m, s, kc, vc, e < m.k ? s_sel[e] : -1, s_meta[2], bh,
-                                  (int)blockIdx.x, (int)gridDim.x, r, sm, part, stride);
+                                  (int)blockIdx.x, (int)gridDim.x, r, sm, part, stride, table);
   } else {
     const int e = sparse_step_entry<BLK>((int)blockIdx.x);
     sparse_body<D, BLK, false, 8>(m, s, kc, vc, e < m.k ? sel[(int64_t)bh * m.k + e] : -1,
                                   meta[bh * 4 + 2], bh, (int)blockIdx.x, (int)gridDim.x, r, sm,
-                                  part, stride);
+                                  part, stride, table);
   }
 }
 
@@ -238,7 +245,8 @@ static void valu_td(const Dims& m, const spla_config& cfg, float s, const spla_c
                      cfg.rms_eps, cfg.flags, (const T*)c.k_cache, (const T*)c.v_cache,
                      (const T*)q, gamma, (const float*)c.lin_state, (const float*)c.lin_norm,
                      (const int32_t*)(base + ws.sel), (const int32_t*)(base + ws.meta),
-                     ws.blocks_per_wg, ws.part_stride, (float*)(base + ws.part));
+                     ws.blocks_per_wg, ws.part_stride, (float*)(base + ws.part),
+                     m.pages > 0 ? c.block_table : nullptr);
 }
 
 // Blocks per thread of the in-workgroup selection (0: use the selection
@@ -265,7 +273,8 @@ static void mfma_dbr(const Dims& m, float s, const spla_cache& c, const void* q,
                      (const float*)c.lin_norm, (const int32_t*)(base + ws.sel),
                      (int32_t*)(base + ws.meta), ws.part_stride, (float*)(base + ws.part),
                      c.seq_lens, (const float*)(base + ws.e_vals),
-                     (const double*)(base + ws.tile_part), sel_out);
+                     (const double*)(base + ws.tile_part), sel_out,
+                     m.pages > 0 ? c.block_table : nullptr);
 }
 
 template <int D, int BLK>

@@ -25,10 +25,11 @@ int compute_units() {
 
 namespace {
 
-int32_t check_cache(const spla_cache* c) {
+int32_t check_cache(const spla_config* cfg, const spla_cache* c) {
   if (!c) return SPLA_ERR_INVALID_ARG;
   if (!c->k_cache || !c->v_cache || !c->blk_stats || !c->lin_state || !c->lin_norm || !c->seq_lens)
     return SPLA_ERR_INVALID_ARG;
+  if ((cfg->kv_pages > 0) != (c->block_table != nullptr)) return SPLA_ERR_INVALID_ARG;
   return SPLA_OK;
 }
 
@@ -93,7 +94,7 @@ int32_t check_decode_args(const spla_config* cfg, const spla_cache* cache, const
                           const float* w, void* out, void* ws, size_t ws_bytes) {
   int32_t s = spla_validate(cfg);
   if (s != SPLA_OK) return s;
-  if ((s = check_cache(cache)) != SPLA_OK) return s;
+  if ((s = check_cache(cfg, cache)) != SPLA_OK) return s;
   if (!q || !w || !out) return SPLA_ERR_INVALID_ARG;
   if (out == q) return SPLA_ERR_INVALID_ARG;
   size_t need = 0;
@@ -106,7 +107,7 @@ int32_t check_decode_args(const spla_config* cfg, const spla_cache* cache, const
 extern "C" int32_t spla_reset(const spla_config* cfg, const spla_cache* cache, void* stream) {
   int32_t s = spla_validate(cfg);
   if (s != SPLA_OK) return s;
-  if ((s = check_cache(cache)) != SPLA_OK) return s;
+  if ((s = check_cache(cfg, cache)) != SPLA_OK) return s;
   size_t b[SPLA_CACHE_NUM_BUFFERS];
   spla_cache_bytes(cfg, b);
   hipStream_t st = static_cast<hipStream_t>(stream);
@@ -133,7 +134,7 @@ extern "C" int32_t spla_append(const spla_config* cfg, const spla_cache* cache, 
                                void* workspace, size_t workspace_bytes, void* stream) {
   int32_t s = spla_validate(cfg);
   if (s != SPLA_OK) return s;
-  if ((s = check_cache(cache)) != SPLA_OK) return s;
+  if ((s = check_cache(cfg, cache)) != SPLA_OK) return s;
   if (max_new < 0) return SPLA_ERR_INVALID_ARG;
   if (max_new > cfg->max_seq_len) return SPLA_ERR_CAPACITY;
   if (max_new == 0) return SPLA_OK;

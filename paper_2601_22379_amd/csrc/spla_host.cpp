@@ -60,6 +60,8 @@ extern "C" int32_t spla_validate(const spla_config* c) {
       return SPLA_ERR_UNSUPPORTED;
     if (c->max_seq_len / c->sel_stride > spla::kMaxWindows) return SPLA_ERR_CAPACITY;
   }
+  if (c->kv_pages < 0) return SPLA_ERR_INVALID_ARG;
+  if (c->kv_pages > (1 << 24)) return SPLA_ERR_CAPACITY;
   // every derived byte count must fit comfortably in 63 bits
   const Dims m = spla::make_dims(*c);
   const double kv = (double)m.bh * m.cap * m.d * 4.0;
@@ -72,8 +74,11 @@ extern "C" int32_t spla_cache_bytes(const spla_config* c, size_t* out) {
   int32_t st = spla_validate(c);
   if (st != SPLA_OK) return st;
   const Dims m = spla::make_dims(*c);
-  out[0] = (size_t)m.bh * m.cap * m.d * m.elem;
-  out[1] = (size_t)m.bh * m.nb_cap * m.d * m.B * m.elem;
+  // K and V: one slot of B * d elements per block (contiguous) or per page
+  // and KV head (paged pool)
+  const size_t slots = m.pages > 0 ? (size_t)m.pages * m.hkv : (size_t)m.bh * m.nb_cap;
+  out[0] = slots * m.B * m.d * m.elem;
+  out[1] = slots * m.B * m.d * m.elem;
   out[2] = (size_t)m.bh * m.n_tiles * 2 * m.d * spla::kTileBlocks * 4;
   out[3] = (size_t)m.bh * m.d * m.d * 4;
   out[4] = (size_t)m.bh * m.d * 4;

@@ -32,6 +32,7 @@ struct Dims {
                  // blocks, us = ul = B, or the strided selection windows)
   int nu_cap;    // units per sequence at capacity
   int n_tiles;   // statistics tiles (64 units) per (sequence, kv head)
+  int pages;     // pages of a paged K/V pool (0: contiguous per-sequence caches)
   int bh;        // batch * hkv
   int elem;      // bytes per q / K / V / out element
 };
@@ -54,6 +55,7 @@ SPLA_HD Dims make_dims(const spla_config& c) {
   m.ul = win ? c.sel_window : c.block_size;
   m.nu_cap = c.max_seq_len / m.us;
   m.n_tiles = (int)ceil_div(m.nu_cap, kTileBlocks);
+  m.pages = c.kv_pages;
   m.bh = c.batch * c.n_kv_heads;
   m.elem = c.dtype == SPLA_F32 ? 4 : 2;
   return m;
@@ -68,18 +70,34 @@ SPLA_HD Dims make_dims(const spla_config& c) {
 //           i % 4, coordinates 32 ks + 8 g .. +7   (l = 16 g + i)
 //   values  chunk t * 64 + l holds coordinate 16 t + i, tokens 8 g .. 8 g + 7
 // so that each load instruction of a wavefront reads 1 KiB in one piece.
-SPLA_HD int64_t k_off(const Dims& m, int64_t bh, int64_t t, int j) {
-  if (m.elem == 4) return (bh * m.cap + t) * m.d + j;
-  const int tt = (int)(t & 31);
+// Every block occupies B * d consecutive elements, its "slot": slot
+// bh * nb_cap + i for block i of a contiguous cache, p * Hkv + h for a block
+// on page p of a paged pool. Offsets of row tb (0 <= tb < B) of a slot:
+SPLA_HD int64_t k_off_slot(const Dims& m, int64_t slot, int tb, int j) {
+  if (m.elem == 4) return (slot * m.B + tb) * m.d + j;
+  const int tt = tb & 31;
   const int mt = (tt >> 2) & 1, i = 4 * (tt >> 3) + (tt & 3);
   const int q = (mt * (m.d >> 5) + (j >> 5)) * 64 + ((j >> 3) & 3) * 16 + i;
-  return (bh * m.cap + (t & ~(int64_t)31)) * m.d + q * 8 + (j & 7);
+  return (slot * m.B + (tb & ~31)) * m.d + q * 8 + (j & 7);
+}
+SPLA_HD int64_t v_off_slot(const Dims& m, int64_t slot, int tb, int c) {
+  if (m.elem == 4) return (slot * m.d + c) * m.B + tb;
+  const int tt = tb & 31;
+  const int q = (c >> 4) * 64 + (tt >> 3) * 16 + (c & 15);
+  return (slot * m.B + (tb & ~31)) * m.d + q * 8 + (tt & 7);
+}
+// Contiguous caches: token t of (sequence, kv head) bh.
+SPLA_HD int64_t k_off(const Dims& m, int64_t bh, int64_t t, int j) {
+  return k_off_slot(m, bh * m.nb_cap + t / m.B, (int)(t % m.B), j);
 }
 SPLA_HD int64_t v_off(const Dims& m, int64_t bh, int64_t t, int c) {
-  if (m.elem == 4) return ((bh * m.nb_cap + t / m.B) * m.d + c) * m.B + (t % m.B);
-  const int tt = (int)(t & 31);
-  const int q = (c >> 4) * 64 + (tt >> 3) * 16 + (c & 15);
-  return (bh * m.cap + (t & ~(int64_t)31)) * m.d + q * 8 + (tt & 7);
+  return v_off_slot(m, bh * m.nb_cap + t / m.B, (int)(t % m.B), c);
+}
+// Page of block i of bh in a paged pool, or -1 when its table entry is out
+// of range.
+SPLA_HD int block_page(const Dims& m, const int32_t* table, int64_t bh, int64_t i) {
+  const int p = table[(bh / m.hkv) * m.nb_cap + i];
+  return (p >= 0 && p < m.pages) ? p : -1;
 }
 // Whether the scoring units are strided selection windows rather than blocks.
 SPLA_HD bool windowed(const Dims& m) { return m.us != m.B || m.ul != m.B; }
@@ -121,7 +139,7 @@ constexpr int kFusedMaxBlocks = 256 * 32;
 constexpr int kFusedMaxGroup = 6;
 SPLA_HD bool use_fused_decode(const Dims& m) {
   return use_mfma_sparse(m) && m.d == 128 && m.group <= kFusedMaxGroup &&
-         m.nb_cap <= kFusedMaxBlocks && !windowed(m);
+         m.nb_cap <= kFusedMaxBlocks && !windowed(m) && m.pages == 0;
 }
 
 // The decode workspace's synchronisation area (int32 words). Every counter

@@ -395,7 +395,8 @@ __device__ __forceinline__ void sparse_body(const Dims& m, float s,
                                             int blk_sel, int L,
                                             int bh, int x, int n_wg, const SparseRegs& r,
                                             SparseSmem<D, GC>& sm, float* __restrict__ part,
-                                            int stride) {
+                                            int stride,
+                                            const int32_t* __restrict__ table = nullptr) {
   constexpr int KS = D / 32;     // k-steps of the first product
   constexpr int MT = D / 16;     // coordinate tiles of the second product
   constexpr int CPB = BLK / 32;  // steps per block
@@ -423,7 +424,15 @@ __device__ __forceinline__ void sparse_body(const Dims& m, float s,
     // chunk (mt KS + ks) 64 + lane and t 64 + lane
     bf16x8 ka[2][KS];
     bf16x8 va[MT];
-    const int64_t step0 = ((int64_t)bh * m.cap + (int64_t)blk * BLK + ch * 32) * D;
+    // the block's slot: per-sequence cache, or its page of a paged pool
+    // (table given; an entry out of range reads page 0)
+    int64_t step0;
+    if (table) {
+      const int p = block_page(m, table, bh, blk);
+      step0 = (((int64_t)(p < 0 ? 0 : p) * m.hkv + bh % m.hkv) * BLK + ch * 32) * D;
+    } else {
+      step0 = ((int64_t)bh * m.cap + (int64_t)blk * BLK + ch * 32) * D;
+    }
     const bf16x8* kst = reinterpret_cast<const bf16x8*>(kc + step0) + lane;
     const bf16x8* vst = reinterpret_cast<const bf16x8*>(vc + step0) + lane;
 #pragma unroll

@@ -21,7 +21,7 @@ HOST_LIB_PATH = os.path.join(_HERE, "libspla_host.so")
 
 F32, BF16 = 0, 1
 FLAG_NO_RLA, FLAG_FIRST_ORDER, FLAG_RLA_NORMALIZE, FLAG_SEPARATE_KERNELS = 1, 2, 4, 8
-DEVERR_CAPACITY, DEVERR_SYNC = 1, 2
+DEVERR_CAPACITY, DEVERR_SYNC, DEVERR_PAGE = 1, 2, 4
 MAX_GROUP, MAX_TOP_K, MAX_BLOCKS, WORKSPACE_ALIGN = 16, 256, 32768, 256
 PHASES = {"append": 0, "score": 1, "select": 2, "sparse": 3, "merge": 4, "decode": 5}
 NUM_PHASES = 8
@@ -49,13 +49,13 @@ class SplaConfig(ctypes.Structure):
                 ("n_sink_blocks", c_int32), ("n_local_blocks", c_int32),
                 ("max_seq_len", c_int32), ("dtype", c_int32), ("softmax_scale", c_float),
                 ("rms_eps", c_float), ("flags", c_uint32), ("sel_window", c_int32),
-                ("sel_stride", c_int32)]
+                ("sel_stride", c_int32), ("kv_pages", c_int32)]
 
 
 class SplaCacheStruct(ctypes.Structure):
     _fields_ = [("k_cache", c_void_p), ("v_cache", c_void_p), ("blk_stats", c_void_p),
                 ("lin_state", c_void_p), ("lin_norm", c_void_p), ("seq_lens", c_void_p),
-                ("err_flags", c_void_p)]
+                ("err_flags", c_void_p), ("block_table", c_void_p)]
 
 
 class SplaEvents(ctypes.Structure):
@@ -136,11 +136,11 @@ def _check(status: int, where: str):
 
 def make_config(batch, n_q_heads, n_kv_heads, head_dim, block_size, top_k, max_seq_len,
                 dtype="bf16", n_sink=1, n_local=4, softmax_scale=0.0, rms_eps=1e-6,
-                flags=0, sel_window=0, sel_stride=0) -> SplaConfig:
+                flags=0, sel_window=0, sel_stride=0, kv_pages=0) -> SplaConfig:
     dt = {"f32": F32, "fp32": F32, "float32": F32, "bf16": BF16, "bfloat16": BF16}.get(dtype, dtype)
     return SplaConfig(batch, n_q_heads, n_kv_heads, head_dim, block_size, top_k, n_sink, n_local,
                       max_seq_len, int(dt), float(softmax_scale), float(rms_eps), int(flags),
-                      int(sel_window), int(sel_stride))
+                      int(sel_window), int(sel_stride), int(kv_pages))
 
 
 def validate(cfg: SplaConfig, library=None) -> int:
@@ -199,9 +199,18 @@ class SplaCache:
     """Device buffers of one SPLA cache, allocated with torch, plus the
     workspaces the calls need. Thin wrapper over the C ABI."""
 
-    def __init__(self, cfg: SplaConfig, device="cuda"):
+    def __init__(self, cfg: SplaConfig, device="cuda", block_table: Optional[torch.Tensor] = None):
+        """block_table: int32 [batch, max_seq_len / block_size] on the device,
+        page of each block, required when cfg.kv_pages > 0 (paged pool)."""
         self.cfg = cfg
         self.device = torch.device(device)
+        if (cfg.kv_pages > 0) != (block_table is not None):
+            raise ValueError("a block table goes with kv_pages > 0, and only then")
+        if block_table is not None:
+            assert block_table.dtype == torch.int32 and block_table.is_contiguous()
+            assert block_table.shape == (cfg.batch, cfg.max_seq_len // cfg.block_size)
+            assert block_table.device == self.device
+        self.block_table = block_table
         sz = cache_bytes(cfg)
         dt = torch_dtype(cfg)
         e = 4 if cfg.dtype == F32 else 2
@@ -220,7 +229,8 @@ class SplaCache:
         self._struct = SplaCacheStruct(self.k.data_ptr(), self.v.data_ptr(),
                                        self.stats.data_ptr(), self.state.data_ptr(),
                                        self.norm.data_ptr(), self.seq_lens.data_ptr(),
-                                       self.err.data_ptr())
+                                       self.err.data_ptr(),
+                                       None if block_table is None else block_table.data_ptr())
 
     @property
     def struct(self) -> SplaCacheStruct:
@@ -297,14 +307,29 @@ class SplaCache:
         s = s.permute(0, 1, 3, 2, 5, 4, 6).reshape(c.batch, c.n_kv_heads, 2, nt * 64, c.head_dim)
         return s[:, :, 0, :nb], s[:, :, 1, :nb]
 
+    def _per_sequence(self, pool):
+        """A K or V buffer in the per-sequence layout ([batch][Hkv][nb][B d]):
+        the buffer itself, or the pages of a paged pool gathered through the
+        block table (entries outside the pool give zeros)."""
+        c = self.cfg
+        if c.kv_pages == 0:
+            return pool
+        bd = c.block_size * c.head_dim
+        pages = pool.view(c.kv_pages, c.n_kv_heads, bd)
+        tab = self.block_table.long()
+        ok = (tab >= 0) & (tab < c.kv_pages)
+        g = pages[tab.clamp(0, c.kv_pages - 1)] * ok[..., None, None].to(pool.dtype)
+        return g.permute(0, 2, 1, 3).contiguous().view(-1)
+
     def k_logical(self):
         """Keys as [batch][Hkv][max_seq_len][d] (undoing the bf16 step order)."""
         c = self.cfg
         B, H, T, d = c.batch, c.n_kv_heads, c.max_seq_len, c.head_dim
+        kbuf = self._per_sequence(self.k)
         if c.dtype == F32:
-            return self.k.view(B, H, T, d)
+            return kbuf.view(B, H, T, d)
         # step chunk (mt, ks, g, a, b) holds token 8a + 4mt + b, coordinates 32ks + 8g ..
-        k = self.k.view(B, H, T // 32, 2, d // 32, 4, 4, 4, 8)
+        k = kbuf.view(B, H, T // 32, 2, d // 32, 4, 4, 4, 8)
         return k.permute(0, 1, 2, 6, 3, 7, 4, 5, 8).reshape(B, H, T, d)
 
     def v_logical(self):
@@ -312,11 +337,12 @@ class SplaCache:
         of fp32 caches and the step order of bf16 ones)."""
         c = self.cfg
         B, H, T, d = c.batch, c.n_kv_heads, c.max_seq_len, c.head_dim
+        vbuf = self._per_sequence(self.v)
         if c.dtype == F32:
-            v = self.v.view(B, H, T // c.block_size, d, c.block_size)
+            v = vbuf.view(B, H, T // c.block_size, d, c.block_size)
             return v.permute(0, 1, 2, 4, 3).reshape(B, H, T, d)
         # step chunk (t, g, i) holds coordinate 16t + i, tokens 8g .. 8g + 7
-        v = self.v.view(B, H, T // 32, d // 16, 4, 16, 8)
+        v = vbuf.view(B, H, T // 32, d // 16, 4, 16, 8)
         return v.permute(0, 1, 2, 4, 6, 3, 5).reshape(B, H, T, d)
 
     def state_logical(self):

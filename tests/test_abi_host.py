@@ -76,6 +76,9 @@ def _cfg(**kw):
     (dict(sel_window=40, sel_stride=16), -2),                  # window not a multiple
     (dict(sel_window=80, sel_stride=16), -2),                  # more than 4 strides
     (dict(sel_window=32, sel_stride=16, max_seq_len=16 * 16385 // 64 * 64 + 64), -3),
+    (dict(kv_pages=100), 0),                                   # paged KV pool
+    (dict(kv_pages=-1), -1),
+    (dict(kv_pages=(1 << 24) + 1), -3),
 ])
 def test_validate_codes(libname, kw, want):
     lib = spla.lib() if libname == "hip" else spla.host_lib()
@@ -95,6 +98,10 @@ def test_sizes_follow_documented_layout():
     w = spla.cache_bytes(_cfg(sel_window=32, sel_stride=16))
     assert w[2] == 4 * 8 * 128 * 2 * 32 * 64 * 4 * 4
     assert w[:2] == b[:2] and w[3:] == b[3:]
+    # paged pool: one page of B rows per KV head and page
+    pg = spla.cache_bytes(_cfg(kv_pages=1000))
+    assert pg[0] == pg[1] == 1000 * 8 * 64 * 128 * 2
+    assert pg[2:] == b[2:]
 
 
 def test_device_calls_reject_bad_arguments_before_launch():
@@ -111,6 +118,13 @@ def test_device_calls_reject_bad_arguments_before_launch():
     # misaligned workspace
     assert lib.spla_decode(ctypes.byref(c), ctypes.byref(fake), 256, 256, 512, None, 8,
                            1 << 40, None) == -4
+    # a paged pool needs its block table, and a contiguous cache has none
+    paged = _cfg(kv_pages=64)
+    assert lib.spla_decode(ctypes.byref(paged), ctypes.byref(fake), 256, 256, 512, None, 256,
+                           1 << 40, None) == -1
+    tabled = spla.SplaCacheStruct(*([256] * 6), None, 256)
+    assert lib.spla_decode(ctypes.byref(c), ctypes.byref(tabled), 256, 256, 512, None, 256,
+                           1 << 40, None) == -1
     # out aliasing q
     assert lib.spla_decode(ctypes.byref(c), ctypes.byref(fake), 256, 256, 256, None, 256,
                            1 << 40, None) == -1
@@ -163,6 +177,7 @@ def test_header_and_host_code_under_sanitizers(tmp_path):
     (dict(dtype="f32"), False),
     (dict(flags=spla.FLAG_SEPARATE_KERNELS), False),
     (dict(sel_window=32, sel_stride=16), False),             # strided selection
+    (dict(kv_pages=4096), False),                            # paged KV pool
 ])
 def test_decode_phase_mask(libname, kw, single):
     lib = spla.lib() if libname == "hip" else spla.host_lib()

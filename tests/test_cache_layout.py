@@ -12,14 +12,15 @@ from paper_2601_22379_amd import spla
 
 
 class _Cfg:
-    def __init__(self, d, B, T, dtype):
+    def __init__(self, d, B, T, dtype, kv_pages=0):
         self.batch, self.n_kv_heads, self.head_dim = 2, 3, d
         self.block_size, self.max_seq_len, self.dtype = B, T, dtype
+        self.kv_pages = kv_pages
 
 
-def _cache(cfg, k_raw, v_raw):
+def _cache(cfg, k_raw, v_raw, table=None):
     c = object.__new__(spla.SplaCache)
-    c.cfg, c.k, c.v = cfg, k_raw, v_raw
+    c.cfg, c.k, c.v, c.block_table = cfg, k_raw, v_raw, table
     return c
 
 
@@ -69,3 +70,34 @@ def test_f32_layout_unchanged():
     assert torch.equal(cache.k_logical().reshape(-1), k)
     vl = cache.v_logical()  # [b][h][t][c] from [b][h][t/B][c][t%B]
     assert vl[0, 0, 33, 5].item() == ((1 * 64 + 5) * 32 + 1)
+
+
+@pytest.mark.parametrize("dtype", [spla.BF16, spla.F32])
+def test_paged_pool_reads_back_through_the_block_table(dtype):
+    """A paged pool (page p holds one block of every KV head at element
+    (p * Hkv + h) * B * d) filled from a per-sequence buffer through a
+    shuffled block table reads back as that buffer; unused pages are
+    ignored."""
+    d, B, T = 64, 32, 128
+    flat = _Cfg(d, B, T, dtype)
+    n = flat.batch * flat.n_kv_heads
+    nb = T // B
+    k = torch.arange(n * T * d, dtype=torch.float32)
+    v = -torch.arange(n * T * d, dtype=torch.float32)
+    pages = flat.batch * nb + 5
+    rng = np.random.default_rng(9)
+    table = torch.from_numpy(rng.permutation(pages)[:flat.batch * nb].reshape(flat.batch, nb)
+                             .astype(np.int32))
+    kp = torch.full((pages * flat.n_kv_heads * B * d,), 7.0)
+    vp = kp.clone()
+    for b in range(flat.batch):
+        for h in range(flat.n_kv_heads):
+            for i in range(nb):
+                src = ((b * flat.n_kv_heads + h) * nb + i) * B * d
+                dst = (int(table[b, i]) * flat.n_kv_heads + h) * B * d
+                kp[dst:dst + B * d] = k[src:src + B * d]
+                vp[dst:dst + B * d] = v[src:src + B * d]
+    ref = _cache(flat, k, v)
+    got = _cache(_Cfg(d, B, T, dtype, kv_pages=pages), kp, vp, table)
+    assert torch.equal(got.k_logical(), ref.k_logical())
+    assert torch.equal(got.v_logical(), ref.v_logical())
