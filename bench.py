@@ -64,16 +64,29 @@ def source_hash(paths):
     return h.hexdigest()[:16]
 
 
-def build_workload(w, replicas, dev, sel_window=0, sel_stride=0):
+def shuffled_block_table(w, seed=7):
+    """A paged pool of batch * nb_cap + 64 pages and a seeded shuffle of it
+    as the block table (int32 [batch][nb_cap])."""
+    import numpy as np
+
+    nb = w.capacity // w.block_size
+    pages = w.batch * nb + 64
+    rng = np.random.default_rng([seed, w.code])
+    return pages, rng.permutation(pages)[:w.batch * nb].reshape(w.batch, nb).astype(np.int32)
+
+
+def build_workload(w, replicas, dev, sel_window=0, sel_stride=0, paged=False):
     import torch
 
     from paper_2601_22379_amd import spla
     import spla_inputs as si
 
+    pages, table = shuffled_block_table(w) if paged else (0, None)
     cfg = spla.make_config(w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, w.block_size,
                            w.top_k, w.capacity, w.dtype, n_sink=w.n_sink, n_local=w.n_local,
-                           sel_window=sel_window, sel_stride=sel_stride)
-    first = spla.SplaCache(cfg, dev)
+                           sel_window=sel_window, sel_stride=sel_stride, kv_pages=pages)
+    tab = None if table is None else torch.from_numpy(table).to(dev)
+    first = spla.SplaCache(cfg, dev, block_table=tab)
     dt = torch.float32 if w.dtype == "f32" else torch.bfloat16
     lens = [w.prefill_length(b) for b in range(w.batch)]
     per_tok = w.batch * w.n_kv_heads * w.head_dim * 8
@@ -87,7 +100,7 @@ def build_workload(w, replicas, dev, sel_window=0, sel_stride=0):
     log(f"filled {w.name} in {time.time() - t0:.1f}s")
     caches = [first]
     for _ in range(replicas - 1):
-        c = spla.SplaCache(cfg, dev)
+        c = spla.SplaCache(cfg, dev, block_table=tab)
         for name in ("k", "v", "stats", "state", "norm", "seq_lens"):
             getattr(c, name).copy_(getattr(first, name))
         caches.append(c)
@@ -95,20 +108,21 @@ def build_workload(w, replicas, dev, sel_window=0, sel_stride=0):
     return cfg, caches
 
 
-def strided_leg(w, R, dev, qs, gamma, outs, sels, K, W, C=32, s=16):
+def strided_leg(w, R, dev, qs, gamma, outs, sels, K, W, C=32, s=16, paged=False):
     """The same decode with strided selection windows (C tokens every s,
-    max-pooled into blocks; the paper's C = 32, s = 16): a cache of its own
-    (one statistics entry per window), K timed steps, then the same steps
-    with every phase bracketed by HIP events. Returns a dict for the JSON
-    line; the scoring kernel, which streams the window statistics, is the
-    dominant one."""
+    max-pooled into blocks; the paper's C = 32, s = 16), or (C = s = B,
+    paged) with the K/V caches in a paged pool behind a shuffled block
+    table: a cache of its own, K timed steps, then the same steps with every
+    phase bracketed by HIP events. Returns a dict for the JSON line; the
+    scoring kernel, which streams the statistics, is the dominant one."""
     import numpy as np
     import torch
 
     from paper_2601_22379_amd import spla
     import spla_inputs as si
 
-    cfg, caches = build_workload(w, R, dev, C, s)
+    win = (C, s) != (w.block_size, w.block_size)
+    cfg, caches = build_workload(w, R, dev, C if win else 0, s if win else 0, paged)
 
     def one(i, events=None):
         r = i % R
@@ -138,14 +152,16 @@ def strided_leg(w, R, dev, qs, gamma, outs, sels, K, W, C=32, s=16):
                        for i in sel_np[b, h] if i >= 0) for h in range(w.n_kv_heads)]
                   for b in range(w.batch)]
     ab = si.algorithmic_bytes(w, sel_counts)
-    ab["stats"] = sum(-(-int(L) // s) for L in lens) * w.n_kv_heads * 2 * w.head_dim * 4
+    if win:
+        ab["stats"] = sum(-(-int(L) // s) for L in lens) * w.n_kv_heads * 2 * w.head_dim * 4
     ab["total"] = ab["q_out"] + ab["stats"] + ab["selected_kv"] + ab["state"] + ab["append"]
     sb = dominant_bytes(w, ab, "score")
     del caches
     torch.cuda.synchronize()
-    log(f"strided selection (C={C}, s={s}): {lat_us:.2f} us/step, phases us: "
-        + ", ".join(f"{k}={v:.2f}" for k, v in phases.items()))
-    return {"window": C, "stride": s, "latency_us": round(lat_us, 3),
+    log(f"{'paged KV' if paged else 'strided selection'} (C={C}, s={s}): {lat_us:.2f} us/step, "
+        "phases us: " + ", ".join(f"{k}={v:.2f}" for k, v in phases.items()))
+    head = {"kv_pages": int(cfg.kv_pages)} if paged else {"window": C, "stride": s}
+    return {**head, "latency_us": round(lat_us, 3),
             "value": round(ab["total"] / (lat_us * 1e-6) / 1e9, 1), "unit": "GB/s",
             "algorithmic_bytes": ab, "phases_us": {k: round(v, 3) for k, v in phases.items()},
             "roofline": {"kernel": "score", "bound": "hbm",
@@ -300,7 +316,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-graph", action="store_true")
     ap.add_argument("--no-strided", action="store_true",
-                    help="skip the strided-selection leg (C = 32, s = 16)")
+                    help="skip the strided-selection (C = 32, s = 16) and paged-KV legs")
     ap.add_argument("--strided-only", action="store_true",
                     help="run only the strided-selection leg and print its JSON (profiling)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -548,9 +564,11 @@ def main():
                 "avg_launch_us": round(dom_us, 3), "avg_launch_method": dom_method,
                 "avg_launch_us_per_launch_events": round(dom_us_events, 3),
                 "profiled_avg_us": prof_us}
-    strided = None
+    strided = paged = None
     if not appending and not args.no_strided:
         strided = strided_leg(w, R, dev, qs, gamma, outs, sels, K, W)
+        paged = strided_leg(w, R, dev, qs, gamma, outs, sels, K, W, C=w.block_size,
+                            s=w.block_size, paged=True)
     cpu = None
     if not args.no_cpu_baseline:
         log("timing the CPU oracle")
@@ -583,6 +601,7 @@ def main():
         "roofline": roofline,
         "cpu_baseline": cpu,
         "strided_selection": strided,
+        "paged_kv": paged,
     }
     print(json.dumps(line), flush=True)
 
