@@ -72,6 +72,7 @@ struct FusedArgs {
   int n_si;     // score items per (sequence, KV head)
   int n_wg;     // sparse items per (sequence, KV head)
   int stride;   // floats per record
+  const int32_t* table;  // block table of a paged K/V pool, or NULL
 };
 
 __device__ __forceinline__ int atomic_add_agent(int32_t* p, int v) {
@@ -213,7 +214,7 @@ void decode_kernel(FusedArgs a) {
   const int v = step < m.k ? s_words[tid >> 6] : 1;  // 0 only after a wait that gave up
   const int blk_sel = __builtin_amdgcn_readfirstlane(v) - 2;
   sparse_body<D, BLK, true, GC>(m, a.s, a.kc, a.vc, blk_sel, L, bh, x, a.n_wg, r, sm.sp, a.part,
-                                a.stride);
+                                a.stride, a.table);
   if (poller) {  // the workgroup's entries, read by it only
 #pragma unroll
     for (int i = 0; i < NE; ++i)
@@ -280,6 +281,7 @@ hipError_t launch_decode_fused(const Dims& m, const spla_config& cfg, const spla
   a.n_si = (int)ceil_div(m.n_tiles, kTilesPerItem);
   a.n_wg = ws.n_wg;
   a.stride = ws.part_stride;
+  a.table = m.pages > 0 ? c.block_table : nullptr;
   switch (m.group) {
     case 1: decode_g<1>(a, st); break;
     case 2: decode_g<2>(a, st); break;

@@ -139,7 +139,7 @@ constexpr int kFusedMaxBlocks = 256 * 32;
 constexpr int kFusedMaxGroup = 6;
 SPLA_HD bool use_fused_decode(const Dims& m) {
   return use_mfma_sparse(m) && m.d == 128 && m.group <= kFusedMaxGroup &&
-         m.nb_cap <= kFusedMaxBlocks && !windowed(m) && m.pages == 0;
+         m.nb_cap <= kFusedMaxBlocks && !windowed(m);
 }
 
 // The decode workspace's synchronisation area (int32 words). Every counter

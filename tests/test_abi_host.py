@@ -177,7 +177,7 @@ def test_header_and_host_code_under_sanitizers(tmp_path):
     (dict(dtype="f32"), False),
     (dict(flags=spla.FLAG_SEPARATE_KERNELS), False),
     (dict(sel_window=32, sel_stride=16), False),             # strided selection
-    (dict(kv_pages=4096), False),                            # paged KV pool
+    (dict(kv_pages=4096), True),                             # paged KV pool
 ])
 def test_decode_phase_mask(libname, kw, single):
     lib = spla.lib() if libname == "hip" else spla.host_lib()

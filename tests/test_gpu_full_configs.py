@@ -129,3 +129,38 @@ def test_full_size_strided_selection(dev):
     infos = [H.check_kv_head(w, b, h, out[b], sel[b, h], q[b], gamma, p) for b, h in pairs]
     H.log(f"strided config 3: worst rel err {max(i['rel_err'] for i in infos):.3e}, "
           f"swaps {sum(i['n_swapped'] for i in infos)}")
+
+
+@pytest.mark.timeout(900)
+def test_full_size_paged_cache(dev):
+    """The 128K workload in a paged pool behind a shuffled block table: the
+    same selection and bit-identical outputs as the per-sequence cache, and
+    sampled units against the oracle."""
+    w = si.config("3")
+    nb = w.capacity // w.block_size
+    pages = w.batch * nb + 64
+    rng = np.random.default_rng([3, w.code])
+    tab = rng.permutation(pages)[:w.batch * nb].reshape(w.batch, nb).astype(np.int32)
+    cfg = spla.make_config(w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, w.block_size,
+                           w.top_k, w.capacity, w.dtype, n_sink=w.n_sink, n_local=w.n_local,
+                           kv_pages=pages)
+    paged = spla.SplaCache(cfg, dev, block_table=torch.from_numpy(tab).to(dev))
+    H.fill_cache(w, paged, device=dev)
+    q = si.gen_q_batch(w)
+    gamma = si.gen_gamma(w)
+    qd, gd = H.to_dev(q, w, dev), torch.from_numpy(gamma).to(dev)
+    out_p, sel_p = paged.decode(qd, gd)
+    torch.cuda.synchronize()
+    del paged
+    flat = spla.SplaCache(H.config_of(w, flags=spla.FLAG_SEPARATE_KERNELS), dev)
+    H.fill_cache(w, flat, device=dev)
+    out_f, sel_f = flat.decode(qd, gd)
+    torch.cuda.synchronize()
+    assert torch.equal(sel_f, sel_p) and torch.equal(out_f, out_p)
+    out = out_p.float().cpu().numpy()
+    sel = sel_p.cpu().numpy()
+    check_properties(w, sel, out, w.lengths)
+    p = H.params_of(w)
+    pairs = sample_pairs(w, 2, 2)
+    infos = [H.check_kv_head(w, b, h, out[b], sel[b, h], q[b], gamma, p) for b, h in pairs]
+    H.log(f"paged config 3: worst rel err {max(i['rel_err'] for i in infos):.3e}")

@@ -115,3 +115,19 @@ def test_strided_step_appends_one_token_then_decodes(dev):
         st = O.build_state(K, V, L + 1, w.block_size, C, s)
         H.check_kv_head(w, 0, 0, out.float().cpu().numpy()[0], sel.cpu().numpy()[0, 0], q[0],
                         gamma, p, L=L + 1, state=st)
+
+
+@pytest.mark.parametrize("flags,kw", [
+    (spla.FLAG_FIRST_ORDER, dict(first_order=True)),
+    (spla.FLAG_NO_RLA | spla.FLAG_FIRST_ORDER, dict(no_rla=True, first_order=True)),
+    (spla.FLAG_RLA_NORMALIZE, dict(rla_normalize=True)),
+])
+def test_strided_selection_with_variant_flags(dev, flags, kw):
+    """The ablation switches of Sec. 4 combined with strided windows."""
+    w = si.custom("winflags", 2, 8, 2, 128, 64, 8, [3000, 4100], kind="block_offsets", code=152)
+    H.log(f"strided flags {flags}")
+    cache, q, gamma, out, sel = run(w, dev, 32, 16, flags=flags)
+    p = H.params_of(w, window=32, stride=16, **kw)
+    for b in range(w.batch):
+        for h in range(w.n_kv_heads):
+            H.check_kv_head(w, b, h, out[b], sel[b, h], q[b], gamma, p)
