@@ -64,6 +64,16 @@ SMALL = {
                              top_k=40, lengths=[20000], kind="pareto_planted", n_planted=8),
     "bf16_empty_and_short": dict(batch=3, n_q_heads=4, n_kv_heads=1, head_dim=128,
                                  block_size=32, top_k=6, lengths=[0, 300, 31], kind="iid"),
+    # library limits: k = SPLA_MAX_TOP_K with G = SPLA_MAX_GROUP (VALU pass) and on
+    # the single-launch kernel; SPLA_MAX_BLOCKS blocks per sequence
+    "bf16_k256_g16": dict(batch=1, n_q_heads=16, n_kv_heads=1, head_dim=64, block_size=32,
+                          top_k=256, lengths=[20000], kind="iid"),
+    "bf16_k256_single_launch": dict(batch=2, n_q_heads=8, n_kv_heads=2, head_dim=128,
+                                    block_size=64, top_k=256, lengths=[40000, 17000],
+                                    kind="block_offsets"),
+    "bf16_32768_blocks": dict(batch=1, n_q_heads=4, n_kv_heads=1, head_dim=64, block_size=32,
+                              top_k=32, lengths=[32768 * 32 - 7], capacity=32768 * 32,
+                              kind="iid"),
 }
 
 
