@@ -191,6 +191,23 @@ __device__ void select_blocks(const Dims& m, int bh, int seq_len,
     for (int h = 0; h < HC; ++h)
       load_run<R, CO>(ev, (int64_t)h * nbp + i0, h < G && i0 < nbp, e[h]);
   }
+  // WIN: the window masses of the first four heads, as runs of four windows
+  // starting at 4 (t + j NT) (16-byte loads; a run holding a window below nu
+  // lies inside the row), issued here so that they overlap the tile weights
+  constexpr int J4 = WIN ? kMaxWindows / (4 * NT) : 1;
+  static_assert(!WIN || kMaxWindows % (4 * NT) == 0, "window staging");
+  const int nu = WIN ? (L + m.us - 1) / m.us : 0;  // windows present
+  uint4 wv[4][J4];
+  if constexpr (WIN) {
+#pragma unroll
+    for (int hh = 0; hh < 4; ++hh)
+#pragma unroll
+      for (int j = 0; j < J4; ++j) {
+        const int u = 4 * (tid + j * NT);
+        wv[hh][j] = Mem<CO>::ld16(ev + (int64_t)min(hh, G - 1) * nbp,
+                                  (uint32_t)(u < nu ? u : 0) * 4u);
+      }
+  }
 
   const int nb = (L + m.B - 1) / m.B;
   if (nb <= k) {  // L == 0 included: nothing or everything is selected
@@ -207,8 +224,7 @@ __device__ void select_blocks(const Dims& m, int bh, int seq_len,
     }
     return;
   }
-  const int nu = WIN ? (L + m.us - 1) / m.us : nb;  // units present
-  const int n_tu = (nu + kTileBlocks - 1) / kTileBlocks;
+  const int n_tu = ((WIN ? nu : nb) + kTileBlocks - 1) / kTileBlocks;  // unit tiles present
   for (int x = tid; x < 1024; x += NT) reinterpret_cast<uint4*>(hist)[x] = make_uint4(0u, 0u, 0u, 0u);
   // --- 1. Z_m and the tile weights of heads m = w, w + NW, ...
   for (int mm = w; kp > 0 && mm < G; mm += NW) {
@@ -260,27 +276,23 @@ __device__ void select_blocks(const Dims& m, int bh, int seq_len,
     float best[R];  // the block's score, rounded to fp32
     if constexpr (WIN) {
       // every window's group score (fp64 sum over the heads, rounded to
-      // fp32) into LDS: thread t takes the runs of four windows starting at
-      // 4 (t + j NT); the loads of four heads are issued together, as
-      // 16-byte loads (a run never leaves the 64-window tile, and a run
-      // holding a window below nu lies inside the row)
-      constexpr int J4 = kMaxWindows / (4 * NT);
-      static_assert(kMaxWindows % (4 * NT) == 0, "window staging");
+      // fp32) into LDS, four heads at a time: the first four heads' masses
+      // were loaded at the start, later ones are loaded per batch
       double g[J4][4];
 #pragma unroll
       for (int j = 0; j < J4; ++j)
 #pragma unroll
         for (int c = 0; c < 4; ++c) g[j][c] = 0.0;
       for (int h0 = 0; h0 < G; h0 += 4) {
-        uint4 v[4][J4];
+        if (h0 > 0) {
 #pragma unroll
-        for (int hh = 0; hh < 4; ++hh) {
-          const int h = min(h0 + hh, G - 1);
+          for (int hh = 0; hh < 4; ++hh)
 #pragma unroll
-          for (int j = 0; j < J4; ++j) {
-            const int u = 4 * (tid + j * NT);
-            v[hh][j] = Mem<CO>::ld16(ev + (int64_t)h * nbp, (uint32_t)(u < nu ? u : 0) * 4u);
-          }
+            for (int j = 0; j < J4; ++j) {
+              const int u = 4 * (tid + j * NT);
+              wv[hh][j] = Mem<CO>::ld16(ev + (int64_t)min(h0 + hh, G - 1) * nbp,
+                                        (uint32_t)(u < nu ? u : 0) * 4u);
+            }
         }
 #pragma unroll
         for (int hh = 0; hh < 4; ++hh) {
@@ -288,11 +300,11 @@ __device__ void select_blocks(const Dims& m, int bh, int seq_len,
 #pragma unroll
             for (int j = 0; j < J4; ++j) {
               const int u = 4 * (tid + j * NT);
-              const double wv = (double)sw[((u < nu ? u : 0) / kTileBlocks) * G + h0 + hh];
-              g[j][0] = fma((double)__uint_as_float(v[hh][j].x), wv, g[j][0]);
-              g[j][1] = fma((double)__uint_as_float(v[hh][j].y), wv, g[j][1]);
-              g[j][2] = fma((double)__uint_as_float(v[hh][j].z), wv, g[j][2]);
-              g[j][3] = fma((double)__uint_as_float(v[hh][j].w), wv, g[j][3]);
+              const double wt = (double)sw[((u < nu ? u : 0) / kTileBlocks) * G + h0 + hh];
+              g[j][0] = fma((double)__uint_as_float(wv[hh][j].x), wt, g[j][0]);
+              g[j][1] = fma((double)__uint_as_float(wv[hh][j].y), wt, g[j][1]);
+              g[j][2] = fma((double)__uint_as_float(wv[hh][j].z), wt, g[j][2]);
+              g[j][3] = fma((double)__uint_as_float(wv[hh][j].w), wt, g[j][3]);
             }
           }
         }
