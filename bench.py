@@ -37,8 +37,38 @@ KERNEL_SOURCES = sorted("paper_2601_22379_amd/csrc/" + f
                         if f.endswith((".hip", ".h")))
 
 
-def traffic_file(kernel):
-    return os.path.join(ROOT, "profiles", f"{kernel}_kernel_traffic.json")
+STRIDED_TAG = "_strided_c32_s16"
+
+
+def traffic_file(kernel, variant=""):
+    return os.path.join(ROOT, "profiles", f"{kernel}{variant}_kernel_traffic.json")
+
+
+def traffic_of(kernel, workload, variant=""):
+    """Calibrated HBM bytes per launch of `kernel` from its committed counter
+    summary, or None when there is none or the kernel sources changed since."""
+    tfile = traffic_file(kernel, variant)
+    if not os.path.exists(tfile):
+        return None
+    with open(tfile) as f:
+        tr = json.load(f)
+    if tr.get("source_sha") == source_hash(KERNEL_SOURCES) and tr.get("workload") == workload:
+        return tr["hbm_bytes_per_launch"]
+    return None
+
+
+def copy_calibration(dev):
+    """A plain elementwise kernel over 1 GiB (1 GiB read, 1 GiB written): the
+    reference the counter passes are scaled by."""
+    import torch
+
+    n = 1 << 28
+    src = torch.ones(n, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    torch.mul(src, 1.0, out=dst)
+    torch.cuda.synchronize()
+    log("copy calibration: 1 GiB read + 1 GiB written by one elementwise kernel")
 
 
 def dominant_bytes(w, ab, kernel):
@@ -166,6 +196,8 @@ def strided_leg(w, R, dev, qs, gamma, outs, sels, K, W, C=32, s=16, paged=False)
     log(f"{'paged KV' if paged else 'strided selection'} (C={C}, s={s}): {lat_us:.2f} us/step, "
         "phases us: " + ", ".join(f"{k}={v:.2f}" for k, v in phases.items()))
     head = {"kv_pages": int(cfg.kv_pages)} if paged else {"window": C, "stride": s}
+    # counter passes exist for the strided variant's scoring kernel only
+    traffic = None if paged else traffic_of(dom, w.name, STRIDED_TAG)
     return {**head, "latency_us": round(lat_us, 3),
             "value": round(ab["total"] / (lat_us * 1e-6) / 1e9, 1), "unit": "GB/s",
             "algorithmic_bytes": ab, "phases_us": {k: round(v, 3) for k, v in phases.items()},
@@ -173,6 +205,7 @@ def strided_leg(w, R, dev, qs, gamma, outs, sels, K, W, C=32, s=16, paged=False)
                          "achieved": round(sb / (dom_us * 1e-6) / 1e9, 1),
                          "peak": PEAK_HBM_GBS, "unit": "GB/s",
                          "frac": round(sb / (dom_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4),
+                         "traffic": traffic,
                          "algorithmic_bytes_per_launch": sb,
                          "avg_launch_us": round(dom_us, 3),
                          "avg_launch_method": ("timed region / launches" if dom == "decode"
@@ -256,7 +289,8 @@ def trace_summary(trace_dir, workload, command, out_path):
     print("\n".join(lines))
 
 
-def traffic_summary(fetch_dir, write_dir, workload, commands, out_md, kernel, kernel_bytes):
+def traffic_summary(fetch_dir, write_dir, workload, commands, out_md, kernel, kernel_bytes,
+                    variant=""):
     """Calibrated HBM bytes per dispatch from FETCH_SIZE / WRITE_SIZE passes.
 
     Both counters are in KiB per dispatch. Each is scaled by what it reads for
@@ -280,7 +314,8 @@ def traffic_summary(fetch_dir, write_dir, workload, commands, out_md, kernel, ke
     gib_kib = float(1 << 20)
     f_scale = gib_kib / fetch[copy[0]]
     w_scale = gib_kib / write[copy[0]]
-    lines = [f"# SPLA decode, {workload}: HBM traffic per dispatch (rocprofv3 counters)", ""]
+    label = workload + (", strided selection windows C = 32, s = 16" if variant else "")
+    lines = [f"# SPLA decode, {label}: HBM traffic per dispatch (rocprofv3 counters)", ""]
     lines += [f"command: `{c}`" for c in commands]
     lines += ["", f"calibration (1 GiB read + 1 GiB written by one elementwise kernel): "
               f"FETCH_SIZE reads {fetch[copy[0]]:.1f} KiB -> scale {f_scale:.4f}; "
@@ -302,7 +337,7 @@ def traffic_summary(fetch_dir, write_dir, workload, commands, out_md, kernel, ke
               f"{dom[1] / 1e6:.3f})"]
     with open(out_md, "w") as f:
         f.write("\n".join(lines) + "\n")
-    with open(traffic_file(kernel), "w") as f:
+    with open(traffic_file(kernel, variant), "w") as f:
         json.dump({"workload": workload, "kernel": kernel,
                    "source_sha": source_hash(KERNEL_SOURCES),
                    "hbm_bytes_per_launch": int(round(dom[0] + dom[1])),
@@ -339,7 +374,7 @@ def main():
     if args.trace_summary or args.traffic_summary:
         import spla_inputs as si
         w = si.config(args.config)
-        tag = f"decode_{w.name}" + ("_strided_c32_s16" if args.strided_only else "")
+        tag = f"decode_{w.name}" + (STRIDED_TAG if args.strided_only else "")
         if args.trace_summary:
             label = w.name + (", strided selection windows C = 32, s = 16"
                               if args.strided_only else "")
@@ -347,9 +382,13 @@ def main():
                           os.path.join(ROOT, "profiles", f"{tag}_kernel_trace.md"))
         if args.traffic_summary:
             ab = si.algorithmic_bytes(w, None)
+            variant = STRIDED_TAG if args.strided_only else ""
+            if args.strided_only:  # window statistics: one entry per 16 tokens
+                ab["stats"] = sum(-(-int(L) // 16) for L in w.lengths) * w.n_kv_heads * 2 * \
+                    w.head_dim * 4
             traffic_summary(args.traffic_summary[0], args.traffic_summary[1], w.name,
                             args.command, os.path.join(ROOT, "profiles", f"{tag}_traffic.md"),
-                            args.kernel, dominant_bytes(w, ab, args.kernel))
+                            args.kernel, dominant_bytes(w, ab, args.kernel), variant)
         return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -376,8 +415,10 @@ def main():
                 for _ in range(R)]
         sels = [torch.empty((w.batch, w.n_kv_heads, w.top_k), dtype=torch.int32, device=dev)
                 for _ in range(R)]
-        print(json.dumps(strided_leg(w, R, dev, qs, gamma, outs, sels, args.steps,
-                                     args.warmup)), flush=True)
+        line = strided_leg(w, R, dev, qs, gamma, outs, sels, args.steps, args.warmup)
+        if args.copy_calibration:
+            copy_calibration(dev)
+        print(json.dumps(line), flush=True)
         return
     cfg, caches = build_workload(w, R, dev)
     dt = torch.float32 if w.dtype == "f32" else torch.bfloat16
@@ -529,13 +570,7 @@ def main():
             log(f"graph measurement skipped: {e!r}")
 
     if args.copy_calibration:
-        n = 1 << 28
-        src = torch.ones(n, dtype=torch.float32, device=dev)
-        dst = torch.empty_like(src)
-        torch.cuda.synchronize()
-        torch.mul(src, 1.0, out=dst)
-        torch.cuda.synchronize()
-        log("copy calibration: 1 GiB read + 1 GiB written by one elementwise kernel")
+        copy_calibration(dev)
 
     sel_counts = None
     if not appending:
@@ -549,13 +584,7 @@ def main():
     value = total / (ms_per_step * 1e-3) / 1e9
     dom_bytes = dominant_bytes(w, ab, dom)
     achieved = dom_bytes / (dom_us * 1e-6) / 1e9
-    traffic = None
-    tfile = traffic_file(dom)
-    if os.path.exists(tfile):
-        with open(tfile) as f:
-            tr = json.load(f)
-        if tr.get("source_sha") == source_hash(KERNEL_SOURCES) and tr.get("workload") == w.name:
-            traffic = tr["hbm_bytes_per_launch"]
+    traffic = traffic_of(dom, w.name)
     # the committed kernel-trace summary's average for the same kernel: the
     # events above also span the kernel's dispatch latency
     prof_us = None
