@@ -34,4 +34,5 @@ from .spla_oracle import (  # noqa: F401
     decode_sequence,
     append_state,
     cutoff_score,
+    prefill_kv_head,
 )

@@ -38,6 +38,10 @@ step it affects):
   weight gamma, eps 1e-6) of the residual to the exact output, with no gate
   beyond gamma (Sec. 3.3).
 * an empty sequence (L = 0) decodes to a zero output with no selection.
+* prefill (Sec. 2 extends the decode formulation to prefill and training):
+  the query at position t gets exactly the output a decode step at t would,
+  over the first t + 1 tokens, including the statistics of its own partial
+  block and S_bar over that prefix.
 * strided block selection (Sec. 3.1, "Strided Block Selection"; optional):
   window w covers tokens [w s, min(w s + C, L)), one window per start below
   L, so the last windows may be partial and use their real counts. Each
@@ -510,3 +514,25 @@ def decode_sequence(q: np.ndarray, K: np.ndarray, V: np.ndarray, L: int, gamma: 
     win = (None, None) if (C, st) == (p.block_size, p.block_size) else (C, st)
     states = [build_state(K[h], V[h], L, p.block_size, *win) for h in range(K.shape[0])]
     return decode_from_state(q, states, K, V, gamma, p, force_selection)
+
+
+# ------------------------------------------------------- chunked prefill
+def prefill_kv_head(Q: np.ndarray, K: np.ndarray, V: np.ndarray, L0: int, gamma: np.ndarray,
+                    p: SplaParams) -> list:
+    """Causal prefill of one KV head group (Sec. 2: the decode formulation
+    carries over to prefill and training). Q [T, G, d] are the queries at
+    positions L0 .. L0 + T - 1; K, V [>= L0 + T, d]. The query at position t
+    sees the tokens 0 .. t, so its output is the decode step on the state of
+    the first t + 1 tokens: its own block selection (the block holding t is
+    partial and its statistics cover tokens up to t), the exact branch over
+    the selected tokens, and the residual linear branch with S_bar taken over
+    the same prefix. Returns a list of T DecodeResult."""
+    Q = np.asarray(Q, dtype=f64)
+    C, st = p.windows()
+    win = (None, None) if (C, st) == (p.block_size, p.block_size) else (C, st)
+    out = []
+    for i in range(Q.shape[0]):
+        n = L0 + i + 1
+        state = build_state(K, V, n, p.block_size, *win)
+        out.append(decode_kv_head(Q[i], state, K[:n], V[:n], gamma, p))
+    return out

@@ -201,3 +201,17 @@ def test_wrong_window_ranges(monkeypatch, mistake):
     _patch(monkeypatch, "window_ranges", bad)
     _expect_failure((W.test_x15_constant_keys_window_and_block_scores_closed_form, ()),
                     (W.test_x16_window_mass_matches_token_sum, (32, 16)))
+
+
+def test_prefill_that_sees_the_whole_chunk(monkeypatch):
+    """Every query of a chunk decoded against the whole chunk (no causal
+    mask) in place of its own prefix."""
+    import test_oracle_prefill as PF
+
+    def bad(Q, K, V, L0, gamma, p):
+        n = L0 + Q.shape[0]
+        state = OS.build_state(K, V, n, p.block_size)
+        return [OS.decode_kv_head(Q[i], state, K[:n], V[:n], gamma, p) for i in range(Q.shape[0])]
+    _patch(monkeypatch, "prefill_kv_head", bad)
+    _expect_failure((PF.test_p1_all_blocks_selected_is_causal_dense_attention, (5, 12)),
+                    (PF.test_p3_later_tokens_do_not_change_earlier_outputs, ()))
