@@ -6,24 +6,35 @@
 
 namespace spla {
 
-template <int G, typename T, int D>
+template <int G, typename T, int D, int NT>
 __global__ __launch_bounds__(256) void score_kernel(
     Dims m, const float* __restrict__ stats, const int32_t* __restrict__ seq_lens,
     const T* __restrict__ q, double s, int first_order, float* __restrict__ e_vals,
     double* __restrict__ tile_part) {
   __shared__ ScoreSmem<G> sm;
-  score_items<G, T, D, false, 1>(m, stats, seq_lens, q, s, first_order, (int)blockIdx.x, e_vals,
-                               tile_part, sm);
+  const int per = (m.n_tiles + NT - 1) / NT;  // items per (sequence, KV head)
+  const int t = ((int)blockIdx.x / per) * m.n_tiles + ((int)blockIdx.x % per) * NT;
+  score_items<G, T, D, false, NT>(m, stats, seq_lens, q, s, first_order, t, e_vals, tile_part,
+                                  sm);
 }
 
 template <int G, typename T, int D>
 static void score_gtd(const Dims& m, const spla_config& cfg, const spla_cache& c, const void* q,
                       const DecodeWs& ws, char* base, hipStream_t st) {
   const double s = cfg.softmax_scale > 0.f ? (double)cfg.softmax_scale : 1.0 / sqrt((double)m.d);
-  hipLaunchKernelGGL((score_kernel<G, T, D>), dim3((unsigned)(m.bh * m.n_tiles)), dim3(256), 0,
-                     st, m, (const float*)c.blk_stats, (const int32_t*)c.seq_lens, (const T*)q, s,
-                     (int)((cfg.flags & SPLA_FLAG_FIRST_ORDER) != 0),
-                     (float*)(base + ws.e_vals), (double*)(base + ws.tile_part));
+  // window statistics (four times the tiles of blocks at s = B / 4): two
+  // tiles per item halve the items and their fixed costs
+  const int fo = (int)((cfg.flags & SPLA_FLAG_FIRST_ORDER) != 0);
+  if (windowed(m))
+    hipLaunchKernelGGL((score_kernel<G, T, D, 2>), dim3((unsigned)(m.bh * ceil_div(m.n_tiles, 2))),
+                       dim3(256), 0, st, m, (const float*)c.blk_stats, (const int32_t*)c.seq_lens,
+                       (const T*)q, s, fo, (float*)(base + ws.e_vals),
+                       (double*)(base + ws.tile_part));
+  else
+    hipLaunchKernelGGL((score_kernel<G, T, D, 1>), dim3((unsigned)(m.bh * m.n_tiles)), dim3(256),
+                       0, st, m, (const float*)c.blk_stats, (const int32_t*)c.seq_lens,
+                       (const T*)q, s, fo, (float*)(base + ws.e_vals),
+                       (double*)(base + ws.tile_part));
 }
 
 template <typename T, int D>
