@@ -55,6 +55,13 @@ CASES = {
                                block_size=128, top_k=6, lengths=[7000], kind="iid"), 32, 16),
     "bf16_C16_s16_B64": (dict(batch=1, n_q_heads=16, n_kv_heads=2, head_dim=64, block_size=64,
                               top_k=10, lengths=[12345], kind="block_offsets"), 16, 16),
+    # G = 16 (the VALU pass; the selection takes its heads four at a time)
+    "bf16_C32_s16_g16": (dict(batch=1, n_q_heads=16, n_kv_heads=1, head_dim=64, block_size=32,
+                              top_k=10, lengths=[9000], kind="drift"), 32, 16),
+    # an odd number of statistics tiles (two tiles per scoring item)
+    "bf16_C32_s16_odd_tiles": (dict(batch=2, n_q_heads=4, n_kv_heads=1, head_dim=128,
+                                    block_size=64, top_k=8, lengths=[3 * 1024 + 17, 1000],
+                                    capacity=3 * 1024 + 64, kind="iid"), 32, 16),
 }
 
 
