@@ -302,6 +302,26 @@ int32_t spla_step(const spla_config* cfg, const spla_cache* cache, const void* k
                   const void* v_new, const void* q, const float* rms_weight, void* out,
                   int32_t* sel_idx, void* workspace, size_t workspace_bytes, void* stream);
 
+/* Causal prefill of n_tokens new tokens per sequence (Sec. 2: the decode
+ * formulation carries over to prefill). For t = 0 .. n_tokens - 1, token t of
+ * every (sequence, KV head) is appended and the queries at that position are
+ * decoded, exactly as spla_step would: the query at position L_b + t sees the
+ * tokens up to and including its own, with its own block selection.
+ *  k_new, v_new: device, dtype [n_tokens][batch][Hkv][d] (position-major).
+ *  q:            device, dtype [n_tokens][batch][Hq][d].
+ *  rms_weight:   device fp32 [Hq][d].
+ *  out:          device, dtype [n_tokens][batch][Hq][d] (may not alias q).
+ *  sel_idx:      device int32 [n_tokens][batch][Hkv][top_k] or NULL.
+ *  workspace:    the decode workspace (spla_workspace_bytes, prepared once by
+ *                spla_workspace_init).
+ * Runs n_tokens append + decode steps on `stream` (one position at a time; no
+ * chunk-wide kernels yet). n_tokens = 0 does nothing; tokens past max_seq_len
+ * are dropped as in spla_step. */
+int32_t spla_prefill(const spla_config* cfg, const spla_cache* cache, int32_t n_tokens,
+                     const void* k_new, const void* v_new, const void* q,
+                     const float* rms_weight, void* out, int32_t* sel_idx, void* workspace,
+                     size_t workspace_bytes, void* stream);
+
 /* spla_step with optional timing events (events may be NULL). */
 int32_t spla_step_ex(const spla_config* cfg, const spla_cache* cache, const void* k_new,
                      const void* v_new, const void* q, const float* rms_weight, void* out,

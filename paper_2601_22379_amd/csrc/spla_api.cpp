@@ -190,3 +190,34 @@ extern "C" int32_t spla_step(const spla_config* cfg, const spla_cache* cache, co
                              int32_t* sel_idx, void* ws, size_t ws_bytes, void* stream) {
   return spla_step_ex(cfg, cache, k_new, v_new, q, w, out, sel_idx, ws, ws_bytes, nullptr, stream);
 }
+
+extern "C" int32_t spla_prefill(const spla_config* cfg, const spla_cache* cache, int32_t n_tokens,
+                                const void* k_new, const void* v_new, const void* q,
+                                const float* w, void* out, int32_t* sel_idx, void* ws,
+                                size_t ws_bytes, void* stream) {
+  int32_t s = check_decode_args(cfg, cache, q, w, out, ws, ws_bytes);
+  if (s != SPLA_OK) return s;
+  if (n_tokens < 0) return SPLA_ERR_INVALID_ARG;
+  if (n_tokens > cfg->max_seq_len) return SPLA_ERR_CAPACITY;
+  if (n_tokens == 0) return SPLA_OK;
+  if (!k_new || !v_new) return SPLA_ERR_INVALID_ARG;
+  const Dims m = spla::make_dims(*cfg);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  // per position: the rows of token t, the queries at t, their outputs
+  const size_t kv_step = (size_t)m.bh * m.d * m.elem;
+  const size_t q_step = (size_t)m.batch * m.hq * m.d * m.elem;
+  const size_t sel_step = (size_t)m.bh * m.k;
+  for (int32_t t = 0; t < n_tokens; ++t) {
+    const char* kt = static_cast<const char*>(k_new) + t * kv_step;
+    const char* vt = static_cast<const char*>(v_new) + t * kv_step;
+    SPLA_TRY(spla::launch_append_blocks(m, *cache, kt, vt, 1, nullptr, st));
+    SPLA_TRY(spla::launch_append_state_rank1(m, *cache, kt, vt, st));
+    SPLA_TRY(spla::launch_append_finish(m, *cache, 1, nullptr, st));
+    if ((s = run_decode(cfg, cache, static_cast<const char*>(q) + t * q_step, w,
+                        static_cast<char*>(out) + t * q_step,
+                        sel_idx ? sel_idx + t * sel_step : nullptr, ws, ws_bytes, nullptr, st)) !=
+        SPLA_OK)
+      return s;
+  }
+  return SPLA_OK;
+}

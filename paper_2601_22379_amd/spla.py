@@ -33,7 +33,7 @@ STATUS = {0: "ok", -1: "invalid argument", -2: "unsupported shape",
 EXPORTS = ["spla_status_string", "spla_phase_name", "spla_validate", "spla_cache_bytes",
            "spla_workspace_bytes", "spla_append_workspace_bytes", "spla_decode_phase_mask",
            "spla_workspace_init", "spla_reset", "spla_append",
-           "spla_decode", "spla_decode_ex", "spla_step", "spla_step_ex"]
+           "spla_decode", "spla_decode_ex", "spla_step", "spla_step_ex", "spla_prefill"]
 HOST_EXPORTS = EXPORTS[:7]
 
 
@@ -100,6 +100,9 @@ def _declare(lib, host_only=False):
     lib.spla_step_ex.restype = c_int32
     lib.spla_step_ex.argtypes = [cfgp, cachep, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
                                  c_void_p, c_void_p, c_size_t, POINTER(SplaEvents), c_void_p]
+    lib.spla_prefill.restype = c_int32
+    lib.spla_prefill.argtypes = [cfgp, cachep, c_int32, c_void_p, c_void_p, c_void_p, c_void_p,
+                                 c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]
     return lib
 
 
@@ -294,6 +297,29 @@ class SplaCache:
                                   _ptr(v_new), _ptr(q), _ptr(gamma), _ptr(out), _ptr(sel),
                                   _ptr(self.workspace), self.workspace.numel(), ev,
                                   _stream(self.device)), "spla_step")
+        return out, sel
+
+    def prefill(self, k_new, v_new, q, gamma, out=None, sel=None):
+        """Causal prefill of T tokens per sequence: k_new, v_new [T, batch,
+        Hkv, d], q [T, batch, Hq, d] (cache dtype) -> out [T, batch, Hq, d],
+        sel [T, batch, Hkv, top_k]; position t is appended, then decoded."""
+        c = self.cfg
+        T = k_new.shape[0]
+        assert k_new.shape == (T, c.batch, c.n_kv_heads, c.head_dim) and k_new.is_contiguous()
+        assert v_new.shape == k_new.shape and v_new.is_contiguous()
+        assert k_new.dtype == torch_dtype(c) and v_new.dtype == torch_dtype(c)
+        assert q.shape == (T, c.batch, c.n_q_heads, c.head_dim) and q.dtype == torch_dtype(c)
+        assert q.is_contiguous()
+        assert gamma.shape == (c.n_q_heads, c.head_dim) and gamma.dtype == torch.float32
+        if out is None:
+            out = torch.empty_like(q)
+        if sel is None:
+            sel = torch.empty((T, c.batch, c.n_kv_heads, c.top_k), dtype=torch.int32,
+                              device=self.device)
+        _check(lib().spla_prefill(ctypes.byref(c), ctypes.byref(self._struct), int(T),
+                                  _ptr(k_new), _ptr(v_new), _ptr(q), _ptr(gamma), _ptr(out),
+                                  _ptr(sel), _ptr(self.workspace), self.workspace.numel(),
+                                  _stream(self.device)), "spla_prefill")
         return out, sel
 
     # ---- layout views (for checks; pure indexing) ----

@@ -118,6 +118,14 @@ def test_device_calls_reject_bad_arguments_before_launch():
     # misaligned workspace
     assert lib.spla_decode(ctypes.byref(c), ctypes.byref(fake), 256, 256, 512, None, 8,
                            1 << 40, None) == -4
+    # prefill: a negative token count, and missing token rows, are rejected;
+    # no tokens is a no-op
+    assert lib.spla_prefill(ctypes.byref(c), ctypes.byref(fake), -1, 256, 256, 256, 256, 512,
+                            None, 256, 1 << 40, None) == -1
+    assert lib.spla_prefill(ctypes.byref(c), ctypes.byref(fake), 3, None, 256, 256, 256, 512,
+                            None, 256, 1 << 40, None) == -1
+    assert lib.spla_prefill(ctypes.byref(c), ctypes.byref(fake), 0, None, None, 256, 256, 512,
+                            None, 256, 1 << 40, None) == 0
     # a paged pool needs its block table, and a contiguous cache has none
     paged = _cfg(kv_pages=64)
     assert lib.spla_decode(ctypes.byref(paged), ctypes.byref(fake), 256, 256, 512, None, 256,
