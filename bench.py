@@ -212,6 +212,52 @@ def strided_leg(w, R, dev, qs, gamma, outs, sels, K, W, C=32, s=16, paged=False)
                                                else "per-launch events")}}
 
 
+def prefill_leg(w, dev, K, T=16):
+    """Causal prefill (spla_prefill) of T tokens per sequence at the
+    workload's context: the cache is filled to capacity - T (K + 1) tokens,
+    then K timed calls each append and decode T positions. Returns a dict for
+    the JSON line (per-token latency over the whole batch)."""
+    import numpy as np
+    import torch
+
+    from paper_2601_22379_amd import spla
+    import spla_inputs as si
+
+    lens = [w.capacity - T * (K + 1)] * w.batch
+    cfg = spla.make_config(w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, w.block_size,
+                           w.top_k, w.capacity, w.dtype, n_sink=w.n_sink, n_local=w.n_local)
+    cache = spla.SplaCache(cfg, dev)
+    dt = torch.float32 if w.dtype == "f32" else torch.bfloat16
+    per_tok = w.batch * w.n_kv_heads * w.head_dim * 8
+    S = int(min(w.capacity, max(256, 1 << (int((1 << 29) // per_tok).bit_length() - 1))))
+    for a in range(0, lens[0], S):
+        Kt, Vt, n = si.gen_kv_slab(w, a, min(a + S, lens[0]), lengths=lens, threads=16)
+        cache.append(torch.from_numpy(Kt).to(dt).to(dev), torch.from_numpy(Vt).to(dt).to(dev),
+                     torch.from_numpy(n).to(dev))
+    rng = np.random.default_rng([w.code, 5])
+    kn = torch.from_numpy(rng.standard_normal((T, w.batch, w.n_kv_heads, w.head_dim))
+                          .astype(np.float32)).to(dt).to(dev)
+    vn = torch.from_numpy(rng.standard_normal(kn.shape).astype(np.float32)).to(dt).to(dev)
+    q = torch.from_numpy(np.stack([si.gen_q_batch(w, t) for t in range(T)])).to(dt).to(dev)
+    gamma = torch.from_numpy(si.gen_gamma(w)).to(dev)
+    out, sel = cache.prefill(kn, vn, q, gamma)  # warm-up call (T positions)
+    torch.cuda.synchronize()
+    a = torch.cuda.Event(enable_timing=True)
+    b = torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(K):
+        cache.prefill(kn, vn, q, gamma, out, sel)
+    b.record()
+    torch.cuda.synchronize()
+    us = a.elapsed_time(b) / K * 1e3
+    assert cache.err.item() == 0
+    log(f"prefill: {T} positions in {us:.1f} us ({us / T:.2f} us per position) at "
+        f"{lens[0]}..{lens[0] + T * (K + 1)} tokens")
+    return {"tokens_per_call": T, "calls": K, "context_start": lens[0],
+            "latency_us_per_call": round(us, 2), "latency_us_per_position": round(us / T, 3),
+            "method": "append + decode per position (spla_prefill)"}
+
+
 def cpu_baseline(w, seconds, n_units=2):
     """The fp64 oracle's decode on a bounded sample of the workload: n_units
     (sequence, KV head) units with their state prebuilt (untimed), decode
@@ -357,7 +403,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-graph", action="store_true")
     ap.add_argument("--no-strided", action="store_true",
-                    help="skip the strided-selection (C = 32, s = 16) and paged-KV legs")
+                    help="skip the strided-selection (C = 32, s = 16), paged-KV and prefill legs")
     ap.add_argument("--strided-only", action="store_true",
                     help="run only the strided-selection leg and print its JSON (profiling)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -599,11 +645,12 @@ def main():
                 "avg_launch_us": round(dom_us, 3), "avg_launch_method": dom_method,
                 "avg_launch_us_per_launch_events": round(dom_us_events, 3),
                 "profiled_avg_us": prof_us}
-    strided = paged = None
+    strided = paged = prefill = None
     if not appending and not args.no_strided:
         strided = strided_leg(w, R, dev, qs, gamma, outs, sels, K, W)
         paged = strided_leg(w, R, dev, qs, gamma, outs, sels, K, W, C=w.block_size,
                             s=w.block_size, paged=True)
+        prefill = prefill_leg(w, dev, K=20)
     cpu = None
     if not args.no_cpu_baseline:
         log("timing the CPU oracle")
@@ -637,6 +684,7 @@ def main():
         "cpu_baseline": cpu,
         "strided_selection": strided,
         "paged_kv": paged,
+        "prefill": prefill,
     }
     print(json.dumps(line), flush=True)
 
