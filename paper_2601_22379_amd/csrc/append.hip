@@ -25,22 +25,23 @@ __device__ __forceinline__ int appended_count(const Dims& m, int L0, int max_new
 // u us <= t < (u + 1) us into the caches, so that each row is copied by
 // exactly one unit. The new tokens' mean and M2 are computed two-pass in fp64
 // and combined with the stored ones by Chan's formula, then rounded to fp32.
+// (unit ux of the units touched, of (sequence, kv head) bh; thread j handles
+// coordinate j)
 template <typename T>
-__global__ __launch_bounds__(128) void append_blocks_kernel(
-    Dims m, T* __restrict__ kc, T* __restrict__ vc, float* __restrict__ stats,
+__device__ __forceinline__ void append_unit(
+    const Dims& m, T* __restrict__ kc, T* __restrict__ vc, float* __restrict__ stats,
     const int32_t* __restrict__ seq_lens, int32_t* __restrict__ err, const T* __restrict__ k_new,
     const T* __restrict__ v_new, int max_new, const int32_t* __restrict__ n_new,
-    const int32_t* __restrict__ table) {
-  const int bh = blockIdx.y;
+    const int32_t* __restrict__ table, int ux, int bh) {
   const int b = bh / m.hkv;
   const int L0 = seq_lens[b];
   bool clipped;
   const int ne = appended_count(m, L0, max_new, n_new, b, &clipped);
-  if (clipped && err && blockIdx.x == 0 && bh % m.hkv == 0 && threadIdx.x == 0)
+  if (clipped && err && ux == 0 && bh % m.hkv == 0 && threadIdx.x == 0)
     atomicOr(err, (int)SPLA_DEVERR_CAPACITY);
   // first unit holding token L0: u us + ul > L0
   const int first = L0 >= m.ul ? (L0 - m.ul) / m.us + 1 : 0;
-  const int i = first + (int)blockIdx.x;
+  const int i = first + ux;
   const int t_lo = max(L0, i * m.us);
   const int t_hi = min(L0 + ne, i * m.us + m.ul);
   const int t_own = min(t_hi, (i + 1) * m.us);  // rows this unit copies: t_lo .. t_own - 1
@@ -91,6 +92,16 @@ __global__ __launch_bounds__(128) void append_blocks_kernel(
   }
   stats[o_mean] = (float)mean;
   stats[o_m2] = (float)m2;
+}
+
+template <typename T>
+__global__ __launch_bounds__(128) void append_blocks_kernel(
+    Dims m, T* __restrict__ kc, T* __restrict__ vc, float* __restrict__ stats,
+    const int32_t* __restrict__ seq_lens, int32_t* __restrict__ err, const T* __restrict__ k_new,
+    const T* __restrict__ v_new, int max_new, const int32_t* __restrict__ n_new,
+    const int32_t* __restrict__ table) {
+  append_unit<T>(m, kc, vc, stats, seq_lens, err, k_new, v_new, max_new, n_new, table,
+                 (int)blockIdx.x, (int)blockIdx.y);
 }
 
 // Partial linear-attention state of one chunk of new tokens:
@@ -202,13 +213,18 @@ __global__ __launch_bounds__(256) void append_state_reduce_kernel(
 }
 
 // Single-token state update: S_bar += phi(k)^T v, z_bar += phi(k) (fp32).
+// Rows rx * 16 .. rx * 16 + 15 of S_bar += phi(k)^T v (and those entries of
+// z_bar += phi(k)) for the single token k, v of (sequence, kv head) bh, by the
+// 256 threads of a workgroup. A sequence at capacity gets nothing.
 template <typename T, int D>
-__global__ __launch_bounds__(256) void append_state_rank1_kernel(
-    Dims m, const int32_t* __restrict__ seq_lens, const T* __restrict__ k_new,
-    const T* __restrict__ v_new, float* __restrict__ S, float* __restrict__ z) {
+__device__ __forceinline__ void append_rank1_rows(const Dims& m,
+                                                  const int32_t* __restrict__ seq_lens,
+                                                  const T* __restrict__ k_new,
+                                                  const T* __restrict__ v_new,
+                                                  float* __restrict__ S, float* __restrict__ z,
+                                                  int rx, int bh) {
   __shared__ float sphi[D];
   __shared__ float sv[D];
-  const int bh = blockIdx.y;
   const int b = bh / m.hkv;
   if (seq_lens[b] >= m.cap) return;
   const int tid = threadIdx.x;
@@ -233,13 +249,32 @@ __global__ __launch_bounds__(256) void append_state_rank1_kernel(
   }
   for (int c = tid; c < D; c += 256) sv[c] = Elem<T>::load(v_new, (int64_t)bh * D + c);
   __syncthreads();
-  const int row0 = blockIdx.x * 16;
+  const int row0 = rx * 16;
   for (int e = tid; e < 16 * D; e += 256) {
     const int row = row0 + e / D, col = e % D;
     const int64_t o = ((int64_t)bh * D + row) * D + col;
     S[o] = fmaf(sphi[row], sv[col], S[o]);
   }
   if (tid < 16) z[(int64_t)bh * D + row0 + tid] += sphi[row0 + tid];
+}
+
+// The single-token append of a decode step in one launch: workgroups
+// x < D / 16 update 16 rows of S_bar each (rank one), the others the
+// statistics units the token falls in (and copy its K/V rows). The two parts
+// touch disjoint memory and only read seq_lens, which append_finish_kernel
+// advances afterwards.
+template <typename T, int D>
+__global__ __launch_bounds__(256) void append_one_kernel(
+    Dims m, T* __restrict__ kc, T* __restrict__ vc, float* __restrict__ stats,
+    const int32_t* __restrict__ seq_lens, int32_t* __restrict__ err, const T* __restrict__ k_new,
+    const T* __restrict__ v_new, const int32_t* __restrict__ table, float* __restrict__ S,
+    float* __restrict__ z) {
+  const int bh = (int)blockIdx.y;
+  if ((int)blockIdx.x < D / 16)
+    append_rank1_rows<T, D>(m, seq_lens, k_new, v_new, S, z, (int)blockIdx.x, bh);
+  else
+    append_unit<T>(m, kc, vc, stats, seq_lens, err, k_new, v_new, 1, nullptr, table,
+                   (int)blockIdx.x - D / 16, bh);
 }
 
 __global__ void append_finish_kernel(Dims m, int32_t* __restrict__ seq_lens, int max_new,
@@ -305,27 +340,26 @@ hipError_t launch_append_state(const Dims& m, const spla_cache& c, const void* k
   return hipGetLastError();
 }
 
-hipError_t launch_append_state_rank1(const Dims& m, const spla_cache& c, const void* k_new,
-                                     const void* v_new, hipStream_t st) {
-  dim3 grid(m.d / 16, m.bh);
+// Units a single token touches: one block, or up to ul / us windows.
+static int64_t units_of_one(const Dims& m) { return windowed(m) ? m.ul / m.us : 1; }
+
+template <typename T, int D>
+static void append_one_td(const Dims& m, const spla_cache& c, const void* k_new,
+                          const void* v_new, hipStream_t st) {
+  hipLaunchKernelGGL((append_one_kernel<T, D>), dim3((unsigned)(D / 16 + units_of_one(m)),
+                     (unsigned)m.bh), dim3(256), 0, st, m, (T*)c.k_cache, (T*)c.v_cache,
+                     c.blk_stats, c.seq_lens, c.err_flags, (const T*)k_new, (const T*)v_new,
+                     m.pages > 0 ? c.block_table : nullptr, c.lin_state, c.lin_norm);
+}
+
+hipError_t launch_append_one(const Dims& m, const spla_cache& c, const void* k_new,
+                             const void* v_new, hipStream_t st) {
   if (m.elem == 4) {
-    if (m.d == 64)
-      hipLaunchKernelGGL((append_state_rank1_kernel<float, 64>), grid, dim3(256), 0, st, m,
-                         c.seq_lens, (const float*)k_new, (const float*)v_new, c.lin_state,
-                         c.lin_norm);
-    else
-      hipLaunchKernelGGL((append_state_rank1_kernel<float, 128>), grid, dim3(256), 0, st, m,
-                         c.seq_lens, (const float*)k_new, (const float*)v_new, c.lin_state,
-                         c.lin_norm);
+    if (m.d == 64) append_one_td<float, 64>(m, c, k_new, v_new, st);
+    else append_one_td<float, 128>(m, c, k_new, v_new, st);
   } else {
-    if (m.d == 64)
-      hipLaunchKernelGGL((append_state_rank1_kernel<bf16_t, 64>), grid, dim3(256), 0, st, m,
-                         c.seq_lens, (const bf16_t*)k_new, (const bf16_t*)v_new, c.lin_state,
-                         c.lin_norm);
-    else
-      hipLaunchKernelGGL((append_state_rank1_kernel<bf16_t, 128>), grid, dim3(256), 0, st, m,
-                         c.seq_lens, (const bf16_t*)k_new, (const bf16_t*)v_new, c.lin_state,
-                         c.lin_norm);
+    if (m.d == 64) append_one_td<bf16_t, 64>(m, c, k_new, v_new, st);
+    else append_one_td<bf16_t, 128>(m, c, k_new, v_new, st);
   }
   return hipGetLastError();
 }

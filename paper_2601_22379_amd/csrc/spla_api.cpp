@@ -178,8 +178,7 @@ extern "C" int32_t spla_step_ex(const spla_config* cfg, const spla_cache* cache,
   hipStream_t st = static_cast<hipStream_t>(stream);
   {
     PhaseMark pm(ev, st, SPLA_PHASE_APPEND);
-    SPLA_TRY(spla::launch_append_blocks(m, *cache, k_new, v_new, 1, nullptr, st));
-    SPLA_TRY(spla::launch_append_state_rank1(m, *cache, k_new, v_new, st));
+    SPLA_TRY(spla::launch_append_one(m, *cache, k_new, v_new, st));
     SPLA_TRY(spla::launch_append_finish(m, *cache, 1, nullptr, st));
   }
   return run_decode(cfg, cache, q, w, out, sel_idx, ws, ws_bytes, ev, st);
@@ -210,8 +209,7 @@ extern "C" int32_t spla_prefill(const spla_config* cfg, const spla_cache* cache,
   for (int32_t t = 0; t < n_tokens; ++t) {
     const char* kt = static_cast<const char*>(k_new) + t * kv_step;
     const char* vt = static_cast<const char*>(v_new) + t * kv_step;
-    SPLA_TRY(spla::launch_append_blocks(m, *cache, kt, vt, 1, nullptr, st));
-    SPLA_TRY(spla::launch_append_state_rank1(m, *cache, kt, vt, st));
+    SPLA_TRY(spla::launch_append_one(m, *cache, kt, vt, st));
     SPLA_TRY(spla::launch_append_finish(m, *cache, 1, nullptr, st));
     if ((s = run_decode(cfg, cache, static_cast<const char*>(q) + t * q_step, w,
                         static_cast<char*>(out) + t * q_step,

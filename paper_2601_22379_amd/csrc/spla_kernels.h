@@ -18,8 +18,10 @@ hipError_t launch_append_blocks(const Dims& m, const spla_cache& c, const void* 
 hipError_t launch_append_state(const Dims& m, const spla_cache& c, const void* k_new,
                                const void* v_new, int max_new, const int32_t* n_new,
                                const AppendWs& ws, char* wsbase, hipStream_t st);
-hipError_t launch_append_state_rank1(const Dims& m, const spla_cache& c, const void* k_new,
-                                     const void* v_new, hipStream_t st);
+// the single-token append of a step (statistics, K/V rows, S_bar, z_bar) in
+// one launch; seq_lens is advanced by launch_append_finish
+hipError_t launch_append_one(const Dims& m, const spla_cache& c, const void* k_new,
+                             const void* v_new, hipStream_t st);
 hipError_t launch_append_finish(const Dims& m, const spla_cache& c, int max_new,
                                 const int32_t* n_new, hipStream_t st);
 hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t st);
