@@ -14,8 +14,13 @@ timed region starts.
 
 Prints one JSON line: whole-step throughput as algorithmic HBM bytes per
 second (value, GB/s), latency (ms_per_step), the roofline of the dominant
-kernel (the statistics scan, timed with HIP events on the library's stream
-over the timed region) and the fp64 CPU oracle timed on a bounded sample.
+kernel (the single-launch decode kernel at this shape: the timed region over
+the launches, with its counter traffic when the committed counter summary
+matches the kernel sources) and the fp64 CPU oracle timed on a bounded
+sample. Three more objects measure the same workload with the library's
+options: strided selection windows (C = 32, s = 16; roofline of its scoring
+kernel), a paged K/V pool behind a shuffled block table, and a causal
+prefill of 16 positions per sequence. --no-strided skips them.
 """
 
 from __future__ import annotations
