@@ -271,9 +271,10 @@ int32_t spla_append(const spla_config* cfg, const spla_cache* cache,
  *              sequence has fewer than top_k blocks.
  *  workspace:  device, at least spla_workspace_bytes(cfg), 256-byte aligned,
  *              prepared once by spla_workspace_init.
- * Bf16 shapes with d = 128, G <= 8 and at most 8192 blocks per sequence run
- * as one kernel launch (unless SPLA_FLAG_SEPARATE_KERNELS); the others as
- * separate score, select, sparse and merge launches.
+ * Bf16 shapes with d = 128, G <= 6, at most 8192 blocks per sequence and no
+ * strided selection run as one kernel launch (unless
+ * SPLA_FLAG_SEPARATE_KERNELS); the others as separate score, select, sparse
+ * and merge launches (spla_decode_phase_mask tells which).
  * For each sequence with L = seq_lens[b] tokens, nb = ceil(L / B) blocks:
  * if nb <= top_k every block is selected and the output is exact attention;
  * otherwise the sink and local blocks plus the top-scored remaining blocks
