@@ -225,9 +225,19 @@ __device__ __forceinline__ void append_rank1_rows(const Dims& m,
                                                   int rx, int bh) {
   __shared__ float sphi[D];
   __shared__ float sv[D];
+  constexpr int PT = 16 * D / 256;  // entries of the 16 rows per thread
   const int b = bh / m.hkv;
   if (seq_lens[b] >= m.cap) return;
   const int tid = threadIdx.x;
+  const int row0 = rx * 16;
+  // this thread's entries of the rows, loaded before phi(k) is formed so that
+  // their latency overlaps it
+  float sr[PT];
+#pragma unroll
+  for (int u = 0; u < PT; ++u) {
+    const int e = tid + 256 * u;
+    sr[u] = S[((int64_t)bh * D + row0 + e / D) * D + e % D];
+  }
   if (tid < 64) {
     float x[D / 64];
     float mx = -INFINITY;
@@ -249,11 +259,11 @@ __device__ __forceinline__ void append_rank1_rows(const Dims& m,
   }
   for (int c = tid; c < D; c += 256) sv[c] = Elem<T>::load(v_new, (int64_t)bh * D + c);
   __syncthreads();
-  const int row0 = rx * 16;
-  for (int e = tid; e < 16 * D; e += 256) {
+#pragma unroll
+  for (int u = 0; u < PT; ++u) {
+    const int e = tid + 256 * u;
     const int row = row0 + e / D, col = e % D;
-    const int64_t o = ((int64_t)bh * D + row) * D + col;
-    S[o] = fmaf(sphi[row], sv[col], S[o]);
+    S[((int64_t)bh * D + row) * D + col] = fmaf(sphi[row], sv[col], sr[u]);
   }
   if (tid < 16) z[(int64_t)bh * D + row0 + tid] += sphi[row0 + tid];
 }
