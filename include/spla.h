@@ -49,7 +49,7 @@ extern "C" {
 typedef enum spla_status {
   SPLA_OK = 0,
   SPLA_ERR_INVALID_ARG = -1, /* NULL pointer, inconsistent or out-of-range value */
-  SPLA_ERR_UNSUPPORTED = -2, /* valid, but a shape this build does not implement */
+  SPLA_ERR_UNSUPPORTED = -2, /* valid, but a shape the library does not implement */
   SPLA_ERR_CAPACITY = -3,    /* a size exceeds the cache capacity or a library limit */
   SPLA_ERR_WORKSPACE = -4,   /* workspace NULL, too small or misaligned */
   SPLA_ERR_HIP = -5          /* the HIP runtime reported an error at launch */
@@ -78,7 +78,7 @@ enum {
                                its rows were not written */
 };
 
-/* Library limits of this build. */
+/* Library limits. */
 enum {
   SPLA_MAX_GROUP = 16,      /* query heads per KV head */
   SPLA_MAX_TOP_K = 256,     /* selected blocks per KV head */
