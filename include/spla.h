@@ -71,9 +71,13 @@ enum {
 /* err_flags bits written by the device */
 enum {
   SPLA_DEVERR_CAPACITY = 1, /* an append was clipped at max_seq_len */
-  SPLA_DEVERR_SYNC = 2,     /* the single-launch decode found its workspace counters not
-                               zero at launch, or gave up a bounded wait: the output of
-                               that call is undefined; spla_workspace_init repairs it */
+  SPLA_DEVERR_SYNC = 2,     /* a bounded wait of the single-launch decode gave up (for
+                               instance because the workspace was never zeroed with
+                               spla_workspace_init and a counter started non-zero): the
+                               outputs and selection of that call are undefined, and
+                               spla_workspace_init repairs the workspace. Only a wait
+                               that gives up is detected; counters left non-zero by
+                               other means are not checked at launch */
   SPLA_DEVERR_PAGE = 4      /* an append met a block_table entry outside [0, kv_pages):
                                its rows were not written */
 };
@@ -103,7 +107,11 @@ typedef struct spla_config {
   int32_t dtype;          /* spla_dtype of q, out and the K/V cache */
   float softmax_scale;    /* s; <= 0 selects 1/sqrt(head_dim). Scales the exact
                              logits and the query inside the block score */
-  float rms_eps;          /* epsilon of the RMSNorm on the residual, >= 0 (1e-6) */
+  float rms_eps;          /* epsilon of the RMSNorm on the residual, >= 0 (1e-6). When
+                             every token is selected there is no residual and the
+                             output is the exact branch at any eps; with eps = 0, a
+                             head whose residual is exactly zero while some token is
+                             unselected has an undefined (0 / 0) output */
   uint32_t flags;         /* SPLA_FLAG_* */
   int32_t sel_window;     /* strided block selection (Sec. 3.1): the block score is
                              the largest group score of the windows of sel_window

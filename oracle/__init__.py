@@ -26,6 +26,7 @@ from .spla_oracle import (  # noqa: F401
     select_blocks,
     selected_token_indices,
     exact_sparse_attention,
+    nothing_unselected,
     residual_linear_attention,
     combine,
     build_state,

@@ -32,8 +32,9 @@ step it affects):
 * the exact branch normalises over the selected tokens only (Eq. 5).
 * the residual linear branch is unnormalised as written in Eqs. (15)-(16);
   when no token is left unselected the residual is exactly zero (decided by
-  a count, not by a float test); an optional normaliser <phi(q), z_bar - z_sel>
-  exists behind a flag.
+  a count, not by a float test) and the output is the exact branch alone, so
+  eps = 0 is allowed; an optional normaliser <phi(q), z_bar - z_sel> exists
+  behind a flag.
 * the combine adds an RMSNorm (per query head, over d, no mean subtraction,
   weight gamma, eps 1e-6) of the residual to the exact output, with no gate
   beyond gamma (Sec. 3.3).
@@ -339,6 +340,13 @@ def exact_sparse_attention(q: np.ndarray, K: np.ndarray, V: np.ndarray, tok: np.
 
 
 # ------------------------------------------------------------- O9 RLA
+def nothing_unselected(n_selected_tokens: int, L: int) -> bool:
+    """Whether the selection holds every cached token, so the residual
+    branch of Eq. (14) has no token to cover. Decided by a count, never by
+    testing a float for zero."""
+    return int(n_selected_tokens) == int(L)
+
+
 def residual_linear_attention(q: np.ndarray, s_bar: np.ndarray, z_bar: np.ndarray,
                               K: np.ndarray, V: np.ndarray, tok: np.ndarray, L: int,
                               normalize: bool = False):
@@ -359,7 +367,7 @@ def residual_linear_attention(q: np.ndarray, s_bar: np.ndarray, z_bar: np.ndarra
     else:
         o_tilde = np.zeros_like(o_bar)
         z_tilde = np.zeros_like(z_bar)
-    if len(tok) == L:
+    if nothing_unselected(len(tok), L):
         return np.zeros_like(o_bar), o_bar, o_tilde
     r = o_bar - o_tilde
     if normalize:
@@ -485,7 +493,12 @@ def decode_kv_head(q: np.ndarray, state: KVState, K: np.ndarray, V: np.ndarray,
                             n_forced, extras)
     r, o_bar, o_tilde = residual_linear_attention(q, state.s_bar, state.z_bar, K, V, tok, L,
                                                   p.rla_normalize)
-    out = combine(o_sparse, r, gamma, p.rms_eps)
+    if nothing_unselected(len(tok), L):
+        # no unselected token: the residual branch is absent, so its RMSNorm
+        # term is zero (also at eps = 0, where gamma 0 / sqrt(0) is undefined)
+        out = o_sparse.copy()
+    else:
+        out = combine(o_sparse, r, gamma, p.rms_eps)
     return DecodeResult(out, sel, score, ell, o_sparse, r, o_bar, o_tilde, n_forced, extras)
 
 

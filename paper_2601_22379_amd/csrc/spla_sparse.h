@@ -168,21 +168,23 @@ __device__ __forceinline__ void merge_head(const Dims& m, float eps, uint32_t fl
 #pragma unroll
     for (int e = 0; e < E; ++e) o[e] = 0.f;
   } else {
-    // residual r = o_bar - o_tilde (over its normaliser with RLA_NORMALIZE),
-    // exactly 0 when every token was selected; out = o_sparse + gamma r / rms(r)
+    // residual r = o_bar - o_tilde (over its normaliser with RLA_NORMALIZE);
+    // out = o_sparse + gamma r / rms(r). When every token was selected there
+    // is no residual branch and out = o_sparse (also at eps = 0)
+    const bool res = rla && !all_sel;
     const float den = (flags & SPLA_FLAG_RLA_NORMALIZE) ? zt : 1.f;
     float rr[E];
     float ss = 0.f;
 #pragma unroll
     for (int e = 0; e < E; ++e) {
       osp[e] /= l;
-      rr[e] = (rla && !all_sel) ? ot[e] / den : 0.f;
+      rr[e] = res ? ot[e] / den : 0.f;
       ss += rr[e] * rr[e];
     }
     ss = wave_sum(hf ? 0.f : ss);  // each coordinate once
     const float inv = 1.0f / sqrtf(ss / D + eps);
 #pragma unroll
-    for (int e = 0; e < E; ++e) o[e] = rla ? fmaf(gm[e] * rr[e], inv, osp[e]) : osp[e];
+    for (int e = 0; e < E; ++e) o[e] = res ? fmaf(gm[e] * rr[e], inv, osp[e]) : osp[e];
   }
   if (hf == 0) {
     if constexpr (E == 4) {

@@ -127,13 +127,50 @@ def test_rmsnorm_sum_instead_of_mean(monkeypatch):
 
 
 def test_residual_not_zeroed_when_all_selected(monkeypatch):
-    orig = OS.residual_linear_attention
+    # the count test never fires: the residual is the cancellation noise of
+    # o_bar - o_tilde, and RMSNorm blows it up to unit scale
+    _patch(monkeypatch, "nothing_unselected", lambda n, L: False)
+    _expect_failure((P.test_x2_selecting_every_block_is_dense_attention, (100,)),
+                    (P.test_x23_every_block_selected_with_zero_eps_is_dense_attention, (37,)))
 
+
+def test_cutoff_is_the_highest_admitted_score(monkeypatch):
+    def bad(score, sel, k, n_sink, n_local):
+        nb = len(score)
+        if nb <= k:
+            return None
+        fset = set(OS.forced_blocks(nb, k, n_sink, n_local))
+        ranked = [float(score[i]) for i in sel if int(i) not in fset]
+        return max(ranked) if ranked else None
+    _patch(monkeypatch, "cutoff_score", bad)
+    _expect_failure(*[(P.test_x21_cutoff_score_hand_worked, (n,)) for n in P.CUTOFF_CASES])
+
+
+def test_cutoff_counts_forced_blocks(monkeypatch):
+    def bad(score, sel, k, n_sink, n_local):
+        if len(score) <= k:
+            return None
+        return min(float(score[i]) for i in sel)
+    _patch(monkeypatch, "cutoff_score", bad)
+    _expect_failure(*[(P.test_x21_cutoff_score_hand_worked, (n,)) for n in P.CUTOFF_CASES])
+
+
+def test_normaliser_over_every_token(monkeypatch):
+    # <phi(q), z_bar> in place of <phi(q), z_bar - z_tilde>
     def bad(q, s_bar, z_bar, K, V, tok, L, normalize=False):
-        r, ob, ot = orig(q, s_bar, z_bar, K, V, tok, L + 1, normalize)
-        return r, ob, ot
+        phiq = OS.feature_map(q)
+        o_bar = phiq @ s_bar
+        phik = OS.feature_map(np.asarray(K, float)[tok])
+        o_tilde = (phiq @ phik.T) @ np.asarray(V, float)[tok]
+        if OS.nothing_unselected(len(tok), L):
+            return np.zeros_like(o_bar), o_bar, o_tilde
+        r = o_bar - o_tilde
+        if normalize:
+            r = r / (phiq @ z_bar)[:, None]
+        return r, o_bar, o_tilde
     _patch(monkeypatch, "residual_linear_attention", bad)
-    _expect_failure((P.test_x2_selecting_every_block_is_dense_attention, (100,)))
+    _expect_failure(*[(P.test_x22_rla_normaliser_is_the_unselected_linear_mass, (s,))
+                      for s in range(3)])
 
 
 def test_strided_instead_of_contiguous_groups(monkeypatch):

@@ -430,3 +430,92 @@ def test_block_ranges_cover_ragged_lengths():
         assert len(rg) == -(-L // B)
         assert sum(b - a for a, b in rg) == L
         assert rg[-1][1] == L
+
+
+# -------------------------------------------------------------------- X21
+# Hand-worked top-k cutoffs. Each case: scores, k, n_sink, n_local, the
+# selection worked out by hand, the cutoff (score of the lowest-scored
+# non-forced admitted block, None when every block is taken or nothing is
+# admitted by rank) and the blocks whose score equals the cutoff.
+CUTOFF_CASES = {
+    # forced {0, 8, 9} hold the three lowest scores; kp = 2 admits 2 and 4
+    "forced_lowest": ([0.01, 0.5, 0.9, 0.3, 0.7, 0.2, 0.6, 0.4, 0.02, 0.03], 5, 1, 2,
+                      [0, 2, 4, 8, 9], 0.7, [4]),
+    # forced {0, 7}; kp = 2: block 2 (0.8), then the first of the three-way
+    # tie at 0.5 (blocks 1, 3, 4) by the lower id
+    "tie_at_cutoff": ([0.1, 0.5, 0.8, 0.5, 0.5, 0.2, 0.3, 0.05], 4, 1, 1,
+                      [0, 1, 2, 7], 0.5, [1, 3, 4]),
+    # no forced blocks: the plain top 3 of 6
+    "no_forced": ([0.3, 0.1, 0.6, 0.6, 0.2, 0.5], 3, 0, 0, [2, 3, 5], 0.5, [5]),
+    # nb <= k: every block, no cutoff
+    "all_selected": ([0.4, 0.1, 0.3, 0.2], 4, 1, 2, [0, 1, 2, 3], None, []),
+    # k equals the forced count: nothing admitted by rank, no cutoff
+    "forced_only": ([0.9, 0.8, 0.7, 0.1, 0.2, 0.3], 3, 1, 2, [0, 4, 5], None, []),
+}
+
+
+@pytest.mark.parametrize("name", list(CUTOFF_CASES))
+def test_x21_cutoff_score_hand_worked(name):
+    """The tie window of index parity is measured from the cutoff: the score
+    of the last block admitted by rank (forced blocks excluded)."""
+    score, k, n_sink, n_local, sel_want, cut_want, at_cut = CUTOFF_CASES[name]
+    score = np.array(score, dtype=float)
+    sel = O.select_blocks(score, k, n_sink, n_local)
+    assert [int(i) for i in sel] == sel_want
+    c = O.cutoff_score(score, sel, k, n_sink, n_local)
+    if cut_want is None:
+        assert c is None
+    else:
+        assert c == cut_want
+        assert [i for i in range(len(score)) if abs(score[i] - c) <= 1e-6 * c] == at_cut
+
+
+# -------------------------------------------------------------------- X22
+@pytest.mark.parametrize("seed", range(3))
+def test_x22_rla_normaliser_is_the_unselected_linear_mass(seed):
+    """With the normaliser switched on, the residual is divided by
+    <phi(q), z_bar - z_tilde>, which is the linear-attention weight of the
+    unselected tokens, sum over t not in T_I of <phi(q), phi(k_t)>, summed
+    here by brute force with an independent softmax."""
+    r = _rng(22, seed)
+    G, d, B, L, k = 3, 16, 8, 83, 4
+    q = 0.7 * r.standard_normal((G, d))
+    K = r.standard_normal((L, d))
+    V = r.standard_normal((L, d))
+    g = np.ones((G, d))
+    st = O.build_state(K, V, L, B)
+    pa = O.SplaParams(block_size=B, top_k=k, n_local=1)
+    pb = O.SplaParams(block_size=B, top_k=k, n_local=1, rla_normalize=True)
+    a = O.decode_kv_head(q, st, K, V, g, pa)
+    b = O.decode_kv_head(q, st, K, V, g, pb, force_selection=a.sel)
+    sel_tok = set()
+    for i in a.sel:
+        sel_tok |= set(range(int(i) * B, min((int(i) + 1) * B, L)))
+    unsel = [t for t in range(L) if t not in sel_tok]
+    assert len(unsel) > 0
+    phq = t_softmax(q)
+    phk = t_softmax(K[unsel])
+    den = np.array([sum(float(np.dot(phq[m], phk[j])) for j in range(len(unsel)))
+                    for m in range(G)])
+    ratio = a.r / b.r                     # the denominator, once per coordinate
+    for m in range(G):
+        np.testing.assert_allclose(ratio[m], den[m], rtol=1e-10, atol=0)
+
+
+# -------------------------------------------------------------------- X23
+@pytest.mark.parametrize("L", [37, 64])
+def test_x23_every_block_selected_with_zero_eps_is_dense_attention(L):
+    """k >= nb with eps = 0: no token is unselected, the residual branch is
+    absent, and the output is dense attention (Eq. 1), not 0 / 0."""
+    r = _rng(23, L)
+    Hq, Hkv, d, B = 4, 2, 16, 8
+    q = r.standard_normal((Hq, d))
+    K = r.standard_normal((Hkv, L, d))
+    V = r.standard_normal((Hkv, L, d))
+    gamma = 1 + 0.1 * r.standard_normal((Hq, d))
+    p = O.SplaParams(block_size=B, top_k=8, rms_eps=0.0)
+    res = O.decode_sequence(q, K, V, L, gamma, p)
+    out = np.concatenate([x.out for x in res])
+    assert np.all(np.isfinite(out))
+    ref = sdpa(q, K, V, 1 / math.sqrt(d))
+    np.testing.assert_allclose(out, ref, rtol=0, atol=1e-12)
