@@ -239,6 +239,23 @@ class SplaCache:
     def struct(self) -> SplaCacheStruct:
         return self._struct
 
+    def device_errors(self) -> int:
+        """The SPLA_DEVERR_* bits the device has set in this cache's error
+        word (waits for the work queued on the current stream)."""
+        return int(self.err.item())
+
+    def clear_device_errors(self):
+        self.err.zero_()
+
+    def check_device_errors(self, allowed: int = 0):
+        """Raises SplaError when a bit outside `allowed` is set: after a
+        SPLA_DEVERR_SYNC the outputs of the call that set it are undefined."""
+        e = self.device_errors()
+        if e & ~allowed:
+            names = [n for n, v in (("CAPACITY", DEVERR_CAPACITY), ("SYNC", DEVERR_SYNC),
+                                    ("PAGE", DEVERR_PAGE)) if e & v]
+            raise SplaError(-5, "device error word: " + "|".join(names))
+
     def reset(self):
         _check(lib().spla_reset(ctypes.byref(self.cfg), ctypes.byref(self._struct),
                                 _stream(self.device)), "spla_reset")
