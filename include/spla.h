@@ -337,6 +337,30 @@ int32_t spla_step_ex(const spla_config* cfg, const spla_cache* cache, const void
                      int32_t* sel_idx, void* workspace, size_t workspace_bytes,
                      const spla_events* events, void* stream);
 
+/* --------------------------------------------- decode without a workspace */
+
+/* Bytes of the library-owned device scratch of spla_decode_noalloc. */
+enum { SPLA_NOALLOC_SCRATCH_BYTES = 64 << 20 };
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc):
+ * spla_decode with the library's own device scratch in place of a caller
+ * workspace. Arguments, outputs and errors as spla_decode, without the
+ * workspace; SPLA_ERR_WORKSPACE when spla_workspace_bytes(cfg) exceeds
+ * SPLA_NOALLOC_SCRATCH_BYTES (the largest workload of 64 sequences x 8 KV
+ * heads x 64K tokens at k = 16 needs about 40 MB).
+ * The scratch is a static device array of SPLA_NOALLOC_SCRATCH_BYTES: every
+ * GPU the library runs on holds one copy until the process ends. The first
+ * call on a device takes its address (hipGetSymbolAddress, with that device
+ * current) and zero-fills it on `stream`; later calls allocate nothing and
+ * call no allocating routine. Every call clears the single-launch decode's
+ * counters in the scratch with a fill kernel before the decode (the previous
+ * call may have used another shape). All calls on one device share the
+ * scratch and it keeps the last call's contents: calls that overlap on one
+ * GPU (other streams or threads) race, and their outputs are undefined. */
+int32_t spla_decode_noalloc(const spla_config* cfg, const spla_cache* cache, const void* q,
+                            const float* rms_weight, void* out, int32_t* sel_idx, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -2,6 +2,8 @@
 // launches of each call on the caller's stream.
 #include <hip/hip_runtime.h>
 
+#include <mutex>
+
 #include "spla_kernels.h"
 
 using spla::Dims;
@@ -218,4 +220,62 @@ extern "C" int32_t spla_prefill(const spla_config* cfg, const spla_cache* cache,
       return s;
   }
   return SPLA_OK;
+}
+
+// ---- decode without a caller workspace (callers that cannot allocate) ------
+// The decode workspace of spla_decode_noalloc: one copy of this array per
+// device, held by every GPU the library runs on until the process ends. In
+// host code `scratch` only names the array; its device address is taken once
+// per device with hipGetSymbolAddress and only that address is handed to
+// kernels.
+static __device__ __align__(256) unsigned char scratch[SPLA_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch[kMaxDevices] = {};
+
+// Device address of the current device's scratch; the first call on a device
+// takes it (with that device current) and zero-fills the array on `st`.
+int32_t device_scratch(hipStream_t st, void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return SPLA_ERR_HIP;
+  if (dev < 0 || dev >= kMaxDevices) return SPLA_ERR_UNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return SPLA_ERR_HIP;
+    if (spla::launch_fill_zero(p, SPLA_NOALLOC_SCRATCH_BYTES, st) != hipSuccess)
+      return SPLA_ERR_HIP;
+    g_scratch[dev] = p;
+  }
+  *out = g_scratch[dev];
+  return SPLA_OK;
+}
+
+}  // namespace
+
+extern "C" int32_t spla_decode_noalloc(const spla_config* cfg, const spla_cache* cache,
+                                       const void* q, const float* w, void* out,
+                                       int32_t* sel_idx, void* stream) {
+  int32_t s = spla_validate(cfg);
+  if (s != SPLA_OK) return s;
+  if ((s = check_cache(cfg, cache)) != SPLA_OK) return s;
+  if (!q || !w || !out || out == q) return SPLA_ERR_INVALID_ARG;
+  size_t need = 0;
+  spla_workspace_bytes(cfg, &need);
+  if (need > (size_t)SPLA_NOALLOC_SCRATCH_BYTES) return SPLA_ERR_WORKSPACE;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  void* base = nullptr;
+  if ((s = device_scratch(st, &base)) != SPLA_OK) return s;
+  const Dims m = spla::make_dims(*cfg);
+  const spla::DecodeWs L = spla::decode_ws_layout(m);
+  // the single-launch decode needs its counters at zero; the previous call
+  // may have left other data there (another layout), so they are cleared
+  // with a fill kernel on every call
+  if (spla::use_fused_decode(m) && !(cfg->flags & SPLA_FLAG_SEPARATE_KERNELS))
+    SPLA_TRY(spla::launch_fill_zero(static_cast<char*>(base) + L.sync, (size_t)(L.total - L.sync),
+                                    st));
+  return run_decode(cfg, cache, q, w, out, sel_idx, base, need, nullptr, st);
 }

@@ -33,7 +33,8 @@ STATUS = {0: "ok", -1: "invalid argument", -2: "unsupported shape",
 EXPORTS = ["spla_status_string", "spla_phase_name", "spla_validate", "spla_cache_bytes",
            "spla_workspace_bytes", "spla_append_workspace_bytes", "spla_decode_phase_mask",
            "spla_workspace_init", "spla_reset", "spla_append",
-           "spla_decode", "spla_decode_ex", "spla_step", "spla_step_ex", "spla_prefill"]
+           "spla_decode", "spla_decode_ex", "spla_step", "spla_step_ex", "spla_prefill",
+           "spla_decode_noalloc"]
 HOST_EXPORTS = EXPORTS[:7]
 
 
@@ -100,6 +101,9 @@ def _declare(lib, host_only=False):
     lib.spla_step_ex.restype = c_int32
     lib.spla_step_ex.argtypes = [cfgp, cachep, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
                                  c_void_p, c_void_p, c_size_t, POINTER(SplaEvents), c_void_p]
+    lib.spla_decode_noalloc.restype = c_int32
+    lib.spla_decode_noalloc.argtypes = [cfgp, cachep, c_void_p, c_void_p, c_void_p, c_void_p,
+                                        c_void_p]
     lib.spla_prefill.restype = c_int32
     lib.spla_prefill.argtypes = [cfgp, cachep, c_int32, c_void_p, c_void_p, c_void_p, c_void_p,
                                  c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]
@@ -300,6 +304,22 @@ class SplaCache:
                                     _ptr(gamma), _ptr(out), _ptr(sel), _ptr(self.workspace),
                                     self.workspace.numel(), ev, _stream(self.device)),
                "spla_decode")
+        return out, sel
+
+    def decode_noalloc(self, q: torch.Tensor, gamma: torch.Tensor, out, sel=None):
+        """spla_decode_noalloc: the decode on the library's own device scratch
+        (no workspace); out must be given (nothing is allocated here either)."""
+        c = self.cfg
+        assert q.shape == (c.batch, c.n_q_heads, c.head_dim) and q.dtype == torch_dtype(c)
+        assert gamma.shape == (c.n_q_heads, c.head_dim) and gamma.dtype == torch.float32
+        assert out is not None and out.shape == q.shape and out.dtype == q.dtype
+        assert q.is_contiguous() and gamma.is_contiguous() and out.is_contiguous()
+        if sel is not None:
+            assert sel.shape == (c.batch, c.n_kv_heads, c.top_k) and sel.dtype == torch.int32
+            assert sel.is_contiguous()
+        _check(lib().spla_decode_noalloc(ctypes.byref(c), ctypes.byref(self._struct), _ptr(q),
+                                         _ptr(gamma), _ptr(out), _ptr(sel),
+                                         _stream(self.device)), "spla_decode_noalloc")
         return out, sel
 
     def step(self, k_new, v_new, q, gamma, out=None, sel=None, events=None):

@@ -192,3 +192,18 @@ def test_decode_phase_mask(libname, kw, single):
     got = spla.decode_phases(_cfg(**kw), lib)
     assert got == (["decode"] if single else ["score", "select", "sparse", "merge"])
 
+
+
+def test_noalloc_rejects_before_launch():
+    """spla_decode_noalloc checks its arguments and the scratch size on the
+    host; a shape whose workspace exceeds the scratch is rejected."""
+    lib = spla.lib()
+    fake = spla.SplaCacheStruct(*([256] * 6), None)
+    big = spla.make_config(128, 32, 8, 128, 64, 256, 1 << 21)
+    assert spla.workspace_bytes(big) > 64 << 20
+    assert lib.spla_decode_noalloc(ctypes.byref(big), ctypes.byref(fake), 256, 256, 512, None,
+                                   None) == -4
+    c = _cfg()
+    assert lib.spla_decode_noalloc(ctypes.byref(c), ctypes.byref(fake), 256, 256, 256, None,
+                                   None) == -1
+    assert lib.spla_decode_noalloc(ctypes.byref(c), None, 256, 256, 512, None, None) == -1
