@@ -263,44 +263,64 @@ def prefill_leg(w, dev, K, T=16):
             "method": "append + decode per position (spla_prefill)"}
 
 
-def cpu_baseline(w, seconds, n_units=2):
+def cpu_baseline(w, seconds, n_units=8):
     """The fp64 oracle's decode on a bounded sample of the workload: n_units
-    (sequence, KV head) units with their state prebuilt (untimed), decode
-    repeated until `seconds` of CPU time accumulate; one BLAS thread."""
+    (sequence, KV head) units with their state prebuilt (untimed), decoded
+    round-robin for `seconds` of wall time by as many threads as the process
+    may use (at most 16, the host share of one GPU; BLAS single-threaded in
+    each), then by one thread for the 1-core figure."""
     import numpy as np
+    from concurrent.futures import ThreadPoolExecutor
     from threadpoolctl import threadpool_limits
 
     import oracle as O
     import spla_inputs as si
 
+    cores = max(1, min(16, len(os.sched_getaffinity(0))))
     p = O.SplaParams(block_size=w.block_size, top_k=w.top_k, n_sink=w.n_sink, n_local=w.n_local)
     rng = np.random.default_rng([w.code, 99])
     allp = [(b, h) for b in range(w.batch) for h in range(w.n_kv_heads)]
     pick = [allp[i] for i in rng.choice(len(allp), size=min(n_units, len(allp)), replace=False)]
     gamma = si.gen_gamma(w)
-    units = []
-    with threadpool_limits(1):
-        for b, h in pick:
-            L = int(w.lengths[b])
-            K, V = si.gen_kv(w, b, h, 0, L, threads=8)
-            st = O.build_state(K, V, L, w.block_size)
-            q = si.gen_q(w, b)[h * w.group:(h + 1) * w.group]
-            units.append((q, st, K, V, gamma[h * w.group:(h + 1) * w.group]))
-        reps, busy = 0, 0.0
-        t_start = time.process_time()
-        while busy < seconds:
-            for u in units:
+
+    def make(bh):
+        b, h = bh
+        L = int(w.lengths[b])
+        K, V = si.gen_kv(w, b, h, 0, L)
+        st = O.build_state(K, V, L, w.block_size)
+        q = si.gen_q(w, b)[h * w.group:(h + 1) * w.group]
+        return (q, st, K, V, gamma[h * w.group:(h + 1) * w.group])
+
+    def timed(n_threads):
+        t0 = time.perf_counter()
+        counts = [0] * n_threads
+
+        def work(i):
+            j = 0
+            while time.perf_counter() - t0 < seconds:
+                u = units[(i + j) % len(units)]
                 O.decode_kv_head(u[0], u[1], u[2], u[3], u[4], p)
-            reps += 1
-            busy = time.process_time() - t_start
-    wall_per_unit = busy / (reps * len(units))
-    import spla_inputs as si2
-    per_unit = si2.algorithmic_bytes(w)["total"] / (w.batch * w.n_kv_heads)
-    return {"value": round(per_unit / wall_per_unit / 1e9, 4), "unit": "GB/s", "cores": 1,
+                j += 1
+            counts[i] = j
+
+        with ThreadPoolExecutor(n_threads) as ex:
+            list(ex.map(work, range(n_threads)))
+        return sum(counts), time.perf_counter() - t0
+
+    with threadpool_limits(1):
+        with ThreadPoolExecutor(cores) as ex:
+            units = list(ex.map(make, pick))
+        n_all, t_all = timed(cores)
+        n_one, t_one = timed(1)
+    per_unit = si.algorithmic_bytes(w)["total"] / (w.batch * w.n_kv_heads)
+    return {"value": round(per_unit * n_all / t_all / 1e9, 4), "unit": "GB/s", "cores": cores,
             "kind": "oracle",
+            "value_1core": round(per_unit * n_one / t_one / 1e9, 4),
             "sample": f"fp64 oracle decode of {len(units)} of {len(allp)} (sequence, KV head) "
-                      f"units of {w.name} (state prebuilt, untimed), repeated {reps}x "
-                      f"({busy:.1f}s CPU); {wall_per_unit * 1e3:.1f} ms per unit",
+                      f"units of {w.name} (state prebuilt, untimed), round-robin for "
+                      f"{seconds:.0f}s wall on {cores} threads ({n_all} unit decodes, "
+                      f"{t_all / n_all * cores * 1e3:.1f} ms each) and on 1 thread "
+                      f"({n_one} decodes, {t_one / max(n_one, 1) * 1e3:.1f} ms each)",
             "cpu": _cpu_model()}
 
 
@@ -397,16 +417,283 @@ def traffic_summary(fetch_dir, write_dir, workload, commands, out_md, kernel, ke
     print("\n".join(lines))
 
 
+def percentiles(xs):
+    import numpy as np
+
+    a = np.asarray(xs, dtype=np.float64)
+    return {"median": round(float(np.median(a)), 3), "p10": round(float(np.percentile(a, 10)), 3),
+            "p90": round(float(np.percentile(a, 90)), 3), "n": int(a.size)}
+
+
+def clone_cache(c):
+    """A second cache with the same contents (device copies)."""
+    from paper_2601_22379_amd import spla
+
+    d = spla.SplaCache(c.cfg, c.device, block_table=c.block_table)
+    for name in ("k", "v", "stats", "state", "norm", "seq_lens"):
+        getattr(d, name).copy_(getattr(c, name))
+    return d
+
+
+def replicas_for(w, requested):
+    """Cache copies decoded in rotation: one for the appending workload
+    (each step's working set, about 0.8 GB, is already well above the 256 MB
+    last-level cache, and its separate-launch replay needs a clone of the
+    cache), else `requested`."""
+    import spla_inputs as si
+
+    big = si.algorithmic_bytes(w)["total"] > (1 << 29)
+    return 1 if (w.appends_per_step > 0 or big) else requested
+
+
+def run_workload(w, R, dev, K, W, headline=False, no_graph=False):
+    """Fills R copies of the workload's cache and times K steps (after W
+    untimed ones) on them in rotation. Every timed step writes an output of
+    its own; afterwards the same steps are replayed on the separate-launch
+    path and every output must match bit for bit, and every cache's device
+    error word must be clear. A second pass brackets each step with events
+    (median / p10 / p90), a third the dominant kernel. Returns the dict of
+    the workload's JSON object (plus the headline-only extras)."""
+    import numpy as np
+    import torch
+
+    from paper_2601_22379_amd import spla
+    import spla_inputs as si
+
+    cfg, caches = build_workload(w, R, dev)
+    dt = torch.float32 if w.dtype == "f32" else torch.bfloat16
+    gamma = torch.from_numpy(si.gen_gamma(w)).to(dev)
+    appending = w.appends_per_step > 0
+    n_steps = 4 * K + W + 2 * R + 1
+    if appending:
+        # per-step token rows and queries, generated before timing: step s
+        # appends position lengths[b] - 1 + s // R of each sequence (each
+        # replica advances on its own)
+        n_pos = (n_steps - 1) // R + 1
+        assert max(w.lengths) - 1 + n_pos <= w.capacity, "appending steps exceed the capacity"
+        kn = np.zeros((n_steps, w.batch, w.n_kv_heads, w.head_dim), np.float32)
+        vn = np.zeros_like(kn)
+        steps = np.arange(n_steps)
+        for b in range(w.batch):
+            p0 = w.lengths[b] - 1
+            for h in range(w.n_kv_heads):
+                kk, vv = si.gen_kv(w, b, h, p0, p0 + n_pos)
+                kn[:, b, h], vn[:, b, h] = kk[steps // R], vv[steps // R]
+        kn_d = torch.from_numpy(kn).to(dt).to(dev)
+        vn_d = torch.from_numpy(vn).to(dt).to(dev)
+        qs = torch.from_numpy(np.stack([si.gen_q_batch(w, s) for s in range(min(n_steps, 64))])).to(
+            dt).to(dev)
+    else:
+        qs = torch.from_numpy(si.gen_q_batch(w)[None]).to(dt).to(dev)
+    outs = torch.empty((K, w.batch, w.n_q_heads, w.head_dim), dtype=dt, device=dev)
+    sels = [torch.empty((w.batch, w.n_kv_heads, w.top_k), dtype=torch.int32, device=dev)
+            for _ in range(R)]
+
+    def one(s, out, cache=None, events=None):
+        r = s % R
+        c = caches[r] if cache is None else cache
+        q = qs[s % qs.shape[0]]
+        if appending:
+            return c.step(kn_d[s], vn_d[s], q, gamma, out, sels[r], events)
+        return c.decode(q, gamma, out, sels[r], events)
+
+    launched = spla.decode_phases(cfg)
+    dom = "decode" if "decode" in launched else "score"
+    for s in range(W):
+        one(s, outs[0])
+    torch.cuda.synchronize()
+    ref_cache = clone_cache(caches[0]) if appending else None
+
+    # timed region: exactly K steps, no instrumentation inside
+    t_a = torch.cuda.Event(enable_timing=True)
+    t_b = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_a.record()
+    for s in range(K):
+        one(W + s, outs[s])
+    t_b.record()
+    torch.cuda.synchronize()
+    ms_per_step = t_a.elapsed_time(t_b) / K
+    errs = [c.device_errors() for c in caches]
+    assert all(e == 0 for e in errs), f"device error word set: {errs}"
+
+    # the same steps on the separate launches, compared bit for bit
+    ref = torch.empty_like(outs[0])
+    mism = 0
+    for c in caches + ([ref_cache] if ref_cache is not None else []):
+        c.cfg.flags |= spla.FLAG_SEPARATE_KERNELS
+    try:
+        if appending:
+            for s in range(K):
+                # replica 0 only (R = 1 for the appending workload)
+                one(W + s, ref, cache=ref_cache)
+                mism += int(not torch.equal(ref, outs[s]))
+        else:
+            for r in range(min(R, K)):
+                one(W + r, ref)
+                for s in range(r, K, R):
+                    mism += int(not torch.equal(ref, outs[s]))
+        torch.cuda.synchronize()
+    finally:
+        for c in caches + ([ref_cache] if ref_cache is not None else []):
+            c.cfg.flags &= ~spla.FLAG_SEPARATE_KERNELS
+    assert mism == 0, f"{mism} of {K} timed steps differ from the separate-launch path"
+    if ref_cache is not None:
+        assert ref_cache.device_errors() == 0
+        del ref_cache
+
+    # each step bracketed by its own events: the distribution
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(K)]
+    off = W + K if appending else W
+    for s in range(K):
+        ev[s][0].record()
+        one(off + s, outs[s])
+        ev[s][1].record()
+    torch.cuda.synchronize()
+    dist = percentiles([a.elapsed_time(b) * 1e3 for a, b in ev])
+
+    # events around the dominant kernel only, recorded by the library
+    dev_ev = [spla.make_events([dom]) for _ in range(K)]
+    off += K if appending else 0
+    torch.cuda.synchronize()
+    for s in range(K):
+        one(off + s, outs[s], events=dev_ev[s][0])
+    torch.cuda.synchronize()
+    dom_us_events = float(np.mean([e[1][dom][0].elapsed_time(e[1][dom][1])
+                                   for e in dev_ev])) * 1e3
+    # a step that is one launch of the dominant kernel and nothing else: the
+    # timed region over the launches is its average launch duration, without
+    # per-launch event records (whose own cost lengthens each launch)
+    only_dom = launched == [dom] and not appending
+    dom_us = ms_per_step * 1e3 if only_dom else dom_us_events
+    dom_method = "timed region / launches" if only_dom else "per-launch events"
+
+    sel_counts = None
+    if not appending:
+        lens = caches[0].seq_lens.cpu().numpy()
+        sel_np = sels[0].cpu().numpy()
+        sel_counts = [[sum(min(w.block_size, int(lens[b]) - int(i) * w.block_size)
+                           for i in sel_np[b, h] if i >= 0) for h in range(w.n_kv_heads)]
+                      for b in range(w.batch)]
+    ab = si.algorithmic_bytes(w, sel_counts)
+    dom_bytes = dominant_bytes(w, ab, dom)
+    achieved = dom_bytes / (dom_us * 1e-6) / 1e9
+    prof_us = None
+    trace_md = os.path.join(ROOT, "profiles", f"decode_{w.name}_kernel_trace.md")
+    if os.path.exists(trace_md):
+        for ln in open(trace_md):
+            if ln.startswith(f"| spla::{dom}_kernel"):
+                prof_us = float(ln.split("|")[3])
+                break
+    leg = {"latency_us": round(ms_per_step * 1e3, 3),
+           "latency_us_per_step_events": dist,
+           "value": round(ab["total"] / (ms_per_step * 1e-3) / 1e9, 1), "unit": "GB/s",
+           "frac_of_peak_hbm": round(ab["total"] / (ms_per_step * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+           "algorithmic_bytes": ab, "kernels": launched + (["append"] if appending else []),
+           "cache_replicas": R, "steps": K,
+           "checked": f"{K} timed steps equal to the separate launches bit for bit; "
+                      "device error word clear",
+           "roofline": {"kernel": dom, "bound": "hbm", "achieved": round(achieved, 1),
+                        "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                        "frac": round(achieved / PEAK_HBM_GBS, 4),
+                        "traffic": traffic_of(dom, w.name),
+                        "algorithmic_bytes_per_launch": dom_bytes,
+                        "avg_launch_us": round(dom_us, 3), "avg_launch_method": dom_method,
+                        "avg_launch_us_per_launch_events": round(dom_us_events, 3),
+                        "profiled_avg_us": prof_us}}
+    log(f"{w.name}: {ms_per_step * 1e3:.2f} us/step (per-step events median {dist['median']:.2f}, "
+        f"p10 {dist['p10']:.2f}, p90 {dist['p90']:.2f}); {dom} kernel {dom_us:.2f} us "
+        f"({dom_method}), {achieved:.0f} GB/s algorithmic")
+    if not headline:
+        del caches
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+        return leg, None
+
+    # headline extras: the separate-kernel path's plain latency and phases
+    sep_names = ["score", "select", "sparse", "merge"] + (["append"] if appending else [])
+    for c in caches:
+        c.cfg.flags |= spla.FLAG_SEPARATE_KERNELS
+    sep_launched = set(spla.decode_phases(caches[0].cfg)) | {"append"}
+    try:
+        for s in range(W):
+            one(s, outs[0])
+        torch.cuda.synchronize()
+        t_a.record()
+        for s in range(K):
+            one(W + s, outs[s])
+        t_b.record()
+        torch.cuda.synchronize()
+        sep_ms = t_a.elapsed_time(t_b) / K
+        evp = [spla.make_events(sep_names) for _ in range(K)]
+        torch.cuda.synchronize()
+        for s in range(K):
+            one(W + 2 * K + s, outs[s], events=evp[s][0])
+        torch.cuda.synchronize()
+    finally:
+        for c in caches:
+            c.cfg.flags &= ~spla.FLAG_SEPARATE_KERNELS
+    phases = {}
+    for name in sep_names:
+        if name in sep_launched:
+            phases[name] = float(np.mean([e[1][name][0].elapsed_time(e[1][name][1])
+                                          for e in evp])) * 1e3
+    log(f"separate kernels {sep_ms * 1e3:.2f} us/step, phases us: "
+        + ", ".join(f"{k}={v:.2f}" for k, v in phases.items()))
+    graph_us = None
+    if not no_graph and not appending:
+        try:
+            graphs = []
+            side = torch.cuda.Stream()
+            side.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(side):
+                for r in range(R):
+                    g = torch.cuda.CUDAGraph()
+                    with torch.cuda.graph(g, stream=side):
+                        one(r, outs[r % K])
+                    graphs.append(g)
+            torch.cuda.current_stream().wait_stream(side)
+            torch.cuda.synchronize()
+            for r in range(R):
+                one(r, outs[r % K])
+            torch.cuda.synchronize()
+            eager = [outs[r % K].clone() for r in range(R)]
+            for _ in range(3):
+                for r in range(R):
+                    graphs[r].replay()
+                torch.cuda.synchronize()
+                for r in range(R):
+                    assert torch.equal(outs[r % K], eager[r]), "graph replay differs from eager"
+            t_a.record()
+            for s in range(K):
+                graphs[s % R].replay()
+            t_b.record()
+            torch.cuda.synchronize()
+            graph_us = t_a.elapsed_time(t_b) / K * 1e3
+        except Exception as e:  # graph capture is an extra measurement only
+            log(f"graph measurement skipped: {e!r}")
+    extras = {"latency_us_separate_kernels": round(sep_ms * 1e3, 3),
+              "phases_us_separate_kernels": {k: round(v, 3) for k, v in phases.items()},
+              "latency_us_hip_graph": None if graph_us is None else round(graph_us, 3)}
+    del caches
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return leg, extras
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--config", default="3")
     ap.add_argument("--replicas", type=int, default=6)
-    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--cpu-seconds", type=float, default=6.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-graph", action="store_true")
+    ap.add_argument("--legs", default="1,2,4,5,g5",
+                    help="other workloads measured after the headline one ('' for none)")
     ap.add_argument("--no-strided", action="store_true",
                     help="skip the strided-selection (C = 32, s = 16), paged-KV and prefill legs")
     ap.add_argument("--strided-only", action="store_true",
@@ -447,7 +734,6 @@ def main():
               "library runs on a single GPU only (no multi-GPU path is built).", file=sys.stderr)
         sys.exit(2)
 
-    import numpy as np
     import torch
 
     from paper_2601_22379_amd import spla
@@ -458,211 +744,52 @@ def main():
     dev = torch.device("cuda:0")
     w = si.config(args.config)
     R = max(1, args.replicas)
+    K, W = args.steps, args.warmup
+    dt = torch.float32 if w.dtype == "f32" else torch.bfloat16
     if args.strided_only:
-        dt = torch.float32 if w.dtype == "f32" else torch.bfloat16
         qs = torch.from_numpy(si.gen_q_batch(w)[None]).to(dt).to(dev)
         gamma = torch.from_numpy(si.gen_gamma(w)).to(dev)
         outs = [torch.empty((w.batch, w.n_q_heads, w.head_dim), dtype=dt, device=dev)
                 for _ in range(R)]
         sels = [torch.empty((w.batch, w.n_kv_heads, w.top_k), dtype=torch.int32, device=dev)
                 for _ in range(R)]
-        line = strided_leg(w, R, dev, qs, gamma, outs, sels, args.steps, args.warmup)
+        line = strided_leg(w, R, dev, qs, gamma, outs, sels, K, W)
         if args.copy_calibration:
             copy_calibration(dev)
         print(json.dumps(line), flush=True)
         return
-    cfg, caches = build_workload(w, R, dev)
-    dt = torch.float32 if w.dtype == "f32" else torch.bfloat16
-    K, W = args.steps, args.warmup
-    gamma = torch.from_numpy(si.gen_gamma(w)).to(dev)
-    appending = w.appends_per_step > 0
-    n_q = 3 * K + W + 2 * R + 1
-    if appending:
-        # per-step inputs generated before timing: token rows and queries
-        # step s appends position lengths[b] - 1 + s // R of each sequence
-        # (each replica advances on its own); one generator call per
-        # (sequence, KV head) covers every step
-        kn = np.zeros((n_q, w.batch, w.n_kv_heads, w.head_dim), np.float32)
-        vn = np.zeros_like(kn)
-        n_pos = (n_q - 1) // R + 1
-        steps = np.arange(n_q)
-        for b in range(w.batch):
-            p0 = w.lengths[b] - 1
-            for h in range(w.n_kv_heads):
-                kk, vv = si.gen_kv(w, b, h, p0, p0 + n_pos)
-                kn[:, b, h], vn[:, b, h] = kk[steps // R], vv[steps // R]
-        log(f"generated the tokens of {n_q} appending steps")
-        kn_d = torch.from_numpy(kn).to(dt).to(dev)
-        vn_d = torch.from_numpy(vn).to(dt).to(dev)
-        qs = torch.from_numpy(np.stack([si.gen_q_batch(w, s) for s in range(min(n_q, 64))])).to(
-            dt).to(dev)
-    else:
-        qs = torch.from_numpy(si.gen_q_batch(w)[None]).to(dt).to(dev)
-    outs = [torch.empty((w.batch, w.n_q_heads, w.head_dim), dtype=dt, device=dev)
-            for _ in range(R)]
-    sels = [torch.empty((w.batch, w.n_kv_heads, w.top_k), dtype=torch.int32, device=dev)
-            for _ in range(R)]
-
-    def one(s, events=None):
-        r = s % R
-        q = qs[s % qs.shape[0]]
-        if appending:
-            return caches[r].step(kn_d[s], vn_d[s], q, gamma, outs[r], sels[r], events)
-        return caches[r].decode(q, gamma, outs[r], sels[r], events)
-
-    # the dominant kernel: the single-launch decode kernel where the shape has
-    # one, else the statistics scan of the separate-kernel path
-    launched = spla.decode_phases(cfg)
-    dom = "decode" if launched == ["decode"] else "score"
-    for s in range(W):
-        one(s)
-    torch.cuda.synchronize()
-
-    # timed region: exactly K steps, no instrumentation inside
-    t_a = torch.cuda.Event(enable_timing=True)
-    t_b = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
     wall0 = time.perf_counter()
-    t_a.record()
-    for s in range(K):
-        one(W + s)
-    t_b.record()
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - wall0
-    ms_per_step = t_a.elapsed_time(t_b) / K
-
-    # the same K steps with HIP events around the dominant kernel only,
-    # recorded by the library on the stream it launches on
-    ev = [spla.make_events([dom]) for _ in range(K)]
-    torch.cuda.synchronize()
-    t_a.record()
-    for s in range(K):
-        one(W + K + s, ev[s][0])
-    t_b.record()
-    torch.cuda.synchronize()
-    ms_per_step_dom_events = t_a.elapsed_time(t_b) / K
-    dom_us_events = float(np.mean([e[1][dom][0].elapsed_time(e[1][dom][1]) for e in ev])) * 1e3
-    # when a step is one launch of the dominant kernel and nothing else, the
-    # two events around the timed region (same stream) give its average
-    # launch duration without per-launch event records, whose own cost
-    # lengthens each bracketed launch by a microsecond or two
-    only_dom = launched == [dom] and not appending
-    dom_us = ms_per_step * 1e3 if only_dom else dom_us_events
-    dom_method = ("timed region / launches" if only_dom else "per-launch events")
-
-    # per-phase breakdown of the separate-kernel path (every phase bracketed;
-    # the extra event records lengthen the step, so this loop only apportions
-    # time between kernels), and that path's plain step latency
-    sep_names = ["score", "select", "sparse", "merge"] + (["append"] if appending else [])
-    for c in caches:
-        c.cfg.flags |= spla.FLAG_SEPARATE_KERNELS
-    sep_launched = set(spla.decode_phases(caches[0].cfg)) | {"append"}
-    try:
-        for s in range(W):
-            one(s)
-        torch.cuda.synchronize()
-        t_a.record()
-        for s in range(K):
-            one(W + s)
-        t_b.record()
-        torch.cuda.synchronize()
-        sep_ms = t_a.elapsed_time(t_b) / K
-        evp = [spla.make_events(sep_names) for _ in range(K)]
-        torch.cuda.synchronize()
-        for s in range(K):
-            one(W + 2 * K + s, evp[s][0])
-        torch.cuda.synchronize()
-    finally:
-        for c in caches:
-            c.cfg.flags &= ~spla.FLAG_SEPARATE_KERNELS
-    phases = {}
-    for name in sep_names:
-        if name in sep_launched:
-            phases[name] = float(np.mean([e[1][name][0].elapsed_time(e[1][name][1])
-                                          for e in evp])) * 1e3
-    log(f"timed {K} steps: {ms_per_step * 1e3:.2f} us/step (wall {wall / K * 1e6:.2f} us/step); "
-        f"{dom} kernel {dom_us:.2f} us ({dom_method}; per-launch events "
-        f"{dom_us_events:.2f}); separate kernels {sep_ms * 1e3:.2f} us/step, phases us: "
-        + ", ".join(f"{k}={v:.2f}" for k, v in phases.items()))
-
-    graph_us = None
-    if not args.no_graph and not appending:
-        try:
-            graphs = []
-            side = torch.cuda.Stream()
-            side.wait_stream(torch.cuda.current_stream())
-            with torch.cuda.stream(side):
-                for r in range(R):
-                    g = torch.cuda.CUDAGraph()
-                    with torch.cuda.graph(g, stream=side):
-                        one(r)
-                    graphs.append(g)
-            torch.cuda.current_stream().wait_stream(side)
-            torch.cuda.synchronize()
-            ref = [o.clone() for o in outs]
-            for r in range(R):
-                one(r)
-            torch.cuda.synchronize()
-            eager = [o.clone() for o in outs]
-            for _ in range(3):
-                for r in range(R):
-                    graphs[r].replay()
-                torch.cuda.synchronize()
-                for r in range(R):
-                    assert torch.equal(outs[r], eager[r]), "graph replay differs from eager"
-            t_a.record()
-            for s in range(K):
-                graphs[s % R].replay()
-            t_b.record()
-            torch.cuda.synchronize()
-            graph_us = t_a.elapsed_time(t_b) / K * 1e3
-            del ref
-        except Exception as e:  # graph capture is an extra measurement only
-            log(f"graph measurement skipped: {e!r}")
-
-    if args.copy_calibration:
-        copy_calibration(dev)
-
-    sel_counts = None
-    if not appending:
-        lens = caches[0].seq_lens.cpu().numpy()
-        sel_np = sels[0].cpu().numpy()
-        sel_counts = [[sum(min(w.block_size, int(lens[b]) - int(i) * w.block_size)
-                           for i in sel_np[b, h] if i >= 0) for h in range(w.n_kv_heads)]
-                      for b in range(w.batch)]
-    ab = si.algorithmic_bytes(w, sel_counts)
-    total = ab["total"]
-    value = total / (ms_per_step * 1e-3) / 1e9
-    dom_bytes = dominant_bytes(w, ab, dom)
-    achieved = dom_bytes / (dom_us * 1e-6) / 1e9
-    traffic = traffic_of(dom, w.name)
-    # the committed kernel-trace summary's average for the same kernel: the
-    # events above also span the kernel's dispatch latency
-    prof_us = None
-    trace_md = os.path.join(ROOT, "profiles", f"decode_{w.name}_kernel_trace.md")
-    if os.path.exists(trace_md):
-        for ln in open(trace_md):
-            if ln.startswith(f"| spla::{dom}_kernel"):
-                prof_us = float(ln.split("|")[3])
-    roofline = {"kernel": dom, "bound": "hbm", "achieved": round(achieved, 1),
-                "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4),
-                "traffic": traffic, "algorithmic_bytes_per_launch": dom_bytes,
-                "avg_launch_us": round(dom_us, 3), "avg_launch_method": dom_method,
-                "avg_launch_us_per_launch_events": round(dom_us_events, 3),
-                "profiled_avg_us": prof_us}
+    head, extras = run_workload(w, replicas_for(w, R), dev, K, W, headline=True,
+                                no_graph=args.no_graph)
     strided = paged = prefill = None
-    if not appending and not args.no_strided:
+    if w.appends_per_step == 0 and not args.no_strided:
+        qs = torch.from_numpy(si.gen_q_batch(w)[None]).to(dt).to(dev)
+        gamma = torch.from_numpy(si.gen_gamma(w)).to(dev)
+        outs = [torch.empty((w.batch, w.n_q_heads, w.head_dim), dtype=dt, device=dev)
+                for _ in range(R)]
+        sels = [torch.empty((w.batch, w.n_kv_heads, w.top_k), dtype=torch.int32, device=dev)
+                for _ in range(R)]
         strided = strided_leg(w, R, dev, qs, gamma, outs, sels, K, W)
         paged = strided_leg(w, R, dev, qs, gamma, outs, sels, K, W, C=w.block_size,
                             s=w.block_size, paged=True)
         prefill = prefill_leg(w, dev, K=20)
+        torch.cuda.empty_cache()
+    legs = {}
+    for cid in [c for c in args.legs.split(",") if c.strip() and c.strip() != args.config]:
+        wl = si.config(cid.strip())
+        # the appending workload has 512 positions of room for all its steps
+        kl = min(K, 100) if wl.appends_per_step else K
+        legs[wl.name], _ = run_workload(wl, replicas_for(wl, R), dev, kl, W)
+    if args.copy_calibration:
+        copy_calibration(dev)
     cpu = None
     if not args.no_cpu_baseline:
         log("timing the CPU oracle")
         cpu = cpu_baseline(w, args.cpu_seconds)
+    ms_per_step = head["latency_us"] / 1e3
     line = {
         "metric": METRIC,
-        "value": round(value, 1),
+        "value": head["value"],
         "unit": "GB/s",
         "n_gpus": 1,
         "steps": K,
@@ -677,19 +804,21 @@ def main():
                    "n_kv_heads": w.n_kv_heads, "head_dim": w.head_dim,
                    "context": int(max(w.lengths)), "block_size": w.block_size,
                    "top_k": w.top_k, "n_sink": w.n_sink, "n_local": w.n_local,
-                   "cache_replicas": R, "appends_per_step": w.appends_per_step},
-        "latency_us": round(ms_per_step * 1e3, 3),
-        "latency_us_with_kernel_events": round(ms_per_step_dom_events * 1e3, 3),
-        "latency_us_separate_kernels": round(sep_ms * 1e3, 3),
-        "latency_us_hip_graph": None if graph_us is None else round(graph_us, 3),
-        "frac_of_peak_hbm": round(value / PEAK_HBM_GBS, 4),
-        "algorithmic_bytes": ab,
-        "phases_us_separate_kernels": {k: round(v, 3) for k, v in phases.items()},
-        "roofline": roofline,
+                   "cache_replicas": head["cache_replicas"],
+                   "appends_per_step": w.appends_per_step},
+        "latency_us": head["latency_us"],
+        "latency_us_per_step_events": head["latency_us_per_step_events"],
+        "frac_of_peak_hbm": head["frac_of_peak_hbm"],
+        "algorithmic_bytes": head["algorithmic_bytes"],
+        "checked": head["checked"],
+        **extras,
+        "roofline": head["roofline"],
         "cpu_baseline": cpu,
+        "workloads": legs,
         "strided_selection": strided,
         "paged_kv": paged,
         "prefill": prefill,
+        "bench_wall_s": round(time.perf_counter() - wall0, 1),
     }
     print(json.dumps(line), flush=True)
 

@@ -275,9 +275,12 @@ def gen_kv_slab(w: Workload, t0: int, t1: int, lengths=None, threads: int = 8):
     n_new = np.array([max(0, min(T, int(lengths[b]) - t0)) for b in range(w.batch)], np.int32)
     jobs = [(b, h) for b in range(w.batch) for h in range(w.n_kv_heads) if n_new[b] > 0]
 
+    # fewer (sequence, KV head) jobs than threads: each job splits its chunks
+    inner = max(1, threads // max(1, len(jobs)))
+
     def run(job):
         b, h = job
-        kk, vv = gen_kv(w, b, h, t0, t0 + int(n_new[b]))
+        kk, vv = gen_kv(w, b, h, t0, t0 + int(n_new[b]), threads=inner)
         K[b, h, :n_new[b]] = kk
         V[b, h, :n_new[b]] = vv
 
