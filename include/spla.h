@@ -238,6 +238,13 @@ int32_t spla_decode_phase_mask(const spla_config* cfg, uint32_t* out_mask);
  * sequence (host-only query). */
 int32_t spla_append_workspace_bytes(const spla_config* cfg, int32_t max_new, size_t* out_bytes);
 
+/* Device workspace that spla_prefill needs for n_tokens positions per
+ * sequence (host-only query): per-query scores, selections, records and
+ * global terms of one chunk of at most 32 positions for the chunked shapes,
+ * the decode workspace for the others. */
+int32_t spla_prefill_workspace_bytes(const spla_config* cfg, int32_t n_tokens,
+                                     size_t* out_bytes);
+
 /* ---------------------------------------------------------- device calls */
 
 /* Zero-fills a decode workspace of workspace_bytes bytes (at least
@@ -312,20 +319,27 @@ int32_t spla_step(const spla_config* cfg, const spla_cache* cache, const void* k
                   int32_t* sel_idx, void* workspace, size_t workspace_bytes, void* stream);
 
 /* Causal prefill of n_tokens new tokens per sequence (Sec. 2: the decode
- * formulation carries over to prefill). For t = 0 .. n_tokens - 1, token t of
- * every (sequence, KV head) is appended and the queries at that position are
- * decoded, exactly as spla_step would: the query at position L_b + t sees the
- * tokens up to and including its own, with its own block selection.
+ * formulation carries over to prefill). Token t of every (sequence, KV head)
+ * is appended at position L_b + t, and the queries at that position get
+ * exactly what spla_step would give them there: they see the tokens up to and
+ * including their own, with their own block selection, the statistics of
+ * their partial blocks up to their position and S_bar over their prefix.
  *  k_new, v_new: device, dtype [n_tokens][batch][Hkv][d] (position-major).
  *  q:            device, dtype [n_tokens][batch][Hq][d].
  *  rms_weight:   device fp32 [Hq][d].
  *  out:          device, dtype [n_tokens][batch][Hq][d] (may not alias q).
  *  sel_idx:      device int32 [n_tokens][batch][Hkv][top_k] or NULL.
- *  workspace:    the decode workspace (spla_workspace_bytes, prepared once by
- *                spla_workspace_init).
- * Runs n_tokens append + decode steps on `stream` (one position at a time; no
- * chunk-wide kernels yet). n_tokens = 0 does nothing; tokens past max_seq_len
- * are dropped as in spla_step. */
+ *  workspace:    at least spla_prefill_workspace_bytes(cfg, n_tokens) bytes,
+ *                256-byte aligned (no preparation needed).
+ * bf16 shapes with G <= 8 run chunks of up to 32 positions through the
+ * chunked kernels (Sec. 3.3 "Kernel Design": a chunkwise linear-attention
+ * kernel for o_bar that also carries S_bar and z_bar past the chunk, and the
+ * fused sparse kernel per query, after per-query scoring that reads each
+ * statistics tile once per chunk and per-query top-k); other shapes (which
+ * never decode in one launch) run the positions one at a time as spla_step
+ * does, on the separate decode launches. n_tokens = 0 does nothing; tokens past max_seq_len
+ * are dropped as in spla_step (SPLA_DEVERR_CAPACITY) and the queries at those
+ * positions decode over the full cache. */
 int32_t spla_prefill(const spla_config* cfg, const spla_cache* cache, int32_t n_tokens,
                      const void* k_new, const void* v_new, const void* q,
                      const float* rms_weight, void* out, int32_t* sel_idx, void* workspace,

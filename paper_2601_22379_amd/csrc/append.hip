@@ -26,13 +26,16 @@ __device__ __forceinline__ int appended_count(const Dims& m, int L0, int max_new
 // exactly one unit. The new tokens' mean and M2 are computed two-pass in fp64
 // and combined with the stored ones by Chan's formula, then rounded to fp32.
 // (unit ux of the units touched, of (sequence, kv head) bh; thread j handles
-// coordinate j)
+// coordinate j). New row r of bh is element bh * s_bh + r * s_row of k_new
+// and v_new: s_bh = max_new d, s_row = d for [batch][Hkv][max_new][d]
+// (spla_append), s_bh = d, s_row = batch Hkv d for position-major rows
+// [max_new][batch][Hkv][d] (the chunked prefill).
 template <typename T>
 __device__ __forceinline__ void append_unit(
     const Dims& m, T* __restrict__ kc, T* __restrict__ vc, float* __restrict__ stats,
     const int32_t* __restrict__ seq_lens, int32_t* __restrict__ err, const T* __restrict__ k_new,
     const T* __restrict__ v_new, int max_new, const int32_t* __restrict__ n_new,
-    const int32_t* __restrict__ table, int ux, int bh) {
+    const int32_t* __restrict__ table, int ux, int bh, int64_t s_bh, int64_t s_row) {
   const int b = bh / m.hkv;
   const int L0 = seq_lens[b];
   bool clipped;
@@ -47,7 +50,7 @@ __device__ __forceinline__ void append_unit(
   const int t_own = min(t_hi, (i + 1) * m.us);  // rows this unit copies: t_lo .. t_own - 1
   const int j = threadIdx.x;
   if (t_hi <= t_lo || j >= m.d) return;
-  const int64_t src0 = ((int64_t)bh * max_new - L0) * m.d + j;  // row t at src0 + t*d
+  const int64_t src0 = (int64_t)bh * s_bh - (int64_t)L0 * s_row + j;  // row t at src0 + t s_row
 
   // the slot of the block that holds the rows this unit copies (they all lie
   // in one block: a unit's first us tokens, us dividing B); -1: a paged
@@ -65,10 +68,10 @@ __device__ __forceinline__ void append_unit(
   }
   double sum = 0.0;
   for (int t = t_lo; t < t_hi; ++t) {
-    const T kv = k_new[src0 + (int64_t)t * m.d];
+    const T kv = k_new[src0 + (int64_t)t * s_row];
     if (t < t_own && slot >= 0) {
       kc[k_off_slot(m, slot, t % m.B, j)] = kv;
-      vc[v_off_slot(m, slot, t % m.B, j)] = v_new[src0 + (int64_t)t * m.d];
+      vc[v_off_slot(m, slot, t % m.B, j)] = v_new[src0 + (int64_t)t * s_row];
     }
     sum += (double)Elem<T>::load(&kv, 0);
   }
@@ -76,7 +79,7 @@ __device__ __forceinline__ void append_unit(
   const double mean_c = sum / nc;
   double m2_c = 0.0;
   for (int t = t_lo; t < t_hi; ++t) {
-    const double x = (double)Elem<T>::load(k_new, src0 + (int64_t)t * m.d) - mean_c;
+    const double x = (double)Elem<T>::load(k_new, src0 + (int64_t)t * s_row) - mean_c;
     m2_c += x * x;
   }
   const int na = t_lo - i * m.us;
@@ -99,9 +102,9 @@ __global__ __launch_bounds__(128) void append_blocks_kernel(
     Dims m, T* __restrict__ kc, T* __restrict__ vc, float* __restrict__ stats,
     const int32_t* __restrict__ seq_lens, int32_t* __restrict__ err, const T* __restrict__ k_new,
     const T* __restrict__ v_new, int max_new, const int32_t* __restrict__ n_new,
-    const int32_t* __restrict__ table) {
+    const int32_t* __restrict__ table, int64_t s_bh, int64_t s_row) {
   append_unit<T>(m, kc, vc, stats, seq_lens, err, k_new, v_new, max_new, n_new, table,
-                 (int)blockIdx.x, (int)blockIdx.y);
+                 (int)blockIdx.x, (int)blockIdx.y, s_bh, s_row);
 }
 
 // Partial linear-attention state of one chunk of new tokens:
@@ -284,7 +287,7 @@ __global__ __launch_bounds__(256) void append_one_kernel(
     append_rank1_rows<T, D>(m, seq_lens, k_new, v_new, S, z, (int)blockIdx.x, bh);
   else
     append_unit<T>(m, kc, vc, stats, seq_lens, err, k_new, v_new, 1, nullptr, table,
-                   (int)blockIdx.x - D / 16, bh);
+                   (int)blockIdx.x - D / 16, bh, D, D);
 }
 
 __global__ void append_finish_kernel(Dims m, int32_t* __restrict__ seq_lens, int max_new,
@@ -305,20 +308,22 @@ __global__ void fill_zero_kernel(uint32_t* __restrict__ p, int64_t n) {
 // ------------------------------------------------------------- launchers
 hipError_t launch_append_blocks(const Dims& m, const spla_cache& c, const void* k_new,
                                 const void* v_new, int max_new, const int32_t* n_new,
-                                hipStream_t st) {
+                                hipStream_t st, bool position_major) {
   // units touched by max_new tokens from any L0 (idle workgroups return)
   const int64_t nx = windowed(m) ? ceil_div(max_new + m.ul, m.us) + 2 : ceil_div(max_new, m.B) + 1;
   dim3 grid((unsigned)nx, (unsigned)m.bh);
+  const int64_t s_bh = position_major ? m.d : (int64_t)max_new * m.d;
+  const int64_t s_row = position_major ? (int64_t)m.bh * m.d : m.d;
   if (m.elem == 4)
     hipLaunchKernelGGL(append_blocks_kernel<float>, grid, dim3(128), 0, st, m, (float*)c.k_cache,
                        (float*)c.v_cache, c.blk_stats, c.seq_lens, c.err_flags,
                        (const float*)k_new, (const float*)v_new, max_new, n_new,
-                       m.pages > 0 ? c.block_table : nullptr);
+                       m.pages > 0 ? c.block_table : nullptr, s_bh, s_row);
   else
     hipLaunchKernelGGL(append_blocks_kernel<bf16_t>, grid, dim3(128), 0, st, m,
                        (bf16_t*)c.k_cache, (bf16_t*)c.v_cache, c.blk_stats, c.seq_lens,
                        c.err_flags, (const bf16_t*)k_new, (const bf16_t*)v_new, max_new, n_new,
-                       m.pages > 0 ? c.block_table : nullptr);
+                       m.pages > 0 ? c.block_table : nullptr, s_bh, s_row);
   return hipGetLastError();
 }
 

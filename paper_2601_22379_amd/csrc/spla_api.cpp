@@ -196,25 +196,43 @@ extern "C" int32_t spla_prefill(const spla_config* cfg, const spla_cache* cache,
                                 const void* k_new, const void* v_new, const void* q,
                                 const float* w, void* out, int32_t* sel_idx, void* ws,
                                 size_t ws_bytes, void* stream) {
-  int32_t s = check_decode_args(cfg, cache, q, w, out, ws, ws_bytes);
+  int32_t s = spla_validate(cfg);
   if (s != SPLA_OK) return s;
+  if ((s = check_cache(cfg, cache)) != SPLA_OK) return s;
+  if (!q || !w || !out || out == q) return SPLA_ERR_INVALID_ARG;
   if (n_tokens < 0) return SPLA_ERR_INVALID_ARG;
   if (n_tokens > cfg->max_seq_len) return SPLA_ERR_CAPACITY;
   if (n_tokens == 0) return SPLA_OK;
   if (!k_new || !v_new) return SPLA_ERR_INVALID_ARG;
+  size_t need = 0;
+  spla_prefill_workspace_bytes(cfg, n_tokens, &need);
+  if ((s = check_ws(ws, ws_bytes, need)) != SPLA_OK) return s;
   const Dims m = spla::make_dims(*cfg);
   hipStream_t st = static_cast<hipStream_t>(stream);
   // per position: the rows of token t, the queries at t, their outputs
   const size_t kv_step = (size_t)m.bh * m.d * m.elem;
   const size_t q_step = (size_t)m.batch * m.hq * m.d * m.elem;
   const size_t sel_step = (size_t)m.bh * m.k;
+  const char* kb = static_cast<const char*>(k_new);
+  const char* vb = static_cast<const char*>(v_new);
+  const char* qb = static_cast<const char*>(q);
+  char* ob = static_cast<char*>(out);
+  if (spla::use_chunked_prefill(m)) {
+    const spla::PrefillWs L = spla::prefill_ws_layout(m, n_tokens);
+    for (int32_t c0 = 0; c0 < n_tokens; c0 += L.T) {
+      const int T = n_tokens - c0 < L.T ? n_tokens - c0 : L.T;
+      SPLA_TRY(spla::launch_prefill_chunk(m, *cfg, *cache, T, kb + c0 * kv_step,
+                                          vb + c0 * kv_step, qb + c0 * q_step, w,
+                                          ob + c0 * q_step,
+                                          sel_idx ? sel_idx + c0 * sel_step : nullptr, L,
+                                          static_cast<char*>(ws), st));
+    }
+    return SPLA_OK;
+  }
   for (int32_t t = 0; t < n_tokens; ++t) {
-    const char* kt = static_cast<const char*>(k_new) + t * kv_step;
-    const char* vt = static_cast<const char*>(v_new) + t * kv_step;
-    SPLA_TRY(spla::launch_append_one(m, *cache, kt, vt, st));
+    SPLA_TRY(spla::launch_append_one(m, *cache, kb + t * kv_step, vb + t * kv_step, st));
     SPLA_TRY(spla::launch_append_finish(m, *cache, 1, nullptr, st));
-    if ((s = run_decode(cfg, cache, static_cast<const char*>(q) + t * q_step, w,
-                        static_cast<char*>(out) + t * q_step,
+    if ((s = run_decode(cfg, cache, qb + t * q_step, w, ob + t * q_step,
                         sel_idx ? sel_idx + t * sel_step : nullptr, ws, ws_bytes, nullptr, st)) !=
         SPLA_OK)
       return s;

@@ -115,3 +115,16 @@ extern "C" int32_t spla_decode_phase_mask(const spla_config* c, uint32_t* out) {
            (1u << SPLA_PHASE_MERGE);
   return SPLA_OK;
 }
+
+extern "C" int32_t spla_prefill_workspace_bytes(const spla_config* c, int32_t n_tokens,
+                                                size_t* out) {
+  if (!out) return SPLA_ERR_INVALID_ARG;
+  int32_t st = spla_validate(c);
+  if (st != SPLA_OK) return st;
+  if (n_tokens < 0) return SPLA_ERR_INVALID_ARG;
+  if (n_tokens > c->max_seq_len) return SPLA_ERR_CAPACITY;
+  const Dims m = spla::make_dims(*c);
+  *out = (size_t)(spla::use_chunked_prefill(m) ? spla::prefill_ws_layout(m, n_tokens).total
+                                               : spla::decode_ws_layout(m).total);
+  return SPLA_OK;
+}

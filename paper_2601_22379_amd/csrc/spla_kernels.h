@@ -12,9 +12,11 @@ namespace spla {
 int compute_units();
 
 // append.hip
+// position_major: the new rows are [max_new][batch][Hkv][d] instead of
+// [batch][Hkv][max_new][d]
 hipError_t launch_append_blocks(const Dims& m, const spla_cache& c, const void* k_new,
                                 const void* v_new, int max_new, const int32_t* n_new,
-                                hipStream_t st);
+                                hipStream_t st, bool position_major = false);
 hipError_t launch_append_state(const Dims& m, const spla_cache& c, const void* k_new,
                                const void* v_new, int max_new, const int32_t* n_new,
                                const AppendWs& ws, char* wsbase, hipStream_t st);
@@ -43,6 +45,14 @@ hipError_t launch_sparse(const Dims& m, const spla_config& cfg, const spla_cache
                          const DecodeWs& ws, char* wsbase, hipStream_t st);
 hipError_t launch_merge(const Dims& m, const spla_config& cfg, const float* rms_weight, void* out,
                         const DecodeWs& ws, char* wsbase, hipStream_t st);
+
+// prefill.hip: one chunk of at most kPrefillChunk positions of the chunked
+// causal prefill (use_chunked_prefill shapes); q, k_new, v_new, out and
+// sel_out point at the chunk's first position
+hipError_t launch_prefill_chunk(const Dims& m, const spla_config& cfg, const spla_cache& c,
+                                int T, const void* k_new, const void* v_new, const void* q,
+                                const float* rms_weight, void* out, int32_t* sel_out,
+                                const PrefillWs& ws, char* wsbase, hipStream_t st);
 
 // decode.hip: the single-launch decode (use_fused_decode shapes)
 hipError_t launch_decode_fused(const Dims& m, const spla_config& cfg, const spla_cache& c,

@@ -190,6 +190,57 @@ SPLA_HD DecodeWs decode_ws_layout(const Dims& m) {
   return w;
 }
 
+// ---- chunked prefill workspace ------------------------------------------------
+constexpr int kPrefillChunk = 32;  // positions per chunk of the chunked prefill
+
+// The chunked prefill covers the matrix-core shapes (bf16, G <= 8); the other
+// shapes run position by position (the single-token append, then a decode).
+SPLA_HD bool use_chunked_prefill(const Dims& m) { return use_mfma_sparse(m); }
+
+struct PrefillWs {
+  int T;            // positions per chunk
+  int nu_touch;     // statistics units that T consecutive tokens can touch
+  int n_wg;         // sparse workgroups per query (as in the decode)
+  int part_stride;  // floats per record
+  int64_t ustat;    // f32 [bh][nu_touch][T][2][d]  running (mean, M2) of the touched units
+  int64_t e_vals;   // f32 [bh T][G][n_tiles*64]    per query, as the decode's
+  int64_t tile_part;  // f64 [bh T][G][n_tiles][2]
+  int64_t sel;      // i32 [bh T][k]
+  int64_t meta;     // i32 [bh T][4]
+  int64_t part;     // f32 [bh T][n_wg][part_stride]
+  int64_t obar;     // f32 [bh][T G][d]  o_bar of every query (row = position G + head)
+  int64_t zq;       // f32 [bh][T G]     <phi(q), z_bar> of every query
+  int64_t total;
+};
+
+SPLA_HD PrefillWs prefill_ws_layout(const Dims& m, int n_tokens) {
+  PrefillWs w;
+  const int64_t A = SPLA_WORKSPACE_ALIGN;
+  int64_t off = 0;
+  auto take = [&](int64_t bytes) {
+    int64_t o = off;
+    off = align_up(off + bytes, A);
+    return o;
+  };
+  w.T = n_tokens < 1 ? 1 : (n_tokens < kPrefillChunk ? n_tokens : kPrefillChunk);
+  // units u with u us < L0 + T and u us + ul > L0
+  w.nu_touch = (int)ceil_div(w.T + m.ul, m.us) + 1;
+  const DecodeWs d = decode_ws_layout(m);
+  w.n_wg = d.n_wg;
+  w.part_stride = d.part_stride;
+  const int64_t nq = (int64_t)m.bh * w.T;
+  w.ustat = take((int64_t)m.bh * w.nu_touch * w.T * 2 * m.d * 4);
+  w.e_vals = take(nq * m.group * m.n_tiles * kTileBlocks * 4);
+  w.tile_part = take(nq * m.n_tiles * m.group * 2 * 8);
+  w.sel = take(nq * m.k * 4);
+  w.meta = take(nq * 4 * 4);
+  w.part = take(nq * w.n_wg * w.part_stride * 4);
+  w.obar = take(nq * m.group * m.d * 4);
+  w.zq = take(nq * m.group * 4);
+  w.total = off;
+  return w;
+}
+
 // ---- append workspace ------------------------------------------------------
 struct AppendWs {
   int64_t part_s;  // f32 [bh][n_chunks][d][d]

@@ -128,20 +128,24 @@ __device__ __forceinline__ void static_for(F&& f) {
 }
 
 // Scores one tile from buf; s_part is this tile's half of the double-buffered
-// cross-wavefront scratch.
+// cross-wavefront scratch. L_arg >= 0 replaces the sequence length and
+// out_row >= 0 the row of e_vals / tile_part (the chunked prefill scores
+// every query of a chunk, each with its own length, from one load of a tile).
 template <int G, int D, bool CO>
 __device__ __forceinline__ void score_tile(const Dims& m, const int32_t* __restrict__ seq_lens,
                                            int first_order, int t, const TileBuf<D / 16>& buf,
                                            const float (*sco)[2 * G * 32],
                                            double (*s_part)[G][2], float* __restrict__ e_vals,
-                                           double* __restrict__ tile_part) {
+                                           double* __restrict__ tile_part, int L_arg = -1,
+                                           int out_row = -1) {
   constexpr int NJ = D / 16;
   constexpr int U = (G + 3) / 4;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int qt = lane >> 4;
   const int bh = t / m.n_tiles, tile = t % m.n_tiles;
   const int blk = tile * kTileBlocks + kScoreGroup * w + (lane & 15);
-  const int L = seq_lens[bh / m.hkv];
+  const int L = L_arg >= 0 ? L_arg : seq_lens[bh / m.hkv];
+  const int orow = out_row >= 0 ? out_row : bh;
   const int nb = (L + m.us - 1) / m.us;  // units (blocks or windows) present
   // this lane's coefficients: cf[k] holds entry 16 k + (lane % 16) of its
   // quarter's table, read once per tile
@@ -210,7 +214,7 @@ __device__ __forceinline__ void score_tile(const Dims& m, const int32_t* __restr
   const float rcp_n = __builtin_amdgcn_rcpf((float)n_i);
   const double ln_n = (double)(__builtin_amdgcn_logf((float)n_i) * kLn2f);
   const int nbp = m.n_tiles * kTileBlocks;
-  float* ev = e_vals + (int64_t)bh * G * nbp;
+  float* ev = e_vals + (int64_t)orow * G * nbp;
   double ell[U];
 #pragma unroll
   for (int u = 0; u < U; ++u) {
@@ -253,7 +257,7 @@ __device__ __forceinline__ void score_tile(const Dims& m, const int32_t* __restr
       mx = fmax(mx, s_part[x][tid][0]);
       sum += s_part[x][tid][1];
     }
-    double* tp = tile_part + (((int64_t)bh * G + tid) * m.n_tiles + tile) * 2;
+    double* tp = tile_part + (((int64_t)orow * G + tid) * m.n_tiles + tile) * 2;
     Mem<CO>::st(tp, mx);
     Mem<CO>::st(tp + 1, sum);
   }

@@ -90,11 +90,17 @@ __device__ __forceinline__ void load_vec(const float* base, uint32_t off, float 
 // one record per lane; every load of a batch (and the gain row) is issued
 // before any arithmetic. CO: the records are read with Mem<true> (written
 // by other workgroups of the same launch).
-template <typename T, int D, bool CO>
+// ADD: the records carry no share of the global term (the chunked prefill
+// computes o_bar and <phi(q), z_bar> for every query in a kernel of its own);
+// obar_add (this query's G x D rows) and zq_add (its G values) are added to
+// the sums of the records' linear fields instead.
+template <typename T, int D, bool CO, bool ADD = false>
 __device__ __forceinline__ void merge_head(const Dims& m, float eps, uint32_t flags,
                                            const float* __restrict__ gamma, int all_sel, int L,
                                            const float* rec, int n_rec, int stride,
-                                           T* __restrict__ out, int bh, int g) {
+                                           T* __restrict__ out, int bh, int g,
+                                           const float* __restrict__ obar_add = nullptr,
+                                           const float* __restrict__ zq_add = nullptr) {
   constexpr int E = D / 32;  // coordinates per lane
   constexpr int NP = 8;      // record pairs per load batch
   const int b = bh / m.hkv, h = bh % m.hkv;
@@ -110,6 +116,10 @@ __device__ __forceinline__ void merge_head(const Dims& m, float eps, uint32_t fl
   float osp[E], ot[E];
 #pragma unroll
   for (int e = 0; e < E; ++e) osp[e] = ot[e] = 0.f;
+  if constexpr (ADD) {  // once per coordinate: the halves are added at the end
+#pragma unroll
+    for (int e = 0; e < E; ++e) ot[e] = hf ? 0.f : obar_add[g * D + c0 + e];
+  }
   for (int x0 = 0; x0 < n_rec; x0 += 64) {
     // headers: lane u holds record x0 + u
     const bool hv = x0 + lane < n_rec;
@@ -163,6 +173,7 @@ __device__ __forceinline__ void merge_head(const Dims& m, float eps, uint32_t fl
     osp[e] += xor32(osp[e]);
     ot[e] += xor32(ot[e]);
   }
+  if constexpr (ADD) zt += zq_add[g];
   float o[E];
   if (L == 0) {
 #pragma unroll
@@ -232,7 +243,9 @@ struct SparseRegs {
 // are zero. The four lanes of a column (g = 0..3) hold all d coordinates of
 // its head, so the softmax of phi(q) needs only the two lane swaps. Also
 // issues the loads of this workgroup's rows of S_bar and z_bar (x of n_wg).
-template <int D, int GC>
+// LIN = false: no share of the global term (no S_bar rows are loaded; ob and
+// zq stay zero), for the chunked prefill.
+template <int D, int GC, bool LIN = true>
 __device__ __forceinline__ void sparse_prologue(const Dims& m, const bf16_t* __restrict__ q,
                                                 const float* __restrict__ S,
                                                 const float* __restrict__ zbar, int bh, int x,
@@ -250,7 +263,12 @@ __device__ __forceinline__ void sparse_prologue(const Dims& m, const bf16_t* __r
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks) raw[ks] = *reinterpret_cast<const uint4*>(qrow + 32 * ks);
   lin_rows(D, x, n_wg, &r.row0, &r.nrows);
-  {
+  if constexpr (!LIN) {
+#pragma unroll
+    for (int u = 0; u < kSparsePre; ++u) r.spre[u] = 0.f;
+    r.zbv = 0.f;
+    r.nrows = 0;
+  } else {
     // loads issued whether or not in range (from row 0 when not): no branch
     const bool s_pre = r.nrows * D <= kSparsePre * 256;
     const float* Sh = S + (int64_t)bh * D * D;
@@ -262,7 +280,7 @@ __device__ __forceinline__ void sparse_prologue(const Dims& m, const bf16_t* __r
       r.spre[u] = ok ? v : 0.f;
     }
   }
-  {
+  if constexpr (LIN) {
     const bool ok = tid < r.nrows;
     const float v = zbar[(int64_t)bh * D + (ok ? r.row0 + tid : 0)];
     r.zbv = ok ? v : 0.f;
@@ -326,9 +344,16 @@ __device__ __forceinline__ void sparse_prologue(const Dims& m, const bf16_t* __r
 // This workgroup's rows x of the global linear term (Eq. 15): ob and zq of r,
 // from the S_bar rows of r and phi(q) (LDS). Needs nothing from the
 // selection, so it runs while the workgroup would otherwise wait for it.
-template <int D, int GC>
+template <int D, int GC, bool LIN = true>
 __device__ __forceinline__ void sparse_linear(const Dims& m, const float* __restrict__ S, int bh,
                                               SparseRegs& r, SparseSmem<D, GC>& sm) {
+  if constexpr (!LIN) {
+    __syncthreads();  // the query operands and phi(q) are in LDS
+#pragma unroll
+    for (int i = 0; i < 4; ++i) r.ob[i] = 0.f;
+    r.zq = 0.f;
+    return;
+  }
   constexpr int NO = (GC * D + 255) / 256;  // outputs (head, coordinate) per thread
   constexpr int RMAX = kSparsePre * 256 / D;  // rows held in LDS
   static_assert(NO <= 4, "ob holds four outputs");
@@ -398,7 +423,8 @@ __device__ __forceinline__ void sparse_body(const Dims& m, float s,
                                             int bh, int x, int n_wg, const SparseRegs& r,
                                             SparseSmem<D, GC>& sm, float* __restrict__ part,
                                             int stride,
-                                            const int32_t* __restrict__ table = nullptr) {
+                                            const int32_t* __restrict__ table = nullptr,
+                                            int64_t rec_row = -1) {
   constexpr int KS = D / 32;     // k-steps of the first product
   constexpr int MT = D / 16;     // coordinate tiles of the second product
   constexpr int CPB = BLK / 32;  // steps per block
@@ -538,7 +564,9 @@ __device__ __forceinline__ void sparse_body(const Dims& m, float s,
     sm.l[w][lane] = l_run;
   }
   __syncthreads();
-  float* rec = part + ((int64_t)bh * n_wg + x) * stride;
+  // the record of workgroup x: row bh of the records, or rec_row (the
+  // chunked prefill keeps one row per (sequence, KV head, position))
+  float* rec = part + ((rec_row >= 0 ? rec_row : (int64_t)bh) * n_wg + x) * stride;
 #pragma unroll
   for (int i = 0; i < NO; ++i) {
     const int e = tid + 256 * i;

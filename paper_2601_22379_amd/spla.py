@@ -30,12 +30,12 @@ STATUS = {0: "ok", -1: "invalid argument", -2: "unsupported shape",
           -5: "HIP runtime error"}
 
 # every symbol include/spla.h declares
-EXPORTS = ["spla_status_string", "spla_phase_name", "spla_validate", "spla_cache_bytes",
-           "spla_workspace_bytes", "spla_append_workspace_bytes", "spla_decode_phase_mask",
-           "spla_workspace_init", "spla_reset", "spla_append",
-           "spla_decode", "spla_decode_ex", "spla_step", "spla_step_ex", "spla_prefill",
-           "spla_decode_noalloc"]
-HOST_EXPORTS = EXPORTS[:7]
+HOST_EXPORTS = ["spla_status_string", "spla_phase_name", "spla_validate", "spla_cache_bytes",
+                "spla_workspace_bytes", "spla_append_workspace_bytes", "spla_decode_phase_mask",
+                "spla_prefill_workspace_bytes"]
+EXPORTS = HOST_EXPORTS + ["spla_workspace_init", "spla_reset", "spla_append", "spla_decode",
+                          "spla_decode_ex", "spla_step", "spla_step_ex", "spla_prefill",
+                          "spla_decode_noalloc"]
 
 
 class SplaError(RuntimeError):
@@ -80,6 +80,8 @@ def _declare(lib, host_only=False):
     lib.spla_append_workspace_bytes.argtypes = [cfgp, c_int32, POINTER(c_size_t)]
     lib.spla_decode_phase_mask.restype = c_int32
     lib.spla_decode_phase_mask.argtypes = [cfgp, POINTER(c_uint32)]
+    lib.spla_prefill_workspace_bytes.restype = c_int32
+    lib.spla_prefill_workspace_bytes.argtypes = [cfgp, c_int32, POINTER(c_size_t)]
     if host_only:
         return lib
     lib.spla_workspace_init.restype = c_int32
@@ -175,6 +177,14 @@ def append_workspace_bytes(cfg: SplaConfig, max_new: int, library=None) -> int:
     return int(n.value)
 
 
+def prefill_workspace_bytes(cfg: SplaConfig, n_tokens: int, library=None) -> int:
+    n = c_size_t(0)
+    _check((library or lib()).spla_prefill_workspace_bytes(ctypes.byref(cfg), int(n_tokens),
+                                                           ctypes.byref(n)),
+           "spla_prefill_workspace_bytes")
+    return int(n.value)
+
+
 def decode_phases(cfg: SplaConfig, library=None) -> list:
     """Names of the phases whose events spla_decode_ex records for cfg."""
     mask = c_uint32(0)
@@ -233,6 +243,7 @@ class SplaCache:
                                          self.workspace.numel(), _stream(self.device)),
                "spla_workspace_init")
         self._append_ws = None
+        self._prefill_ws = None
         self._struct = SplaCacheStruct(self.k.data_ptr(), self.v.data_ptr(),
                                        self.stats.data_ptr(), self.state.data_ptr(),
                                        self.norm.data_ptr(), self.seq_lens.data_ptr(),
@@ -353,9 +364,13 @@ class SplaCache:
         if sel is None:
             sel = torch.empty((T, c.batch, c.n_kv_heads, c.top_k), dtype=torch.int32,
                               device=self.device)
+        need = prefill_workspace_bytes(c, T)
+        if self._prefill_ws is None or self._prefill_ws.numel() < need:
+            self._prefill_ws = _aligned_workspace(need, self.device)
+        ws = self._prefill_ws
         _check(lib().spla_prefill(ctypes.byref(c), ctypes.byref(self._struct), int(T),
                                   _ptr(k_new), _ptr(v_new), _ptr(q), _ptr(gamma), _ptr(out),
-                                  _ptr(sel), _ptr(self.workspace), self.workspace.numel(),
+                                  _ptr(sel), _ptr(ws), ws.numel(),
                                   _stream(self.device)), "spla_prefill")
         return out, sel
 
