@@ -217,18 +217,21 @@ def strided_leg(w, R, dev, qs, gamma, outs, sels, K, W, C=32, s=16, paged=False)
                                                else "per-launch events")}}
 
 
-def prefill_leg(w, dev, K, T=16):
+def prefill_leg(w, dev, K, T=32):
     """Causal prefill (spla_prefill) of T tokens per sequence at the
-    workload's context: the cache is filled to capacity - T (K + 1) tokens,
-    then K timed calls each append and decode T positions. Returns a dict for
-    the JSON line (per-token latency over the whole batch)."""
+    workload's context: the cache is filled to capacity - T (2 K + 1) tokens,
+    then K timed calls each prefill T positions (one chunk of the chunked
+    kernels for bf16, G <= 8). Returns a dict for the JSON line: latency per
+    call and per position, tokens per second over the whole batch, and the
+    bytes the chunk's kernels must move (the statistics once per chunk, every
+    query's selected K/V rows, S_bar read and written, the new rows)."""
     import numpy as np
     import torch
 
     from paper_2601_22379_amd import spla
     import spla_inputs as si
 
-    lens = [w.capacity - T * (K + 1)] * w.batch
+    lens = [w.capacity - T * (2 * K + 1)] * w.batch  # room for every call below
     cfg = spla.make_config(w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, w.block_size,
                            w.top_k, w.capacity, w.dtype, n_sink=w.n_sink, n_local=w.n_local)
     cache = spla.SplaCache(cfg, dev)
@@ -255,12 +258,48 @@ def prefill_leg(w, dev, K, T=16):
     b.record()
     torch.cuda.synchronize()
     us = a.elapsed_time(b) / K * 1e3
-    assert cache.err.item() == 0
-    log(f"prefill: {T} positions in {us:.1f} us ({us / T:.2f} us per position) at "
-        f"{lens[0]}..{lens[0] + T * (K + 1)} tokens")
+    # the same calls with every phase bracketed by events (recorded by the
+    # library on its stream): the split between the chunk's kernels
+    names = ["append", "linear", "score", "select", "sparse", "merge"]
+    evs = [spla.make_events(names) for _ in range(K)]
+    torch.cuda.synchronize()
+    for i in range(K):
+        cache.prefill(kn, vn, q, gamma, out, sel, events=evs[i][0])
+    torch.cuda.synchronize()
+    phases = {n: float(np.mean([e[1][n][0].elapsed_time(e[1][n][1]) for e in evs])) * 1e3
+              for n in names}
+    assert cache.device_errors() == 0
+    e = 4 if w.dtype == "f32" else 2
+    d, B = w.head_dim, w.block_size
+    L_end = int(cache.seq_lens[0].item())
+    nb = -(-L_end // B)
+    sel_np = sel.cpu().numpy()
+    sel_tok = int(sum(min(B, L_end - int(i) * B) for i in sel_np.reshape(-1) if i >= 0))
+    bh = w.batch * w.n_kv_heads
+    ab = {"stats": bh * nb * 2 * d * 4, "selected_kv_all_queries": sel_tok * d * 2 * e,
+          "state_rw": 2 * bh * (d * d + d) * 4, "new_rows": bh * T * 2 * d * e,
+          "q_out": 2 * T * w.batch * w.n_q_heads * d * e}
+    ab["total"] = sum(ab.values())
+    tok_s = w.batch * T / (us * 1e-6)
+    # dominant kernel: the per-query fused sparse pass, whose bytes are every
+    # query's selected K/V rows plus its query rows
+    sp_bytes = ab["selected_kv_all_queries"] + T * w.batch * w.n_q_heads * d * e
+    sp_ach = sp_bytes / (phases["sparse"] * 1e-6) / 1e9
+    log(f"prefill: {T} positions in {us:.1f} us ({us / T:.2f} us per position, "
+        f"{tok_s / 1e6:.2f} M tokens/s) from {lens[0]} tokens; phases us: "
+        + ", ".join(f"{k}={v:.1f}" for k, v in phases.items()))
     return {"tokens_per_call": T, "calls": K, "context_start": lens[0],
             "latency_us_per_call": round(us, 2), "latency_us_per_position": round(us / T, 3),
-            "method": "append + decode per position (spla_prefill)"}
+            "tokens_per_s": round(tok_s, 1), "algorithmic_bytes_per_call": ab,
+            "achieved_GBs_per_call": round(ab["total"] / (us * 1e-6) / 1e9, 1),
+            "phases_us": {k: round(v, 2) for k, v in phases.items()},
+            "roofline": {"kernel": "prefill_sparse", "bound": "hbm", "achieved": round(sp_ach, 1),
+                         "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                         "frac": round(sp_ach / PEAK_HBM_GBS, 4),
+                         "algorithmic_bytes_per_launch": sp_bytes,
+                         "avg_launch_us": round(phases["sparse"], 3),
+                         "avg_launch_method": "per-launch events"},
+            "method": "chunked prefill (spla_prefill, one chunk of T positions per call)"}
 
 
 def cpu_baseline(w, seconds, n_units=8):
@@ -698,6 +737,8 @@ def main():
                     help="skip the strided-selection (C = 32, s = 16), paged-KV and prefill legs")
     ap.add_argument("--strided-only", action="store_true",
                     help="run only the strided-selection leg and print its JSON (profiling)")
+    ap.add_argument("--prefill-only", action="store_true",
+                    help="run only the prefill leg and print its JSON (profiling)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB copy kernel (for counter scaling)")
     ap.add_argument("--trace-summary", metavar="DIR",
@@ -757,6 +798,9 @@ def main():
         if args.copy_calibration:
             copy_calibration(dev)
         print(json.dumps(line), flush=True)
+        return
+    if args.prefill_only:
+        print(json.dumps(prefill_leg(w, dev, K=K)), flush=True)
         return
     wall0 = time.perf_counter()
     head, extras = run_workload(w, replicas_for(w, R), dev, K, W, headline=True,

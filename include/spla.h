@@ -191,13 +191,19 @@ enum {
                             with the rows of o_bar = phi(q) S_bar split over its workgroups */
   SPLA_PHASE_MERGE = 4,  /* merge of that pass, residual, RMSNorm, output */
   SPLA_PHASE_DECODE = 5, /* the single-launch decode kernel (all of phases 1-4) */
+  SPLA_PHASE_LINEAR = 6, /* chunked prefill: the chunkwise linear-attention kernel
+                            (o_bar of every query, S_bar and z_bar past the chunk) */
   SPLA_NUM_PHASES = 8
 };
 
 /* Optional timing hooks: each non-NULL start[p] / stop[p] (a hipEvent_t) is
  * recorded on the call's stream right before / after the launch(es) of phase
  * p. The phases a call records are given by spla_decode_phase_mask (plus
- * SPLA_PHASE_APPEND for spla_step_ex); the others record nothing. */
+ * SPLA_PHASE_APPEND for spla_step_ex); the others record nothing. The chunked
+ * prefill (spla_prefill_ex) records APPEND (the running unit statistics and
+ * the rows and statistics of the chunk), LINEAR, SCORE, SELECT,
+ * SPARSE and MERGE for every chunk, so with several chunks the events end up
+ * bracketing the last one. */
 typedef struct spla_events {
   void* start[SPLA_NUM_PHASES];
   void* stop[SPLA_NUM_PHASES];
@@ -344,6 +350,13 @@ int32_t spla_prefill(const spla_config* cfg, const spla_cache* cache, int32_t n_
                      const void* k_new, const void* v_new, const void* q,
                      const float* rms_weight, void* out, int32_t* sel_idx, void* workspace,
                      size_t workspace_bytes, void* stream);
+
+/* spla_prefill with optional timing events (events may be NULL; recorded by
+ * the chunked shapes only). */
+int32_t spla_prefill_ex(const spla_config* cfg, const spla_cache* cache, int32_t n_tokens,
+                        const void* k_new, const void* v_new, const void* q,
+                        const float* rms_weight, void* out, int32_t* sel_idx, void* workspace,
+                        size_t workspace_bytes, const spla_events* events, void* stream);
 
 /* spla_step with optional timing events (events may be NULL). */
 int32_t spla_step_ex(const spla_config* cfg, const spla_cache* cache, const void* k_new,

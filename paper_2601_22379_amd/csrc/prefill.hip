@@ -10,11 +10,11 @@
 //
 //   prefill_unit_stats_kernel  running (mean, M2) of the units the chunk
 //                              touches, after each of its positions
+//   (append_blocks_kernel)     the chunk's K/V rows and unit statistics
 //   prefill_linear_kernel      o_bar = phi(Q) S_bar(before the chunk) plus the
 //                              causally masked phi(Q) phi(K)^T V inside the
 //                              chunk, on matrix-core tiles; then S_bar and
 //                              z_bar carried past the chunk
-//   (append_blocks_kernel)     the chunk's K/V rows and unit statistics
 //   prefill_score_kernel       every query's block scores; each statistics
 //                              tile is loaded once for the chunk's queries
 //   prefill_select_kernel      every query's top-k
@@ -71,10 +71,16 @@ __global__ __launch_bounds__(128) void prefill_unit_stats_kernel(
     m2 = stats[stats_off4(m, bh, u, 1, j / 4) + (j & 3)];
   }
   float* out = ustat + ((int64_t)bh * nu_touch + ur) * T_ * 2 * m.d + j;
-  for (int i = 0; i < T_; ++i) {
+  float xs[kPrefillChunk];  // the chunk's values of coordinate j, all loads issued first
+#pragma unroll
+  for (int i = 0; i < kPrefillChunk; ++i)
+    xs[i] = Elem<T>::load(k_new, ((int64_t)min(i, T_ - 1) * m.bh + bh) * m.d + j);
+#pragma unroll
+  for (int i = 0; i < kPrefillChunk; ++i) {
+    if (i >= T_) break;
     const int64_t t = (int64_t)L0 + i;
     if (i < nv && t >= u0 && t < u1) {
-      const double x = (double)Elem<T>::load(k_new, ((int64_t)i * m.bh + bh) * m.d + j);
+      const double x = (double)xs[i];
       n += 1.0;
       const double delta = x - mean;
       mean += delta / n;
@@ -151,22 +157,29 @@ __global__ __launch_bounds__(kPrefSelThreads) void prefill_select_kernel(
 // ------------------------------------------------------ fused sparse pass
 // As the decode's pass, per query: its G heads' operands from its row of q,
 // its selection, its length; no share of the global term.
+// Workgroups are handed to the eight XCDs round-robin by index, each XCD
+// with its own L2: the item of workgroup p is (p % 8) * (n / 8) + p / 8, so
+// that consecutive items (the queries of one sequence x KV head, which
+// largely select the same blocks) share an XCD and its L2. n_wg workgroups
+// per query; the grid is n items rounded up to a multiple of 8.
 template <int D, int BLK>
 __global__ __launch_bounds__(256) void prefill_sparse_kernel(
     Dims m, int T_, float s, const bf16_t* __restrict__ kc, const bf16_t* __restrict__ vc,
     const bf16_t* __restrict__ q, const int32_t* __restrict__ sel,
     const int32_t* __restrict__ meta, int stride, float* __restrict__ part,
-    const int32_t* __restrict__ table) {
+    const int32_t* __restrict__ table, int n_wg, int n_items) {
   __shared__ SparseSmem<D, 8> sm;
-  const int x = blockIdx.x, vh = blockIdx.y, bh = vh / T_, i = vh % T_;
+  const int per = (int)(gridDim.x / 8);
+  const int item = ((int)blockIdx.x % 8) * per + (int)blockIdx.x / 8;
+  if (item >= n_items) return;
+  const int x = item % n_wg, vh = item / n_wg, bh = vh / T_, i = vh % T_;
   SparseRegs r;
   sparse_prologue<D, 8, false>(m, q + (int64_t)i * m.batch * m.hq * D, nullptr, nullptr, bh, x,
-                               (int)gridDim.x, r, sm);
+                               n_wg, r, sm);
   sparse_linear<D, 8, false>(m, nullptr, bh, r, sm);
   const int e = sparse_step_entry<BLK>(x);
   sparse_body<D, BLK, false, 8>(m, s, kc, vc, e < m.k ? sel[(int64_t)vh * m.k + e] : -1,
-                                meta[vh * 4 + 2], bh, x, (int)gridDim.x, r, sm, part, stride,
-                                table, vh);
+                                meta[vh * 4 + 2], bh, x, n_wg, r, sm, part, stride, table, vh);
 }
 
 // ---------------------------------------------------------------- merge
@@ -237,16 +250,22 @@ __device__ __forceinline__ float row16_sum(float v) {
   return v;
 }
 
-// phi(x) of one row of D elements (softmax over the features), lane holding
-// elements lane + 64 e; zero when !ok.
+// One row of D elements, lane holding elements lane + 64 e (row 0 when !ok,
+// so that the load is issued either way).
 template <int D>
-__device__ __forceinline__ void phi_row(const bf16_t* __restrict__ src, bool ok, float (&ph)[D / 64]) {
+__device__ __forceinline__ void load_row(const bf16_t* __restrict__ src, float (&x)[D / 64]) {
   const int lane = threadIdx.x & 63;
-  float x[D / 64];
+#pragma unroll
+  for (int e = 0; e < D / 64; ++e) x[e] = bf16_to_f32(src[lane + 64 * e].bits);
+}
+
+// phi(x) of such a row (softmax over the features); zero when !ok.
+template <int D>
+__device__ __forceinline__ void phi_row(float (&x)[D / 64], bool ok, float (&ph)[D / 64]) {
   float mx = -INFINITY;
 #pragma unroll
   for (int e = 0; e < D / 64; ++e) {
-    x[e] = ok ? bf16_to_f32(src[lane + 64 * e].bits) : 0.f;
+    x[e] = ok ? x[e] : 0.f;
     mx = fmaxf(mx, x[e]);
   }
   mx = wave_max(mx);
@@ -278,10 +297,17 @@ __global__ __launch_bounds__(256) void prefill_linear_kernel(
   int L0, nv;
   chunk_bounds(m, seq_lens, b, T_, &L0, &nv);
 
-  // phi(K) of the chunk's keys (rows past nv, or past T, are zero)
-  for (int i = w; i < TP; i += 4) {
+  // phi(K) of the chunk's keys (rows past nv, or past T, are zero); every
+  // row's loads are issued before the first softmax
+  float kx[TP / 4][D / 64];
+#pragma unroll
+  for (int r = 0; r < TP / 4; ++r)
+    load_row<D>(k_new + ((int64_t)min(w + 4 * r, T_ - 1) * m.bh + bh) * D, kx[r]);
+#pragma unroll
+  for (int r = 0; r < TP / 4; ++r) {
+    const int i = w + 4 * r;
     float ph[D / 64];
-    phi_row<D>(k_new + ((int64_t)i * m.bh + bh) * D, i < nv, ph);
+    phi_row<D>(kx[r], i < nv, ph);
 #pragma unroll
     for (int e = 0; e < D / 64; ++e) {
       const int col = lane + 64 * e;
@@ -313,12 +339,20 @@ __global__ __launch_bounds__(256) void prefill_linear_kernel(
   for (int rt0 = 0; rt0 < n_rt; rt0 += 4) {
     const int rt = rt0 + w;
     const bool act = rt < n_rt;
+    float qx[16][D / 64];  // the tile's 16 query rows, all loads issued first
+#pragma unroll
     for (int rr = 0; rr < 16; ++rr) {
       const int row = rt * 16 + rr;
       const bool ok = act && row < R;
       const int i = ok ? row / G : 0, g = ok ? row % G : 0;
+      load_row<D>(q + (((int64_t)i * m.batch + b) * m.hq + h * G + g) * D, qx[rr]);
+    }
+#pragma unroll
+    for (int rr = 0; rr < 16; ++rr) {
+      const int row = rt * 16 + rr;
+      const bool ok = act && row < R;
       float ph[D / 64];
-      phi_row<D>(q + (((int64_t)i * m.batch + b) * m.hq + h * G + g) * D, ok, ph);
+      phi_row<D>(qx[rr], ok, ph);
 #pragma unroll
       for (int e = 0; e < D / 64; ++e)
         split_bf16(ph[e], sm.pq_h[w][rr][lane + 64 * e], sm.pq_l[w][rr][lane + 64 * e]);
@@ -468,12 +502,12 @@ static void prefill_select_r(const Dims& m, int T, const spla_cache& c, int32_t*
 template <int D, int BLK>
 static void prefill_sparse_db(const Dims& m, int T, float s, const spla_cache& c, const void* q,
                               const PrefillWs& ws, char* base, hipStream_t st) {
-  hipLaunchKernelGGL((prefill_sparse_kernel<D, BLK>),
-                     dim3((unsigned)ws.n_wg, (unsigned)((int64_t)m.bh * T)), dim3(256), 0, st, m,
-                     T, s, (const bf16_t*)c.k_cache, (const bf16_t*)c.v_cache, (const bf16_t*)q,
-                     (const int32_t*)(base + ws.sel), (const int32_t*)(base + ws.meta),
-                     ws.part_stride, (float*)(base + ws.part),
-                     m.pages > 0 ? c.block_table : nullptr);
+  const int64_t items = (int64_t)ws.n_wg * m.bh * T;
+  hipLaunchKernelGGL((prefill_sparse_kernel<D, BLK>), dim3((unsigned)align_up(items, 8)),
+                     dim3(256), 0, st, m, T, s, (const bf16_t*)c.k_cache,
+                     (const bf16_t*)c.v_cache, (const bf16_t*)q, (const int32_t*)(base + ws.sel),
+                     (const int32_t*)(base + ws.meta), ws.part_stride, (float*)(base + ws.part),
+                     m.pages > 0 ? c.block_table : nullptr, ws.n_wg, (int)items);
 }
 
 template <int D>
@@ -489,29 +523,37 @@ static void prefill_linear_d(const Dims& m, const spla_cache& c, int T, const vo
 hipError_t launch_prefill_chunk(const Dims& m, const spla_config& cfg, const spla_cache& c,
                                 int T, const void* k_new, const void* v_new, const void* q,
                                 const float* gamma, void* out, int32_t* sel_out,
-                                const PrefillWs& ws, char* base, hipStream_t st) {
+                                const PrefillWs& ws, char* base, const spla_events* ev,
+                                hipStream_t st) {
   if (T < 1 || T > ws.T) return hipErrorInvalidValue;
   const double s_score =
       cfg.softmax_scale > 0.f ? (double)cfg.softmax_scale : 1.0 / sqrt((double)m.d);
   const float s = cfg.softmax_scale > 0.f ? cfg.softmax_scale : (float)(1.0 / sqrt((double)m.d));
   const int fo = (cfg.flags & SPLA_FLAG_FIRST_ORDER) ? 1 : 0;
   hipError_t e;
-  // 1. running statistics of the touched units, from the statistics before the chunk
+  // 1. running statistics of the touched units, from the statistics before the
+  // chunk; then the chunk's K/V rows and the statistics of the units it touches
+  mark_phase(ev, SPLA_PHASE_APPEND, false, st);
   hipLaunchKernelGGL(prefill_unit_stats_kernel<bf16_t>, dim3((unsigned)ws.nu_touch, (unsigned)m.bh),
                      dim3(128), 0, st, m, T, (const float*)c.blk_stats,
                      (const int32_t*)c.seq_lens, (const bf16_t*)k_new, ws.nu_touch,
                      (float*)(base + ws.ustat));
+  if ((e = launch_append_blocks(m, c, k_new, v_new, T, nullptr, st, true)) != hipSuccess) return e;
+  mark_phase(ev, SPLA_PHASE_APPEND, true, st);
   // 2. the global linear term of every query; S_bar and z_bar past the chunk
+  mark_phase(ev, SPLA_PHASE_LINEAR, false, st);
   if (m.d == 64) prefill_linear_d<64>(m, c, T, k_new, v_new, q, ws, base, st);
   else prefill_linear_d<128>(m, c, T, k_new, v_new, q, ws, base, st);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  // 3. the chunk's K/V rows and the statistics of the units it touches
-  if ((e = launch_append_blocks(m, c, k_new, v_new, T, nullptr, st, true)) != hipSuccess) return e;
-  // 4. block scores of every query
+  mark_phase(ev, SPLA_PHASE_LINEAR, true, st);
+  // 3. block scores of every query
+  mark_phase(ev, SPLA_PHASE_SCORE, false, st);
   if (m.d == 64) prefill_score_d<64>(m, T, c, q, s_score, fo, ws, base, st);
   else prefill_score_d<128>(m, T, c, q, s_score, fo, ws, base, st);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  // 5. selection of every query (blocks per thread of a 1024-thread workgroup)
+  mark_phase(ev, SPLA_PHASE_SCORE, true, st);
+  // 4. selection of every query (blocks per thread of a 1024-thread workgroup)
+  mark_phase(ev, SPLA_PHASE_SELECT, false, st);
   const int per = (int)ceil_div(m.nb_cap, kPrefSelThreads);
   if (per <= 1) prefill_select_r<1>(m, T, c, sel_out, ws, base, st);
   else if (per <= 2) prefill_select_r<2>(m, T, c, sel_out, ws, base, st);
@@ -520,7 +562,9 @@ hipError_t launch_prefill_chunk(const Dims& m, const spla_config& cfg, const spl
   else if (per <= 16) prefill_select_r<16>(m, T, c, sel_out, ws, base, st);
   else prefill_select_r<32>(m, T, c, sel_out, ws, base, st);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  // 6. the fused sparse pass of every query
+  mark_phase(ev, SPLA_PHASE_SELECT, true, st);
+  // 5. the fused sparse pass of every query
+  mark_phase(ev, SPLA_PHASE_SPARSE, false, st);
   if (m.d == 64) {
     if (m.B == 32) prefill_sparse_db<64, 32>(m, T, s, c, q, ws, base, st);
     else if (m.B == 64) prefill_sparse_db<64, 64>(m, T, s, c, q, ws, base, st);
@@ -531,7 +575,9 @@ hipError_t launch_prefill_chunk(const Dims& m, const spla_config& cfg, const spl
     else prefill_sparse_db<128, 128>(m, T, s, c, q, ws, base, st);
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  // 7. merge: records + o_bar, residual, RMSNorm, outputs
+  mark_phase(ev, SPLA_PHASE_SPARSE, true, st);
+  // 6. merge: records + o_bar, residual, RMSNorm, outputs
+  mark_phase(ev, SPLA_PHASE_MERGE, false, st);
   const unsigned nq = (unsigned)((int64_t)m.bh * T);
   if (m.d == 64)
     hipLaunchKernelGGL((prefill_merge_kernel<64>), dim3(nq), dim3(64 * m.group), 0, st, m, T,
@@ -546,7 +592,8 @@ hipError_t launch_prefill_chunk(const Dims& m, const spla_config& cfg, const spl
                        (const float*)(base + ws.obar), (const float*)(base + ws.zq),
                        (bf16_t*)out);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  // 8. the sequences' lengths
+  mark_phase(ev, SPLA_PHASE_MERGE, true, st);
+  // 7. the sequences' lengths
   return launch_append_finish(m, c, T, nullptr, st);
 }
 

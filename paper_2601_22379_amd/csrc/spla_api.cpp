@@ -192,10 +192,11 @@ extern "C" int32_t spla_step(const spla_config* cfg, const spla_cache* cache, co
   return spla_step_ex(cfg, cache, k_new, v_new, q, w, out, sel_idx, ws, ws_bytes, nullptr, stream);
 }
 
-extern "C" int32_t spla_prefill(const spla_config* cfg, const spla_cache* cache, int32_t n_tokens,
-                                const void* k_new, const void* v_new, const void* q,
-                                const float* w, void* out, int32_t* sel_idx, void* ws,
-                                size_t ws_bytes, void* stream) {
+extern "C" int32_t spla_prefill_ex(const spla_config* cfg, const spla_cache* cache,
+                                   int32_t n_tokens, const void* k_new, const void* v_new,
+                                   const void* q, const float* w, void* out, int32_t* sel_idx,
+                                   void* ws, size_t ws_bytes, const spla_events* ev,
+                                   void* stream) {
   int32_t s = spla_validate(cfg);
   if (s != SPLA_OK) return s;
   if ((s = check_cache(cfg, cache)) != SPLA_OK) return s;
@@ -225,7 +226,7 @@ extern "C" int32_t spla_prefill(const spla_config* cfg, const spla_cache* cache,
                                           vb + c0 * kv_step, qb + c0 * q_step, w,
                                           ob + c0 * q_step,
                                           sel_idx ? sel_idx + c0 * sel_step : nullptr, L,
-                                          static_cast<char*>(ws), st));
+                                          static_cast<char*>(ws), ev, st));
     }
     return SPLA_OK;
   }
@@ -238,6 +239,14 @@ extern "C" int32_t spla_prefill(const spla_config* cfg, const spla_cache* cache,
       return s;
   }
   return SPLA_OK;
+}
+
+extern "C" int32_t spla_prefill(const spla_config* cfg, const spla_cache* cache, int32_t n_tokens,
+                                const void* k_new, const void* v_new, const void* q,
+                                const float* w, void* out, int32_t* sel_idx, void* ws,
+                                size_t ws_bytes, void* stream) {
+  return spla_prefill_ex(cfg, cache, n_tokens, k_new, v_new, q, w, out, sel_idx, ws, ws_bytes,
+                         nullptr, stream);
 }
 
 // ---- decode without a caller workspace (callers that cannot allocate) ------

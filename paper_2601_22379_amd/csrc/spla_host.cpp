@@ -28,6 +28,7 @@ extern "C" const char* spla_phase_name(int32_t p) {
     case SPLA_PHASE_SPARSE: return "sparse";
     case SPLA_PHASE_MERGE: return "merge";
     case SPLA_PHASE_DECODE: return "decode";
+    case SPLA_PHASE_LINEAR: return "linear";
     default: return nullptr;
   }
 }

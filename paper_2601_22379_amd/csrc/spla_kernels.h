@@ -11,6 +11,13 @@ namespace spla {
 // Compute units of the current device (queried once).
 int compute_units();
 
+// Records the start (stop = false) or stop event of phase p, if given.
+inline void mark_phase(const spla_events* ev, int p, bool stop, hipStream_t st) {
+  if (!ev) return;
+  void* e = stop ? ev->stop[p] : ev->start[p];
+  if (e) hipEventRecord((hipEvent_t)e, st);
+}
+
 // append.hip
 // position_major: the new rows are [max_new][batch][Hkv][d] instead of
 // [batch][Hkv][max_new][d]
@@ -52,7 +59,8 @@ hipError_t launch_merge(const Dims& m, const spla_config& cfg, const float* rms_
 hipError_t launch_prefill_chunk(const Dims& m, const spla_config& cfg, const spla_cache& c,
                                 int T, const void* k_new, const void* v_new, const void* q,
                                 const float* rms_weight, void* out, int32_t* sel_out,
-                                const PrefillWs& ws, char* wsbase, hipStream_t st);
+                                const PrefillWs& ws, char* wsbase, const spla_events* ev,
+                                hipStream_t st);
 
 // decode.hip: the single-launch decode (use_fused_decode shapes)
 hipError_t launch_decode_fused(const Dims& m, const spla_config& cfg, const spla_cache& c,

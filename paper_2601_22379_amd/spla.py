@@ -23,7 +23,8 @@ F32, BF16 = 0, 1
 FLAG_NO_RLA, FLAG_FIRST_ORDER, FLAG_RLA_NORMALIZE, FLAG_SEPARATE_KERNELS = 1, 2, 4, 8
 DEVERR_CAPACITY, DEVERR_SYNC, DEVERR_PAGE = 1, 2, 4
 MAX_GROUP, MAX_TOP_K, MAX_BLOCKS, WORKSPACE_ALIGN = 16, 256, 32768, 256
-PHASES = {"append": 0, "score": 1, "select": 2, "sparse": 3, "merge": 4, "decode": 5}
+PHASES = {"append": 0, "score": 1, "select": 2, "sparse": 3, "merge": 4, "decode": 5,
+          "linear": 6}
 NUM_PHASES = 8
 STATUS = {0: "ok", -1: "invalid argument", -2: "unsupported shape",
           -3: "capacity or library limit exceeded", -4: "workspace missing, too small or misaligned",
@@ -35,7 +36,7 @@ HOST_EXPORTS = ["spla_status_string", "spla_phase_name", "spla_validate", "spla_
                 "spla_prefill_workspace_bytes"]
 EXPORTS = HOST_EXPORTS + ["spla_workspace_init", "spla_reset", "spla_append", "spla_decode",
                           "spla_decode_ex", "spla_step", "spla_step_ex", "spla_prefill",
-                          "spla_decode_noalloc"]
+                          "spla_prefill_ex", "spla_decode_noalloc"]
 
 
 class SplaError(RuntimeError):
@@ -103,6 +104,10 @@ def _declare(lib, host_only=False):
     lib.spla_step_ex.restype = c_int32
     lib.spla_step_ex.argtypes = [cfgp, cachep, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
                                  c_void_p, c_void_p, c_size_t, POINTER(SplaEvents), c_void_p]
+    lib.spla_prefill_ex.restype = c_int32
+    lib.spla_prefill_ex.argtypes = [cfgp, cachep, c_int32, c_void_p, c_void_p, c_void_p,
+                                    c_void_p, c_void_p, c_void_p, c_void_p, c_size_t,
+                                    POINTER(SplaEvents), c_void_p]
     lib.spla_decode_noalloc.restype = c_int32
     lib.spla_decode_noalloc.argtypes = [cfgp, cachep, c_void_p, c_void_p, c_void_p, c_void_p,
                                         c_void_p]
@@ -347,7 +352,7 @@ class SplaCache:
                                   _stream(self.device)), "spla_step")
         return out, sel
 
-    def prefill(self, k_new, v_new, q, gamma, out=None, sel=None):
+    def prefill(self, k_new, v_new, q, gamma, out=None, sel=None, events=None):
         """Causal prefill of T tokens per sequence: k_new, v_new [T, batch,
         Hkv, d], q [T, batch, Hq, d] (cache dtype) -> out [T, batch, Hq, d],
         sel [T, batch, Hkv, top_k]; position t is appended, then decoded."""
@@ -368,10 +373,11 @@ class SplaCache:
         if self._prefill_ws is None or self._prefill_ws.numel() < need:
             self._prefill_ws = _aligned_workspace(need, self.device)
         ws = self._prefill_ws
-        _check(lib().spla_prefill(ctypes.byref(c), ctypes.byref(self._struct), int(T),
-                                  _ptr(k_new), _ptr(v_new), _ptr(q), _ptr(gamma), _ptr(out),
-                                  _ptr(sel), _ptr(ws), ws.numel(),
-                                  _stream(self.device)), "spla_prefill")
+        ev = None if events is None else ctypes.byref(events)
+        _check(lib().spla_prefill_ex(ctypes.byref(c), ctypes.byref(self._struct), int(T),
+                                     _ptr(k_new), _ptr(v_new), _ptr(q), _ptr(gamma), _ptr(out),
+                                     _ptr(sel), _ptr(ws), ws.numel(), ev,
+                                     _stream(self.device)), "spla_prefill")
         return out, sel
 
     # ---- layout views (for checks; pure indexing) ----
