@@ -302,6 +302,57 @@ def prefill_leg(w, dev, K, T=32):
             "method": "chunked prefill (spla_prefill, one chunk of T positions per call)"}
 
 
+def append_leg(w, dev, K, T=16384):
+    """Bulk append (spla_append) of T tokens per (sequence, KV head) into an
+    empty cache of the workload's shape: K calls, each after spla_reset
+    (outside the timed events). Returns a dict for the JSON line: latency per
+    call, tokens per second, and the bytes the append must move (the new K
+    and V rows read and written into the cache, the block statistics
+    written, S_bar and z_bar read and written)."""
+    import numpy as np
+    import torch
+
+    from paper_2601_22379_amd import spla
+    import spla_inputs as si
+
+    T = min(T, w.capacity)
+    cfg = spla.make_config(w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, w.block_size,
+                           w.top_k, w.capacity, w.dtype, n_sink=w.n_sink, n_local=w.n_local)
+    cache = spla.SplaCache(cfg, dev)
+    dt = torch.float32 if w.dtype == "f32" else torch.bfloat16
+    lens = [T] * w.batch
+    Kt, Vt, n = si.gen_kv_slab(w, 0, T, lengths=lens, threads=16)
+    kd = torch.from_numpy(Kt).to(dt).to(dev)
+    vd = torch.from_numpy(Vt).to(dt).to(dev)
+    del Kt, Vt
+    times = []
+    for i in range(K + 1):
+        cache.reset()
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record()
+        cache.append(kd, vd)
+        b.record()
+        torch.cuda.synchronize()
+        if i > 0:
+            times.append(a.elapsed_time(b) * 1e3)
+    assert cache.device_errors() == 0
+    us = float(np.median(times))
+    e = 4 if w.dtype == "f32" else 2
+    bh, d = w.batch * w.n_kv_heads, w.head_dim
+    nb = -(-T // w.block_size)
+    ab = {"kv_read": bh * T * 2 * d * e, "kv_written": bh * T * 2 * d * e,
+          "stats_written": bh * nb * 2 * d * 4, "state_rw": 2 * bh * (d * d + d) * 4}
+    ab["total"] = sum(ab.values())
+    ach = ab["total"] / (us * 1e-6) / 1e9
+    log(f"append: {T} tokens per (sequence, KV head) in {us:.1f} us "
+        f"({bh * T / (us * 1e-6) / 1e9:.2f} G token-rows/s, {ach:.0f} GB/s algorithmic)")
+    return {"tokens_per_sequence": T, "calls": K, "latency_us_median": round(us, 2),
+            "token_rows_per_s": round(bh * T / (us * 1e-6), 1), "algorithmic_bytes": ab,
+            "achieved_GBs": round(ach, 1), "frac_of_peak_hbm": round(ach / PEAK_HBM_GBS, 4),
+            "method": "spla_append into an empty cache (events around the call)"}
+
+
 def cpu_baseline(w, seconds, n_units=8):
     """The fp64 oracle's decode on a bounded sample of the workload: n_units
     (sequence, KV head) units with their state prebuilt (untimed), decoded
@@ -739,6 +790,8 @@ def main():
                     help="run only the strided-selection leg and print its JSON (profiling)")
     ap.add_argument("--prefill-only", action="store_true",
                     help="run only the prefill leg and print its JSON (profiling)")
+    ap.add_argument("--append-only", action="store_true",
+                    help="run only the bulk-append leg and print its JSON (profiling)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB copy kernel (for counter scaling)")
     ap.add_argument("--trace-summary", metavar="DIR",
@@ -802,10 +855,13 @@ def main():
     if args.prefill_only:
         print(json.dumps(prefill_leg(w, dev, K=K)), flush=True)
         return
+    if args.append_only:
+        print(json.dumps(append_leg(w, dev, K=min(K, 20))), flush=True)
+        return
     wall0 = time.perf_counter()
     head, extras = run_workload(w, replicas_for(w, R), dev, K, W, headline=True,
                                 no_graph=args.no_graph)
-    strided = paged = prefill = None
+    strided = paged = prefill = append = None
     if w.appends_per_step == 0 and not args.no_strided:
         qs = torch.from_numpy(si.gen_q_batch(w)[None]).to(dt).to(dev)
         gamma = torch.from_numpy(si.gen_gamma(w)).to(dev)
@@ -817,6 +873,8 @@ def main():
         paged = strided_leg(w, R, dev, qs, gamma, outs, sels, K, W, C=w.block_size,
                             s=w.block_size, paged=True)
         prefill = prefill_leg(w, dev, K=20)
+        torch.cuda.empty_cache()
+        append = append_leg(w, dev, K=10)
         torch.cuda.empty_cache()
     legs = {}
     for cid in [c for c in args.legs.split(",") if c.strip() and c.strip() != args.config]:
@@ -862,6 +920,7 @@ def main():
         "strided_selection": strided,
         "paged_kv": paged,
         "prefill": prefill,
+        "append": append,
         "bench_wall_s": round(time.perf_counter() - wall0, 1),
     }
     print(json.dumps(line), flush=True)

@@ -97,14 +97,159 @@ __device__ __forceinline__ void append_unit(
   stats[o_m2] = (float)m2;
 }
 
+// Bulk form of append_unit: 256 threads per unit. Thread (token lane tl,
+// coordinate group cq) moves VEC = 16 / element-size coordinates of a row as
+// one 16-byte access; with NQ = d / VEC groups there are TS = 256 / NQ token
+// lanes, and lane tl takes the unit's tokens tl, tl + TS, ... . Key rows go
+// to the cache as they are (a 16-byte piece of a row is one piece of the
+// cache layout); value rows are staged in LDS and written out as the pieces
+// of the cache layout (8 tokens of one coordinate for bf16, 4 for fp32);
+// pieces not wholly inside the rows this unit copies are written element by
+// element. Statistics as in append_unit: two passes in fp64 over the new
+// tokens (partial sums of the token lanes added in a fixed order), Chan's
+// combination with the stored ones, rounded to fp32.
+constexpr int kAppendUnitRows = 128;  // rows a unit copies at most (us <= B <= 128)
+
 template <typename T>
-__global__ __launch_bounds__(128) void append_blocks_kernel(
+__global__ __launch_bounds__(256) void append_blocks_kernel(
     Dims m, T* __restrict__ kc, T* __restrict__ vc, float* __restrict__ stats,
     const int32_t* __restrict__ seq_lens, int32_t* __restrict__ err, const T* __restrict__ k_new,
     const T* __restrict__ v_new, int max_new, const int32_t* __restrict__ n_new,
     const int32_t* __restrict__ table, int64_t s_bh, int64_t s_row) {
-  append_unit<T>(m, kc, vc, stats, seq_lens, err, k_new, v_new, max_new, n_new, table,
-                 (int)blockIdx.x, (int)blockIdx.y, s_bh, s_row);
+  constexpr int VEC = 16 / (int)sizeof(T);
+  __shared__ double part[256 * VEC];
+  __shared__ double smean[128];
+  __shared__ __align__(16) T sV[kAppendUnitRows * 128];
+  const int ux = (int)blockIdx.x, bh = (int)blockIdx.y;
+  const int b = bh / m.hkv;
+  const int L0 = seq_lens[b];
+  bool clipped;
+  const int ne = appended_count(m, L0, max_new, n_new, b, &clipped);
+  if (clipped && err && ux == 0 && bh % m.hkv == 0 && threadIdx.x == 0)
+    atomicOr(err, (int)SPLA_DEVERR_CAPACITY);
+  const int first = L0 >= m.ul ? (L0 - m.ul) / m.us + 1 : 0;
+  const int i = first + ux;
+  const int t_lo = max(L0, i * m.us);
+  const int t_hi = min(L0 + ne, i * m.us + m.ul);
+  const int t_own = min(t_hi, (i + 1) * m.us);  // rows this unit copies: t_lo .. t_own - 1
+  if (t_hi <= t_lo) return;  // uniform over the workgroup
+  const int d = m.d, NQ = d / VEC, TS = 256 / NQ;
+  const int tid = (int)threadIdx.x, cq = tid % NQ, tl = tid / NQ, c0 = cq * VEC;
+  const int64_t src0 = (int64_t)bh * s_bh - (int64_t)L0 * s_row + c0;  // row t at src0 + t s_row
+  int64_t slot = -1;
+  if (t_own > t_lo) {
+    const int blk = t_lo / m.B;
+    if (!table) {
+      slot = (int64_t)bh * m.nb_cap + blk;
+    } else {
+      const int p = block_page(m, table, bh, blk);
+      slot = p < 0 ? -1 : (int64_t)p * m.hkv + bh % m.hkv;
+      if (p < 0 && err && tid == 0) atomicOr(err, (int)SPLA_DEVERR_PAGE);
+    }
+  }
+  // pass 1: key rows to the cache, value rows to LDS, sums of the keys
+  double sum[VEC];
+#pragma unroll
+  for (int e = 0; e < VEC; ++e) sum[e] = 0.0;
+  for (int t0 = t_lo + tl; t0 < t_hi; t0 += TS * 4) {
+    uint4 kv[4], vv[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int t = min(t0 + u * TS, t_hi - 1);
+      kv[u] = *reinterpret_cast<const uint4*>(k_new + src0 + (int64_t)t * s_row);
+      vv[u] = *reinterpret_cast<const uint4*>(v_new + src0 + (int64_t)t * s_row);
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int t = t0 + u * TS;
+      if (t < t_hi) {
+        if (t < t_own && slot >= 0) {
+          *reinterpret_cast<uint4*>(kc + k_off_slot(m, slot, t % m.B, c0)) = kv[u];
+          *reinterpret_cast<uint4*>(sV + (t - t_lo) * d + c0) = vv[u];
+        }
+        const T* x = reinterpret_cast<const T*>(&kv[u]);
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) sum[e] += (double)Elem<T>::load(x, e);
+      }
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < VEC; ++e) part[tl * d + c0 + e] = sum[e];
+  __syncthreads();
+  // value pieces: PV tokens of one coordinate each
+  if (slot >= 0) {
+    constexpr int PV = VEC;
+    const int g_lo = t_lo - t_lo % PV;
+    const int n_pieces = ((t_own + PV - 1) / PV - g_lo / PV) * d;
+    for (int pc = tid; pc < n_pieces; pc += 256) {
+      const int c = pc % d, tg = g_lo + (pc / d) * PV;  // first token of the piece
+      if (tg >= t_lo && tg + PV <= t_own) {
+        T x[PV];
+#pragma unroll
+        for (int e = 0; e < PV; ++e) x[e] = sV[(tg + e - t_lo) * d + c];
+        *reinterpret_cast<uint4*>(vc + v_off_slot(m, slot, tg % m.B, c)) =
+            *reinterpret_cast<const uint4*>(x);
+      } else {
+        for (int e = 0; e < PV; ++e) {
+          const int t = tg + e;
+          if (t >= t_lo && t < t_own) vc[v_off_slot(m, slot, t % m.B, c)] = sV[(t - t_lo) * d + c];
+        }
+      }
+    }
+  }
+  const int nc = t_hi - t_lo;
+  double mean_c[VEC];
+#pragma unroll
+  for (int e = 0; e < VEC; ++e) {
+    double tot = 0.0;
+    for (int x = 0; x < TS; ++x) tot += part[x * d + c0 + e];
+    mean_c[e] = tot / nc;
+    if (tl == 0) smean[c0 + e] = mean_c[e];
+  }
+  __syncthreads();
+  // pass 2: sum of squared deviations from the new tokens' mean
+  double m2[VEC];
+#pragma unroll
+  for (int e = 0; e < VEC; ++e) m2[e] = 0.0;
+  for (int t0 = t_lo + tl; t0 < t_hi; t0 += TS * 4) {
+    uint4 kv[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      kv[u] = *reinterpret_cast<const uint4*>(k_new + src0 +
+                                              (int64_t)min(t0 + u * TS, t_hi - 1) * s_row);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const T* x = reinterpret_cast<const T*>(&kv[u]);
+      const bool ok = t0 + u * TS < t_hi;
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) {
+        const double dx = (double)Elem<T>::load(x, e) - mean_c[e];
+        m2[e] += ok ? dx * dx : 0.0;
+      }
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < VEC; ++e) part[tl * d + c0 + e] = m2[e];
+  __syncthreads();
+  // coordinate j = tid (d threads): combine with the stored statistics
+  if (tid >= d) return;
+  const int j = tid;
+  double m2s = 0.0;
+  for (int x = 0; x < TS; ++x) m2s += part[x * d + j];
+  const double mc = smean[j];
+  const int na = t_lo - i * m.us;
+  const int64_t o_mean = stats_off4(m, bh, i, 0, j / 4) + (j & 3);
+  const int64_t o_m2 = stats_off4(m, bh, i, 1, j / 4) + (j & 3);
+  double mean = mc, m2v = m2s;
+  if (na > 0) {
+    const double mean_a = stats[o_mean], m2_a = stats[o_m2];
+    const double n = (double)(na + nc);
+    const double delta = mc - mean_a;
+    mean = mean_a + delta * (nc / n);
+    m2v = m2_a + m2s + delta * delta * ((double)na * nc / n);
+  }
+  stats[o_mean] = (float)mean;
+  stats[o_m2] = (float)m2v;
 }
 
 // Partial linear-attention state of one chunk of new tokens:
@@ -193,6 +338,143 @@ __global__ __launch_bounds__(256) void append_state_partial_kernel(
   }
 }
 
+// The same partial state on the matrix cores (bf16 keys and values), one
+// workgroup per (chunk, sequence x KV head). Per 32-token step, phi(k) of the
+// step's keys (softmax over d, fp32) goes to LDS transposed as bf16 hi + lo
+// (the A operand, rows = coordinates j, k = tokens), the values transposed
+// (the B operand, columns = coordinates c); then
+//   P[j][c] += sum_t phi(k_t)_j v_t,c
+// on v_mfma_f32_16x16x32_bf16 (hi and lo products, fp32 accumulation).
+// Wavefront w owns columns (D / 4) w .. of P: D / 16 row tiles x D / 64
+// column tiles. Pz accumulates phi(k) in fp32 per lane.
+typedef __bf16 abf16x8 __attribute__((ext_vector_type(8)));
+typedef float afloatx4 __attribute__((ext_vector_type(4)));
+
+template <int D>
+struct alignas(16) StateSmem {
+  static constexpr int TPP = kSubTokens + 8;
+  uint16_t kT_h[D][TPP], kT_l[D][TPP];  // phi(k)^T of the step
+  uint16_t vT[D][TPP];                  // v^T of the step
+  float z[4][D];                        // per-wavefront sums of phi(k)
+};
+
+template <int D>
+__global__ __launch_bounds__(256) void append_state_mfma_kernel(
+    Dims m, const int32_t* __restrict__ seq_lens, const bf16_t* __restrict__ k_new,
+    const bf16_t* __restrict__ v_new, int max_new, const int32_t* __restrict__ n_new, int n_chunks,
+    int chunk_tokens, float* __restrict__ part_s, float* __restrict__ part_z) {
+  constexpr int RT = D / 16;        // row tiles (coordinates j)
+  constexpr int CT = D / 64;        // column tiles per wavefront
+  constexpr int E = D / 64;         // elements of a row per lane (lane + 64 e)
+  __shared__ StateSmem<D> sm;
+  const int bh = blockIdx.y;
+  const int b = bh / m.hkv;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int li = lane & 15, lg = lane >> 4;
+  bool clipped;
+  const int ne = appended_count(m, seq_lens[b], max_new, n_new, b, &clipped);
+  const int t0 = blockIdx.x * chunk_tokens;
+  const int t1 = min(t0 + chunk_tokens, ne);
+  afloatx4 acc[RT][CT];
+#pragma unroll
+  for (int r = 0; r < RT; ++r)
+#pragma unroll
+    for (int c = 0; c < CT; ++c) acc[r][c] = afloatx4{0.f, 0.f, 0.f, 0.f};
+  float zacc[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) zacc[e] = 0.f;
+  const bf16_t* kb = k_new + (int64_t)bh * max_new * D;
+  const bf16_t* vb = v_new + (int64_t)bh * max_new * D;
+  // wavefront w takes tokens 8 w .. 8 w + 7 of each 32-token step, lane l
+  // coordinates l + 64 e; the next step's rows are loaded while the current
+  // one is processed
+  uint16_t kx[8][E], vx[8][E];
+  auto load_step = [&](int tt) {
+#pragma unroll
+    for (int r = 0; r < 8; ++r) {
+      const int row = min(tt + 8 * w + r, t1 - 1);
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        kx[r][e] = kb[(int64_t)row * D + lane + 64 * e].bits;
+        vx[r][e] = vb[(int64_t)row * D + lane + 64 * e].bits;
+      }
+    }
+  };
+  if (t0 < t1) load_step(t0);
+  for (int tt = t0; tt < t1; tt += kSubTokens) {
+    const int nt = min(kSubTokens, t1 - tt);
+    float kf[8][E];
+    uint16_t vv[8][E];
+#pragma unroll
+    for (int r = 0; r < 8; ++r)
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        kf[r][e] = bf16_to_f32(kx[r][e]);
+        vv[r][e] = vx[r][e];
+      }
+    if (tt + kSubTokens < t1) load_step(tt + kSubTokens);
+#pragma unroll
+    for (int r = 0; r < 8; ++r) {
+      const int t = 8 * w + r;
+      const bool ok = t < nt;
+      float mx = -INFINITY;
+#pragma unroll
+      for (int e = 0; e < E; ++e) mx = fmaxf(mx, kf[r][e]);
+      mx = wave_max(mx);
+      float sum = 0.f;
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        kf[r][e] = expf(kf[r][e] - mx);
+        sum += kf[r][e];
+      }
+      sum = wave_sum(sum);
+      const float inv = ok ? 1.0f / sum : 0.f;
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        const float ph = kf[r][e] * inv;
+        const __bf16 hi = (__bf16)ph;
+        const __bf16 lo = (__bf16)(ph - (float)hi);
+        const int col = lane + 64 * e;
+        sm.kT_h[col][t] = __builtin_bit_cast(uint16_t, hi);
+        sm.kT_l[col][t] = __builtin_bit_cast(uint16_t, lo);
+        sm.vT[col][t] = ok ? vv[r][e] : (uint16_t)0;
+        zacc[e] += ph;
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < RT; ++r) {
+      const abf16x8 ah = __builtin_bit_cast(abf16x8, *reinterpret_cast<const uint4*>(&sm.kT_h[16 * r + li][8 * lg]));
+      const abf16x8 al = __builtin_bit_cast(abf16x8, *reinterpret_cast<const uint4*>(&sm.kT_l[16 * r + li][8 * lg]));
+#pragma unroll
+      for (int c = 0; c < CT; ++c) {
+        const int col = (D / 4) * w + 16 * c + li;
+        const abf16x8 bv = __builtin_bit_cast(abf16x8, *reinterpret_cast<const uint4*>(&sm.vT[col][8 * lg]));
+        acc[r][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bv, acc[r][c], 0, 0, 0);
+        acc[r][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, bv, acc[r][c], 0, 0, 0);
+      }
+    }
+    __syncthreads();
+  }
+  float* ps = part_s + ((int64_t)bh * n_chunks + blockIdx.x) * D * D;
+#pragma unroll
+  for (int r = 0; r < RT; ++r)
+#pragma unroll
+    for (int c = 0; c < CT; ++c)
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4)
+        ps[(16 * r + 4 * lg + r4) * D + (D / 4) * w + 16 * c + li] = acc[r][c][r4];
+#pragma unroll
+  for (int e = 0; e < E; ++e) sm.z[w][lane + 64 * e] = zacc[e];
+  __syncthreads();
+  if (tid < D) {
+    float z = 0.f;
+#pragma unroll
+    for (int x = 0; x < 4; ++x) z += sm.z[x][tid];
+    part_z[((int64_t)bh * n_chunks + blockIdx.x) * D + tid] = z;
+  }
+}
+
 // S_bar += sum of the chunk partials, accumulated in fp64 in chunk order.
 __global__ __launch_bounds__(256) void append_state_reduce_kernel(
     Dims m, int n_chunks, const float* __restrict__ part_s, const float* __restrict__ part_z,
@@ -204,7 +486,14 @@ __global__ __launch_bounds__(256) void append_state_reduce_kernel(
     const int row = row0 + e / D, col = e % D;
     const int64_t o = ((int64_t)bh * D + row) * D + col;
     double s = S[o];
-    for (int c = 0; c < n_chunks; ++c) s += part_s[(((int64_t)bh * n_chunks + c) * D + row) * D + col];
+    const float* p = part_s + ((int64_t)bh * n_chunks * D + row) * D + col;  // chunk c at + c D D
+    for (int c0 = 0; c0 < n_chunks; c0 += 8) {  // eight loads in flight, added in chunk order
+      float x[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) x[u] = p[(int64_t)min(c0 + u, n_chunks - 1) * D * D];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) s += c0 + u < n_chunks ? (double)x[u] : 0.0;
+    }
     S[o] = (float)s;
   }
   if (threadIdx.x < 16) {
@@ -315,12 +604,12 @@ hipError_t launch_append_blocks(const Dims& m, const spla_cache& c, const void* 
   const int64_t s_bh = position_major ? m.d : (int64_t)max_new * m.d;
   const int64_t s_row = position_major ? (int64_t)m.bh * m.d : m.d;
   if (m.elem == 4)
-    hipLaunchKernelGGL(append_blocks_kernel<float>, grid, dim3(128), 0, st, m, (float*)c.k_cache,
+    hipLaunchKernelGGL(append_blocks_kernel<float>, grid, dim3(256), 0, st, m, (float*)c.k_cache,
                        (float*)c.v_cache, c.blk_stats, c.seq_lens, c.err_flags,
                        (const float*)k_new, (const float*)v_new, max_new, n_new,
                        m.pages > 0 ? c.block_table : nullptr, s_bh, s_row);
   else
-    hipLaunchKernelGGL(append_blocks_kernel<bf16_t>, grid, dim3(128), 0, st, m,
+    hipLaunchKernelGGL(append_blocks_kernel<bf16_t>, grid, dim3(256), 0, st, m,
                        (bf16_t*)c.k_cache, (bf16_t*)c.v_cache, c.blk_stats, c.seq_lens,
                        c.err_flags, (const bf16_t*)k_new, (const bf16_t*)v_new, max_new, n_new,
                        m.pages > 0 ? c.block_table : nullptr, s_bh, s_row);
@@ -331,10 +620,16 @@ template <typename T, int D>
 static void state_partial(const Dims& m, const spla_cache& c, const void* k_new, const void* v_new,
                           int max_new, const int32_t* n_new, const AppendWs& ws, char* base,
                           hipStream_t st) {
-  hipLaunchKernelGGL((append_state_partial_kernel<T, D>), dim3(ws.n_chunks, m.bh), dim3(256), 0,
-                     st, m, c.seq_lens, (const T*)k_new, (const T*)v_new, max_new, n_new,
-                     ws.n_chunks, ws.chunk_tokens, (float*)(base + ws.part_s),
-                     (float*)(base + ws.part_z));
+  if constexpr (sizeof(T) == 2)
+    hipLaunchKernelGGL((append_state_mfma_kernel<D>), dim3(ws.n_chunks, m.bh), dim3(256), 0, st,
+                       m, c.seq_lens, (const bf16_t*)k_new, (const bf16_t*)v_new, max_new, n_new,
+                       ws.n_chunks, ws.chunk_tokens, (float*)(base + ws.part_s),
+                       (float*)(base + ws.part_z));
+  else
+    hipLaunchKernelGGL((append_state_partial_kernel<T, D>), dim3(ws.n_chunks, m.bh), dim3(256), 0,
+                       st, m, c.seq_lens, (const T*)k_new, (const T*)v_new, max_new, n_new,
+                       ws.n_chunks, ws.chunk_tokens, (float*)(base + ws.part_s),
+                       (float*)(base + ws.part_z));
 }
 
 hipError_t launch_append_state(const Dims& m, const spla_cache& c, const void* k_new,

@@ -15,7 +15,7 @@ int compute_units();
 inline void mark_phase(const spla_events* ev, int p, bool stop, hipStream_t st) {
   if (!ev) return;
   void* e = stop ? ev->stop[p] : ev->start[p];
-  if (e) hipEventRecord((hipEvent_t)e, st);
+  if (e) (void)hipEventRecord((hipEvent_t)e, st);
 }
 
 // append.hip

@@ -18,7 +18,7 @@ namespace spla {
 
 constexpr int kTileBlocks = 64;   // blocks per statistics tile (one wavefront)
 constexpr int kSubTokens = 32;    // tokens per sparse-pass sub-tile
-constexpr int kAppendChunkTarget = 2048;  // append state-partial workgroups to aim for
+constexpr int kAppendChunkTarget = 512;   // append state-partial workgroups to aim for
 constexpr int kMaxWindows = 16384;  // strided selection windows per sequence at capacity
 
 SPLA_HD int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
