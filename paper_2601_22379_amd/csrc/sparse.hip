@@ -12,16 +12,17 @@
 namespace spla {
 
 // ---------------------------------------------------------------- merge
-// One workgroup per (sequence, KV head), one wavefront per query head.
+// One single-wavefront workgroup per (sequence, KV head, query head): the
+// records of a head are read by G compute units rather than one.
 template <typename T, int D>
-__global__ __launch_bounds__(1024) void merge_kernel(
+__global__ __launch_bounds__(64) void merge_kernel(
     Dims m, float eps, uint32_t flags, const float* __restrict__ gamma,
     const int32_t* __restrict__ meta, const float* __restrict__ part, int n_rec, int stride,
     T* __restrict__ out) {
   const int bh = blockIdx.x;
   merge_head<T, D, false>(m, eps, flags, gamma, meta[bh * 4 + 1], meta[bh * 4 + 2],
                    part + (int64_t)bh * n_rec * stride, n_rec, stride, out, bh,
-                   (int)(threadIdx.x >> 6));
+                   (int)blockIdx.y);
 }
 
 // ------------------------------------------------------------ VALU pass
@@ -300,7 +301,7 @@ static void mfma_d(const Dims& m, float s, const spla_cache& c, const void* q, i
 template <typename T, int D>
 static void merge_td(const Dims& m, const spla_config& cfg, const float* gamma, void* out,
                      const DecodeWs& ws, char* base, hipStream_t st) {
-  hipLaunchKernelGGL((merge_kernel<T, D>), dim3(m.bh), dim3(64 * m.group), 0, st, m, cfg.rms_eps,
+  hipLaunchKernelGGL((merge_kernel<T, D>), dim3(m.bh, m.group), dim3(64), 0, st, m, cfg.rms_eps,
                      cfg.flags, gamma, (const int32_t*)(base + ws.meta),
                      (const float*)(base + ws.part), ws.n_wg, ws.part_stride, (T*)out);
 }
