@@ -579,13 +579,18 @@ __global__ __launch_bounds__(256) void append_one_kernel(
                    (int)blockIdx.x - D / 16, bh, D, D);
 }
 
+// seq_lens[b] += the tokens appended; appended (if not NULL) receives that
+// count per sequence.
 __global__ void append_finish_kernel(Dims m, int32_t* __restrict__ seq_lens, int max_new,
-                                     const int32_t* __restrict__ n_new) {
+                                     const int32_t* __restrict__ n_new,
+                                     int32_t* __restrict__ appended) {
   const int b = blockIdx.x * blockDim.x + threadIdx.x;
   if (b >= m.batch) return;
   bool clipped;
   const int L0 = seq_lens[b];
-  seq_lens[b] = L0 + appended_count(m, L0, max_new, n_new, b, &clipped);
+  const int n = appended_count(m, L0, max_new, n_new, b, &clipped);
+  seq_lens[b] = L0 + n;
+  if (appended) appended[b] = n;
 }
 
 __global__ void fill_zero_kernel(uint32_t* __restrict__ p, int64_t n) {
@@ -655,7 +660,14 @@ static int64_t units_of_one(const Dims& m) { return windowed(m) ? m.ul / m.us : 
 
 template <typename T, int D>
 static void append_one_td(const Dims& m, const spla_cache& c, const void* k_new,
-                          const void* v_new, hipStream_t st) {
+                          const void* v_new, hipStream_t st, bool rank1) {
+  if (!rank1) {  // statistics and rows only
+    hipLaunchKernelGGL(append_blocks_kernel<T>, dim3((unsigned)units_of_one(m), (unsigned)m.bh),
+                       dim3(256), 0, st, m, (T*)c.k_cache, (T*)c.v_cache, c.blk_stats,
+                       c.seq_lens, c.err_flags, (const T*)k_new, (const T*)v_new, 1, nullptr,
+                       m.pages > 0 ? c.block_table : nullptr, (int64_t)D, (int64_t)D);
+    return;
+  }
   hipLaunchKernelGGL((append_one_kernel<T, D>), dim3((unsigned)(D / 16 + units_of_one(m)),
                      (unsigned)m.bh), dim3(256), 0, st, m, (T*)c.k_cache, (T*)c.v_cache,
                      c.blk_stats, c.seq_lens, c.err_flags, (const T*)k_new, (const T*)v_new,
@@ -663,21 +675,21 @@ static void append_one_td(const Dims& m, const spla_cache& c, const void* k_new,
 }
 
 hipError_t launch_append_one(const Dims& m, const spla_cache& c, const void* k_new,
-                             const void* v_new, hipStream_t st) {
+                             const void* v_new, hipStream_t st, bool rank1) {
   if (m.elem == 4) {
-    if (m.d == 64) append_one_td<float, 64>(m, c, k_new, v_new, st);
-    else append_one_td<float, 128>(m, c, k_new, v_new, st);
+    if (m.d == 64) append_one_td<float, 64>(m, c, k_new, v_new, st, rank1);
+    else append_one_td<float, 128>(m, c, k_new, v_new, st, rank1);
   } else {
-    if (m.d == 64) append_one_td<bf16_t, 64>(m, c, k_new, v_new, st);
-    else append_one_td<bf16_t, 128>(m, c, k_new, v_new, st);
+    if (m.d == 64) append_one_td<bf16_t, 64>(m, c, k_new, v_new, st, rank1);
+    else append_one_td<bf16_t, 128>(m, c, k_new, v_new, st, rank1);
   }
   return hipGetLastError();
 }
 
 hipError_t launch_append_finish(const Dims& m, const spla_cache& c, int max_new,
-                                const int32_t* n_new, hipStream_t st) {
+                                const int32_t* n_new, hipStream_t st, int32_t* appended) {
   hipLaunchKernelGGL(append_finish_kernel, dim3((unsigned)ceil_div(m.batch, 256)), dim3(256), 0,
-                     st, m, c.seq_lens, max_new, n_new);
+                     st, m, c.seq_lens, max_new, n_new, appended);
   return hipGetLastError();
 }
 

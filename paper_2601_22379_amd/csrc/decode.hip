@@ -73,6 +73,11 @@ struct FusedArgs {
   int n_wg;     // sparse items per (sequence, KV head)
   int stride;   // floats per record
   const int32_t* table;  // block table of a paged K/V pool, or NULL
+  // fused step: the token appended to each (sequence, KV head) and how many
+  // tokens each sequence received (0 at capacity), or NULL
+  const bf16_t* k_step;
+  const bf16_t* v_step;
+  const int32_t* appended;
 };
 
 __device__ __forceinline__ int atomic_add_agent(int32_t* p, int v) {
@@ -107,7 +112,8 @@ __device__ __forceinline__ bool arrive_last(int32_t* ctr, int n, int* s_flag) {
 constexpr int kDecodeWaves = 3;
 
 // R: blocks per thread of the selection (256 R >= blocks per sequence).
-template <int G, int BLK, int R>
+// STEP: the sparse items first apply the step's rank-one update (step_rank1).
+template <int G, int BLK, int R, bool STEP>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(kDecodeWaves, kDecodeWaves)))
 void decode_kernel(FusedArgs a) {
   constexpr int D = 128;
@@ -176,6 +182,9 @@ void decode_kernel(FusedArgs a) {
   const int L = min(max(a.seq_lens[bh / m.hkv], 0), m.cap);  // not produced in this launch
   SparseRegs r;
   sparse_prologue<D, GC>(m, a.q, a.S, a.zbar, bh, x, a.n_wg, r, sm.sp);
+  if constexpr (STEP)
+    step_rank1<D>(m, a.k_step, a.v_step, a.appended, const_cast<float*>(a.S),
+                  const_cast<float*>(a.zbar), bh, r);
   sparse_linear<D, GC>(m, a.S, bh, r, sm.sp);
   if (poller && !ready(cv)) {
     // three polls in flight: each turn issues one and takes the oldest, so
@@ -234,7 +243,11 @@ void decode_kernel(FusedArgs a) {
 template <int G, int BLK, int R>
 static void decode_gbr(const FusedArgs& a, hipStream_t st) {
   const int grid = a.m.bh * (a.n_si + a.n_wg);
-  hipLaunchKernelGGL((decode_kernel<G, BLK, R>), dim3((unsigned)grid), dim3(256), 0, st, a);
+  if (a.appended)
+    hipLaunchKernelGGL((decode_kernel<G, BLK, R, true>), dim3((unsigned)grid), dim3(256), 0, st, a);
+  else
+    hipLaunchKernelGGL((decode_kernel<G, BLK, R, false>), dim3((unsigned)grid), dim3(256), 0, st,
+                       a);
 }
 
 template <int G, int R>
@@ -250,9 +263,10 @@ static void decode_g(const FusedArgs& a, hipStream_t st) {
   else decode_gr<G, 32>(a, st);
 }
 
-hipError_t launch_decode_fused(const Dims& m, const spla_config& cfg, const spla_cache& c,
+static hipError_t decode_fused(const Dims& m, const spla_config& cfg, const spla_cache& c,
                                const void* q, const float* gamma, void* out, int32_t* sel_out,
-                               const DecodeWs& ws, char* base, hipStream_t st) {
+                               const DecodeWs& ws, char* base, hipStream_t st,
+                               const void* k_step, const void* v_step) {
   FusedArgs a;
   a.m = m;
   a.stats = c.blk_stats;
@@ -282,6 +296,9 @@ hipError_t launch_decode_fused(const Dims& m, const spla_config& cfg, const spla
   a.n_wg = ws.n_wg;
   a.stride = ws.part_stride;
   a.table = m.pages > 0 ? c.block_table : nullptr;
+  a.k_step = (const bf16_t*)k_step;
+  a.v_step = (const bf16_t*)v_step;
+  a.appended = k_step ? (const int32_t*)(base + ws.appended) : nullptr;
   switch (m.group) {
     case 1: decode_g<1>(a, st); break;
     case 2: decode_g<2>(a, st); break;
@@ -292,6 +309,20 @@ hipError_t launch_decode_fused(const Dims& m, const spla_config& cfg, const spla
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
+}
+
+hipError_t launch_decode_fused(const Dims& m, const spla_config& cfg, const spla_cache& c,
+                               const void* q, const float* gamma, void* out, int32_t* sel_out,
+                               const DecodeWs& ws, char* base, hipStream_t st) {
+  return decode_fused(m, cfg, c, q, gamma, out, sel_out, ws, base, st, nullptr, nullptr);
+}
+
+hipError_t launch_decode_fused_step(const Dims& m, const spla_config& cfg, const spla_cache& c,
+                                    const void* k_new, const void* v_new, const void* q,
+                                    const float* gamma, void* out, int32_t* sel_out,
+                                    const DecodeWs& ws, char* base, hipStream_t st) {
+  if (!step_fusable(m) || !use_fused_decode(m)) return hipErrorInvalidValue;
+  return decode_fused(m, cfg, c, q, gamma, out, sel_out, ws, base, st, k_new, v_new);
 }
 
 }  // namespace spla

@@ -202,14 +202,18 @@ __global__ __launch_bounds__(256) void sparse_valu_kernel(
 // workgroup of the pair computes the same selection), so no selection kernel
 // runs; workgroup 0 publishes the selection and the meta words. R = 0: the
 // selection comes from the selection kernel.
-template <int D, int BLK, int R>
+// STEP (R = 0 only): first apply the step's rank-one update to this
+// workgroup's rows of S_bar (step_rank1), as the single-launch step does.
+template <int D, int BLK, int R, bool STEP = false>
 __global__ __launch_bounds__(256) void sparse_mfma_kernel(
     Dims m, float s, const bf16_t* __restrict__ kc, const bf16_t* __restrict__ vc,
-    const bf16_t* __restrict__ q, const float* __restrict__ S, const float* __restrict__ zbar,
+    const bf16_t* __restrict__ q, float* __restrict__ S, float* __restrict__ zbar,
     const int32_t* __restrict__ sel, int32_t* __restrict__ meta, int stride,
     float* __restrict__ part, const int32_t* __restrict__ seq_lens,
     const float* __restrict__ e_vals, const double* __restrict__ tile_part,
-    int32_t* __restrict__ sel_out, const int32_t* __restrict__ table) {
+    int32_t* __restrict__ sel_out, const int32_t* __restrict__ table,
+    const bf16_t* __restrict__ k_step = nullptr, const bf16_t* __restrict__ v_step = nullptr,
+    const int32_t* __restrict__ appended = nullptr) {
   constexpr int SWN = R > 0 ? kTileBlocks * 8 : 4;  // tile weights: <= 64 tiles x 8 heads
   __shared__ SelectSmem<256, SWN> ssm;
   __shared__ int32_t s_sel[R > 0 ? SPLA_MAX_TOP_K : 1];
@@ -218,6 +222,7 @@ __global__ __launch_bounds__(256) void sparse_mfma_kernel(
   const int bh = blockIdx.y;
   SparseRegs r;
   sparse_prologue<D, 8>(m, q, S, zbar, bh, (int)blockIdx.x, (int)gridDim.x, r, sm);
+  if constexpr (STEP) step_rank1<D>(m, k_step, v_step, appended, S, zbar, bh, r);
   sparse_linear<D, 8>(m, S, bh, r, sm);
   if constexpr (R > 0) {
     select_blocks<256, R, SWN, false>(m, bh, seq_lens[bh / m.hkv], e_vals, tile_part, ssm, s_sel,
@@ -254,48 +259,54 @@ static void valu_td(const Dims& m, const spla_config& cfg, float s, const spla_c
 // kernel). Every workgroup repeats the selection of its (sequence, KV head),
 // which pays only while the grid is small (about two workgroups per compute
 // unit) and the block count is at most 4096.
-static int sparse_select_r(const Dims& m) {
-  if (!use_mfma_sparse(m) || m.nb_cap > 256 * 16 || windowed(m)) return 0;
+static int sparse_select_r(const Dims& m, bool step) {
+  if (step || !use_mfma_sparse(m) || m.nb_cap > 256 * 16 || windowed(m)) return 0;
   const DecodeWs ws = decode_ws_layout(m);
   if ((int64_t)ws.n_wg * m.bh > 2 * (int64_t)compute_units()) return 0;
   const int per = (int)ceil_div(m.nb_cap, 256);
   return per <= 2 ? 2 : (per <= 4 ? 4 : (per <= 8 ? 8 : 16));
 }
 
-bool sparse_selects(const Dims& m) { return sparse_select_r(m) > 0; }
+bool sparse_selects(const Dims& m, bool step) { return sparse_select_r(m, step) > 0; }
 
-template <int D, int BLK, int R>
+template <int D, int BLK, int R, bool STEP>
 static void mfma_dbr(const Dims& m, float s, const spla_cache& c, const void* q,
-                     int32_t* sel_out,
-                     const DecodeWs& ws, char* base, hipStream_t st) {
-  hipLaunchKernelGGL((sparse_mfma_kernel<D, BLK, R>), dim3(ws.n_wg, m.bh), dim3(256), 0, st, m, s,
-                     (const bf16_t*)c.k_cache, (const bf16_t*)c.v_cache,
-                     (const bf16_t*)q, (const float*)c.lin_state,
-                     (const float*)c.lin_norm, (const int32_t*)(base + ws.sel),
+                     int32_t* sel_out, const DecodeWs& ws, char* base, hipStream_t st,
+                     const void* k_step, const void* v_step) {
+  hipLaunchKernelGGL((sparse_mfma_kernel<D, BLK, R, STEP>), dim3(ws.n_wg, m.bh), dim3(256), 0, st,
+                     m, s, (const bf16_t*)c.k_cache, (const bf16_t*)c.v_cache, (const bf16_t*)q,
+                     c.lin_state, c.lin_norm, (const int32_t*)(base + ws.sel),
                      (int32_t*)(base + ws.meta), ws.part_stride, (float*)(base + ws.part),
                      c.seq_lens, (const float*)(base + ws.e_vals),
                      (const double*)(base + ws.tile_part), sel_out,
-                     m.pages > 0 ? c.block_table : nullptr);
+                     m.pages > 0 ? c.block_table : nullptr, (const bf16_t*)k_step,
+                     (const bf16_t*)v_step, (const int32_t*)(base + ws.appended));
 }
 
 template <int D, int BLK>
 static void mfma_db(const Dims& m, float s, const spla_cache& c, const void* q, int32_t* sel_out,
-                    const DecodeWs& ws, char* base, hipStream_t st) {
-  switch (sparse_select_r(m)) {
-    case 2: mfma_dbr<D, BLK, 2>(m, s, c, q, sel_out, ws, base, st); break;
-    case 4: mfma_dbr<D, BLK, 4>(m, s, c, q, sel_out, ws, base, st); break;
-    case 8: mfma_dbr<D, BLK, 8>(m, s, c, q, sel_out, ws, base, st); break;
-    case 16: mfma_dbr<D, BLK, 16>(m, s, c, q, sel_out, ws, base, st); break;
-    default: mfma_dbr<D, BLK, 0>(m, s, c, q, sel_out, ws, base, st); break;
+                    const DecodeWs& ws, char* base, hipStream_t st, const void* k_step,
+                    const void* v_step) {
+  if (k_step) {
+    mfma_dbr<D, BLK, 0, true>(m, s, c, q, sel_out, ws, base, st, k_step, v_step);
+    return;
+  }
+  switch (sparse_select_r(m, false)) {
+    case 2: mfma_dbr<D, BLK, 2, false>(m, s, c, q, sel_out, ws, base, st, nullptr, nullptr); break;
+    case 4: mfma_dbr<D, BLK, 4, false>(m, s, c, q, sel_out, ws, base, st, nullptr, nullptr); break;
+    case 8: mfma_dbr<D, BLK, 8, false>(m, s, c, q, sel_out, ws, base, st, nullptr, nullptr); break;
+    case 16: mfma_dbr<D, BLK, 16, false>(m, s, c, q, sel_out, ws, base, st, nullptr, nullptr); break;
+    default: mfma_dbr<D, BLK, 0, false>(m, s, c, q, sel_out, ws, base, st, nullptr, nullptr); break;
   }
 }
 
 template <int D>
 static void mfma_d(const Dims& m, float s, const spla_cache& c, const void* q, int32_t* sel_out,
-                   const DecodeWs& ws, char* base, hipStream_t st) {
-  if (m.B == 32) mfma_db<D, 32>(m, s, c, q, sel_out, ws, base, st);
-  else if (m.B == 64) mfma_db<D, 64>(m, s, c, q, sel_out, ws, base, st);
-  else mfma_db<D, 128>(m, s, c, q, sel_out, ws, base, st);
+                   const DecodeWs& ws, char* base, hipStream_t st, const void* k_step,
+                   const void* v_step) {
+  if (m.B == 32) mfma_db<D, 32>(m, s, c, q, sel_out, ws, base, st, k_step, v_step);
+  else if (m.B == 64) mfma_db<D, 64>(m, s, c, q, sel_out, ws, base, st, k_step, v_step);
+  else mfma_db<D, 128>(m, s, c, q, sel_out, ws, base, st, k_step, v_step);
 }
 
 template <typename T, int D>
@@ -308,11 +319,13 @@ static void merge_td(const Dims& m, const spla_config& cfg, const float* gamma, 
 
 hipError_t launch_sparse(const Dims& m, const spla_config& cfg, const spla_cache& c,
                          const void* q, const float* gamma, void* out, int32_t* sel_out,
-                         const DecodeWs& ws, char* base, hipStream_t st) {
+                         const DecodeWs& ws, char* base, hipStream_t st, const void* k_step,
+                         const void* v_step) {
   const float s = cfg.softmax_scale > 0.f ? cfg.softmax_scale : (float)(1.0 / sqrt((double)m.d));
+  if (k_step && !step_fusable(m)) return hipErrorInvalidValue;
   if (use_mfma_sparse(m)) {
-    if (m.d == 64) mfma_d<64>(m, s, c, q, sel_out, ws, base, st);
-    else mfma_d<128>(m, s, c, q, sel_out, ws, base, st);
+    if (m.d == 64) mfma_d<64>(m, s, c, q, sel_out, ws, base, st, k_step, v_step);
+    else mfma_d<128>(m, s, c, q, sel_out, ws, base, st, k_step, v_step);
   } else if (m.elem == 4) {
     if (m.d == 64) valu_td<float, 64>(m, cfg, s, c, q, gamma, out, ws, base, st);
     else valu_td<float, 128>(m, cfg, s, c, q, gamma, out, ws, base, st);

@@ -60,22 +60,30 @@ struct PhaseMark {
     if (e_ != hipSuccess) return SPLA_ERR_HIP;       \
   } while (0)
 
+// k_step, v_step (or NULL): a step's token whose rank-one update of S_bar the
+// decode's sparse pass applies (step_fusable shapes, rows and statistics
+// already appended, ws.appended written by the finish kernel).
 int32_t run_decode(const spla_config* cfg, const spla_cache* cache, const void* q,
                    const float* w, void* out, int32_t* sel_idx, void* ws, size_t ws_bytes,
-                   const spla_events* ev, hipStream_t st) {
+                   const spla_events* ev, hipStream_t st, const void* k_step = nullptr,
+                   const void* v_step = nullptr) {
   const Dims m = spla::make_dims(*cfg);
   const spla::DecodeWs L = spla::decode_ws_layout(m);
   char* base = static_cast<char*>(ws);
   if (spla::use_fused_decode(m) && !(cfg->flags & SPLA_FLAG_SEPARATE_KERNELS)) {
     PhaseMark pm(ev, st, SPLA_PHASE_DECODE);
-    SPLA_TRY(spla::launch_decode_fused(m, *cfg, *cache, q, w, out, sel_idx, L, base, st));
+    if (k_step)
+      SPLA_TRY(spla::launch_decode_fused_step(m, *cfg, *cache, k_step, v_step, q, w, out, sel_idx,
+                                              L, base, st));
+    else
+      SPLA_TRY(spla::launch_decode_fused(m, *cfg, *cache, q, w, out, sel_idx, L, base, st));
     return SPLA_OK;
   }
   {
     PhaseMark pm(ev, st, SPLA_PHASE_SCORE);
     SPLA_TRY(spla::launch_score(m, *cfg, *cache, q, L, base, st));
   }
-  if (!spla::sparse_selects(m)) {
+  if (!spla::sparse_selects(m, k_step != nullptr)) {
     PhaseMark pm(ev, st, SPLA_PHASE_SELECT);
     SPLA_TRY(spla::launch_select(m, *cache, L, base, sel_idx, st));
   } else {
@@ -83,7 +91,8 @@ int32_t run_decode(const spla_config* cfg, const spla_cache* cache, const void* 
   }
   {
     PhaseMark pm(ev, st, SPLA_PHASE_SPARSE);
-    SPLA_TRY(spla::launch_sparse(m, *cfg, *cache, q, w, out, sel_idx, L, base, st));
+    SPLA_TRY(spla::launch_sparse(m, *cfg, *cache, q, w, out, sel_idx, L, base, st, k_step,
+                                 v_step));
   }
   {
     PhaseMark pm(ev, st, SPLA_PHASE_MERGE);
@@ -178,6 +187,19 @@ extern "C" int32_t spla_step_ex(const spla_config* cfg, const spla_cache* cache,
   if (!k_new || !v_new) return SPLA_ERR_INVALID_ARG;
   const Dims m = spla::make_dims(*cfg);
   hipStream_t st = static_cast<hipStream_t>(stream);
+  if (spla::step_fusable(m)) {
+    // the token's rows and statistics first; its rank-one update of S_bar is
+    // applied by the decode's sparse pass to the rows it reads anyway
+    const spla::DecodeWs L = spla::decode_ws_layout(m);
+    char* base = static_cast<char*>(ws);
+    {
+      PhaseMark pm(ev, st, SPLA_PHASE_APPEND);
+      SPLA_TRY(spla::launch_append_one(m, *cache, k_new, v_new, st, false));
+      SPLA_TRY(spla::launch_append_finish(m, *cache, 1, nullptr, st,
+                                          reinterpret_cast<int32_t*>(base + L.appended)));
+    }
+    return run_decode(cfg, cache, q, w, out, sel_idx, ws, ws_bytes, ev, st, k_new, v_new);
+  }
   {
     PhaseMark pm(ev, st, SPLA_PHASE_APPEND);
     SPLA_TRY(spla::launch_append_one(m, *cache, k_new, v_new, st));

@@ -27,12 +27,15 @@ hipError_t launch_append_blocks(const Dims& m, const spla_cache& c, const void* 
 hipError_t launch_append_state(const Dims& m, const spla_cache& c, const void* k_new,
                                const void* v_new, int max_new, const int32_t* n_new,
                                const AppendWs& ws, char* wsbase, hipStream_t st);
-// the single-token append of a step (statistics, K/V rows, S_bar, z_bar) in
-// one launch; seq_lens is advanced by launch_append_finish
+// the single-token append of a step (statistics, K/V rows and, with rank1,
+// the rank-one update of S_bar and z_bar) in one launch; seq_lens is advanced
+// by launch_append_finish, which also writes the count each sequence received
+// to appended (if not NULL)
 hipError_t launch_append_one(const Dims& m, const spla_cache& c, const void* k_new,
-                             const void* v_new, hipStream_t st);
+                             const void* v_new, hipStream_t st, bool rank1 = true);
 hipError_t launch_append_finish(const Dims& m, const spla_cache& c, int max_new,
-                                const int32_t* n_new, hipStream_t st);
+                                const int32_t* n_new, hipStream_t st,
+                                int32_t* appended = nullptr);
 hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t st);
 
 // score.hip: block scoring
@@ -44,12 +47,16 @@ hipError_t launch_select(const Dims& m, const spla_cache& c, const DecodeWs& ws,
                          int32_t* sel_out, hipStream_t st);
 
 // sparse.hip: fused pass over the selected blocks (records), then the merge.
-// When sparse_selects(m), the sparse pass makes the selection itself (and
-// writes sel_out) and launch_select must not be called.
-bool sparse_selects(const Dims& m);
+// When sparse_selects(m, step), the sparse pass makes the selection itself
+// (and writes sel_out) and launch_select must not be called; step: the pass
+// applies a step's rank-one update (k_step given to launch_sparse).
+bool sparse_selects(const Dims& m, bool step);
+// k_step, v_step (or NULL): the step's token, whose rank-one update of S_bar
+// the matrix-core pass applies as the fused decode does (step_fusable shapes)
 hipError_t launch_sparse(const Dims& m, const spla_config& cfg, const spla_cache& c,
                          const void* q, const float* rms_weight, void* out, int32_t* sel_out,
-                         const DecodeWs& ws, char* wsbase, hipStream_t st);
+                         const DecodeWs& ws, char* wsbase, hipStream_t st,
+                         const void* k_step = nullptr, const void* v_step = nullptr);
 hipError_t launch_merge(const Dims& m, const spla_config& cfg, const float* rms_weight, void* out,
                         const DecodeWs& ws, char* wsbase, hipStream_t st);
 
@@ -67,5 +74,14 @@ hipError_t launch_decode_fused(const Dims& m, const spla_config& cfg, const spla
                                const void* q, const float* rms_weight, void* out,
                                int32_t* sel_out, const DecodeWs& ws, char* wsbase,
                                hipStream_t st);
+// The single-launch decode of a step whose token rows and statistics are
+// already appended (launch_append_one without rank1, then launch_append_finish
+// with ws.appended; step_fusable shapes): its sparse items add phi(k) v^T of
+// the token to the rows of S_bar (and z_bar) they read, use them, and write
+// them back, for each sequence that received the token.
+hipError_t launch_decode_fused_step(const Dims& m, const spla_config& cfg, const spla_cache& c,
+                                    const void* k_new, const void* v_new, const void* q,
+                                    const float* rms_weight, void* out, int32_t* sel_out,
+                                    const DecodeWs& ws, char* wsbase, hipStream_t st);
 
 }  // namespace spla

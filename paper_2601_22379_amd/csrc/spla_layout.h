@@ -112,6 +112,7 @@ SPLA_HD int64_t stats_off4(const Dims& m, int64_t bh, int64_t blk, int part, int
 // ---- decode workspace ------------------------------------------------------
 constexpr int kPartHead = 48;     // per-record header: m[16], l[16], zw[16]
 constexpr int kSparseWaves = 4;   // waves per sparse workgroup
+constexpr int kSparsePre = 4;     // S_bar entries per thread a sparse workgroup holds
 
 struct DecodeWs {
   int64_t e_vals;     // f32 [bh][G][n_tiles*64]   exp(ell - tile max), per unit
@@ -119,6 +120,7 @@ struct DecodeWs {
   int64_t sel;        // i32 [bh][k]               selected blocks, ascending
   int64_t meta;       // i32 [bh][4]               (n_selected, all_selected, length, 0)
   int64_t part;       // f32 [bh][n_wg][part_stride]  sparse workgroup partials
+  int64_t appended;   // i32 [batch]               tokens a step appended (fused step)
   int64_t sync;       // i32 [sync_layout(m).words]  counters of the single-launch decode;
                       //   zero between calls
   int64_t total;
@@ -132,14 +134,19 @@ struct DecodeWs {
 SPLA_HD bool use_mfma_sparse(const Dims& m) { return m.elem == 2 && m.group <= 8; }
 
 // The single-launch decode covers the matrix-core shapes with d = 128,
-// G <= 6 (larger groups exceed its register budget) and at most 8192 blocks
+// G <= 6 (larger groups exceed its register budget), at most 8192 blocks
 // per sequence (its selection runs in one 256-thread workgroup, at most 32
-// blocks per thread).
+// blocks per thread) and at most 128 (sequence, KV head) units: with more,
+// every phase of the separate launches already fills the GPU and the
+// hand-offs between workgroups cost more than the overlap gains (64
+// sequences x 8 KV heads at 16K-64K tokens: 229 us in one launch, 211 us on
+// the separate launches).
 constexpr int kFusedMaxBlocks = 256 * 32;
 constexpr int kFusedMaxGroup = 6;
+constexpr int kFusedMaxUnits = 128;
 SPLA_HD bool use_fused_decode(const Dims& m) {
   return use_mfma_sparse(m) && m.d == 128 && m.group <= kFusedMaxGroup &&
-         m.nb_cap <= kFusedMaxBlocks && !windowed(m);
+         m.nb_cap <= kFusedMaxBlocks && !windowed(m) && m.bh <= kFusedMaxUnits;
 }
 
 // The decode workspace's synchronisation area (int32 words). Every counter
@@ -185,9 +192,19 @@ SPLA_HD DecodeWs decode_ws_layout(const Dims& m) {
   w.sel = take((int64_t)m.bh * m.k * 4);
   w.meta = take((int64_t)m.bh * 4 * 4);
   w.part = take((int64_t)m.bh * w.n_wg * w.part_stride * 4);
+  w.appended = take((int64_t)m.batch * 4);
   w.sync = take(sync_layout(m).words * 4);
   w.total = off;
   return w;
+}
+
+// spla_step folds the token's rank-one update of S_bar into the rows of
+// S_bar the matrix-core sparse pass reads (for o_bar) when every sparse
+// workgroup holds all its rows in registers.
+SPLA_HD bool step_fusable(const Dims& m) {
+  if (!use_mfma_sparse(m)) return false;
+  const DecodeWs ws = decode_ws_layout(m);
+  return ceil_div(m.d, ws.n_wg) * m.d <= kSparsePre * 256;
 }
 
 // ---- chunked prefill workspace ------------------------------------------------

@@ -208,7 +208,6 @@ __device__ __forceinline__ void merge_head(const Dims& m, float eps, uint32_t fl
 }
 
 // ------------------------------------------------------ matrix-core pass
-constexpr int kSparsePre = 4;  // S_bar entries per thread loaded up front
 
 // LDS of one sparse workgroup for groups of at most GC heads: the B
 // operands of the first products (q, phi(q) hi, phi(q) lo per k-step, in
@@ -392,6 +391,61 @@ __device__ __forceinline__ void sparse_linear(const Dims& m, const float* __rest
     }
   }
   r.zq = zq;
+}
+
+// The rank-one update of a step (spla_step) for the rows of S_bar (and z_bar)
+// a sparse workgroup holds (its lin_rows, all in r.spre / r.zbv, loaded by
+// sparse_prologue): S_bar[j][c] += phi(k)_j v_c, z_bar[j] += phi(k)_j, with
+// phi(k) the softmax of the appended key over d computed exactly as the
+// single-token append does; the updated rows are written back. Nothing
+// happens for a sequence that received no token (at capacity).
+template <int D>
+__device__ __forceinline__ void step_rank1(const Dims& m, const bf16_t* __restrict__ k_step,
+                                           const bf16_t* __restrict__ v_step,
+                                           const int32_t* __restrict__ appended, float* S,
+                                           float* zbar, int bh, SparseRegs& r) {
+  const int tid = threadIdx.x, lane = tid & 63;
+  if (appended[bh / m.hkv] <= 0) return;  // uniform over the workgroup
+  float x[D / 64];
+  float mx = -INFINITY;
+#pragma unroll
+  for (int e = 0; e < D / 64; ++e) {
+    x[e] = bf16_to_f32(k_step[(int64_t)bh * D + lane + 64 * e].bits);
+    mx = fmaxf(mx, x[e]);
+  }
+  mx = wave_max(mx);
+  float sum = 0.f;
+#pragma unroll
+  for (int e = 0; e < D / 64; ++e) {
+    x[e] = expf(x[e] - mx);
+    sum += x[e];
+  }
+  sum = wave_sum(sum);
+  float ph[D / 64];
+#pragma unroll
+  for (int e = 0; e < D / 64; ++e) ph[e] = x[e] / sum;
+  const float vc = bf16_to_f32(v_step[(int64_t)bh * D + tid % D].bits);
+  float* Sh = S + (int64_t)bh * D * D;
+#pragma unroll
+  for (int u = 0; u < kSparsePre; ++u) {
+    const int e = tid + 256 * u;
+    const int row = r.row0 + e / D;  // uniform over the wavefront
+    const float pr = lane_f32(ph[(row % D) / 64], row % 64);
+    if (e < r.nrows * D) {
+      r.spre[u] = fmaf(pr, vc, r.spre[u]);
+      Sh[r.row0 * D + e] = r.spre[u];
+    }
+  }
+  const int row = r.row0 + tid;
+  float pz = __shfl(ph[0], row % 64, kWave);
+  if constexpr (D / 64 > 1) {
+    const float p1 = __shfl(ph[1], row % 64, kWave);
+    pz = (row % D) / 64 ? p1 : pz;
+  }
+  if (tid < r.nrows) {
+    r.zbv += pz;
+    zbar[(int64_t)bh * D + row] = r.zbv;
+  }
 }
 
 // Selected block of this wavefront's step: entry p of the selection, where

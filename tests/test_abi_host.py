@@ -186,6 +186,9 @@ def test_header_and_host_code_under_sanitizers(tmp_path):
     (dict(flags=spla.FLAG_SEPARATE_KERNELS), False),
     (dict(sel_window=32, sel_stride=16), False),             # strided selection
     (dict(kv_pages=4096), True),                             # paged KV pool
+    (dict(batch=16), True),                                  # 128 units: the limit
+    (dict(batch=17), False),
+    (dict(batch=64, block_size=128, max_seq_len=65536, top_k=16), False),  # high batch
 ])
 def test_decode_phase_mask(libname, kw, single):
     lib = spla.lib() if libname == "hip" else spla.host_lib()

@@ -203,3 +203,49 @@ def test_step_at_capacity_leaves_the_state_unchanged(dev):
                                gamma[h * w.group:(h + 1) * w.group], p)
         assert [int(x) for x in sel[1, h][:len(res.sel)]] == [int(x) for x in res.sel]
         assert H.row_rel_err(out[1, h * w.group:(h + 1) * w.group], res.out) <= H.TOL["bf16"]
+
+
+@pytest.mark.parametrize("d,B,k", [(128, 128, 16), (128, 64, 32)])
+def test_fused_step_equals_separate_step(dev, d, B, k):
+    """spla_step on the single-launch kernel folds the token's rank-one update
+    of S_bar into the rows its sparse items read; three steps must leave the
+    same cache (statistics, S_bar, z_bar, K/V rows, lengths) and give the
+    same outputs and selections, bit for bit, as the separate launches (which
+    append with the single-token kernel), also for a sequence at capacity,
+    and match the oracle."""
+    cap = 32 * B
+    w = si.custom(f"fstep{B}", 3, 8, 2, d, B, k, [cap - 700, 17 * B + 5, cap], kind="drift",
+                  code=135 + B, capacity=cap)
+    caches = []
+    for flags in (0, spla.FLAG_SEPARATE_KERNELS):
+        c = spla.SplaCache(H.config_of(w, flags=flags), dev)
+        H.fill_cache(w, c, device=dev)
+        caches.append(c)
+    assert spla.decode_phases(caches[0].cfg) == ["decode"]
+    gamma = si.gen_gamma(w)
+    rng = np.random.default_rng(136)
+    p = H.params_of(w)
+    for step in range(3):
+        kn = si.round_bf16(rng.standard_normal((3, 2, d)).astype(np.float32))
+        vn = si.round_bf16(rng.standard_normal((3, 2, d)).astype(np.float32))
+        q = si.gen_q_batch(w, step)
+        res = [c.step(H.to_dev(kn, w, dev), H.to_dev(vn, w, dev), H.to_dev(q, w, dev),
+                      torch.from_numpy(gamma).to(dev)) for c in caches]
+        torch.cuda.synchronize()
+        assert torch.equal(res[0][0], res[1][0]) and torch.equal(res[0][1], res[1][1]), step
+        for n in ("k", "v", "stats", "state", "norm", "seq_lens"):
+            assert torch.equal(getattr(caches[0], n), getattr(caches[1], n)), (step, n)
+    assert caches[0].device_errors() & spla.DEVERR_CAPACITY
+    # the oracle on sequence 1 after the three steps (its appended rows are the
+    # random ones above)
+    out = res[0][0].float().cpu().numpy()
+    sel = res[0][1].cpu().numpy()
+    L = w.lengths[1] + 3
+    kl = caches[0].k_logical()[1, :, :L].float().cpu().numpy()
+    vl = caches[0].v_logical()[1, :, :L].float().cpu().numpy()
+    for h in range(2):
+        st = O.build_state(kl[h], vl[h], L, B)
+        r = O.decode_kv_head(q[1, h * 4:(h + 1) * 4], st, kl[h], vl[h],
+                             gamma[h * 4:(h + 1) * 4], p)
+        assert [int(x) for x in sel[1, h][:len(r.sel)]] == [int(x) for x in r.sel]
+        assert H.row_rel_err(out[1, h * 4:(h + 1) * 4], r.out) <= H.TOL["bf16"]
