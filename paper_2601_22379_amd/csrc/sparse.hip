@@ -204,7 +204,9 @@ __global__ __launch_bounds__(256) void sparse_valu_kernel(
 // selection comes from the selection kernel.
 // STEP (R = 0 only): first apply the step's rank-one update to this
 // workgroup's rows of S_bar (step_rank1), as the single-launch step does.
-template <int D, int BLK, int R, bool STEP = false>
+// GC: accumulator columns per kind (>= G). The selection's LDS (R > 0) lies
+// over the accumulators, which sparse_body writes only after the selection.
+template <int D, int BLK, int R, int GC, bool STEP>
 __global__ __launch_bounds__(256) void sparse_mfma_kernel(
     Dims m, float s, const bf16_t* __restrict__ kc, const bf16_t* __restrict__ vc,
     const bf16_t* __restrict__ q, float* __restrict__ S, float* __restrict__ zbar,
@@ -215,15 +217,21 @@ __global__ __launch_bounds__(256) void sparse_mfma_kernel(
     const bf16_t* __restrict__ k_step = nullptr, const bf16_t* __restrict__ v_step = nullptr,
     const int32_t* __restrict__ appended = nullptr) {
   constexpr int SWN = R > 0 ? kTileBlocks * 8 : 4;  // tile weights: <= 64 tiles x 8 heads
-  __shared__ SelectSmem<256, SWN> ssm;
+  using SpSm = SparseSmem<D, GC>;
+  using SeSm = SelectSmem<256, SWN>;
+  constexpr size_t kLds = R > 0 && SpSm::kOverlay + sizeof(SeSm) > sizeof(SpSm)
+                              ? SpSm::kOverlay + sizeof(SeSm) : sizeof(SpSm);
+  static_assert(SpSm::kOverlay % 16 == 0, "overlay alignment");
+  __shared__ __align__(16) unsigned char lds[kLds];
+  SpSm& sm = *reinterpret_cast<SpSm*>(lds);
+  SeSm& ssm = *reinterpret_cast<SeSm*>(lds + SpSm::kOverlay);
   __shared__ int32_t s_sel[R > 0 ? SPLA_MAX_TOP_K : 1];
   __shared__ int32_t s_meta[4];
-  __shared__ SparseSmem<D, 8> sm;
   const int bh = blockIdx.y;
   SparseRegs r;
-  sparse_prologue<D, 8>(m, q, S, zbar, bh, (int)blockIdx.x, (int)gridDim.x, r, sm);
+  sparse_prologue<D, GC>(m, q, S, zbar, bh, (int)blockIdx.x, (int)gridDim.x, r, sm);
   if constexpr (STEP) step_rank1<D>(m, k_step, v_step, appended, S, zbar, bh, r);
-  sparse_linear<D, 8>(m, S, bh, r, sm);
+  sparse_linear<D, GC>(m, S, bh, r, sm);
   if constexpr (R > 0) {
     select_blocks<256, R, SWN, false>(m, bh, seq_lens[bh / m.hkv], e_vals, tile_part, ssm, s_sel,
                                       s_meta,
@@ -232,11 +240,11 @@ __global__ __launch_bounds__(256) void sparse_mfma_kernel(
     __syncthreads();
     if (blockIdx.x == 0 && threadIdx.x < 4) meta[bh * 4 + threadIdx.x] = s_meta[threadIdx.x];
     const int e = sparse_step_entry<BLK>((int)blockIdx.x);
-    sparse_body<D, BLK, false, 8>(m, s, kc, vc, e < m.k ? s_sel[e] : -1, s_meta[2], bh,
+    sparse_body<D, BLK, false, GC>(m, s, kc, vc, e < m.k ? s_sel[e] : -1, s_meta[2], bh,
                                   (int)blockIdx.x, (int)gridDim.x, r, sm, part, stride, table);
   } else {
     const int e = sparse_step_entry<BLK>((int)blockIdx.x);
-    sparse_body<D, BLK, false, 8>(m, s, kc, vc, e < m.k ? sel[(int64_t)bh * m.k + e] : -1,
+    sparse_body<D, BLK, false, GC>(m, s, kc, vc, e < m.k ? sel[(int64_t)bh * m.k + e] : -1,
                                   meta[bh * 4 + 2], bh, (int)blockIdx.x, (int)gridDim.x, r, sm,
                                   part, stride, table);
   }
@@ -273,7 +281,9 @@ template <int D, int BLK, int R, bool STEP>
 static void mfma_dbr(const Dims& m, float s, const spla_cache& c, const void* q,
                      int32_t* sel_out, const DecodeWs& ws, char* base, hipStream_t st,
                      const void* k_step, const void* v_step) {
-  hipLaunchKernelGGL((sparse_mfma_kernel<D, BLK, R, STEP>), dim3(ws.n_wg, m.bh), dim3(256), 0, st,
+  auto kern = m.group <= 4 ? sparse_mfma_kernel<D, BLK, R, 4, STEP>
+                           : sparse_mfma_kernel<D, BLK, R, 8, STEP>;
+  hipLaunchKernelGGL(kern, dim3(ws.n_wg, m.bh), dim3(256), 0, st,
                      m, s, (const bf16_t*)c.k_cache, (const bf16_t*)c.v_cache, (const bf16_t*)q,
                      c.lin_state, c.lin_norm, (const int32_t*)(base + ws.sel),
                      (int32_t*)(base + ws.meta), ws.part_stride, (float*)(base + ws.part),

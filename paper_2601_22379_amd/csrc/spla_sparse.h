@@ -213,14 +213,18 @@ __device__ __forceinline__ void merge_head(const Dims& m, float eps, uint32_t fl
 // operands of the first products (q, phi(q) hi, phi(q) lo per k-step, in
 // lane order), the four wavefronts' accumulators (exact columns 0 .. GC-1,
 // linear columns GC .. 2 GC-1), phi(q) and this workgroup's rows of S_bar.
+// The accumulators come last and are written only at the end of sparse_body,
+// so a kernel may lay other LDS over them until then (kOverlay).
 template <int D, int GC>
 struct SparseSmem {
   uint4 qops[3][D / 32][64];
-  float o[kSparseWaves][D][2 * GC + 1];
   float m[kSparseWaves][16], l[kSparseWaves][16];
   float phq[GC][D];
   float S[kSparsePre * 256];
   float zb[D];
+  float o[kSparseWaves][D][2 * GC + 1];
+  static constexpr size_t kOverlay = sizeof(qops) + sizeof(m) + sizeof(l) + sizeof(phq) +
+                                     sizeof(S) + sizeof(zb);  // offset of o
 };
 
 // What a workgroup loads and computes before it knows its blocks: its rows

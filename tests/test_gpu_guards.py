@@ -153,7 +153,7 @@ def test_append_without_counts(dev):
             np.testing.assert_allclose(mean[b, h, :nb], st.mean, rtol=0, atol=2e-6)
             np.testing.assert_allclose(m2[b, h, :nb] / st.counts[:, None], st.var, rtol=2e-5,
                                        atol=1e-6)
-            np.testing.assert_allclose(S[b, h], st.s_bar, rtol=2e-5, atol=2e-5)
+            np.testing.assert_allclose(S[b, h], st.s_bar, rtol=2e-4, atol=2e-4)
             np.testing.assert_allclose(z[b, h], st.z_bar, rtol=2e-5, atol=1e-5)
     q, gamma = si.gen_q_batch(w), si.gen_gamma(w)
     out, sel = _decode(cache, w, q, gamma, dev)
@@ -163,10 +163,11 @@ def test_append_without_counts(dev):
     assert cache.device_errors() == 0
 
 
-def test_step_at_capacity_leaves_the_state_unchanged(dev):
+@pytest.mark.parametrize("separate", [False, True])
+def test_step_at_capacity_leaves_the_state_unchanged(dev, separate):
     w = si.custom("stepcap", 2, 8, 2, 128, 64, 6, [512, 300], kind="iid", code=134,
                   capacity=512)
-    cfg = H.config_of(w)
+    cfg = H.config_of(w, flags=spla.FLAG_SEPARATE_KERNELS if separate else 0)
     cache = spla.SplaCache(cfg, dev)
     H.fill_cache(w, cache, device=dev)
     torch.cuda.synchronize()
@@ -207,12 +208,13 @@ def test_step_at_capacity_leaves_the_state_unchanged(dev):
 
 @pytest.mark.parametrize("d,B,k", [(128, 128, 16), (128, 64, 32)])
 def test_fused_step_equals_separate_step(dev, d, B, k):
-    """spla_step on the single-launch kernel folds the token's rank-one update
-    of S_bar into the rows its sparse items read; three steps must leave the
-    same cache (statistics, S_bar, z_bar, K/V rows, lengths) and give the
-    same outputs and selections, bit for bit, as the separate launches (which
-    append with the single-token kernel), also for a sequence at capacity,
-    and match the oracle."""
+    """spla_step folds the token's rank-one update of S_bar into the rows the
+    decode's sparse pass reads, on the single launch and on the separate
+    launches alike; three steps must leave the same cache (statistics,
+    S_bar, z_bar, K/V rows, lengths) and give the same outputs and
+    selections, bit for bit, on both, also for a sequence at capacity. The
+    state after the steps matches the oracle's state built from every row
+    the cache holds, and the outputs match the oracle."""
     cap = 32 * B
     w = si.custom(f"fstep{B}", 3, 8, 2, d, B, k, [cap - 700, 17 * B + 5, cap], kind="drift",
                   code=135 + B, capacity=cap)
@@ -243,6 +245,15 @@ def test_fused_step_equals_separate_step(dev, d, B, k):
     L = w.lengths[1] + 3
     kl = caches[0].k_logical()[1, :, :L].float().cpu().numpy()
     vl = caches[0].v_logical()[1, :, :L].float().cpu().numpy()
+    S, z = (x.cpu().numpy() for x in caches[0].state_logical())
+    for b in range(3):
+        Lb = min(w.lengths[b] + 3, cap)
+        kb = caches[0].k_logical()[b, :, :Lb].float().cpu().numpy()
+        vb = caches[0].v_logical()[b, :, :Lb].float().cpu().numpy()
+        for h in range(2):
+            st = O.build_state(kb[h], vb[h], Lb, B)
+            np.testing.assert_allclose(S[b, h], st.s_bar, rtol=2e-4, atol=2e-4)
+            np.testing.assert_allclose(z[b, h], st.z_bar, rtol=2e-5, atol=1e-5)
     for h in range(2):
         st = O.build_state(kl[h], vl[h], L, B)
         r = O.decode_kv_head(q[1, h * 4:(h + 1) * 4], st, kl[h], vl[h],
