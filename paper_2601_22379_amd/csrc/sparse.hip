@@ -207,7 +207,8 @@ __global__ __launch_bounds__(256) void sparse_valu_kernel(
 // GC: accumulator columns per kind (>= G). The selection's LDS (R > 0) lies
 // over the accumulators, which sparse_body writes only after the selection.
 template <int D, int BLK, int R, int GC, bool STEP>
-__global__ __launch_bounds__(256) void sparse_mfma_kernel(
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(GC <= 4 ? 3 : 2)))
+void sparse_mfma_kernel(
     Dims m, float s, const bf16_t* __restrict__ kc, const bf16_t* __restrict__ vc,
     const bf16_t* __restrict__ q, float* __restrict__ S, float* __restrict__ zbar,
     const int32_t* __restrict__ sel, int32_t* __restrict__ meta, int stride,
@@ -228,25 +229,43 @@ __global__ __launch_bounds__(256) void sparse_mfma_kernel(
   __shared__ int32_t s_sel[R > 0 ? SPLA_MAX_TOP_K : 1];
   __shared__ int32_t s_meta[4];
   const int bh = blockIdx.y;
+  const int x = (int)blockIdx.x;
   SparseRegs r;
-  sparse_prologue<D, GC>(m, q, S, zbar, bh, (int)blockIdx.x, (int)gridDim.x, r, sm);
-  if constexpr (STEP) step_rank1<D>(m, k_step, v_step, appended, S, zbar, bh, r);
-  sparse_linear<D, GC>(m, S, bh, r, sm);
-  if constexpr (R > 0) {
+  if constexpr (R == 0) {
+    // the selection is known at the start: the step's keys and values are
+    // loaded first, behind only the query and S_bar loads, so that their
+    // latency overlaps the prologue's arithmetic (loads complete in order)
+    const int e = sparse_step_entry<BLK>(x);
+    const int blk_sel = e < m.k ? sel[(int64_t)bh * m.k + e] : -1;
+    int L = meta[bh * 4 + 2];
+    uint4 raw[D / 32];
+    sparse_prologue_load<D, GC>(m, q, S, zbar, bh, x, (int)gridDim.x, r, raw);
+    StepIn<D> sin;
+    if constexpr (STEP) step_load<D>(m, k_step, v_step, appended, bh, sin);
+    SparseKV<D> kv;
+    const int blk = sparse_step_block<BLK>(m, blk_sel, L, x, &kv.n_valid);
+    sparse_load<D, BLK>(m, kc, vc, blk < 0 ? 0 : blk, bh, x, table, kv);
+    sparse_prologue_finish<D, GC>(m, raw, sm);
+    if constexpr (STEP) step_apply<D>(m, sin, S, zbar, bh, r);
+    sparse_linear<D, GC>(m, S, bh, r, sm);
+    floatx4 acc_o[D / 16];
+#pragma unroll
+    for (int t = 0; t < D / 16; ++t) acc_o[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+    float m_run = -INFINITY, l_run = 0.f;
+    if (kv.n_valid > 0) sparse_mma<D, GC>(s, kv, sm, acc_o, m_run, l_run);
+    sparse_record<D, false, GC>(m, acc_o, m_run, l_run, bh, x, (int)gridDim.x, r, sm, part,
+                                stride, -1);
+  } else {  // every workgroup makes its head's selection itself
+    sparse_prologue<D, GC>(m, q, S, zbar, bh, x, (int)gridDim.x, r, sm);
+    sparse_linear<D, GC>(m, S, bh, r, sm);
     select_blocks<256, R, SWN, false>(m, bh, seq_lens[bh / m.hkv], e_vals, tile_part, ssm, s_sel,
-                                      s_meta,
-                                      blockIdx.x == 0 && sel_out ? sel_out + (int64_t)bh * m.k
-                                                                 : nullptr);
+                                      s_meta, x == 0 && sel_out ? sel_out + (int64_t)bh * m.k
+                                                                : nullptr);
     __syncthreads();
-    if (blockIdx.x == 0 && threadIdx.x < 4) meta[bh * 4 + threadIdx.x] = s_meta[threadIdx.x];
-    const int e = sparse_step_entry<BLK>((int)blockIdx.x);
-    sparse_body<D, BLK, false, GC>(m, s, kc, vc, e < m.k ? s_sel[e] : -1, s_meta[2], bh,
-                                  (int)blockIdx.x, (int)gridDim.x, r, sm, part, stride, table);
-  } else {
-    const int e = sparse_step_entry<BLK>((int)blockIdx.x);
-    sparse_body<D, BLK, false, GC>(m, s, kc, vc, e < m.k ? sel[(int64_t)bh * m.k + e] : -1,
-                                  meta[bh * 4 + 2], bh, (int)blockIdx.x, (int)gridDim.x, r, sm,
-                                  part, stride, table);
+    if (x == 0 && threadIdx.x < 4) meta[bh * 4 + threadIdx.x] = s_meta[threadIdx.x];
+    const int e = sparse_step_entry<BLK>(x);
+    sparse_body<D, BLK, false, GC>(m, s, kc, vc, e < m.k ? s_sel[e] : -1, s_meta[2], bh, x,
+                                   (int)gridDim.x, r, sm, part, stride, table);
   }
 }
 

@@ -239,20 +239,14 @@ struct SparseRegs {
   float zq;
 };
 
-// With g = lane / 16 and j = lane % 16 (the MFMA column), the B operands of
-// the first product hold coordinates 32 ks + 8 g .. +7 of head j (columns
-// 0..7: q itself, for the exact-branch logits) or of head j - 8 (columns
-// 8..15: phi(q) as a bf16 hi + lo pair, for the linear weights); absent heads
-// are zero. The four lanes of a column (g = 0..3) hold all d coordinates of
-// its head, so the softmax of phi(q) needs only the two lane swaps. Also
-// issues the loads of this workgroup's rows of S_bar and z_bar (x of n_wg).
-// LIN = false: no share of the global term (no S_bar rows are loaded; ob and
-// zq stay zero), for the chunked prefill.
+// The loads of sparse_prologue: this lane's query elements (raw) and this
+// workgroup's rows of S_bar and z_bar (into r).
 template <int D, int GC, bool LIN = true>
-__device__ __forceinline__ void sparse_prologue(const Dims& m, const bf16_t* __restrict__ q,
-                                                const float* __restrict__ S,
-                                                const float* __restrict__ zbar, int bh, int x,
-                                                int n_wg, SparseRegs& r, SparseSmem<D, GC>& sm) {
+__device__ __forceinline__ void sparse_prologue_load(const Dims& m, const bf16_t* __restrict__ q,
+                                                     const float* __restrict__ S,
+                                                     const float* __restrict__ zbar, int bh,
+                                                     int x, int n_wg, SparseRegs& r,
+                                                     uint4 (&raw)[D / 32]) {
   constexpr int KS = D / 32;
   const int b = bh / m.hkv, h = bh % m.hkv;
   const int G = m.group;
@@ -262,7 +256,6 @@ __device__ __forceinline__ void sparse_prologue(const Dims& m, const bf16_t* __r
   const int head = exact_col ? j : j - 8;
   const bool live = head < G;
   const bf16_t* qrow = q + ((int64_t)b * m.hq + h * G + (live ? head : 0)) * D + 8 * g;
-  uint4 raw[KS];
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks) raw[ks] = *reinterpret_cast<const uint4*>(qrow + 32 * ks);
   lin_rows(D, x, n_wg, &r.row0, &r.nrows);
@@ -288,6 +281,19 @@ __device__ __forceinline__ void sparse_prologue(const Dims& m, const bf16_t* __r
     const float v = zbar[(int64_t)bh * D + (ok ? r.row0 + tid : 0)];
     r.zbv = ok ? v : 0.f;
   }
+}
+
+// The arithmetic of the prologue, from the query elements raw.
+template <int D, int GC>
+__device__ __forceinline__ void sparse_prologue_finish(const Dims& m, const uint4 (&raw)[D / 32],
+                                                       SparseSmem<D, GC>& sm) {
+  constexpr int KS = D / 32;
+  const int G = m.group;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int j = lane & 15, g = lane >> 4;
+  const bool exact_col = j < 8;
+  const int head = exact_col ? j : j - 8;
+  const bool live = head < G;
   // phi(q) of this lane's head (every lane computes it; columns 0..7 discard it)
   float xv[KS][8];
   float mx = -INFINITY;
@@ -342,6 +348,25 @@ __device__ __forceinline__ void sparse_prologue(const Dims& m, const bf16_t* __r
       }
     }
   }
+}
+
+// With g = lane / 16 and j = lane % 16 (the MFMA column), the B operands of
+// the first product hold coordinates 32 ks + 8 g .. +7 of head j (columns
+// 0..7: q itself, for the exact-branch logits) or of head j - 8 (columns
+// 8..15: phi(q) as a bf16 hi + lo pair, for the linear weights); absent heads
+// are zero. The four lanes of a column (g = 0..3) hold all d coordinates of
+// its head, so the softmax of phi(q) needs only the two lane swaps. Also
+// issues the loads of this workgroup's rows of S_bar and z_bar (x of n_wg).
+// LIN = false: no share of the global term (no S_bar rows are loaded; ob and
+// zq stay zero), for the chunked prefill.
+template <int D, int GC, bool LIN = true>
+__device__ __forceinline__ void sparse_prologue(const Dims& m, const bf16_t* __restrict__ q,
+                                                const float* __restrict__ S,
+                                                const float* __restrict__ zbar, int bh, int x,
+                                                int n_wg, SparseRegs& r, SparseSmem<D, GC>& sm) {
+  uint4 raw[D / 32];
+  sparse_prologue_load<D, GC, LIN>(m, q, S, zbar, bh, x, n_wg, r, raw);
+  sparse_prologue_finish<D, GC>(m, raw, sm);
 }
 
 // This workgroup's rows x of the global linear term (Eq. 15): ob and zq of r,
@@ -403,32 +428,47 @@ __device__ __forceinline__ void sparse_linear(const Dims& m, const float* __rest
 // phi(k) the softmax of the appended key over d computed exactly as the
 // single-token append does; the updated rows are written back. Nothing
 // happens for a sequence that received no token (at capacity).
+// The inputs of step_rank1, loaded ahead of their use by step_load: this
+// lane's key elements, this thread's value element, the tokens appended.
 template <int D>
-__device__ __forceinline__ void step_rank1(const Dims& m, const bf16_t* __restrict__ k_step,
-                                           const bf16_t* __restrict__ v_step,
-                                           const int32_t* __restrict__ appended, float* S,
-                                           float* zbar, int bh, SparseRegs& r) {
-  const int tid = threadIdx.x, lane = tid & 63;
-  if (appended[bh / m.hkv] <= 0) return;  // uniform over the workgroup
+struct StepIn {
   float x[D / 64];
+  float vc;
+  int app;
+};
+
+template <int D>
+__device__ __forceinline__ void step_load(const Dims& m, const bf16_t* __restrict__ k_step,
+                                          const bf16_t* __restrict__ v_step,
+                                          const int32_t* __restrict__ appended, int bh,
+                                          StepIn<D>& in) {
+  const int tid = threadIdx.x, lane = tid & 63;
+  in.app = appended[bh / m.hkv];
+#pragma unroll
+  for (int e = 0; e < D / 64; ++e)
+    in.x[e] = bf16_to_f32(k_step[(int64_t)bh * D + lane + 64 * e].bits);
+  in.vc = bf16_to_f32(v_step[(int64_t)bh * D + tid % D].bits);
+}
+
+template <int D>
+__device__ __forceinline__ void step_apply(const Dims& m, StepIn<D>& in, float* S, float* zbar,
+                                           int bh, SparseRegs& r) {
+  const int tid = threadIdx.x;
+  if (in.app <= 0) return;  // uniform over the workgroup
   float mx = -INFINITY;
 #pragma unroll
-  for (int e = 0; e < D / 64; ++e) {
-    x[e] = bf16_to_f32(k_step[(int64_t)bh * D + lane + 64 * e].bits);
-    mx = fmaxf(mx, x[e]);
-  }
+  for (int e = 0; e < D / 64; ++e) mx = fmaxf(mx, in.x[e]);
   mx = wave_max(mx);
   float sum = 0.f;
 #pragma unroll
   for (int e = 0; e < D / 64; ++e) {
-    x[e] = expf(x[e] - mx);
-    sum += x[e];
+    in.x[e] = expf(in.x[e] - mx);
+    sum += in.x[e];
   }
   sum = wave_sum(sum);
   float ph[D / 64];
 #pragma unroll
-  for (int e = 0; e < D / 64; ++e) ph[e] = x[e] / sum;
-  const float vc = bf16_to_f32(v_step[(int64_t)bh * D + tid % D].bits);
+  for (int e = 0; e < D / 64; ++e) ph[e] = in.x[e] / sum;
   float* Sh = S + (int64_t)bh * D * D;
 #pragma unroll
   for (int u = 0; u < kSparsePre; ++u) {
@@ -436,7 +476,7 @@ __device__ __forceinline__ void step_rank1(const Dims& m, const bf16_t* __restri
     const int row = r.row0 + e / D;  // uniform over the wavefront
     const float pr = lane_f32(ph[(row % D) / 64], row % 64);
     if (e < r.nrows * D) {
-      r.spre[u] = fmaf(pr, vc, r.spre[u]);
+      r.spre[u] = fmaf(pr, in.vc, r.spre[u]);
       Sh[r.row0 * D + e] = r.spre[u];
     }
   }
@@ -450,6 +490,16 @@ __device__ __forceinline__ void step_rank1(const Dims& m, const bf16_t* __restri
     r.zbv += pz;
     zbar[(int64_t)bh * D + row] = r.zbv;
   }
+}
+
+template <int D>
+__device__ __forceinline__ void step_rank1(const Dims& m, const bf16_t* __restrict__ k_step,
+                                           const bf16_t* __restrict__ v_step,
+                                           const int32_t* __restrict__ appended, float* S,
+                                           float* zbar, int bh, SparseRegs& r) {
+  StepIn<D> in;
+  step_load<D>(m, k_step, v_step, appended, bh, in);
+  step_apply<D>(m, in, S, zbar, bh, r);
 }
 
 // Selected block of this wavefront's step: entry p of the selection, where
@@ -473,143 +523,170 @@ __device__ __forceinline__ int sparse_step_entry(int x) {
 // as bf16 hi + lo pairs (about 16 mantissa bits); accumulation is fp32. CO:
 // the record is written with Mem<true> (merged by another workgroup of the
 // same launch).
-template <int D, int BLK, bool CO, int GC>
-__device__ __forceinline__ void sparse_body(const Dims& m, float s,
-                                            const bf16_t* __restrict__ kc,
-                                            const bf16_t* __restrict__ vc,
-                                            int blk_sel, int L,
-                                            int bh, int x, int n_wg, const SparseRegs& r,
-                                            SparseSmem<D, GC>& sm, float* __restrict__ part,
-                                            int stride,
-                                            const int32_t* __restrict__ table = nullptr,
-                                            int64_t rec_row = -1) {
-  constexpr int KS = D / 32;     // k-steps of the first product
-  constexpr int MT = D / 16;     // coordinate tiles of the second product
-  constexpr int CPB = BLK / 32;  // steps per block
-  const int G = m.group;
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int j = lane & 15, g = lane >> 4, i = lane & 15;
-  const int ch = (x * kSparseWaves + w) % CPB;
-  const bool exact_col = j < 8;
-  const int head = exact_col ? j : j - 8;
-  const bool live = head < G;
+// The keys and values of one wavefront's step, as loaded (k_off / v_off
+// order: chunk (mt KS + ks) 64 + lane and t 64 + lane), and how many of its
+// 32 tokens exist.
+template <int D>
+struct SparseKV {
+  bf16x8 ka[2][D / 32];
+  bf16x8 va[D / 16];
+  int n_valid;
+};
+
+// This wavefront's block and step: the block selected for it (blk_sel, -1 for
+// none; clipped to the last block) and its valid token count (0: nothing).
+template <int BLK>
+__device__ __forceinline__ int sparse_step_block(const Dims& m, int blk_sel, int& L, int x,
+                                                 int* n_valid) {
+  const int ch = (x * kSparseWaves + (int)(threadIdx.x >> 6)) % (BLK / 32);
   L = min(max(L, 0), m.cap);
   const int nb = (L + BLK - 1) / BLK;
   const int blk = blk_sel >= nb ? nb - 1 : blk_sel;
-  const int n_valid = (blk_sel >= 0 && nb > 0) ? min(32, block_count(L, BLK, blk) - ch * 32) : 0;
-  floatx4 acc_o[MT];
-#pragma unroll
-  for (int t = 0; t < MT; ++t) acc_o[t] = floatx4{0.f, 0.f, 0.f, 0.f};
-  float m_run = -INFINITY, l_run = 0.f;  // exact columns: max / sum; linear columns: sum
-  constexpr int NO = (GC * D + 255) / 256;  // outputs (head, coordinate) per thread
-  // loads and their use in one branch: a load issued in one branch and used
-  // in another leaves the compiler assuming it may still be in flight after
-  // them, and it then waits for every store before the record's next ones
-  if (n_valid > 0) {
-    // the step's keys and values, stored in load order (k_off, v_off):
-    // chunk (mt KS + ks) 64 + lane and t 64 + lane
-    bf16x8 ka[2][KS];
-    bf16x8 va[MT];
-    // the block's slot: per-sequence cache, or its page of a paged pool
-    // (table given; an entry out of range reads page 0)
-    int64_t step0;
-    if (table) {
-      const int p = block_page(m, table, bh, blk);
-      step0 = (((int64_t)(p < 0 ? 0 : p) * m.hkv + bh % m.hkv) * BLK + ch * 32) * D;
-    } else {
-      step0 = ((int64_t)bh * m.cap + (int64_t)blk * BLK + ch * 32) * D;
-    }
-    const bf16x8* kst = reinterpret_cast<const bf16x8*>(kc + step0) + lane;
-    const bf16x8* vst = reinterpret_cast<const bf16x8*>(vc + step0) + lane;
-#pragma unroll
-    for (int mt = 0; mt < 2; ++mt)
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) ka[mt][ks] = kst[(mt * KS + ks) * 64];
-#pragma unroll
-    for (int t = 0; t < MT; ++t) va[t] = vst[t * 64];
-    floatx4 sw[2];
-    float zinv[2];  // 1 / sum exp(k - max k) of this lane's key row, per tile
-#pragma unroll
-    for (int mt = 0; mt < 2; ++mt) {
-      sw[mt] = floatx4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks)
-        sw[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-            ka[mt][ks], __builtin_bit_cast(bf16x8, sm.qops[0][ks][lane]), sw[mt], 0, 0, 0);
-      // exp(k - max k) of this lane's key row (row i of the tile), spread over
-      // lanes i + 16 g'; the 1 / sum of phi(k) is applied to the result rows
-      float mx = -INFINITY;
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) mx = fmaxf(mx, (float)ka[mt][ks][e]);
-      mx = fmaxf(mx, xor16(mx));
-      mx = fmaxf(mx, xor32(mx));
-      const float mxl = mx * kLog2e;
-      // exp(k - max k) k-step by k-step, each step straight into its products
-      float sum = 0.f;
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        bf16x8 fh, fl;
-        float f[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          f[e] = __builtin_amdgcn_exp2f(fmaf((float)ka[mt][ks][e], kLog2e, -mxl));
-          sum += f[e];
-        }
-        split_bf16x8(f, fh, fl);
-        const bf16x8 ph = __builtin_bit_cast(bf16x8, sm.qops[1][ks][lane]);
-        const bf16x8 pl = __builtin_bit_cast(bf16x8, sm.qops[2][ks][lane]);
-        sw[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fh, ph, sw[mt], 0, 0, 0);
-        sw[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fh, pl, sw[mt], 0, 0, 0);
-        sw[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fl, ph, sw[mt], 0, 0, 0);
-      }
-      sum += xor16(sum);
-      sum += xor32(sum);
-      zinv[mt] = 1.0f / sum;
-    }
-    // tokens 8g .. 8g+7 of this step: tile 0 rows 4g..4g+3, tile 1 rows 4g..4g+3
-    // (result row 4g + r of tile t is token 8g + 4t + r; its 1 / Z sits in
-    // lane 4g + r)
-    float val[8];
-    float cmax = -INFINITY;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const bool ok = 8 * g + e < n_valid;
-      const float zi = __shfl(zinv[e >> 2], 4 * g + (e & 3), kWave);
-      const float xx = sw[e >> 2][e & 3];
-      val[e] = exact_col ? (ok ? xx * s : -INFINITY) : (ok ? xx * zi : 0.f);
-      cmax = fmaxf(cmax, val[e]);
-    }
-    cmax = fmaxf(cmax, xor16(cmax));
-    cmax = fmaxf(cmax, xor32(cmax));
-    float psum = 0.f;
-    bf16x8 bh8, bl8;
-    float pv[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      pv[e] = exact_col ? __builtin_amdgcn_exp2f((val[e] - cmax) * kLog2e) : val[e];
-      psum += pv[e];
-    }
-    split_bf16x8(pv, bh8, bl8);
-    psum += xor16(psum);
-    psum += xor32(psum);
-    m_run = exact_col ? cmax : -INFINITY;
-    l_run = psum;
-    if (n_valid < 32) {  // rows past the sequence end may hold anything: zero them
-#pragma unroll
-      for (int t = 0; t < MT; ++t)
-#pragma unroll
-        for (int e = 0; e < 8; ++e)
-          if (8 * g + e >= n_valid) va[t][e] = (__bf16)0.f;
-    }
-#pragma unroll
-    for (int t = 0; t < MT; ++t) {
-      acc_o[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va[t], bh8, acc_o[t], 0, 0, 0);
-      acc_o[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va[t], bl8, acc_o[t], 0, 0, 0);
-    }
+  *n_valid = (blk_sel >= 0 && nb > 0) ? min(32, block_count(L, BLK, blk) - ch * 32) : 0;
+  return blk;
+}
+
+// Issues the loads of step ch of block blk of (sequence, KV head) bh: from the
+// per-sequence cache, or from the block's page of a paged pool (table given;
+// an entry out of range reads page 0). blk >= 0.
+template <int D, int BLK>
+__device__ __forceinline__ void sparse_load(const Dims& m, const bf16_t* __restrict__ kc,
+                                            const bf16_t* __restrict__ vc, int blk, int bh,
+                                            int x, const int32_t* __restrict__ table,
+                                            SparseKV<D>& kv) {
+  constexpr int KS = D / 32, MT = D / 16;
+  const int lane = threadIdx.x & 63;
+  const int ch = (x * kSparseWaves + (int)(threadIdx.x >> 6)) % (BLK / 32);
+  int64_t step0;
+  if (table) {
+    const int p = block_page(m, table, bh, blk);
+    step0 = (((int64_t)(p < 0 ? 0 : p) * m.hkv + bh % m.hkv) * BLK + ch * 32) * D;
+  } else {
+    step0 = ((int64_t)bh * m.cap + (int64_t)blk * BLK + ch * 32) * D;
   }
-  // ---- merge the four wavefronts of the workgroup into one record
+  const bf16x8* kst = reinterpret_cast<const bf16x8*>(kc + step0) + lane;
+  const bf16x8* vst = reinterpret_cast<const bf16x8*>(vc + step0) + lane;
+#pragma unroll
+  for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) kv.ka[mt][ks] = kst[(mt * KS + ks) * 64];
+#pragma unroll
+  for (int t = 0; t < MT; ++t) kv.va[t] = vst[t * 64];
+}
+
+// The two products of one step (n_valid > 0): S = K [q | phi(q)]^T, the
+// step's softmax over the exact columns, and acc_o = V^T P; m_run / l_run get
+// the step's max and sum (exact columns) or the sum of the linear weights.
+template <int D, int GC>
+__device__ __forceinline__ void sparse_mma(float s, SparseKV<D>& kv, SparseSmem<D, GC>& sm,
+                                           floatx4 (&acc_o)[D / 16], float& m_run,
+                                           float& l_run) {
+  constexpr int KS = D / 32;     // k-steps of the first product
+  constexpr int MT = D / 16;     // coordinate tiles of the second product
+  const int lane = threadIdx.x & 63;
+  const int j = lane & 15, g = lane >> 4;
+  const bool exact_col = j < 8;
+  const int n_valid = kv.n_valid;
+  floatx4 sw[2];
+  float zinv[2];  // 1 / sum exp(k - max k) of this lane's key row, per tile
+#pragma unroll
+  for (int mt = 0; mt < 2; ++mt) {
+    sw[mt] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+      sw[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+          kv.ka[mt][ks], __builtin_bit_cast(bf16x8, sm.qops[0][ks][lane]), sw[mt], 0, 0, 0);
+    // exp(k - max k) of this lane's key row (row i of the tile), spread over
+    // lanes i + 16 g'; the 1 / sum of phi(k) is applied to the result rows
+    float mx = -INFINITY;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) mx = fmaxf(mx, (float)kv.ka[mt][ks][e]);
+    mx = fmaxf(mx, xor16(mx));
+    mx = fmaxf(mx, xor32(mx));
+    const float mxl = mx * kLog2e;
+    // exp(k - max k) k-step by k-step, each step straight into its products
+    float sum = 0.f;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      bf16x8 fh, fl;
+      float f[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        f[e] = __builtin_amdgcn_exp2f(fmaf((float)kv.ka[mt][ks][e], kLog2e, -mxl));
+        sum += f[e];
+      }
+      split_bf16x8(f, fh, fl);
+      const bf16x8 ph = __builtin_bit_cast(bf16x8, sm.qops[1][ks][lane]);
+      const bf16x8 pl = __builtin_bit_cast(bf16x8, sm.qops[2][ks][lane]);
+      sw[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fh, ph, sw[mt], 0, 0, 0);
+      sw[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fh, pl, sw[mt], 0, 0, 0);
+      sw[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fl, ph, sw[mt], 0, 0, 0);
+    }
+    sum += xor16(sum);
+    sum += xor32(sum);
+    zinv[mt] = 1.0f / sum;
+  }
+  // tokens 8g .. 8g+7 of this step: tile 0 rows 4g..4g+3, tile 1 rows 4g..4g+3
+  // (result row 4g + r of tile t is token 8g + 4t + r; its 1 / Z sits in
+  // lane 4g + r)
+  float val[8];
+  float cmax = -INFINITY;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const bool ok = 8 * g + e < n_valid;
+    const float zi = __shfl(zinv[e >> 2], 4 * g + (e & 3), kWave);
+    const float xx = sw[e >> 2][e & 3];
+    val[e] = exact_col ? (ok ? xx * s : -INFINITY) : (ok ? xx * zi : 0.f);
+    cmax = fmaxf(cmax, val[e]);
+  }
+  cmax = fmaxf(cmax, xor16(cmax));
+  cmax = fmaxf(cmax, xor32(cmax));
+  float psum = 0.f;
+  bf16x8 bh8, bl8;
+  float pv[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    pv[e] = exact_col ? __builtin_amdgcn_exp2f((val[e] - cmax) * kLog2e) : val[e];
+    psum += pv[e];
+  }
+  split_bf16x8(pv, bh8, bl8);
+  psum += xor16(psum);
+  psum += xor32(psum);
+  m_run = exact_col ? cmax : -INFINITY;
+  l_run = psum;
+  if (n_valid < 32) {  // rows past the sequence end may hold anything: zero them
+#pragma unroll
+    for (int t = 0; t < MT; ++t)
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        if (8 * g + e >= n_valid) kv.va[t][e] = (__bf16)0.f;
+  }
+#pragma unroll
+  for (int t = 0; t < MT; ++t) {
+    acc_o[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kv.va[t], bh8, acc_o[t], 0, 0, 0);
+    acc_o[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kv.va[t], bl8, acc_o[t], 0, 0, 0);
+  }
+}
+
+// Merges the four wavefronts' accumulators into the record of workgroup x:
+// row bh of the records, or rec_row (the chunked prefill keeps one row per
+// (sequence, KV head, position)).
+template <int D, bool CO, int GC>
+__device__ __forceinline__ void sparse_record(const Dims& m, const floatx4 (&acc_o)[D / 16],
+                                              float m_run, float l_run, int bh, int x, int n_wg,
+                                              const SparseRegs& r, SparseSmem<D, GC>& sm,
+                                              float* __restrict__ part, int stride,
+                                              int64_t rec_row) {
+  constexpr int MT = D / 16;
+  constexpr int NO = (GC * D + 255) / 256;  // outputs (head, coordinate) per thread
+  const int G = m.group;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int j = lane & 15, g = lane >> 4;
+  const bool exact_col = j < 8;
+  const int head = exact_col ? j : j - 8;
+  const bool live = head < G;
   if (live) {  // only the live columns: exact heads to 0 .., linear heads to GC ..
     const int cj = exact_col ? head : GC + head;
 #pragma unroll
@@ -622,8 +699,6 @@ __device__ __forceinline__ void sparse_body(const Dims& m, float s,
     sm.l[w][lane] = l_run;
   }
   __syncthreads();
-  // the record of workgroup x: row bh of the records, or rec_row (the
-  // chunked prefill keeps one row per (sequence, KV head, position))
   float* rec = part + ((rec_row >= 0 ? rec_row : (int64_t)bh) * n_wg + x) * stride;
 #pragma unroll
   for (int i = 0; i < NO; ++i) {
@@ -657,6 +732,47 @@ __device__ __forceinline__ void sparse_body(const Dims& m, float s,
     Mem<CO>::st(rec + 16 + tid, l);
     Mem<CO>::st(rec + 32 + tid, r.zq - zw);
   }
+}
+
+// One 32-token step of one selected block per wavefront, then the record of
+// workgroup x (of n_wg) of sequence x KV head bh. blk_sel: this wavefront's
+// block (entry sparse_step_entry of the selection; -1 for none); L: the
+// sequence length. For the two 16-row tiles of a step the key row loaded by
+// lane l is token 8 (i / 4) + 4 tile + (i % 4), i = l % 16 (the bf16 cache
+// stores each step in exactly this order: k_off, v_off), so that after
+// S = K [Q | phi(Q)]^T the accumulator rows held by lane l are exactly the
+// tokens 8 g .. 8 g + 7 of the step, in order - the layout the second product
+// needs for its B operand. Columns 0..7 carry the exact-branch logits of heads
+// 0..G-1, columns 8..15 the linear weights <phi(q), phi(k)> of the same heads;
+// one accumulator holds both. phi(k) and the probabilities enter the products
+// as bf16 hi + lo pairs (about 16 mantissa bits); accumulation is fp32. CO:
+// the record is written with Mem<true> (merged by another workgroup of the
+// same launch).
+template <int D, int BLK, bool CO, int GC>
+__device__ __forceinline__ void sparse_body(const Dims& m, float s,
+                                            const bf16_t* __restrict__ kc,
+                                            const bf16_t* __restrict__ vc,
+                                            int blk_sel, int L,
+                                            int bh, int x, int n_wg, const SparseRegs& r,
+                                            SparseSmem<D, GC>& sm, float* __restrict__ part,
+                                            int stride,
+                                            const int32_t* __restrict__ table = nullptr,
+                                            int64_t rec_row = -1) {
+  constexpr int MT = D / 16;
+  SparseKV<D> kv;
+  const int blk = sparse_step_block<BLK>(m, blk_sel, L, x, &kv.n_valid);
+  floatx4 acc_o[MT];
+#pragma unroll
+  for (int t = 0; t < MT; ++t) acc_o[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+  float m_run = -INFINITY, l_run = 0.f;  // exact columns: max / sum; linear columns: sum
+  // loads and their use in one branch: a load issued in one branch and used
+  // in another leaves the compiler assuming it may still be in flight after
+  // them, and it then waits for every store before the record's next ones
+  if (kv.n_valid > 0) {
+    sparse_load<D, BLK>(m, kc, vc, blk, bh, x, table, kv);
+    sparse_mma<D, GC>(s, kv, sm, acc_o, m_run, l_run);
+  }
+  sparse_record<D, CO, GC>(m, acc_o, m_run, l_run, bh, x, n_wg, r, sm, part, stride, rec_row);
 }
 
 }  // namespace spla
