@@ -1,5 +1,6 @@
 // Block scoring kernel (Sec. 3.1): one workgroup per (sequence, KV head,
-// tile of 64 blocks) item; every item's loads are in flight from the start.
+// tile of 64 blocks) item; every item's loads are in flight from the start
+// (after the sequence length, which skips the tiles past the end).
 // The per-tile arithmetic is score_items (spla_score.h).
 #include "spla_kernels.h"
 #include "spla_score.h"
@@ -14,6 +15,10 @@ __global__ __launch_bounds__(256) void score_kernel(
   __shared__ ScoreSmem<G> sm;
   const int per = (m.n_tiles + NT - 1) / NT;  // items per (sequence, KV head)
   const int t = ((int)blockIdx.x / per) * m.n_tiles + ((int)blockIdx.x % per) * NT;
+  // a tile wholly past the sequence end is neither read nor scored: the
+  // selection reads the tiles that hold units only
+  const int L = min(max(seq_lens[t / m.n_tiles / m.hkv], 0), m.cap);
+  if ((t % m.n_tiles) * kTileBlocks * m.us >= L) return;
   score_items<G, T, D, false, NT>(m, stats, seq_lens, q, s, first_order, t, e_vals, tile_part,
                                   sm);
 }
