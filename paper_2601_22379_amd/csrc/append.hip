@@ -579,6 +579,17 @@ __global__ __launch_bounds__(256) void append_one_kernel(
                    (int)blockIdx.x - D / 16, bh, D, D);
 }
 
+// The statistics units and K/V rows of a single-token append alone (the
+// state's rank-one update is applied elsewhere): append_unit, d threads.
+template <typename T>
+__global__ __launch_bounds__(128) void append_unit_kernel(
+    Dims m, T* __restrict__ kc, T* __restrict__ vc, float* __restrict__ stats,
+    const int32_t* __restrict__ seq_lens, int32_t* __restrict__ err, const T* __restrict__ k_new,
+    const T* __restrict__ v_new, const int32_t* __restrict__ table) {
+  append_unit<T>(m, kc, vc, stats, seq_lens, err, k_new, v_new, 1, nullptr, table,
+                 (int)blockIdx.x, (int)blockIdx.y, m.d, m.d);
+}
+
 // seq_lens[b] += the tokens appended; appended (if not NULL) receives that
 // count per sequence.
 __global__ void append_finish_kernel(Dims m, int32_t* __restrict__ seq_lens, int max_new,
@@ -662,10 +673,10 @@ template <typename T, int D>
 static void append_one_td(const Dims& m, const spla_cache& c, const void* k_new,
                           const void* v_new, hipStream_t st, bool rank1) {
   if (!rank1) {  // statistics and rows only
-    hipLaunchKernelGGL(append_blocks_kernel<T>, dim3((unsigned)units_of_one(m), (unsigned)m.bh),
-                       dim3(256), 0, st, m, (T*)c.k_cache, (T*)c.v_cache, c.blk_stats,
-                       c.seq_lens, c.err_flags, (const T*)k_new, (const T*)v_new, 1, nullptr,
-                       m.pages > 0 ? c.block_table : nullptr, (int64_t)D, (int64_t)D);
+    hipLaunchKernelGGL(append_unit_kernel<T>, dim3((unsigned)units_of_one(m), (unsigned)m.bh),
+                       dim3(D), 0, st, m, (T*)c.k_cache, (T*)c.v_cache, c.blk_stats, c.seq_lens,
+                       c.err_flags, (const T*)k_new, (const T*)v_new,
+                       m.pages > 0 ? c.block_table : nullptr);
     return;
   }
   hipLaunchKernelGGL((append_one_kernel<T, D>), dim3((unsigned)(D / 16 + units_of_one(m)),
