@@ -79,10 +79,14 @@ def copy_calibration(dev):
 def dominant_bytes(w, ab, kernel):
     """Algorithmic bytes one launch of the dominant kernel moves: the whole
     decode (everything but the append) for the single-launch kernel, the
-    statistics plus the queries for the scoring kernel."""
+    statistics plus the queries for the scoring kernel, the selected rows,
+    the state and the queries for the sparse pass."""
+    q = w.batch * w.n_q_heads * w.head_dim * (4 if w.dtype == "f32" else 2)
     if kernel == "decode":
         return ab["total"] - ab["append"]
-    return ab["stats"] + w.batch * w.n_q_heads * w.head_dim * (4 if w.dtype == "f32" else 2)
+    if kernel == "sparse":  # selected rows, the state (written back too by a step), queries
+        return ab["selected_kv"] + ab["state"] * (2 if w.appends_per_step else 1) + q
+    return ab["stats"] + q
 
 
 
@@ -432,11 +436,11 @@ def _kernel_short(name):
     return name.split("(")[0].replace("void ", "")
 
 
-def trace_summary(trace_dir, workload, command, out_path):
+def trace_summary(trace_dir, workload, command, out_path, path="decode"):
     """Per-kernel averages of a `rocprofv3 --kernel-trace --stats` pass."""
     import csv
     rows = list(csv.DictReader(open(os.path.join(trace_dir, "run_kernel_stats.csv"))))
-    lines = [f"# SPLA decode, {workload}: kernel trace", "",
+    lines = [f"# SPLA {path}, {workload}: kernel trace", "",
              f"command: `{command}`", "",
              "| kernel | calls | avg us | min us | max us |", "|---|---|---|---|---|"]
     for r in rows:
@@ -490,7 +494,8 @@ def traffic_summary(fetch_dir, write_dir, workload, commands, out_md, kernel, ke
         fr, wr = fetch[k] * f_scale * 1024, write.get(k, 0.0) * w_scale * 1024
         lines.append(f"| {_kernel_short(k)} | {fetch[k]:.1f} | {write.get(k, 0.0):.1f} | "
                      f"{fr / 1e6:.3f} | {wr / 1e6:.3f} |")
-        if f"{kernel}_kernel" in k:
+        if f"::{kernel}_" in k:
+            assert dom is None, f"several {kernel} kernels in the counter passes"
             dom = (fr, wr)
     assert dom is not None, f"no {kernel} kernel in the counter passes"
     lines += ["", f"{kernel} kernel: algorithmic {kernel_bytes / 1e6:.3f} MB per dispatch, counted "
@@ -588,7 +593,9 @@ def run_workload(w, R, dev, K, W, headline=False, no_graph=False):
         return c.decode(q, gamma, out, sels[r], events)
 
     launched = spla.decode_phases(cfg)
-    dom = "decode" if "decode" in launched else "score"
+    # dominant kernel: the single launch, else the longer of the statistics
+    # scan and the sparse pass (decided from their per-launch events below)
+    cands = ["decode"] if "decode" in launched else ["score", "sparse"]
     for s in range(W):
         one(s, outs[0])
     torch.cuda.synchronize()
@@ -643,15 +650,17 @@ def run_workload(w, R, dev, K, W, headline=False, no_graph=False):
     torch.cuda.synchronize()
     dist = percentiles([a.elapsed_time(b) * 1e3 for a, b in ev])
 
-    # events around the dominant kernel only, recorded by the library
-    dev_ev = [spla.make_events([dom]) for _ in range(K)]
+    # events around the candidate kernels only, recorded by the library
+    dev_ev = [spla.make_events(cands) for _ in range(K)]
     off += K if appending else 0
     torch.cuda.synchronize()
     for s in range(K):
         one(off + s, outs[s], events=dev_ev[s][0])
     torch.cuda.synchronize()
-    dom_us_events = float(np.mean([e[1][dom][0].elapsed_time(e[1][dom][1])
-                                   for e in dev_ev])) * 1e3
+    ev_us = {c: float(np.mean([e[1][c][0].elapsed_time(e[1][c][1]) for e in dev_ev])) * 1e3
+             for c in cands}
+    dom = max(cands, key=lambda c: ev_us[c])
+    dom_us_events = ev_us[dom]
     # a step that is one launch of the dominant kernel and nothing else: the
     # timed region over the launches is its average launch duration, without
     # per-launch event records (whose own cost lengthens each launch)
@@ -673,7 +682,7 @@ def run_workload(w, R, dev, K, W, headline=False, no_graph=False):
     trace_md = os.path.join(ROOT, "profiles", f"decode_{w.name}_kernel_trace.md")
     if os.path.exists(trace_md):
         for ln in open(trace_md):
-            if ln.startswith(f"| spla::{dom}_kernel"):
+            if ln.startswith(f"| spla::{dom}_"):
                 prof_us = float(ln.split("|")[3])
                 break
     leg = {"latency_us": round(ms_per_step * 1e3, 3),
@@ -798,7 +807,7 @@ def main():
                     help="write the profiles/ summary of a kernel-trace pass in DIR and exit")
     ap.add_argument("--traffic-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="write the profiles/ traffic summary of two counter passes and exit")
-    ap.add_argument("--kernel", default="decode", choices=["decode", "score"],
+    ap.add_argument("--kernel", default="decode", choices=["decode", "score", "sparse"],
                     help="dominant kernel of a --traffic-summary")
     ap.add_argument("--command", action="append", default=[],
                     help="profiling command quoted in a summary (repeatable)")
@@ -806,12 +815,13 @@ def main():
     if args.trace_summary or args.traffic_summary:
         import spla_inputs as si
         w = si.config(args.config)
-        tag = f"decode_{w.name}" + (STRIDED_TAG if args.strided_only else "")
+        path = "prefill" if args.prefill_only else ("append" if args.append_only else "decode")
+        tag = f"{path}_{w.name}" + (STRIDED_TAG if args.strided_only else "")
         if args.trace_summary:
             label = w.name + (", strided selection windows C = 32, s = 16"
                               if args.strided_only else "")
             trace_summary(args.trace_summary, label, " && ".join(args.command),
-                          os.path.join(ROOT, "profiles", f"{tag}_kernel_trace.md"))
+                          os.path.join(ROOT, "profiles", f"{tag}_kernel_trace.md"), path)
         if args.traffic_summary:
             ab = si.algorithmic_bytes(w, None)
             variant = STRIDED_TAG if args.strided_only else ""
