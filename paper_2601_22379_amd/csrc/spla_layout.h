@@ -20,6 +20,7 @@ constexpr int kTileBlocks = 64;   // blocks per statistics tile (one wavefront)
 constexpr int kSubTokens = 32;    // tokens per sparse-pass sub-tile
 constexpr int kAppendChunkTarget = 512;   // append state-partial workgroups to aim for
 constexpr int kMaxWindows = 16384;  // strided selection windows per sequence at capacity
+constexpr int kSliceBlocks = 1024;  // blocks per slice of the two-stage selection
 
 SPLA_HD int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 SPLA_HD int64_t align_up(int64_t a, int64_t b) { return ceil_div(a, b) * b; }
@@ -102,6 +103,10 @@ SPLA_HD int block_page(const Dims& m, const int32_t* table, int64_t bh, int64_t 
 // Whether the scoring units are strided selection windows rather than blocks.
 SPLA_HD bool windowed(const Dims& m) { return m.us != m.B || m.ul != m.B; }
 
+// The separate selection runs in two stages (slices, then a pick) past 4096
+// blocks per sequence; a single workgroup per (sequence, KV head) otherwise.
+SPLA_HD bool two_stage_select(const Dims& m) { return !windowed(m) && m.nb_cap > 4 * kSliceBlocks; }
+
 // blk_stats [bh][n_tiles][2][d/4][64][4]; returns the offset of the float4
 // holding coordinates 4*j4 .. 4*j4+3 of unit `blk`, part 0 (mean) or 1 (M2).
 SPLA_HD int64_t stats_off4(const Dims& m, int64_t bh, int64_t blk, int part, int j4) {
@@ -121,9 +126,13 @@ struct DecodeWs {
   int64_t meta;       // i32 [bh][4]               (n_selected, all_selected, length, 0)
   int64_t part;       // f32 [bh][n_wg][part_stride]  sparse workgroup partials
   int64_t appended;   // i32 [batch]               tokens a step appended (fused step)
+  int64_t cand_key;   // u32 [bh][n_sl][k]         two-stage selection: slice candidates' keys
+  int64_t cand_id;    // i32 [bh][n_sl][k]         ... their block ids (ascending per slice)
+  int64_t cand_n;     // i32 [bh][n_sl]            ... their count per slice
   int64_t sync;       // i32 [sync_layout(m).words]  counters of the single-launch decode;
                       //   zero between calls
   int64_t total;
+  int n_sl;           // slices of the two-stage selection
   int n_wg;           // sparse workgroups per (sequence, kv head)
   int blocks_per_wg;  // selected blocks per VALU-pass workgroup
   int part_stride;    // floats per record: header + acc[G][d] + accw[G][d]
@@ -193,6 +202,10 @@ SPLA_HD DecodeWs decode_ws_layout(const Dims& m) {
   w.meta = take((int64_t)m.bh * 4 * 4);
   w.part = take((int64_t)m.bh * w.n_wg * w.part_stride * 4);
   w.appended = take((int64_t)m.batch * 4);
+  w.n_sl = (int)ceil_div(m.nb_cap, kSliceBlocks);
+  w.cand_key = take((int64_t)m.bh * w.n_sl * m.k * 4);
+  w.cand_id = take((int64_t)m.bh * w.n_sl * m.k * 4);
+  w.cand_n = take((int64_t)m.bh * w.n_sl * 4);
   w.sync = take(sync_layout(m).words * 4);
   w.total = off;
   return w;

@@ -442,4 +442,281 @@ __device__ void select_blocks(const Dims& m, int bh, int seq_len,
   }
 }
 
+// ------------------------------------------------------------------------
+// Two-stage selection for long sequences. One workgroup per (sequence, KV
+// head) leaves most of the GPU idle when a head has tens of thousands of
+// blocks and there are few heads (one sequence of 1M tokens: 8 workgroups).
+// Instead, slices of kSliceBlocks blocks each take their own top-kp
+// candidates (kp = k - forced blocks) under the same order as select_blocks
+// (score descending, lower block id first), then one workgroup per head
+// picks the top kp among the candidates. Every block of the global top kp
+// has fewer than kp blocks ahead of it in its own slice, so the candidates
+// hold the whole top set and the result is select_blocks' exactly: the keys
+// are computed with the same arithmetic in the same order.
+
+constexpr int kSliceThreads = 256;
+constexpr int kSliceR = kSliceBlocks / kSliceThreads;     // blocks per thread
+constexpr int kSliceTiles = kSliceBlocks / kTileBlocks;   // 16 statistics tiles
+constexpr int kPickThreads = 1024;
+
+// The kp-th largest of the keys held R per thread by the NT threads (0: not
+// a candidate), found digit by digit as in select_blocks: keys above gt are
+// taken and, of the keys equal to eqv, the first eq_need in thread order.
+// Fewer than kp candidates: every candidate (gt = 0). hist: 4096 words,
+// zeroed by the caller before a barrier.
+template <int NT, int R>
+__device__ __forceinline__ void radix_cut(const uint32_t (&key)[R], uint32_t kp, uint32_t* hist,
+                                          uint32_t& gt, uint32_t& eqv, uint32_t& eq_need) {
+  gt = 0xFFFFFFFFu;
+  eqv = 0u;
+  eq_need = 0u;
+  uint32_t prefix = 0u, need = kp;
+#pragma unroll
+  for (int rd = 0; rd < 3; ++rd) {
+    const int sh = 20 - 10 * rd;
+    const uint32_t msk = rd == 0 ? 0x7FFu : 0x3FFu;
+    uint32_t* H = hist + (rd == 0 ? 0 : 1024 + 1024 * rd);
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      const bool in = (key[r] != 0u) & ((rd == 0) | ((key[r] >> (sh + 10)) == prefix));
+      if (__ballot(in) != 0ull) atomicAdd(&H[(key[r] >> sh) & msk], in ? 1u : 0u);
+    }
+    __syncthreads();
+    const RadixPick p = rd == 0 ? radix_pick<32>(H, need) : radix_pick<16>(H, need);
+    if (rd == 0 && p.total < need) {
+      gt = 0u;
+      return;
+    }
+    need -= p.above;
+    prefix = (prefix << 10) | p.digit;
+    if (need == p.cnt) {
+      const uint32_t lo = prefix << sh;
+      gt = lo == 0u ? 0u : lo - 1u;
+      return;
+    }
+    if (rd == 2) {
+      gt = prefix;
+      eqv = prefix;
+      eq_need = need;
+    }
+  }
+}
+
+// Slice sl (blocks sl kSliceBlocks ..) of sequence x KV head bh: the
+// candidates' keys and ids, ascending by id, to ck / ci (k slots) and their
+// count to *cn. Z_m comes from every tile partial of the head (TJ tiles per
+// lane), exactly as select_blocks forms it. Nothing for a head whose blocks
+// all fit in k (the pick selects them all). GM >= G: heads loaded.
+template <int TJ, int GM>
+__device__ void select_slice(const Dims& m, int bh, int sl, const int32_t* __restrict__ seq_lens,
+                             const float* __restrict__ e_vals,
+                             const double* __restrict__ tile_part, uint32_t* __restrict__ ck,
+                             int32_t* __restrict__ ci, int32_t* __restrict__ cn, float* sw,
+                             uint32_t* hist, uint32_t* scan) {
+  constexpr int R = kSliceR, NW = kSliceThreads / 64;
+  const int G = m.group, k = m.k;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int nbp = m.n_tiles * kTileBlocks;
+  const int kp = k - m.n_sink - m.n_local;
+  const int i0 = sl * kSliceBlocks + tid * R;
+  const double* tp = tile_part + (int64_t)bh * m.n_tiles * G * 2;
+  const float* ev = e_vals + (int64_t)bh * G * nbp;
+  // loads first: this wave's first head's tile partials, this thread's masses
+  double tm[TJ], ts[TJ];
+#pragma unroll
+  for (int j = 0; j < TJ; ++j) {
+    const int t = lane + 64 * j;
+    load_tile_part<false>(tp + (int64_t)(w < G ? w : 0) * m.n_tiles * 2, t,
+                          w < G && t < m.n_tiles, tm[j], ts[j]);
+  }
+  float e[GM][R];
+#pragma unroll
+  for (int h = 0; h < GM; ++h)
+    load_run<R, false>(ev, (int64_t)(h < G ? h : 0) * nbp + i0, h < G && i0 < nbp, e[h]);
+  const int L = min(max(seq_lens[bh / m.hkv], 0), m.cap);
+  const int nb = (L + m.B - 1) / m.B;
+  if (nb <= k || kp <= 0 || sl * kSliceBlocks >= nb) {  // uniform over the workgroup
+    if (tid == 0) *cn = 0;
+    return;
+  }
+  const int n_tu = (nb + kTileBlocks - 1) / kTileBlocks;
+  for (int x = tid; x < 1024; x += kSliceThreads)
+    reinterpret_cast<uint4*>(hist)[x] = make_uint4(0u, 0u, 0u, 0u);
+  // --- Z_m of heads m = w, w + NW, ... and the weights of this slice's tiles
+  const int jt = (sl * kSliceTiles) / 64, lt = (sl * kSliceTiles) % 64;  // slice tiles' lanes
+  for (int mm = w; mm < G; mm += NW) {
+    if (mm != w) {
+#pragma unroll
+      for (int j = 0; j < TJ; ++j) {
+        const int t = lane + 64 * j;
+        load_tile_part<false>(tp + (int64_t)mm * m.n_tiles * 2, t, t < m.n_tiles, tm[j], ts[j]);
+      }
+    }
+    double mx = -INFINITY;
+#pragma unroll
+    for (int j = 0; j < TJ; ++j)
+      if (lane + 64 * j < n_tu) mx = fmax(mx, tm[j]);
+    mx = wave_max_u(mx);
+    float et[TJ];
+    double s = 0.0;
+#pragma unroll
+    for (int j = 0; j < TJ; ++j) {
+      const bool on = lane + 64 * j < n_tu && tm[j] > -INFINITY;
+      const double d = on ? tm[j] - mx : 0.0;
+      const float dh = (float)d, dl = (float)(d - (double)dh);
+      const float eh = expf(dh);
+      et[j] = on ? fmaf(eh, dl, eh) : 0.f;
+      s += ts[j] * (double)et[j];
+    }
+    s = wave_sum_u(s);
+    const double inv = 1.0 / s;
+    float mine = 0.f;  // this lane's entry of register jt
+#pragma unroll
+    for (int j = 0; j < TJ; ++j) mine = j == jt ? et[j] : mine;
+    const float etv = __shfl(mine, lt + (lane & (kSliceTiles - 1)), kWave);
+    const int t = sl * kSliceTiles + lane;
+    if (lane < kSliceTiles && t < n_tu) sw[lane * G + mm] = (float)((double)etv * inv);
+  }
+  __syncthreads();
+  // --- keys (as select_blocks: fp64 sum over the heads in order)
+  const int tt = (i0 - sl * kSliceBlocks) / kTileBlocks;  // this thread's tile in the slice
+  const bool tile_on = sl * kSliceTiles + tt < n_tu;
+  double sc[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) sc[r] = 0.0;
+#pragma unroll
+  for (int h = 0; h < GM; ++h) {
+    if (h < G) {
+      const double wv = tile_on ? (double)sw[tt * G + h] : 0.0;
+#pragma unroll
+      for (int r = 0; r < R; ++r) sc[r] = fma((double)e[h][r], wv, sc[r]);
+    }
+  }
+  uint32_t key[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const int i = i0 + r;
+    const bool cand = (i < nb) & (i >= m.n_sink) & (i < nb - m.n_local);
+    key[r] = cand ? __float_as_uint((float)sc[r]) + 1u : 0u;
+  }
+  uint32_t gt, eqv, eq_need;
+  radix_cut<kSliceThreads, R>(key, (uint32_t)kp, hist, gt, eqv, eq_need);
+  // --- the candidates, ascending by id: (taken above) | (ties) << 16, one scan
+  bool tk[R], tq[R];
+  uint32_t na = 0u, ne = 0u;
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    tk[r] = (key[r] != 0u) & (key[r] > gt);
+    tq[r] = !tk[r] & (eq_need > 0u) & (key[r] == eqv);
+    na += tk[r] ? 1u : 0u;
+    ne += tq[r] ? 1u : 0u;
+  }
+  uint32_t tot_p;
+  const uint32_t before = block_excl_scan_u32<NW>(na | (ne << 16), scan, &tot_p);
+  uint32_t a_run = before & 0xFFFFu, e_run = before >> 16;
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const uint32_t pg = a_run + (e_run < eq_need ? e_run : eq_need);
+    const uint32_t pq = e_run < eq_need ? a_run + e_run : 0xFFFFFFFFu;
+    const uint32_t pos = tk[r] ? pg : (tq[r] ? pq : 0xFFFFFFFFu);
+    a_run += tk[r] ? 1u : 0u;
+    e_run += tq[r] ? 1u : 0u;
+    if (pos < (uint32_t)k) {
+      ck[pos] = key[r];
+      ci[pos] = i0 + r;
+    }
+  }
+  const uint32_t ta = tot_p & 0xFFFFu, te = tot_p >> 16;
+  if (tid == 0) *cn = (int)(ta + (te < eq_need ? te : eq_need));
+}
+
+// The pick of sequence x KV head bh from the candidates of its n_sl slices
+// (k slots each, ck / ci / cn as select_slice wrote them): the kp largest,
+// ties to the lower id, and the forced blocks, ascending, to sel[0 .. k)
+// (-1 padded) and so (if not NULL); meta4 as select_blocks writes it. R2:
+// candidate slots per thread (kPickThreads R2 >= n_sl k); the slots in
+// thread order are ascending by id.
+template <int R2>
+__device__ void select_pick(const Dims& m, int bh, int n_sl, const int32_t* __restrict__ seq_lens,
+                            const uint32_t* __restrict__ ck, const int32_t* __restrict__ ci,
+                            const int32_t* __restrict__ cn, int32_t* __restrict__ sel,
+                            int32_t* __restrict__ meta4, int32_t* __restrict__ so,
+                            uint32_t* hist, uint32_t* scan, int32_t* out) {
+  constexpr int NT = kPickThreads, NW = NT / 64;
+  const int k = m.k, tid = threadIdx.x;
+  const int kp = k - m.n_sink - m.n_local;
+  uint32_t key[R2];
+  int32_t id[R2];
+#pragma unroll
+  for (int r = 0; r < R2; ++r) {
+    const int q = tid * R2 + r, s = q / k, j = q % k;
+    const bool ok = s < n_sl;
+    const int qq = ok ? q : 0;
+    const int n = cn[ok ? s : 0];
+    const uint32_t kv = ck[qq];
+    const int32_t iv = ci[qq];
+    key[r] = ok && j < n ? kv : 0u;
+    id[r] = iv;
+  }
+  const int L = min(max(seq_lens[bh / m.hkv], 0), m.cap);
+  const int nb = (L + m.B - 1) / m.B;
+  if (nb <= k) {  // every block (or none) is selected
+    for (int x = tid; x < k; x += NT) {
+      const int v = x < nb ? x : -1;
+      sel[x] = v;
+      if (so) so[x] = v;
+    }
+    if (tid == 0 && meta4) {
+      meta4[0] = nb;
+      meta4[1] = 1;
+      meta4[2] = L;
+      meta4[3] = 0;
+    }
+    return;
+  }
+  for (int x = tid; x < 1024; x += NT) reinterpret_cast<uint4*>(hist)[x] = make_uint4(0u, 0u, 0u, 0u);
+  __syncthreads();
+  uint32_t gt = 0u, eqv = 0u, eq_need = 0u;
+  if (kp > 0) radix_cut<NT, R2>(key, (uint32_t)kp, hist, gt, eqv, eq_need);
+  bool tk[R2], tq[R2];
+  uint32_t na = 0u, ne = 0u;
+#pragma unroll
+  for (int r = 0; r < R2; ++r) {
+    tk[r] = (key[r] != 0u) & (key[r] > gt);
+    tq[r] = !tk[r] & (eq_need > 0u) & (key[r] == eqv);
+    na += tk[r] ? 1u : 0u;
+    ne += tq[r] ? 1u : 0u;
+  }
+  uint32_t tot_p;
+  const uint32_t before = block_excl_scan_u32<NW>(na | (ne << 16), scan, &tot_p);
+  uint32_t a_run = before & 0xFFFFu, e_run = before >> 16;
+  const int ns = m.n_sink;
+#pragma unroll
+  for (int r = 0; r < R2; ++r) {
+    const uint32_t pg = a_run + (e_run < eq_need ? e_run : eq_need);
+    const uint32_t pq = e_run < eq_need ? a_run + e_run : 0xFFFFFFFFu;
+    const uint32_t pos = tk[r] ? pg : (tq[r] ? pq : 0xFFFFFFFFu);
+    a_run += tk[r] ? 1u : 0u;
+    e_run += tq[r] ? 1u : 0u;
+    if (pos < (uint32_t)kp) out[ns + (int)pos] = id[r];
+  }
+  const uint32_t ta = tot_p & 0xFFFFu, te = tot_p >> 16;
+  const int taken = (int)(ta + (te < eq_need ? te : eq_need));
+  const int tot = ns + taken + m.n_local;  // <= k: taken <= kp
+  if (tid < ns) out[tid] = tid;
+  if (tid < m.n_local) out[ns + taken + tid] = nb - m.n_local + tid;
+  __syncthreads();
+  for (int x = tid; x < k; x += NT) {
+    const int v = x < tot ? out[x] : -1;
+    sel[x] = v;
+    if (so) so[x] = v;
+  }
+  if (tid == 0 && meta4) {
+    meta4[0] = tot;
+    meta4[1] = 0;
+    meta4[2] = L;
+    meta4[3] = tot;
+  }
+}
+
 }  // namespace spla
