@@ -548,7 +548,9 @@ def run_workload(w, R, dev, K, W, headline=False, no_graph=False):
     path and every output must match bit for bit, and every cache's device
     error word must be clear. A second pass brackets each step with events
     (median / p10 / p90), a third the dominant kernel. Returns the dict of
-    the workload's JSON object (plus the headline-only extras)."""
+    the workload's JSON object and the extras (separate-launch latency and
+    phases, graph replay; None for an appending workload that is not the
+    headline)."""
     import numpy as np
     import torch
 
@@ -704,13 +706,14 @@ def run_workload(w, R, dev, K, W, headline=False, no_graph=False):
     log(f"{w.name}: {ms_per_step * 1e3:.2f} us/step (per-step events median {dist['median']:.2f}, "
         f"p10 {dist['p10']:.2f}, p90 {dist['p90']:.2f}); {dom} kernel {dom_us:.2f} us "
         f"({dom_method}), {achieved:.0f} GB/s algorithmic")
-    if not headline:
+    if not headline and appending:
         del caches
         torch.cuda.synchronize()
         torch.cuda.empty_cache()
         return leg, None
 
-    # headline extras: the separate-kernel path's plain latency and phases
+    # extras: the separate-kernel path's plain latency and phases, and a graph
+    # replay of the steps
     sep_names = ["score", "select", "sparse", "merge"] + (["append"] if appending else [])
     for c in caches:
         c.cfg.flags |= spla.FLAG_SEPARATE_KERNELS
@@ -892,7 +895,8 @@ def main():
         wl = si.config(cid.strip())
         # the appending workload has 512 positions of room for all its steps
         kl = min(K, 100) if wl.appends_per_step else K
-        legs[wl.name], _ = run_workload(wl, replicas_for(wl, R), dev, kl, W)
+        leg, ex = run_workload(wl, replicas_for(wl, R), dev, kl, W)
+        legs[wl.name] = {**leg, **(ex or {})}
     if args.copy_calibration:
         copy_calibration(dev)
     cpu = None

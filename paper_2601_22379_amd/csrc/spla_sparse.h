@@ -265,13 +265,14 @@ __device__ __forceinline__ void sparse_prologue_load(const Dims& m, const bf16_t
     r.zbv = 0.f;
     r.nrows = 0;
   } else {
-    // loads issued whether or not in range (from row 0 when not): no branch
-    const bool s_pre = r.nrows * D <= kSparsePre * 256;
+    // the first kSparsePre * 256 / D rows (sparse_linear reads any further
+    // ones itself); loads issued whether or not in range (from row 0 when
+    // not): no branch
     const float* Sh = S + (int64_t)bh * D * D;
 #pragma unroll
     for (int u = 0; u < kSparsePre; ++u) {
       const int e = tid + 256 * u;
-      const bool ok = s_pre && e < r.nrows * D;
+      const bool ok = e < r.nrows * D;
       const float v = Sh[ok ? r.row0 * D + e : 0];
       r.spre[u] = ok ? v : 0.f;
     }
@@ -387,37 +388,47 @@ __device__ __forceinline__ void sparse_linear(const Dims& m, const float* __rest
   static_assert(NO <= 4, "ob holds four outputs");
   const int G = m.group, tid = threadIdx.x;
   const int row0 = r.row0, nrows = r.nrows;
-  const bool s_pre = nrows <= RMAX;
 #pragma unroll
   for (int u = 0; u < kSparsePre; ++u) sm.S[tid + 256 * u] = r.spre[u];
   if (tid < D) sm.zb[tid] = r.zbv;
   __syncthreads();  // the query operands, phi(q) and the S_bar rows are in LDS
-  // rows past nrows are zero in LDS; their phi(q) index is clamped
+  // the first RMAX rows from LDS (rows past nrows are zero there; their
+  // phi(q) index is clamped), in row order
+  const int c = tid % D;  // the coordinate of every output of this thread
+  float acc[NO];
 #pragma unroll
   for (int i = 0; i < NO; ++i) {
-    const int e = tid + 256 * i;
-    const int hh = e / D, c = e % D;
-    float acc = 0.f;
-    if (e < G * D) {
-      if (s_pre) {
+    const int hh = (tid + 256 * i) / D;
+    acc[i] = 0.f;
 #pragma unroll
-        for (int rr = 0; rr < RMAX; ++rr)
-          acc = fmaf(sm.phq[hh][min(row0 + rr, D - 1)], sm.S[rr * D + c], acc);
-      } else {
-        const float* Sb = S + (int64_t)bh * D * D;
-        for (int rr = row0; rr < row0 + nrows; ++rr) acc = fmaf(sm.phq[hh][rr], Sb[rr * D + c], acc);
+    for (int rr = 0; rr < RMAX; ++rr)
+      acc[i] = fmaf(sm.phq[hh < G ? hh : 0][min(row0 + rr, D - 1)], sm.S[rr * D + c], acc[i]);
+  }
+  // a workgroup with more rows (few sparse workgroups per head) reads the
+  // rest from global memory, eight rows per batch of loads, in row order
+  if (nrows > RMAX) {  // uniform over the workgroup
+    const float* Sb = S + (int64_t)bh * D * D + c;
+    const int rend = row0 + nrows;
+    for (int r0 = row0 + RMAX; r0 < rend; r0 += 8) {
+      float v[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) v[j] = Sb[(int64_t)(r0 + j < rend ? r0 + j : row0) * D];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float vj = r0 + j < rend ? v[j] : 0.f;
+#pragma unroll
+        for (int i = 0; i < NO; ++i) {
+          const int hh = (tid + 256 * i) / D;
+          acc[i] = fmaf(sm.phq[hh < G ? hh : 0][min(r0 + j, D - 1)], vj, acc[i]);
+        }
       }
     }
-    r.ob[i] = acc;
   }
+#pragma unroll
+  for (int i = 0; i < NO; ++i) r.ob[i] = tid + 256 * i < G * D ? acc[i] : 0.f;
   float zq = 0.f;
   if (tid < G) {
-    if (s_pre) {
-#pragma unroll
-      for (int rr = 0; rr < RMAX; ++rr) zq = fmaf(sm.phq[tid][min(row0 + rr, D - 1)], sm.zb[rr], zq);
-    } else {
-      for (int rr = 0; rr < nrows; ++rr) zq = fmaf(sm.phq[tid][row0 + rr], sm.zb[rr], zq);
-    }
+    for (int rr = 0; rr < nrows; ++rr) zq = fmaf(sm.phq[tid][row0 + rr], sm.zb[rr], zq);
   }
   r.zq = zq;
 }
