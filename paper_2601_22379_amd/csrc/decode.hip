@@ -234,9 +234,16 @@ void decode_kernel(FusedArgs a) {
   const int nb = (L + BLK - 1) / BLK;
   const int all_sel = nb <= m.k;
   const float* rec = a.part + (int64_t)bh * a.n_wg * a.stride;
-  for (int g = tid >> 6; g < G; g += 4)
-    merge_head<bf16_t, D, true>(m, a.eps, a.flags, a.gamma, all_sel, L, rec, a.n_wg, a.stride,
-                                a.out, bh, g);
+  if constexpr (G > 4) {  // two query heads per wavefront (merge_halves)
+    const int g = 2 * (tid >> 6);
+    if (g < G)
+      merge_head<bf16_t, D, true, false, true>(m, a.eps, a.flags, a.gamma, all_sel, L, rec,
+                                               a.n_wg, a.stride, a.out, bh, g);
+  } else {
+    for (int g = tid >> 6; g < G; g += 4)
+      merge_head<bf16_t, D, true>(m, a.eps, a.flags, a.gamma, all_sel, L, rec, a.n_wg, a.stride,
+                                  a.out, bh, g);
+  }
   if (tid == 0) store_agent(recs, 0);  // last, as for the item counter
 }
 

@@ -12,17 +12,23 @@
 namespace spla {
 
 // ---------------------------------------------------------------- merge
-// One single-wavefront workgroup per (sequence, KV head, query head): the
-// records of a head are read by G compute units rather than one.
+// One single-wavefront workgroup per (sequence, KV head, query head), or per
+// pair of query heads for groups of 5 or 6 (merge_halves): the records of a
+// head are read by several compute units rather than one.
 template <typename T, int D>
 __global__ __launch_bounds__(64) void merge_kernel(
     Dims m, float eps, uint32_t flags, const float* __restrict__ gamma,
     const int32_t* __restrict__ meta, const float* __restrict__ part, int n_rec, int stride,
     T* __restrict__ out) {
   const int bh = blockIdx.x;
-  merge_head<T, D, false>(m, eps, flags, gamma, meta[bh * 4 + 1], meta[bh * 4 + 2],
-                   part + (int64_t)bh * n_rec * stride, n_rec, stride, out, bh,
-                   (int)blockIdx.y);
+  if (merge_halves(m.group))  // uniform: two query heads per workgroup
+    merge_head<T, D, false, false, true>(m, eps, flags, gamma, meta[bh * 4 + 1],
+                                         meta[bh * 4 + 2], part + (int64_t)bh * n_rec * stride,
+                                         n_rec, stride, out, bh, 2 * (int)blockIdx.y);
+  else
+    merge_head<T, D, false>(m, eps, flags, gamma, meta[bh * 4 + 1], meta[bh * 4 + 2],
+                            part + (int64_t)bh * n_rec * stride, n_rec, stride, out, bh,
+                            (int)blockIdx.y);
 }
 
 // ------------------------------------------------------------ VALU pass
@@ -341,7 +347,8 @@ static void mfma_d(const Dims& m, float s, const spla_cache& c, const void* q, i
 template <typename T, int D>
 static void merge_td(const Dims& m, const spla_config& cfg, const float* gamma, void* out,
                      const DecodeWs& ws, char* base, hipStream_t st) {
-  hipLaunchKernelGGL((merge_kernel<T, D>), dim3(m.bh, m.group), dim3(64), 0, st, m, cfg.rms_eps,
+  const int gy = merge_halves(m.group) ? (m.group + 1) / 2 : m.group;
+  hipLaunchKernelGGL((merge_kernel<T, D>), dim3(m.bh, gy), dim3(64), 0, st, m, cfg.rms_eps,
                      cfg.flags, gamma, (const int32_t*)(base + ws.meta),
                      (const float*)(base + ws.part), ws.n_wg, ws.part_stride, (T*)out);
 }

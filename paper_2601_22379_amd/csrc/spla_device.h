@@ -113,6 +113,23 @@ __device__ __forceinline__ float wave_sum(float v) {
   v += dpp_rot<0xB1>(v);   // quad_perm [1,0,3,2]
   return v;
 }
+// The same over each half-wavefront (lanes 0..31, 32..63) on its own.
+__device__ __forceinline__ float half_wave_sum(float v) {
+  v += xor16(v);
+  v += dpp_rot<0x128>(v);
+  v += dpp_rot<0x124>(v);
+  v += dpp_rot<0x4E>(v);
+  v += dpp_rot<0xB1>(v);
+  return v;
+}
+__device__ __forceinline__ float half_wave_max(float v) {
+  v = fmaxf(v, xor16(v));
+  v = fmaxf(v, dpp_rot<0x128>(v));
+  v = fmaxf(v, dpp_rot<0x124>(v));
+  v = fmaxf(v, dpp_rot<0x4E>(v));
+  v = fmaxf(v, dpp_rot<0xB1>(v));
+  return v;
+}
 __device__ __forceinline__ float wave_max(float v) {
   v = fmaxf(v, xor32(v));
   v = fmaxf(v, xor16(v));

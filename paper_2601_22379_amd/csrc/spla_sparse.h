@@ -90,28 +90,39 @@ __device__ __forceinline__ void load_vec(const float* base, uint32_t off, float 
 // one record per lane; every load of a batch (and the gain row) is issued
 // before any arithmetic. CO: the records are read with Mem<true> (written
 // by other workgroups of the same launch).
+// HALF: each half-wavefront merges a query head of its own, g + (lane / 32)
+// (none past G), over every record, with headers in batches of 32: a
+// wavefront then merges two heads at once (groups of 5 or 6 heads; the
+// single-launch kernel and the separate merge use the same form, so their
+// outputs agree bit for bit).
 // ADD: the records carry no share of the global term (the chunked prefill
 // computes o_bar and <phi(q), z_bar> for every query in a kernel of its own);
 // obar_add (this query's G x D rows) and zq_add (its G values) are added to
 // the sums of the records' linear fields instead.
-template <typename T, int D, bool CO, bool ADD = false>
+template <typename T, int D, bool CO, bool ADD = false, bool HALF = false>
 __device__ __forceinline__ void merge_head(const Dims& m, float eps, uint32_t flags,
                                            const float* __restrict__ gamma, int all_sel, int L,
                                            const float* rec, int n_rec, int stride,
                                            T* __restrict__ out, int bh, int g,
                                            const float* __restrict__ obar_add = nullptr,
                                            const float* __restrict__ zq_add = nullptr) {
-  constexpr int E = D / 32;  // coordinates per lane
-  constexpr int NP = 8;      // record pairs per load batch
+  static_assert(!(ADD && HALF), "one head per wavefront with ADD");
+  constexpr int E = D / 32;            // coordinates per lane
+  constexpr int NP = 8;                // record pairs (HALF: records) per load batch
+  constexpr int HB = HALF ? 32 : 64;   // records per batch of headers
+  constexpr int RS = HALF ? NP : 2 * NP;  // records per batch of bodies
   const int b = bh / m.hkv, h = bh % m.hkv;
   const int G = m.group;
   const int lane = threadIdx.x & 63, hf = lane >> 5;
+  const int gh = HALF ? g + hf : g;       // this lane's head
+  const bool gon = gh < G;                // HALF with odd G: the last half idles
+  const int gg = gon ? gh : g;            // its row in the records
   const int c0 = E * (lane & 31);
-  const int64_t orow = ((int64_t)b * m.hq + h * G + g) * D + c0;
+  const int64_t orow = ((int64_t)b * m.hq + h * G + gg) * D + c0;
   const bool rla = !(flags & SPLA_FLAG_NO_RLA);
   float gm[E];
 #pragma unroll
-  for (int e = 0; e < E; ++e) gm[e] = gamma[(int64_t)(h * G + g) * D + c0 + e];
+  for (int e = 0; e < E; ++e) gm[e] = gamma[(int64_t)(h * G + gg) * D + c0 + e];
   float M = -INFINITY, l = 0.f, zt = 0.f;
   float osp[E], ot[E];
 #pragma unroll
@@ -120,46 +131,59 @@ __device__ __forceinline__ void merge_head(const Dims& m, float eps, uint32_t fl
 #pragma unroll
     for (int e = 0; e < E; ++e) ot[e] = hf ? 0.f : obar_add[g * D + c0 + e];
   }
-  for (int x0 = 0; x0 < n_rec; x0 += 64) {
-    // headers: lane u holds record x0 + u
-    const bool hv = x0 + lane < n_rec;
-    const float* hr = rec + (int64_t)(hv ? x0 + lane : 0) * stride;
+  auto red_max = [](float v) { return HALF ? half_wave_max(v) : wave_max(v); };
+  auto red_sum = [](float v) { return HALF ? half_wave_sum(v) : wave_sum(v); };
+  for (int x0 = 0; x0 < n_rec; x0 += HB) {
+    // headers: lane u holds record x0 + u (HALF: lane u of each half)
+    const int ul = HALF ? (lane & 31) : lane;
+    const bool hv = x0 + ul < n_rec;
+    const float* hr = rec + (int64_t)(hv ? x0 + ul : 0) * stride;
     // loaded whether or not hv (no branch), selected after the first bodies
     // are issued, so that no wait for them comes before those loads
-    const float hm0 = Mem<CO>::ld(hr + g), hl0 = Mem<CO>::ld(hr + 16 + g);
-    const float hz0 = Mem<CO>::ld(hr + 32 + g);
-    const int nb_here = n_rec - x0 < 64 ? n_rec - x0 : 64;
+    const float hm0 = Mem<CO>::ld(hr + gg), hl0 = Mem<CO>::ld(hr + 16 + gg);
+    const float hz0 = Mem<CO>::ld(hr + 32 + gg);
+    const int nb_here = n_rec - x0 < HB ? n_rec - x0 : HB;
     float sc_l = 0.f;  // lane u: weight exp(m - M) of record x0 + u
-    // bodies, NP pairs at a time (the first batch is issued with the headers)
-    for (int u0 = 0; u0 < nb_here; u0 += 2 * NP) {
+    // bodies, RS records at a time (the first batch is issued with the headers)
+    for (int u0 = 0; u0 < nb_here; u0 += RS) {
       float a[NP][E], aw[NP][E];
 #pragma unroll
       for (int u = 0; u < NP; ++u) {
-        const int xr = x0 + u0 + 2 * u + hf;
+        const int xr = HALF ? x0 + u0 + u : x0 + u0 + 2 * u + hf;
         const uint32_t o = (uint32_t)((int64_t)(xr < n_rec ? xr : 0) * stride + kPartHead + c0) * 4u;
-        load_vec<E, CO>(rec, o + (uint32_t)(g * D) * 4u, a[u]);
-        load_vec<E, CO>(rec, o + (uint32_t)((G + g) * D) * 4u, aw[u]);
+        load_vec<E, CO>(rec, o + (uint32_t)(gg * D) * 4u, a[u]);
+        load_vec<E, CO>(rec, o + (uint32_t)((G + gg) * D) * 4u, aw[u]);
       }
       __builtin_amdgcn_sched_barrier(0);
       if (u0 == 0) {  // fold this batch of headers into the running max
         const float hm = hv ? hm0 : -INFINITY, hl = hv ? hl0 : 0.f, hz = hv ? hz0 : 0.f;
-        const float bm = fmaxf(M, wave_max(hm));
+        const float bm = fmaxf(M, red_max(hm));
         const float alpha = M == -INFINITY ? 0.f : __expf(M - bm);
         l *= alpha;
 #pragma unroll
         for (int e = 0; e < E; ++e) osp[e] *= alpha;
         M = bm;
-        l += wave_sum(hm == -INFINITY ? 0.f : hl * __expf(hm - M));
-        zt += wave_sum(hz);
+        l += red_sum(hm == -INFINITY ? 0.f : hl * __expf(hm - M));
+        zt += red_sum(hz);
         sc_l = hm == -INFINITY ? 0.f : __expf(hm - M);
       }
 #pragma unroll
       for (int u = 0; u < NP; ++u) {
-        const int r0 = u0 + 2 * u;  // this pair's records within the batch: r0, r0 + 1
-        const float s0 = r0 < nb_here ? lane_f32(sc_l, r0) : 0.f;
-        const float s1 = r0 + 1 < nb_here ? lane_f32(sc_l, r0 + 1) : 0.f;
-        const bool ok = r0 + hf < nb_here;
-        const float sc = hf ? s1 : s0;
+        float sc;
+        bool ok;
+        if constexpr (HALF) {
+          const int r = u0 + u;  // this record within the batch, in each half
+          const float s0 = r < nb_here ? lane_f32(sc_l, r) : 0.f;
+          const float s1 = r < nb_here ? lane_f32(sc_l, 32 + r) : 0.f;
+          ok = r < nb_here;
+          sc = hf ? s1 : s0;
+        } else {
+          const int r0 = u0 + 2 * u;  // this pair's records within the batch: r0, r0 + 1
+          const float s0 = r0 < nb_here ? lane_f32(sc_l, r0) : 0.f;
+          const float s1 = r0 + 1 < nb_here ? lane_f32(sc_l, r0 + 1) : 0.f;
+          ok = r0 + hf < nb_here;
+          sc = hf ? s1 : s0;
+        }
 #pragma unroll
         for (int e = 0; e < E; ++e) {
           osp[e] = fmaf(a[u][e], sc, osp[e]);
@@ -168,10 +192,12 @@ __device__ __forceinline__ void merge_head(const Dims& m, float eps, uint32_t fl
       }
     }
   }
+  if constexpr (!HALF) {
 #pragma unroll
-  for (int e = 0; e < E; ++e) {  // the two halves' records
-    osp[e] += xor32(osp[e]);
-    ot[e] += xor32(ot[e]);
+    for (int e = 0; e < E; ++e) {  // the two halves' records
+      osp[e] += xor32(osp[e]);
+      ot[e] += xor32(ot[e]);
+    }
   }
   if constexpr (ADD) zt += zq_add[g];
   float o[E];
@@ -192,12 +218,12 @@ __device__ __forceinline__ void merge_head(const Dims& m, float eps, uint32_t fl
       rr[e] = res ? ot[e] / den : 0.f;
       ss += rr[e] * rr[e];
     }
-    ss = wave_sum(hf ? 0.f : ss);  // each coordinate once
+    ss = HALF ? half_wave_sum(ss) : wave_sum(hf ? 0.f : ss);  // each coordinate once
     const float inv = 1.0f / sqrtf(ss / D + eps);
 #pragma unroll
     for (int e = 0; e < E; ++e) o[e] = res ? fmaf(gm[e] * rr[e], inv, osp[e]) : osp[e];
   }
-  if (hf == 0) {
+  if (HALF ? gon : hf == 0) {
     if constexpr (E == 4) {
       Elem<T>::store4(out, orow, o);
     } else {
@@ -206,6 +232,10 @@ __device__ __forceinline__ void merge_head(const Dims& m, float eps, uint32_t fl
     }
   }
 }
+
+// Whether a group's merge takes two query heads per wavefront (HALF): the
+// groups above four heads that the single-launch kernel also runs.
+SPLA_HD bool merge_halves(int G) { return G > 4 && G <= kFusedMaxGroup; }
 
 // ------------------------------------------------------ matrix-core pass
 
