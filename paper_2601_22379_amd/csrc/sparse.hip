@@ -264,9 +264,9 @@ void sparse_mfma_kernel(
   } else {  // every workgroup makes its head's selection itself
     sparse_prologue<D, GC>(m, q, S, zbar, bh, x, (int)gridDim.x, r, sm);
     sparse_linear<D, GC>(m, S, bh, r, sm);
-    select_blocks<256, R, SWN, false>(m, bh, seq_lens[bh / m.hkv], e_vals, tile_part, ssm, s_sel,
-                                      s_meta, x == 0 && sel_out ? sel_out + (int64_t)bh * m.k
-                                                                : nullptr);
+    select_blocks<256, R, SWN, false, 0, false, GC>(
+        m, bh, seq_lens[bh / m.hkv], e_vals, tile_part, ssm, s_sel, s_meta,
+        x == 0 && sel_out ? sel_out + (int64_t)bh * m.k : nullptr);
     __syncthreads();
     if (x == 0 && threadIdx.x < 4) meta[bh * 4 + threadIdx.x] = s_meta[threadIdx.x];
     const int e = sparse_step_entry<BLK>(x);

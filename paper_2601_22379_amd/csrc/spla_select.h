@@ -156,15 +156,21 @@ struct SelectSmem {
 // WIN: the scoring units are strided selection windows (unit u: tokens
 // u us .. u us + ul - 1, Sec. 3.1) and a block's score is the largest group
 // score among the windows that share a token with it (max-pooling); wsc is
-// LDS for kMaxWindows window scores.
-template <int NT, int R, int SWN, bool CO, int SEL_OFF = 0, bool WIN = false>
+// LDS for kMaxWindows window scores. GMAX >= G (known at compile time): with
+// at most eight heads and eight blocks per thread every head's masses load
+// in one batch, and a wavefront that takes a second head's tile partials
+// loads them with the first head's.
+template <int NT, int R, int SWN, bool CO, int SEL_OFF = 0, bool WIN = false,
+          int GMAX = SPLA_MAX_GROUP>
 __device__ void select_blocks(const Dims& m, int bh, int seq_len,
                               const float* __restrict__ e_vals,
                               const double* __restrict__ tile_part, SelectSmem<NT, SWN>& sm,
                               int32_t* sel, int32_t* meta4, int32_t* so,
                               float* wsc = nullptr) {
   constexpr int NW = NT / 64;
-  constexpr int HC = R <= 2 ? 16 / R : (R <= 8 ? 4 : 32 / R);  // heads per load batch
+  constexpr int HC0 = R <= 2 ? 16 / R : (R <= 8 ? 4 : 32 / R);
+  constexpr int HC = (R <= 8 && GMAX <= 8 && GMAX > HC0) ? GMAX : HC0;  // heads per load batch
+  constexpr bool PRE2 = !WIN && GMAX > NW && GMAX <= 2 * NW;  // heads w and w + NW preloaded
   // tiles per lane: n_tiles <= NT R / 64 blocks, or <= kMaxWindows / 64 windows
   constexpr int TJ = WIN ? kMaxWindows / 4096 : (NT * R + 4095) / 4096;
   float* sw = sm.sw;
@@ -184,6 +190,15 @@ __device__ void select_blocks(const Dims& m, int bh, int seq_len,
     const int t = lane + 64 * j;
     load_tile_part<CO>(tp + (int64_t)(w < G ? w : 0) * m.n_tiles * 2, t, w < G && t < m.n_tiles,
                        tm[j], ts[j]);
+  }
+  double tm2[PRE2 ? TJ : 1], ts2[PRE2 ? TJ : 1];  // head w + NW
+  if constexpr (PRE2) {
+#pragma unroll
+    for (int j = 0; j < TJ; ++j) {
+      const int t = lane + 64 * j, w2 = w + NW;
+      load_tile_part<CO>(tp + (int64_t)(w2 < G ? w2 : 0) * m.n_tiles * 2, t,
+                         w2 < G && t < m.n_tiles, tm2[j], ts2[j]);
+    }
   }
   float e[HC][R];  // nbp is a multiple of 64 >= R: a thread's run is all in or all out
   if constexpr (!WIN) {
@@ -229,10 +244,18 @@ __device__ void select_blocks(const Dims& m, int bh, int seq_len,
   // --- 1. Z_m and the tile weights of heads m = w, w + NW, ...
   for (int mm = w; kp > 0 && mm < G; mm += NW) {
     if (mm != w) {  // the first head's partials were loaded above
+      if constexpr (PRE2) {  // and so were the second's
 #pragma unroll
-      for (int j = 0; j < TJ; ++j) {
-        const int t = lane + 64 * j;
-        load_tile_part<CO>(tp + (int64_t)mm * m.n_tiles * 2, t, t < m.n_tiles, tm[j], ts[j]);
+        for (int j = 0; j < TJ; ++j) {
+          tm[j] = tm2[j];
+          ts[j] = ts2[j];
+        }
+      } else {
+#pragma unroll
+        for (int j = 0; j < TJ; ++j) {
+          const int t = lane + 64 * j;
+          load_tile_part<CO>(tp + (int64_t)mm * m.n_tiles * 2, t, t < m.n_tiles, tm[j], ts[j]);
+        }
       }
     }
     double mx = -INFINITY;
