@@ -108,13 +108,17 @@ __device__ __forceinline__ bool arrive_last(int32_t* ctr, int n, int* s_flag) {
 }
 
 // Built for three waves per SIMD (at most 168 registers per lane; measured
-// faster than two, and than four with its 128-register budget).
+// faster than two, and than four with its 128-register budget, at the 128K
+// workload). A launch whose items would not all be resident at three but are
+// at four (32K: 1024 items) takes the four-wave build: then no sparse item
+// starts after its selection (27.3 -> 25.2 us).
 constexpr int kDecodeWaves = 3;
 
 // R: blocks per thread of the selection (256 R >= blocks per sequence).
 // STEP: the sparse items first apply the step's rank-one update (step_rank1).
-template <int G, int BLK, int R, bool STEP>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(kDecodeWaves, kDecodeWaves)))
+// WAVES: waves per SIMD the kernel is built for (3 or 4).
+template <int G, int BLK, int R, bool STEP, int WAVES>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WAVES, WAVES)))
 void decode_kernel(FusedArgs a) {
   constexpr int D = 128;
   constexpr int SWN = 4 * R * G;  // tile weights: n_tiles <= 4 R
@@ -250,11 +254,17 @@ void decode_kernel(FusedArgs a) {
 template <int G, int BLK, int R>
 static void decode_gbr(const FusedArgs& a, hipStream_t st) {
   const int grid = a.m.bh * (a.n_si + a.n_wg);
+  const int cus = compute_units();  // one workgroup per wave of each SIMD
+  const bool four = grid > kDecodeWaves * cus && grid <= 4 * cus;
   if (a.appended)
-    hipLaunchKernelGGL((decode_kernel<G, BLK, R, true>), dim3((unsigned)grid), dim3(256), 0, st, a);
+    hipLaunchKernelGGL((decode_kernel<G, BLK, R, true, kDecodeWaves>), dim3((unsigned)grid),
+                       dim3(256), 0, st, a);
+  else if (four)
+    hipLaunchKernelGGL((decode_kernel<G, BLK, R, false, 4>), dim3((unsigned)grid), dim3(256), 0,
+                       st, a);
   else
-    hipLaunchKernelGGL((decode_kernel<G, BLK, R, false>), dim3((unsigned)grid), dim3(256), 0, st,
-                       a);
+    hipLaunchKernelGGL((decode_kernel<G, BLK, R, false, kDecodeWaves>), dim3((unsigned)grid),
+                       dim3(256), 0, st, a);
 }
 
 template <int G, int R>

@@ -86,6 +86,10 @@ SHAPES = {
     "g3_B64_8k_blocks": dict(batch=1, n_q_heads=6, n_kv_heads=2, head_dim=128, block_size=64,
                              top_k=24, lengths=[8192 * 64 - 5], kind="pareto_planted",
                              n_planted=4),
+    # 128 units x (4 score + 4 sparse items) = 1024 items: the four-wave build
+    "g4_B32_four_waves": dict(batch=32, n_q_heads=16, n_kv_heads=4, head_dim=128,
+                              block_size=32, top_k=16, lengths=[8192 - 37 * i for i in range(32)],
+                              capacity=8192, kind="block_offsets"),
 }
 
 
