@@ -57,6 +57,23 @@ __global__ __launch_bounds__(256) void sparse_valu_kernel(
   const int L = meta[bh * 4 + 2];
   const int nb = (L + m.B - 1) / m.B;
   const int p0 = split * bps, p1 = min(p0 + bps, nsel);
+  // this workgroup's rows of S_bar and z_bar for the global linear term: the
+  // first kLinPre rows loaded now (they land while the blocks are processed),
+  // any further ones at the end, kLinPre rows per batch of loads
+  constexpr int kLinPre = 8;
+  int row0, nrows;
+  lin_rows(D, split, gridDim.x, &row0, &nrows);
+  const int rend = row0 + nrows;
+  const int cS = tid % D;  // the coordinate of every (head, coordinate) output of this thread
+  const float* Sb = S + (int64_t)bh * D * D + cS;
+  const float* zb = zbar + (int64_t)bh * D;
+  float sv[kLinPre], zv[kLinPre];
+#pragma unroll
+  for (int u = 0; u < kLinPre; ++u) {
+    const int j = row0 + u < rend ? row0 + u : 0;
+    sv[u] = Sb[(int64_t)j * D];
+    zv[u] = zb[j];
+  }
 
   for (int mm = w; mm < G; mm += 4) {
     float x[D / 64];
@@ -102,11 +119,23 @@ __global__ __launch_bounds__(256) void sparse_valu_kernel(
     for (int sub = 0; sub * kSubTokens < n_i; ++sub) {
       const int tb0 = sub * kSubTokens;
       const int nt = min(kSubTokens, n_i - sub * kSubTokens);
-      for (int e = tid; e < kSubTokens * D; e += 256) {
-        const int row = e / D, col = e % D;
-        sK[row][col] = row < nt ? Elem<T>::load(kc, k_off_slot(m, slot, tb0 + row, col)) : 0.f;
-        const int c2 = e / kSubTokens, r2 = e % kSubTokens;
-        sV[c2][r2] = r2 < nt ? Elem<T>::load(vc, v_off_slot(m, slot, tb0 + r2, c2)) : 0.f;
+      // every load of the sub-tile issued before any is used (rows past nt
+      // read the sub-tile's first row and are masked)
+      constexpr int NE = kSubTokens * D / 256;
+      float kx[NE], vx[NE];
+#pragma unroll
+      for (int i = 0; i < NE; ++i) {
+        const int e = tid + 256 * i;
+        const int row = e / D, col = e % D, c2 = e / kSubTokens, r2 = e % kSubTokens;
+        kx[i] = Elem<T>::load(kc, k_off_slot(m, slot, tb0 + (row < nt ? row : 0), col));
+        vx[i] = Elem<T>::load(vc, v_off_slot(m, slot, tb0 + (r2 < nt ? r2 : 0), c2));
+      }
+#pragma unroll
+      for (int i = 0; i < NE; ++i) {
+        const int e = tid + 256 * i;
+        const int row = e / D, col = e % D, c2 = e / kSubTokens, r2 = e % kSubTokens;
+        sK[row][col] = row < nt ? kx[i] : 0.f;
+        sV[c2][r2] = r2 < nt ? vx[i] : 0.f;
       }
       __syncthreads();
       for (int r = 0; r < kSubTokens / 4; ++r) {  // phi(k) rows
@@ -142,22 +171,24 @@ __global__ __launch_bounds__(256) void sparse_valu_kernel(
         sW[mm][t] = t < nt ? wl : 0.f;
       }
       __syncthreads();
-      if (tid < G) {  // online softmax bookkeeping, one head per thread
-        const int mm = tid;
-        float mx = s_m[mm];
-        for (int t = 0; t < nt; ++t) mx = fmaxf(mx, sP[mm][t]);
+      // online softmax bookkeeping: wavefront w takes heads w, w + 4, ..., lane
+      // t < kSubTokens token t
+      static_assert(kSubTokens <= 64, "one token per lane");
+      for (int mm = w; mm < G; mm += 4) {
+        const bool on = lane < nt;
+        const float lg = on ? sP[mm][lane] : -INFINITY;
+        const float mx = fmaxf(s_m[mm], wave_max(lg));
         const float alpha = expf(s_m[mm] - mx);
-        float l = s_l[mm] * alpha, zw = s_zw[mm];
-        for (int t = 0; t < kSubTokens; ++t) {
-          const float pv = t < nt ? expf(sP[mm][t] - mx) : 0.f;
-          sP[mm][t] = pv;
-          l += pv;
-          zw += sW[mm][t];
+        const float pv = on ? expf(lg - mx) : 0.f;
+        const float l = s_l[mm] * alpha + wave_sum(pv);
+        const float zw = s_zw[mm] + wave_sum(lane < kSubTokens ? sW[mm][lane] : 0.f);
+        if (lane < kSubTokens) sP[mm][lane] = pv;
+        if (lane == 0) {
+          s_m[mm] = mx;
+          s_l[mm] = l;
+          s_alpha[mm] = alpha;
+          s_zw[mm] = zw;
         }
-        s_m[mm] = mx;
-        s_l[mm] = l;
-        s_alpha[mm] = alpha;
-        s_zw[mm] = zw;
       }
       __syncthreads();
 #pragma unroll
@@ -177,25 +208,46 @@ __global__ __launch_bounds__(256) void sparse_valu_kernel(
       __syncthreads();
     }
   }
-  // this workgroup's rows of the global linear term, minus its selected terms
-  int row0, nrows;
-  lin_rows(D, split, gridDim.x, &row0, &nrows);
-  const float* Sb = S + (int64_t)bh * D * D;
+  // this workgroup's rows of the global linear term, minus its selected
+  // terms (rows in ascending order)
+  float ob[PER], zq = 0.f;
+#pragma unroll
+  for (int r = 0; r < PER; ++r) ob[r] = 0.f;
+  const int gz = tid < G ? tid : 0;
+  auto add_rows = [&](int j0, const float (&v)[kLinPre], const float (&z)[kLinPre]) {
+#pragma unroll
+    for (int u = 0; u < kLinPre; ++u) {
+      const bool ok = j0 + u < rend;
+      const int jc = ok ? j0 + u : row0;
+#pragma unroll
+      for (int r = 0; r < PER; ++r) {
+        const int mm = (tid + 256 * r) / D;
+        ob[r] = fmaf(sphq[mm < MG ? mm : 0][jc], ok ? v[u] : 0.f, ob[r]);
+      }
+      zq = fmaf(sphq[gz][jc], ok ? z[u] : 0.f, zq);
+    }
+  };
+  add_rows(row0, sv, zv);
+  for (int j0 = row0 + kLinPre; j0 < rend; j0 += kLinPre) {
+#pragma unroll
+    for (int u = 0; u < kLinPre; ++u) {
+      const int j = j0 + u < rend ? j0 + u : row0;
+      sv[u] = Sb[(int64_t)j * D];
+      zv[u] = zb[j];
+    }
+    add_rows(j0, sv, zv);
+  }
   float* rec = part + ((int64_t)bh * gridDim.x + split) * stride;
 #pragma unroll
   for (int r = 0; r < PER; ++r) {
     const int idx = tid + 256 * r;
     if (idx < G * D) {
       const int mm = idx / D, c = idx % D;
-      float ob = 0.f;
-      for (int j = row0; j < row0 + nrows; ++j) ob = fmaf(sphq[mm][j], Sb[j * D + c], ob);
       rec[kPartHead + mm * D + c] = acc[r];
-      rec[kPartHead + (G + mm) * D + c] = ob - accw[r];
+      rec[kPartHead + (G + mm) * D + c] = ob[r] - accw[r];
     }
   }
   if (tid < G) {
-    float zq = 0.f;
-    for (int j = row0; j < row0 + nrows; ++j) zq = fmaf(sphq[tid][j], zbar[(int64_t)bh * D + j], zq);
     rec[tid] = s_m[tid];
     rec[16 + tid] = s_l[tid];
     rec[32 + tid] = zq - s_zw[tid];
