@@ -161,25 +161,28 @@ __global__ __launch_bounds__(kPrefSelThreads) void prefill_select_kernel(
 // with its own L2: the item of workgroup p is (p % 8) * (n / 8) + p / 8, so
 // that consecutive items (the queries of one sequence x KV head, which
 // largely select the same blocks) share an XCD and its L2. n_wg workgroups
-// per query; the grid is n items rounded up to a multiple of 8.
-template <int D, int BLK>
-__global__ __launch_bounds__(256) void prefill_sparse_kernel(
+// per query; the grid is n items rounded up to a multiple of 8. GC:
+// accumulator columns per kind (>= G; 4 fits three workgroups per compute
+// unit, 8 two).
+template <int D, int BLK, int GC>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(GC <= 4 ? 3 : 2)))
+void prefill_sparse_kernel(
     Dims m, int T_, float s, const bf16_t* __restrict__ kc, const bf16_t* __restrict__ vc,
     const bf16_t* __restrict__ q, const int32_t* __restrict__ sel,
     const int32_t* __restrict__ meta, int stride, float* __restrict__ part,
     const int32_t* __restrict__ table, int n_wg, int n_items) {
-  __shared__ SparseSmem<D, 8> sm;
+  __shared__ SparseSmem<D, GC> sm;
   const int per = (int)(gridDim.x / 8);
   const int item = ((int)blockIdx.x % 8) * per + (int)blockIdx.x / 8;
   if (item >= n_items) return;
   const int x = item % n_wg, vh = item / n_wg, bh = vh / T_, i = vh % T_;
   SparseRegs r;
-  sparse_prologue<D, 8, false>(m, q + (int64_t)i * m.batch * m.hq * D, nullptr, nullptr, bh, x,
-                               n_wg, r, sm);
-  sparse_linear<D, 8, false>(m, nullptr, bh, r, sm);
+  sparse_prologue<D, GC, false>(m, q + (int64_t)i * m.batch * m.hq * D, nullptr, nullptr, bh, x,
+                                n_wg, r, sm);
+  sparse_linear<D, GC, false>(m, nullptr, bh, r, sm);
   const int e = sparse_step_entry<BLK>(x);
-  sparse_body<D, BLK, false, 8>(m, s, kc, vc, e < m.k ? sel[(int64_t)vh * m.k + e] : -1,
-                                meta[vh * 4 + 2], bh, x, n_wg, r, sm, part, stride, table, vh);
+  sparse_body<D, BLK, false, GC>(m, s, kc, vc, e < m.k ? sel[(int64_t)vh * m.k + e] : -1,
+                                 meta[vh * 4 + 2], bh, x, n_wg, r, sm, part, stride, table, vh);
 }
 
 // ---------------------------------------------------------------- merge
@@ -503,7 +506,8 @@ template <int D, int BLK>
 static void prefill_sparse_db(const Dims& m, int T, float s, const spla_cache& c, const void* q,
                               const PrefillWs& ws, char* base, hipStream_t st) {
   const int64_t items = (int64_t)ws.n_wg * m.bh * T;
-  hipLaunchKernelGGL((prefill_sparse_kernel<D, BLK>), dim3((unsigned)align_up(items, 8)),
+  auto kern = m.group <= 4 ? prefill_sparse_kernel<D, BLK, 4> : prefill_sparse_kernel<D, BLK, 8>;
+  hipLaunchKernelGGL(kern, dim3((unsigned)align_up(items, 8)),
                      dim3(256), 0, st, m, T, s, (const bf16_t*)c.k_cache,
                      (const bf16_t*)c.v_cache, (const bf16_t*)q, (const int32_t*)(base + ws.sel),
                      (const int32_t*)(base + ws.meta), ws.part_stride, (float*)(base + ws.part),
