@@ -89,21 +89,25 @@ hipError_t launch_select(const Dims& m, const spla_cache& c, const DecodeWs& ws,
   const double* tp = (const double*)(base + ws.tile_part);
   int32_t* sel = (int32_t*)(base + ws.sel);
   int32_t* meta = (int32_t*)(base + ws.meta);
+  // blocks per thread: at most 4096 blocks here without windows (two stages
+  // past that); with windows at most kMaxWindows windows, so at most 16384
+  // blocks
   const int per = (int)ceil_div(m.nb_cap, kSelThreads);
-#define SPLA_R(r)                                                                            \
-  if (windowed(m))                                                                           \
-    hipLaunchKernelGGL((select_kernel<r, true>), dim3(m.bh), dim3(kSelThreads), 0, st, m,    \
-                       c.seq_lens, ev, tp, sel, sel_out, meta);                              \
-  else                                                                                       \
-    hipLaunchKernelGGL((select_kernel<r, false>), dim3(m.bh), dim3(kSelThreads), 0, st, m,   \
-                       c.seq_lens, ev, tp, sel, sel_out, meta)
-  if (per <= 1) SPLA_R(1);
-  else if (per <= 2) SPLA_R(2);
-  else if (per <= 4) SPLA_R(4);
-  else if (per <= 8) SPLA_R(8);
-  else if (per <= 16) SPLA_R(16);
-  else SPLA_R(32);
-#undef SPLA_R
+  auto launch = [&](auto kern) {
+    hipLaunchKernelGGL(kern, dim3(m.bh), dim3(kSelThreads), 0, st, m, c.seq_lens, ev, tp, sel,
+                       sel_out, meta);
+  };
+  if (windowed(m)) {
+    if (per <= 1) launch(select_kernel<1, true>);
+    else if (per <= 2) launch(select_kernel<2, true>);
+    else if (per <= 4) launch(select_kernel<4, true>);
+    else if (per <= 8) launch(select_kernel<8, true>);
+    else launch(select_kernel<16, true>);
+  } else {
+    if (per <= 1) launch(select_kernel<1, false>);
+    else if (per <= 2) launch(select_kernel<2, false>);
+    else launch(select_kernel<4, false>);
+  }
   return hipGetLastError();
 }
 
