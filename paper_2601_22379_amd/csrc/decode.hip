@@ -145,7 +145,7 @@ void decode_kernel(FusedArgs a) {
     // the selection is on the path to the head's output: its wavefronts go
     // ahead of the score items that share their SIMDs
     __builtin_amdgcn_s_setprio(3);
-    select_blocks<256, R, SWN, true, 2, false, G>(m, bh, L, a.e_vals, a.tile_part, sm.se,
+    select_blocks<256, R, SWN, true, 2, false, G, true>(m, bh, L, a.e_vals, a.tile_part, sm.se,
                                         sy + y.sel_ready + (int64_t)bh * m.k, nullptr,
                                         a.sel_out ? a.sel_out + (int64_t)bh * m.k : nullptr);
     // reset last: vmcnt counts stores, so an earlier store would hold up

@@ -49,11 +49,12 @@ __device__ __forceinline__ uint32_t block_excl_scan_u32(uint32_t v, uint32_t* ld
   return base + x - v;
 }
 
-// R consecutive floats at base + off (4R-byte aligned; zeros when !ok); base
-// is wave-uniform. The loads are issued whether or not ok (from base when
-// not): a load under a branch makes the compiler wait for it inside the
-// branch, before the loads after it are issued.
-template <int R, bool CO>
+// R consecutive floats at base + off (4R-byte aligned; zeros when !ok, or
+// whatever base holds when !MASK); base is wave-uniform. The loads are issued
+// whether or not ok (from base when not): a load under a branch makes the
+// compiler wait for it inside the branch, before the loads after it are
+// issued.
+template <int R, bool CO, bool MASK = true>
 __device__ __forceinline__ void load_run(const float* base, int64_t off, bool ok,
                                          float (&out)[R]) {
   const int64_t o = ok ? off : 0;
@@ -73,8 +74,10 @@ __device__ __forceinline__ void load_run(const float* base, int64_t off, bool ok
       out[4 * j + 3] = __uint_as_float(v.w);
     }
   }
+  if constexpr (MASK) {
 #pragma unroll
-  for (int r = 0; r < R; ++r) out[r] = ok ? out[r] : 0.f;
+    for (int r = 0; r < R; ++r) out[r] = ok ? out[r] : 0.f;
+  }
 }
 
 // The (max, sum) partial of tile t of the head whose partials start at tp
@@ -131,14 +134,14 @@ __device__ __forceinline__ RadixPick radix_pick(const uint32_t* hist, uint32_t n
 }
 
 // LDS of one selection: tile weights [tile][head] (SWN >= n_tiles * G), the
-// digit histograms (2048 + 1024 + 1024 bins), the scan totals and the
-// staging of the output (k slots, then one spare slot per thread).
+// digit histograms (2048 + 1024 + 1024 bins), each thread's taken and tie
+// bits (one word per thread and kind) and the staging of the k output slots.
 template <int NT, int SWN>
 struct SelectSmem {
   float sw[SWN];
   __align__(16) uint32_t hist[4096];
-  uint32_t scan[NT / 64];
-  int32_t out[SPLA_MAX_TOP_K + NT];
+  uint32_t bits[2][NT];
+  int32_t out[SPLA_MAX_TOP_K + 1];
 };
 
 // The selection of sequence x KV head bh (length seq_len, clipped to the
@@ -159,9 +162,9 @@ struct SelectSmem {
 // LDS for kMaxWindows window scores. GMAX >= G (known at compile time): with
 // at most eight heads and eight blocks per thread every head's masses load
 // in one batch, and a wavefront that takes a second head's tile partials
-// loads them with the first head's.
+// loads them with the first head's. GEX: the group is GMAX exactly.
 template <int NT, int R, int SWN, bool CO, int SEL_OFF = 0, bool WIN = false,
-          int GMAX = SPLA_MAX_GROUP>
+          int GMAX = SPLA_MAX_GROUP, bool GEX = false>
 __device__ void select_blocks(const Dims& m, int bh, int seq_len,
                               const float* __restrict__ e_vals,
                               const double* __restrict__ tile_part, SelectSmem<NT, SWN>& sm,
@@ -175,7 +178,7 @@ __device__ void select_blocks(const Dims& m, int bh, int seq_len,
   constexpr int TJ = WIN ? kMaxWindows / 4096 : (NT * R + 4095) / 4096;
   float* sw = sm.sw;
   uint32_t* hist = sm.hist;
-  const int G = m.group, k = m.k;
+  const int G = GEX ? GMAX : m.group, k = m.k;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int nbp = m.n_tiles * kTileBlocks;
   const int i0 = tid * R;
@@ -200,11 +203,14 @@ __device__ void select_blocks(const Dims& m, int bh, int seq_len,
                          w2 < G && t < m.n_tiles, tm2[j], ts2[j]);
     }
   }
-  float e[HC][R];  // nbp is a multiple of 64 >= R: a thread's run is all in or all out
+  // nbp is a multiple of 64 >= R: a thread's run is all in or all out; the
+  // masses of a run past nbp, or of a head past G, are never used (the keys
+  // of blocks past the sequence are 0 whatever they hold)
+  float e[HC][R];
   if constexpr (!WIN) {
 #pragma unroll
     for (int h = 0; h < HC; ++h)
-      load_run<R, CO>(ev, (int64_t)h * nbp + i0, h < G && i0 < nbp, e[h]);
+      load_run<R, CO, false>(ev, (int64_t)h * nbp + i0, h < G && i0 < nbp, e[h]);
   }
   // WIN: the window masses of the first four heads, as runs of four windows
   // starting at 4 (t + j NT) (16-byte loads; a run holding a window below nu
@@ -366,7 +372,8 @@ __device__ void select_blocks(const Dims& m, int bh, int seq_len,
       if (h0 > 0) {
 #pragma unroll
         for (int h = 0; h < HC; ++h)
-          load_run<R, CO>(ev, (int64_t)(h0 + h) * nbp + i0, h0 + h < G && i0 < nbp, e[h]);
+          load_run<R, CO, false>(ev, (int64_t)(h0 + h) * nbp + i0, h0 + h < G && i0 < nbp,
+                                 e[h]);
       }
 #pragma unroll
       for (int h = 0; h < HC; ++h) {
@@ -423,41 +430,77 @@ __device__ void select_blocks(const Dims& m, int bh, int seq_len,
     }
   }
 
-  // --- 4. ascending output: (taken above/forced) | (ties) << 16, one scan;
-  // every thread writes its taken ids to their slots in LDS (ids not taken go
-  // to the thread's spare slot), then the first k threads copy the k slots out
-  bool tk[R], tq[R];
-  uint32_t na = 0u, ne = 0u;
+  // --- 4. ascending output. Each thread leaves one word of taken bits (keys
+  // above the threshold, forced blocks) and one of tie bits (keys equal to
+  // it) for its R blocks; wavefront 0 then reads them NT / 64 threads per
+  // lane (lane order is block order), keeps the first eq_need ties in block
+  // order, places every taken block by one wave-wide prefix sum and writes
+  // the k entries out.
+  uint32_t tkb = 0u, tqb = 0u;
 #pragma unroll
   for (int r = 0; r < R; ++r) {
     const int i = i0 + r;
     const bool forced = (i < nb) & ((i < m.n_sink) | (i >= nb - m.n_local));
-    tk[r] = forced | ((key[r] != 0u) & (key[r] > gt));
-    tq[r] = !tk[r] & (eq_need > 0u) & (key[r] == eqv);
-    na += tk[r] ? 1u : 0u;
-    ne += tq[r] ? 1u : 0u;
+    const bool tk = forced | ((key[r] != 0u) & (key[r] > gt));
+    const bool tq = !tk & (eq_need > 0u) & (key[r] == eqv);
+    tkb |= (tk ? 1u : 0u) << r;
+    tqb |= (tq ? 1u : 0u) << r;
   }
-  uint32_t tot_p;
-  const uint32_t before = block_excl_scan_u32<NW>(na | (ne << 16), sm.scan, &tot_p);
-  uint32_t a_run = before & 0xFFFFu, e_run = before >> 16;
-#pragma unroll
-  for (int r = 0; r < R; ++r) {
-    const uint32_t pg = a_run + (e_run < eq_need ? e_run : eq_need);
-    const uint32_t pq = e_run < eq_need ? a_run + e_run : 0xFFFFFFFFu;
-    const uint32_t pos = tk[r] ? pg : (tq[r] ? pq : 0xFFFFFFFFu);
-    a_run += tk[r] ? 1u : 0u;
-    e_run += tq[r] ? 1u : 0u;
-    sm.out[pos < (uint32_t)k ? (int)pos : SPLA_MAX_TOP_K + tid] = i0 + r;
-  }
-  const uint32_t ta = tot_p & 0xFFFFu, te = tot_p >> 16;
-  const int tot = (int)(ta + (te < eq_need ? te : eq_need));
+  sm.bits[0][tid] = tkb;
+  sm.bits[1][tid] = tqb;
   __syncthreads();
-  for (int x = tid; x < k; x += NT) {
+  if (w != 0) return;
+  // lane l covers blocks l TPL R .. (l + 1) TPL R - 1 as LW words (thread
+  // q of the lane at bit q R: R divides 32, so no thread straddles a word)
+  constexpr int TPL = NT / 64;  // threads per lane
+  constexpr int LW = (TPL * R + 31) / 32;
+  uint32_t tkw[LW], tqw[LW];
+#pragma unroll
+  for (int u = 0; u < LW; ++u) tkw[u] = tqw[u] = 0u;
+#pragma unroll
+  for (int q = 0; q < TPL; ++q) {
+    tkw[q * R / 32] |= sm.bits[0][lane * TPL + q] << (q * R % 32);
+    tqw[q * R / 32] |= sm.bits[1][lane * TPL + q] << (q * R % 32);
+  }
+  uint32_t ct = 0u, cq = 0u;
+#pragma unroll
+  for (int u = 0; u < LW; ++u) {
+    ct += (uint32_t)__builtin_popcount(tkw[u]);
+    cq += (uint32_t)__builtin_popcount(tqw[u]);
+  }
+  if (eq_need > 0u) {  // the first eq_need ties, in block order
+    const uint32_t before = wave_incl_scan_u32(cq) - cq;
+    uint32_t left = eq_need > before ? eq_need - before : 0u;
+#pragma unroll
+    for (int u = 0; u < LW; ++u) {
+      uint32_t x = tqw[u];
+      while (x != 0u && left > 0u) {
+        const uint32_t bit = x & (0u - x);
+        tkw[u] |= bit;
+        x ^= bit;
+        --left;
+        ++ct;
+      }
+    }
+  }
+  const uint32_t incl = wave_incl_scan_u32(ct);
+  const int tot = (int)lane_u32(incl, 63);
+  int pos = (int)(incl - ct);
+#pragma unroll
+  for (int u = 0; u < LW; ++u) {
+    const int id0 = lane * TPL * R + 32 * u;
+    for (uint32_t x = tkw[u]; x != 0u; x &= x - 1u) {
+      sm.out[pos < k ? pos : SPLA_MAX_TOP_K] = id0 + __builtin_ctz(x);  // never past k
+      ++pos;
+    }
+  }
+  // (one wavefront's LDS accesses complete in order)
+  for (int x = lane; x < k; x += 64) {
     const int v = x < tot ? sm.out[x] : -1;
     Mem<CO>::st(sel + x, v + SEL_OFF);
     if (so) so[x] = v;
   }
-  if (tid == 0 && meta4) {
+  if (lane == 0 && meta4) {
     Mem<CO>::st(meta4 + 0, tot < k ? tot : k);
     Mem<CO>::st(meta4 + 1, 0);
     Mem<CO>::st(meta4 + 2, L);
