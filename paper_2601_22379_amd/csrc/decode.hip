@@ -77,32 +77,12 @@ struct FusedArgs {
   const int32_t* appended;
 };
 
-__device__ __forceinline__ int atomic_add_agent(int32_t* p, int v) {
-  return __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ int load_agent(const int32_t* p) {
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ void store_agent(int32_t* p, int v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
 
 __device__ __forceinline__ void report_sync_error(const FusedArgs& a) {
   atomic_add_agent(a.sync + a.y.err, 1);
   if (a.err_flags) atomicOr(a.err_flags, (int)SPLA_DEVERR_SYNC);
 }
 
-// Every thread: waits until its stores (Mem<true>, so device-coherent once
-// complete) have completed, then the workgroup counts itself in *ctr. True in
-// every thread of the workgroup that arrived as the n-th; that workgroup reads
-// what the others published with Mem<true> loads.
-__device__ __forceinline__ bool arrive_last(int32_t* ctr, int n, int* s_flag) {
-  wait_memory();
-  __syncthreads();
-  if (threadIdx.x == 0) *s_flag = atomic_add_agent(ctr, 1) == n - 1;
-  __syncthreads();
-  return *s_flag != 0;
-}
 
 // Built for three waves per SIMD (at most 168 registers per lane; measured
 // faster than two, and than four with its 128-register budget, at the 128K

@@ -1,6 +1,7 @@
 // Block selection kernels: one 1024-thread workgroup per (sequence, KV head)
 // (select_blocks), or past 4096 blocks per sequence the two-stage selection
-// (select_slice, select_pick); the device code is in spla_select.h.
+// (select_slice, then select_pick in the last slice of each head to finish);
+// the device code is in spla_select.h.
 #include "spla_kernels.h"
 #include "spla_select.h"
 
@@ -21,62 +22,65 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
       meta + bh * 4, sel_out ? sel_out + (int64_t)bh * m.k : nullptr, wsc);
 }
 
-// Two-stage selection (select_slice, select_pick): grid (n_sl, bh), then bh.
-template <int TJ, int GM>
-__global__ __launch_bounds__(kSliceThreads) void select_slice_kernel(
+// Two-stage selection in one launch, grid (n_sl, bh): every workgroup takes
+// its slice's candidates (select_slice); the last slice of a (sequence, KV
+// head) to finish (a counter in the synchronisation area, zero between
+// calls and reset by that workgroup) picks from all of them (select_pick).
+// No workgroup waits for another.
+template <int TJ, int GM, int R2>
+__global__ __launch_bounds__(kSliceThreads) void select_two_stage_kernel(
     Dims m, const int32_t* __restrict__ seq_lens, const float* __restrict__ e_vals,
     const double* __restrict__ tile_part, uint32_t* __restrict__ cand_key,
-    int32_t* __restrict__ cand_id, int32_t* __restrict__ cand_n) {
+    int32_t* __restrict__ cand_id, int32_t* __restrict__ cand_n, int32_t* __restrict__ sel_ws,
+    int32_t* __restrict__ sel_out, int32_t* __restrict__ meta, int32_t* __restrict__ ctr) {
   __shared__ float sw[kSliceTiles * SPLA_MAX_GROUP];
   __shared__ __align__(16) uint32_t hist[4096];
   __shared__ uint32_t scan[kSliceThreads / 64];
-  const int sl = blockIdx.x, bh = blockIdx.y, n_sl = gridDim.x;
-  const int64_t row = (int64_t)bh * n_sl + sl;
-  select_slice<TJ, GM>(m, bh, sl, seq_lens, e_vals, tile_part, cand_key + row * m.k,
-                       cand_id + row * m.k, cand_n + row, sw, hist, scan);
-}
-
-template <int R2>
-__global__ __launch_bounds__(kPickThreads) void select_pick_kernel(
-    Dims m, int n_sl, const int32_t* __restrict__ seq_lens, const uint32_t* __restrict__ cand_key,
-    const int32_t* __restrict__ cand_id, const int32_t* __restrict__ cand_n,
-    int32_t* __restrict__ sel_ws, int32_t* __restrict__ sel_out, int32_t* __restrict__ meta) {
-  __shared__ __align__(16) uint32_t hist[4096];
-  __shared__ uint32_t scan[kPickThreads / 64];
   __shared__ int32_t out[SPLA_MAX_TOP_K];
-  const int bh = blockIdx.x;
+  __shared__ int s_flag;
+  const int sl = blockIdx.x, bh = blockIdx.y, n_sl = gridDim.x;
   const int64_t row = (int64_t)bh * n_sl;
-  select_pick<R2>(m, bh, n_sl, seq_lens, cand_key + row * m.k, cand_id + row * m.k,
-                  cand_n + row, sel_ws + (int64_t)bh * m.k, meta + bh * 4,
-                  sel_out ? sel_out + (int64_t)bh * m.k : nullptr, hist, scan, out);
+  select_slice<TJ, GM>(m, bh, sl, seq_lens, e_vals, tile_part, cand_key + (row + sl) * m.k,
+                       cand_id + (row + sl) * m.k, cand_n + row + sl, sw, hist, scan);
+  int32_t* c = ctr + (int64_t)bh * kSyncLine;
+  if (!arrive_last(c, n_sl, &s_flag)) return;
+  select_pick<R2, kSliceThreads>(m, bh, n_sl, seq_lens, cand_key + row * m.k,
+                                 cand_id + row * m.k, cand_n + row, sel_ws + (int64_t)bh * m.k,
+                                 meta + bh * 4, sel_out ? sel_out + (int64_t)bh * m.k : nullptr,
+                                 hist, scan, out);
+  if (threadIdx.x == 0) store_agent(c, 0);
 }
 
-template <int TJ>
-static void slice_t(const Dims& m, const spla_cache& c, const DecodeWs& ws, char* base,
-                    hipStream_t st) {
-  auto kern = m.group <= 4 ? select_slice_kernel<TJ, 4>
-                           : (m.group <= 8 ? select_slice_kernel<TJ, 8>
-                                           : select_slice_kernel<TJ, SPLA_MAX_GROUP>);
+template <int TJ, int GM>
+static void two_stage_t(const Dims& m, const spla_cache& c, const DecodeWs& ws, char* base,
+                        int32_t* sel_out, hipStream_t st) {
+  // candidate slots per thread of the pick
+  const int64_t r2 = ceil_div((int64_t)ws.n_sl * m.k, kSliceThreads);
+  auto kern = r2 <= 4 ? select_two_stage_kernel<TJ, GM, 4>
+                      : (r2 <= 16 ? select_two_stage_kernel<TJ, GM, 16>
+                                  : select_two_stage_kernel<TJ, GM, 32>);
   hipLaunchKernelGGL(kern, dim3((unsigned)ws.n_sl, (unsigned)m.bh), dim3(kSliceThreads), 0, st,
                      m, c.seq_lens, (const float*)(base + ws.e_vals),
                      (const double*)(base + ws.tile_part), (uint32_t*)(base + ws.cand_key),
-                     (int32_t*)(base + ws.cand_id), (int32_t*)(base + ws.cand_n));
+                     (int32_t*)(base + ws.cand_id), (int32_t*)(base + ws.cand_n),
+                     (int32_t*)(base + ws.sel), sel_out, (int32_t*)(base + ws.meta),
+                     (int32_t*)(base + ws.sync) + sync_layout(m).items_done);
+}
+
+template <int TJ>
+static void two_stage_tj(const Dims& m, const spla_cache& c, const DecodeWs& ws, char* base,
+                         int32_t* sel_out, hipStream_t st) {
+  if (m.group <= 4) two_stage_t<TJ, 4>(m, c, ws, base, sel_out, st);
+  else if (m.group <= 8) two_stage_t<TJ, 8>(m, c, ws, base, sel_out, st);
+  else two_stage_t<TJ, SPLA_MAX_GROUP>(m, c, ws, base, sel_out, st);
 }
 
 static void launch_select_two_stage(const Dims& m, const spla_cache& c, const DecodeWs& ws,
                                     char* base, int32_t* sel_out, hipStream_t st) {
   const int tj = (int)ceil_div(m.n_tiles, 64);  // tile partials per lane for Z
-  if (tj <= 2) slice_t<2>(m, c, ws, base, st);
-  else if (tj <= 4) slice_t<4>(m, c, ws, base, st);
-  else slice_t<8>(m, c, ws, base, st);
-  const int64_t r2 = ceil_div((int64_t)ws.n_sl * m.k, kPickThreads);
-  auto kern = r2 <= 1 ? select_pick_kernel<1>
-                      : (r2 <= 2 ? select_pick_kernel<2>
-                                 : (r2 <= 4 ? select_pick_kernel<4> : select_pick_kernel<8>));
-  hipLaunchKernelGGL(kern, dim3((unsigned)m.bh), dim3(kPickThreads), 0, st, m, ws.n_sl,
-                     c.seq_lens, (const uint32_t*)(base + ws.cand_key),
-                     (const int32_t*)(base + ws.cand_id), (const int32_t*)(base + ws.cand_n),
-                     (int32_t*)(base + ws.sel), sel_out, (int32_t*)(base + ws.meta));
+  if (tj <= 2) two_stage_tj<2>(m, c, ws, base, sel_out, st);
+  else if (tj <= 4) two_stage_tj<4>(m, c, ws, base, sel_out, st);
+  else two_stage_tj<8>(m, c, ws, base, sel_out, st);
 }
 
 hipError_t launch_select(const Dims& m, const spla_cache& c, const DecodeWs& ws, char* base,

@@ -281,6 +281,29 @@ struct Mem<true> {
 // The memory clobber keeps the compiler from moving accesses across it.
 __device__ __forceinline__ void wait_memory() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
+// Agent-scope (whole device) relaxed atomics on int32 counters and words.
+__device__ __forceinline__ int atomic_add_agent(int32_t* p, int v) {
+  return __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ int load_agent(const int32_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void store_agent(int32_t* p, int v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Every thread: waits until its stores (Mem<true>, so device-coherent once
+// complete) have completed, then the workgroup counts itself in *ctr. True in
+// every thread of the workgroup that arrived as the n-th; that workgroup reads
+// what the others published with Mem<true> loads.
+__device__ __forceinline__ bool arrive_last(int32_t* ctr, int n, int* s_flag) {
+  wait_memory();
+  __syncthreads();
+  if (threadIdx.x == 0) *s_flag = atomic_add_agent(ctr, 1) == n - 1;
+  __syncthreads();
+  return *s_flag != 0;
+}
+
 // Number of tokens of block i in a sequence of length L.
 __device__ __forceinline__ int block_count(int L, int B, int i) {
   int n = L - i * B;

@@ -514,8 +514,9 @@ __device__ void select_blocks(const Dims& m, int bh, int seq_len,
 // blocks and there are few heads (one sequence of 1M tokens: 8 workgroups).
 // Instead, slices of kSliceBlocks blocks each take their own top-kp
 // candidates (kp = k - forced blocks) under the same order as select_blocks
-// (score descending, lower block id first), then one workgroup per head
-// picks the top kp among the candidates. Every block of the global top kp
+// (score descending, lower block id first), then the last slice of each
+// head to finish picks the top kp among the candidates (the same launch:
+// one kernel boundary less). Every block of the global top kp
 // has fewer than kp blocks ahead of it in its own slice, so the candidates
 // hold the whole top set and the result is select_blocks' exactly: the keys
 // are computed with the same arithmetic in the same order.
@@ -523,7 +524,6 @@ __device__ void select_blocks(const Dims& m, int bh, int seq_len,
 constexpr int kSliceThreads = 256;
 constexpr int kSliceR = kSliceBlocks / kSliceThreads;     // blocks per thread
 constexpr int kSliceTiles = kSliceBlocks / kTileBlocks;   // 16 statistics tiles
-constexpr int kPickThreads = 1024;
 
 // The kp-th largest of the keys held R per thread by the NT threads (0: not
 // a candidate), found digit by digit as in select_blocks: keys above gt are
@@ -570,9 +570,12 @@ __device__ __forceinline__ void radix_cut(const uint32_t (&key)[R], uint32_t kp,
 
 // Slice sl (blocks sl kSliceBlocks ..) of sequence x KV head bh: the
 // candidates' keys and ids, ascending by id, to ck / ci (k slots) and their
-// count to *cn. Z_m comes from every tile partial of the head (TJ tiles per
-// lane), exactly as select_blocks forms it. Nothing for a head whose blocks
-// all fit in k (the pick selects them all). GM >= G: heads loaded.
+// count to *cn, written device-coherent (the pick runs in another workgroup
+// of the same launch). Z_m comes from every tile partial of the head (TJ
+// tiles per lane), exactly as select_blocks forms it; a wavefront with two
+// heads loads the second head's partials with the first's. Nothing for a
+// head whose blocks all fit in k (the pick selects them all). GM >= G: heads
+// loaded.
 template <int TJ, int GM>
 __device__ void select_slice(const Dims& m, int bh, int sl, const int32_t* __restrict__ seq_lens,
                              const float* __restrict__ e_vals,
@@ -580,6 +583,7 @@ __device__ void select_slice(const Dims& m, int bh, int sl, const int32_t* __res
                              int32_t* __restrict__ ci, int32_t* __restrict__ cn, float* sw,
                              uint32_t* hist, uint32_t* scan) {
   constexpr int R = kSliceR, NW = kSliceThreads / 64;
+  constexpr bool PRE2 = GM > NW && GM <= 2 * NW;  // heads w and w + NW preloaded
   const int G = m.group, k = m.k;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int nbp = m.n_tiles * kTileBlocks;
@@ -595,6 +599,15 @@ __device__ void select_slice(const Dims& m, int bh, int sl, const int32_t* __res
     load_tile_part<false>(tp + (int64_t)(w < G ? w : 0) * m.n_tiles * 2, t,
                           w < G && t < m.n_tiles, tm[j], ts[j]);
   }
+  double tm2[PRE2 ? TJ : 1], ts2[PRE2 ? TJ : 1];  // head w + NW
+  if constexpr (PRE2) {
+#pragma unroll
+    for (int j = 0; j < TJ; ++j) {
+      const int t = lane + 64 * j, w2 = w + NW;
+      load_tile_part<false>(tp + (int64_t)(w2 < G ? w2 : 0) * m.n_tiles * 2, t,
+                            w2 < G && t < m.n_tiles, tm2[j], ts2[j]);
+    }
+  }
   float e[GM][R];
 #pragma unroll
   for (int h = 0; h < GM; ++h)
@@ -602,7 +615,7 @@ __device__ void select_slice(const Dims& m, int bh, int sl, const int32_t* __res
   const int L = min(max(seq_lens[bh / m.hkv], 0), m.cap);
   const int nb = (L + m.B - 1) / m.B;
   if (nb <= k || kp <= 0 || sl * kSliceBlocks >= nb) {  // uniform over the workgroup
-    if (tid == 0) *cn = 0;
+    if (tid == 0) Mem<true>::st(cn, 0);
     return;
   }
   const int n_tu = (nb + kTileBlocks - 1) / kTileBlocks;
@@ -612,10 +625,19 @@ __device__ void select_slice(const Dims& m, int bh, int sl, const int32_t* __res
   const int jt = (sl * kSliceTiles) / 64, lt = (sl * kSliceTiles) % 64;  // slice tiles' lanes
   for (int mm = w; mm < G; mm += NW) {
     if (mm != w) {
+      if constexpr (PRE2) {  // loaded at the start
 #pragma unroll
-      for (int j = 0; j < TJ; ++j) {
-        const int t = lane + 64 * j;
-        load_tile_part<false>(tp + (int64_t)mm * m.n_tiles * 2, t, t < m.n_tiles, tm[j], ts[j]);
+        for (int j = 0; j < TJ; ++j) {
+          tm[j] = tm2[j];
+          ts[j] = ts2[j];
+        }
+      } else {
+#pragma unroll
+        for (int j = 0; j < TJ; ++j) {
+          const int t = lane + 64 * j;
+          load_tile_part<false>(tp + (int64_t)mm * m.n_tiles * 2, t, t < m.n_tiles, tm[j],
+                                ts[j]);
+        }
       }
     }
     double mx = -INFINITY;
@@ -688,27 +710,28 @@ __device__ void select_slice(const Dims& m, int bh, int sl, const int32_t* __res
     a_run += tk[r] ? 1u : 0u;
     e_run += tq[r] ? 1u : 0u;
     if (pos < (uint32_t)k) {
-      ck[pos] = key[r];
-      ci[pos] = i0 + r;
+      Mem<true>::st(ck + pos, key[r]);
+      Mem<true>::st(ci + pos, i0 + r);
     }
   }
   const uint32_t ta = tot_p & 0xFFFFu, te = tot_p >> 16;
-  if (tid == 0) *cn = (int)(ta + (te < eq_need ? te : eq_need));
+  if (tid == 0) Mem<true>::st(cn, (int)(ta + (te < eq_need ? te : eq_need)));
 }
 
 // The pick of sequence x KV head bh from the candidates of its n_sl slices
 // (k slots each, ck / ci / cn as select_slice wrote them): the kp largest,
 // ties to the lower id, and the forced blocks, ascending, to sel[0 .. k)
-// (-1 padded) and so (if not NULL); meta4 as select_blocks writes it. R2:
-// candidate slots per thread (kPickThreads R2 >= n_sl k); the slots in
-// thread order are ascending by id.
-template <int R2>
+// (-1 padded) and so (if not NULL); meta4 as select_blocks writes it. NT
+// threads, R2 candidate slots per thread (NT R2 >= n_sl k); the slots in
+// thread order are ascending by id. The candidates are read device-coherent
+// (other workgroups of the same launch wrote them).
+template <int R2, int NT>
 __device__ void select_pick(const Dims& m, int bh, int n_sl, const int32_t* __restrict__ seq_lens,
                             const uint32_t* __restrict__ ck, const int32_t* __restrict__ ci,
                             const int32_t* __restrict__ cn, int32_t* __restrict__ sel,
                             int32_t* __restrict__ meta4, int32_t* __restrict__ so,
                             uint32_t* hist, uint32_t* scan, int32_t* out) {
-  constexpr int NT = kPickThreads, NW = NT / 64;
+  constexpr int NW = NT / 64;
   const int k = m.k, tid = threadIdx.x;
   const int kp = k - m.n_sink - m.n_local;
   uint32_t key[R2];
@@ -718,9 +741,9 @@ __device__ void select_pick(const Dims& m, int bh, int n_sl, const int32_t* __re
     const int q = tid * R2 + r, s = q / k, j = q % k;
     const bool ok = s < n_sl;
     const int qq = ok ? q : 0;
-    const int n = cn[ok ? s : 0];
-    const uint32_t kv = ck[qq];
-    const int32_t iv = ci[qq];
+    const int n = Mem<true>::ld(cn + (ok ? s : 0));
+    const uint32_t kv = Mem<true>::ld(ck + qq);
+    const int32_t iv = Mem<true>::ld(ci + qq);
     key[r] = ok && j < n ? kv : 0u;
     id[r] = iv;
   }
