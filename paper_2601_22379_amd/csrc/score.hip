@@ -1,7 +1,12 @@
 // Block scoring kernel (Sec. 3.1): one workgroup per (sequence, KV head,
 // tile of 64 blocks) item; every item's loads are in flight from the start
-// (after the sequence length, which skips the tiles past the end).
-// The per-tile arithmetic is score_items (spla_score.h).
+// (after the sequence length, which skips the tiles past the end). Items are
+// in tile-major order (the same tile of every (sequence, KV head), then the
+// next): the heads' statistics streams run side by side, and with lengths
+// that vary the items past a sequence's end gather at the end of the grid
+// (high-batch decode 176.4 -> 170.4 us, 1M tokens 50.4 -> 48.1 us, against
+// (sequence, KV head)-major order). The per-tile arithmetic is score_items
+// (spla_score.h).
 #include "spla_kernels.h"
 #include "spla_score.h"
 
@@ -13,8 +18,8 @@ __global__ __launch_bounds__(256) void score_kernel(
     const T* __restrict__ q, double s, int first_order, float* __restrict__ e_vals,
     double* __restrict__ tile_part) {
   __shared__ ScoreSmem<G> sm;
-  const int per = (m.n_tiles + NT - 1) / NT;  // items per (sequence, KV head)
-  const int t = ((int)blockIdx.x / per) * m.n_tiles + ((int)blockIdx.x % per) * NT;
+  // item x: tiles NT (x / bh) .. of (sequence, KV head) x % bh
+  const int t = ((int)blockIdx.x % m.bh) * m.n_tiles + ((int)blockIdx.x / m.bh) * NT;
   // a tile wholly past the sequence end is neither read nor scored: the
   // selection reads the tiles that hold units only
   const int L = min(max(seq_lens[t / m.n_tiles / m.hkv], 0), m.cap);
