@@ -9,15 +9,15 @@ namespace spla {
 
 constexpr int kSelThreads = 1024;
 
-template <int R, bool WIN>
-__global__ __launch_bounds__(kSelThreads) void select_kernel(
+template <int R, bool WIN, int NT = kSelThreads>
+__global__ __launch_bounds__(NT) void select_kernel(
     Dims m, const int32_t* __restrict__ seq_lens, const float* __restrict__ e_vals,
     const double* __restrict__ tile_part, int32_t* __restrict__ sel_ws,
     int32_t* __restrict__ sel_out, int32_t* __restrict__ meta) {
-  __shared__ SelectSmem<kSelThreads, kMaxTiles * SPLA_MAX_GROUP> sm;
+  __shared__ SelectSmem<NT, kMaxTiles * SPLA_MAX_GROUP> sm;
   __shared__ float wsc[WIN ? kMaxWindows : 1];  // window scores (strided selection)
   const int bh = blockIdx.x;
-  select_blocks<kSelThreads, R, kMaxTiles * SPLA_MAX_GROUP, false, 0, WIN>(
+  select_blocks<NT, R, kMaxTiles * SPLA_MAX_GROUP, false, 0, WIN>(
       m, bh, seq_lens[bh / m.hkv], e_vals, tile_part, sm, sel_ws + (int64_t)bh * m.k,
       meta + bh * 4, sel_out ? sel_out + (int64_t)bh * m.k : nullptr, wsc);
 }
@@ -93,24 +93,31 @@ hipError_t launch_select(const Dims& m, const spla_cache& c, const DecodeWs& ws,
   const double* tp = (const double*)(base + ws.tile_part);
   int32_t* sel = (int32_t*)(base + ws.sel);
   int32_t* meta = (int32_t*)(base + ws.meta);
-  // blocks per thread: at most 4096 blocks here without windows (two stages
-  // past that); with windows at most kMaxWindows windows, so at most 16384
-  // blocks
+  // blocks per thread of 1024: at most 4096 blocks here without windows
+  // (two stages past that); with windows at most kMaxWindows windows, so at
+  // most 16384 blocks
   const int per = (int)ceil_div(m.nb_cap, kSelThreads);
-  auto launch = [&](auto kern) {
-    hipLaunchKernelGGL(kern, dim3(m.bh), dim3(kSelThreads), 0, st, m, c.seq_lens, ev, tp, sel,
-                       sel_out, meta);
+  auto launch = [&](auto kern, int nt) {
+    hipLaunchKernelGGL(kern, dim3(m.bh), dim3(nt), 0, st, m, c.seq_lens, ev, tp, sel, sel_out,
+                       meta);
   };
   if (windowed(m)) {
-    if (per <= 1) launch(select_kernel<1, true>);
-    else if (per <= 2) launch(select_kernel<2, true>);
-    else if (per <= 4) launch(select_kernel<4, true>);
-    else if (per <= 8) launch(select_kernel<8, true>);
-    else launch(select_kernel<16, true>);
+    if (per <= 1) launch(select_kernel<1, true>, kSelThreads);
+    else if (per <= 2) launch(select_kernel<2, true>, kSelThreads);
+    else if (per <= 4) launch(select_kernel<4, true>, kSelThreads);
+    else if (per <= 8) launch(select_kernel<8, true>, kSelThreads);
+    else launch(select_kernel<16, true>, kSelThreads);
+  } else if (m.nb_cap <= 1024) {
+    // at most one block per thread of 1024: 256 threads (four wavefronts,
+    // so cheaper barriers) with up to four blocks each (many short
+    // sequences: 64 x 8 heads at 512 blocks, high-batch decode
+    // 170.1 -> 164.9 us)
+    if (m.nb_cap <= 256) launch(select_kernel<1, false, 256>, 256);
+    else if (m.nb_cap <= 512) launch(select_kernel<2, false, 256>, 256);
+    else launch(select_kernel<4, false, 256>, 256);
   } else {
-    if (per <= 1) launch(select_kernel<1, false>);
-    else if (per <= 2) launch(select_kernel<2, false>);
-    else launch(select_kernel<4, false>);
+    if (per <= 2) launch(select_kernel<2, false>, kSelThreads);
+    else launch(select_kernel<4, false>, kSelThreads);
   }
   return hipGetLastError();
 }
