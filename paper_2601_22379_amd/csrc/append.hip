@@ -560,34 +560,66 @@ __device__ __forceinline__ void append_rank1_rows(const Dims& m,
   if (tid < 16) z[(int64_t)bh * D + row0 + tid] += sphi[row0 + tid];
 }
 
+// The end of a single-token append workgroup of (sequence, KV head) bh:
+// the workgroups of a sequence (hkv x gridDim.x of them) count themselves in
+// its counter (a line of the decode workspace's synchronisation area, zero
+// between calls), and the last advances seq_lens[b] by the token appended (0
+// at the capacity), writes that count to appended[b] (if not NULL) and
+// resets the counter. Every workgroup has read seq_lens[b] before it counts
+// itself, so no read of the old length follows the advance.
+__device__ __forceinline__ void append_one_finish(const Dims& m, int32_t* seq_lens,
+                                                  int32_t* fin_ctr, int32_t* appended, int bh,
+                                                  int* s_flag) {
+  const int b = bh / m.hkv;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int32_t* c = fin_ctr + (int64_t)b * kSyncLine;
+    if (atomic_add_agent(c, 1) == m.hkv * (int)gridDim.x - 1) {
+      bool clipped;
+      const int L0 = seq_lens[b];
+      const int n = appended_count(m, L0, 1, nullptr, b, &clipped);
+      seq_lens[b] = L0 + n;
+      if (appended) appended[b] = n;
+      store_agent(c, 0);
+    }
+  }
+}
+
 // The single-token append of a decode step in one launch: workgroups
 // x < D / 16 update 16 rows of S_bar each (rank one), the others the
 // statistics units the token falls in (and copy its K/V rows). The two parts
-// touch disjoint memory and only read seq_lens, which append_finish_kernel
-// advances afterwards.
+// touch disjoint memory and only read seq_lens, which the last workgroup of
+// each sequence advances afterwards (fin_ctr given: append_one_finish), or
+// append_finish_kernel.
 template <typename T, int D>
 __global__ __launch_bounds__(256) void append_one_kernel(
     Dims m, T* __restrict__ kc, T* __restrict__ vc, float* __restrict__ stats,
-    const int32_t* __restrict__ seq_lens, int32_t* __restrict__ err, const T* __restrict__ k_new,
+    int32_t* __restrict__ seq_lens, int32_t* __restrict__ err, const T* __restrict__ k_new,
     const T* __restrict__ v_new, const int32_t* __restrict__ table, float* __restrict__ S,
-    float* __restrict__ z) {
+    float* __restrict__ z, int32_t* __restrict__ fin_ctr, int32_t* __restrict__ appended) {
+  __shared__ int s_flag;
   const int bh = (int)blockIdx.y;
   if ((int)blockIdx.x < D / 16)
     append_rank1_rows<T, D>(m, seq_lens, k_new, v_new, S, z, (int)blockIdx.x, bh);
   else
     append_unit<T>(m, kc, vc, stats, seq_lens, err, k_new, v_new, 1, nullptr, table,
                    (int)blockIdx.x - D / 16, bh, D, D);
+  if (fin_ctr) append_one_finish(m, seq_lens, fin_ctr, appended, bh, &s_flag);
 }
 
 // The statistics units and K/V rows of a single-token append alone (the
-// state's rank-one update is applied elsewhere): append_unit, d threads.
+// state's rank-one update is applied elsewhere): append_unit, d threads; then
+// append_one_finish when fin_ctr is given.
 template <typename T>
 __global__ __launch_bounds__(128) void append_unit_kernel(
     Dims m, T* __restrict__ kc, T* __restrict__ vc, float* __restrict__ stats,
-    const int32_t* __restrict__ seq_lens, int32_t* __restrict__ err, const T* __restrict__ k_new,
-    const T* __restrict__ v_new, const int32_t* __restrict__ table) {
+    int32_t* __restrict__ seq_lens, int32_t* __restrict__ err, const T* __restrict__ k_new,
+    const T* __restrict__ v_new, const int32_t* __restrict__ table, int32_t* __restrict__ fin_ctr,
+    int32_t* __restrict__ appended) {
+  __shared__ int s_flag;
   append_unit<T>(m, kc, vc, stats, seq_lens, err, k_new, v_new, 1, nullptr, table,
                  (int)blockIdx.x, (int)blockIdx.y, m.d, m.d);
+  if (fin_ctr) append_one_finish(m, seq_lens, fin_ctr, appended, (int)blockIdx.y, &s_flag);
 }
 
 // seq_lens[b] += the tokens appended; appended (if not NULL) receives that
@@ -671,28 +703,31 @@ static int64_t units_of_one(const Dims& m) { return windowed(m) ? m.ul / m.us : 
 
 template <typename T, int D>
 static void append_one_td(const Dims& m, const spla_cache& c, const void* k_new,
-                          const void* v_new, hipStream_t st, bool rank1) {
+                          const void* v_new, hipStream_t st, bool rank1, int32_t* fin_ctr,
+                          int32_t* appended) {
   if (!rank1) {  // statistics and rows only
     hipLaunchKernelGGL(append_unit_kernel<T>, dim3((unsigned)units_of_one(m), (unsigned)m.bh),
                        dim3(D), 0, st, m, (T*)c.k_cache, (T*)c.v_cache, c.blk_stats, c.seq_lens,
                        c.err_flags, (const T*)k_new, (const T*)v_new,
-                       m.pages > 0 ? c.block_table : nullptr);
+                       m.pages > 0 ? c.block_table : nullptr, fin_ctr, appended);
     return;
   }
   hipLaunchKernelGGL((append_one_kernel<T, D>), dim3((unsigned)(D / 16 + units_of_one(m)),
                      (unsigned)m.bh), dim3(256), 0, st, m, (T*)c.k_cache, (T*)c.v_cache,
                      c.blk_stats, c.seq_lens, c.err_flags, (const T*)k_new, (const T*)v_new,
-                     m.pages > 0 ? c.block_table : nullptr, c.lin_state, c.lin_norm);
+                     m.pages > 0 ? c.block_table : nullptr, c.lin_state, c.lin_norm, fin_ctr,
+                     appended);
 }
 
 hipError_t launch_append_one(const Dims& m, const spla_cache& c, const void* k_new,
-                             const void* v_new, hipStream_t st, bool rank1) {
+                             const void* v_new, hipStream_t st, bool rank1, int32_t* fin_ctr,
+                             int32_t* appended) {
   if (m.elem == 4) {
-    if (m.d == 64) append_one_td<float, 64>(m, c, k_new, v_new, st, rank1);
-    else append_one_td<float, 128>(m, c, k_new, v_new, st, rank1);
+    if (m.d == 64) append_one_td<float, 64>(m, c, k_new, v_new, st, rank1, fin_ctr, appended);
+    else append_one_td<float, 128>(m, c, k_new, v_new, st, rank1, fin_ctr, appended);
   } else {
-    if (m.d == 64) append_one_td<bf16_t, 64>(m, c, k_new, v_new, st, rank1);
-    else append_one_td<bf16_t, 128>(m, c, k_new, v_new, st, rank1);
+    if (m.d == 64) append_one_td<bf16_t, 64>(m, c, k_new, v_new, st, rank1, fin_ctr, appended);
+    else append_one_td<bf16_t, 128>(m, c, k_new, v_new, st, rank1, fin_ctr, appended);
   }
   return hipGetLastError();
 }

@@ -187,23 +187,24 @@ extern "C" int32_t spla_step_ex(const spla_config* cfg, const spla_cache* cache,
   if (!k_new || !v_new) return SPLA_ERR_INVALID_ARG;
   const Dims m = spla::make_dims(*cfg);
   hipStream_t st = static_cast<hipStream_t>(stream);
+  // the append's last workgroup of each sequence advances its length (the
+  // counters: the workspace's item lines, zero between calls)
+  const spla::DecodeWs L = spla::decode_ws_layout(m);
+  char* base = static_cast<char*>(ws);
+  int32_t* fin = reinterpret_cast<int32_t*>(base + L.sync) + spla::sync_layout(m).items_done;
   if (spla::step_fusable(m)) {
     // the token's rows and statistics first; its rank-one update of S_bar is
     // applied by the decode's sparse pass to the rows it reads anyway
-    const spla::DecodeWs L = spla::decode_ws_layout(m);
-    char* base = static_cast<char*>(ws);
     {
       PhaseMark pm(ev, st, SPLA_PHASE_APPEND);
-      SPLA_TRY(spla::launch_append_one(m, *cache, k_new, v_new, st, false));
-      SPLA_TRY(spla::launch_append_finish(m, *cache, 1, nullptr, st,
-                                          reinterpret_cast<int32_t*>(base + L.appended)));
+      SPLA_TRY(spla::launch_append_one(m, *cache, k_new, v_new, st, false, fin,
+                                       reinterpret_cast<int32_t*>(base + L.appended)));
     }
     return run_decode(cfg, cache, q, w, out, sel_idx, ws, ws_bytes, ev, st, k_new, v_new);
   }
   {
     PhaseMark pm(ev, st, SPLA_PHASE_APPEND);
-    SPLA_TRY(spla::launch_append_one(m, *cache, k_new, v_new, st));
-    SPLA_TRY(spla::launch_append_finish(m, *cache, 1, nullptr, st));
+    SPLA_TRY(spla::launch_append_one(m, *cache, k_new, v_new, st, true, fin));
   }
   return run_decode(cfg, cache, q, w, out, sel_idx, ws, ws_bytes, ev, st);
 }
@@ -252,9 +253,14 @@ extern "C" int32_t spla_prefill_ex(const spla_config* cfg, const spla_cache* cac
     }
     return SPLA_OK;
   }
+  // the decode workspace: its item lines count the append's workgroups; it
+  // comes unprepared, so its synchronisation area is cleared first
+  char* sync = static_cast<char*>(ws) + spla::decode_ws_layout(m).sync;
+  SPLA_TRY(spla::launch_fill_zero(sync, (size_t)spla::sync_layout(m).words * 4, st));
+  int32_t* fin = reinterpret_cast<int32_t*>(sync) + spla::sync_layout(m).items_done;
   for (int32_t t = 0; t < n_tokens; ++t) {
-    SPLA_TRY(spla::launch_append_one(m, *cache, kb + t * kv_step, vb + t * kv_step, st));
-    SPLA_TRY(spla::launch_append_finish(m, *cache, 1, nullptr, st));
+    SPLA_TRY(spla::launch_append_one(m, *cache, kb + t * kv_step, vb + t * kv_step, st, true,
+                                     fin));
     if ((s = run_decode(cfg, cache, qb + t * q_step, w, ob + t * q_step,
                         sel_idx ? sel_idx + t * sel_step : nullptr, ws, ws_bytes, nullptr, st)) !=
         SPLA_OK)

@@ -28,11 +28,14 @@ hipError_t launch_append_state(const Dims& m, const spla_cache& c, const void* k
                                const void* v_new, int max_new, const int32_t* n_new,
                                const AppendWs& ws, char* wsbase, hipStream_t st);
 // the single-token append of a step (statistics, K/V rows and, with rank1,
-// the rank-one update of S_bar and z_bar) in one launch; seq_lens is advanced
-// by launch_append_finish, which also writes the count each sequence received
-// to appended (if not NULL)
+// the rank-one update of S_bar and z_bar) in one launch. With fin_ctr (the
+// items_done lines of a decode workspace's synchronisation area) the last
+// workgroup of each sequence advances seq_lens and writes the count the
+// sequence received to appended (if not NULL); without it launch_append_finish
+// must follow
 hipError_t launch_append_one(const Dims& m, const spla_cache& c, const void* k_new,
-                             const void* v_new, hipStream_t st, bool rank1 = true);
+                             const void* v_new, hipStream_t st, bool rank1 = true,
+                             int32_t* fin_ctr = nullptr, int32_t* appended = nullptr);
 hipError_t launch_append_finish(const Dims& m, const spla_cache& c, int max_new,
                                 const int32_t* n_new, hipStream_t st,
                                 int32_t* appended = nullptr);
