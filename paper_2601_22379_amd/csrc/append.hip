@@ -346,16 +346,26 @@ __global__ __launch_bounds__(256) void append_state_partial_kernel(
 //   P[j][c] += sum_t phi(k_t)_j v_t,c
 // on v_mfma_f32_16x16x32_bf16 (hi and lo products, fp32 accumulation).
 // Wavefront w owns columns (D / 4) w .. of P: D / 16 row tiles x D / 64
-// column tiles. Pz accumulates phi(k) in fp32 per lane.
+// column tiles. Each wavefront reads its 8 tokens of a step with 16-byte
+// loads, D / 8 lanes per token, and takes the softmax's max and sum over a
+// token's lanes by DPP (two-byte loads, one token at a time with full-wave
+// reductions, took 146 us for a 16K-token slab at 128K). Pz accumulates
+// phi(k) in fp32 per lane.
 typedef __bf16 abf16x8 __attribute__((ext_vector_type(8)));
 typedef float afloatx4 __attribute__((ext_vector_type(4)));
 
+// Coordinate c's row of a transposed array starts at c TPP + 8 (c / 8): the
+// pad after every 8 rows puts the 16 coordinate groups a wavefront writes at
+// once (one token of 8 coordinates per lane) on 16 different banks, and
+// keeps every row 16-byte aligned for the operand reads.
 template <int D>
 struct alignas(16) StateSmem {
   static constexpr int TPP = kSubTokens + 8;
-  uint16_t kT_h[D][TPP], kT_l[D][TPP];  // phi(k)^T of the step
-  uint16_t vT[D][TPP];                  // v^T of the step
-  float z[4][D];                        // per-wavefront sums of phi(k)
+  static constexpr int N = D * TPP + D;
+  static __device__ __forceinline__ int at(int c, int t) { return c * TPP + 8 * (c >> 3) + t; }
+  uint16_t kT_h[N], kT_l[N];  // phi(k)^T of the step
+  uint16_t vT[N];             // v^T of the step
+  float z[4][D];              // per-wavefront sums of phi(k)
 };
 
 template <int D>
@@ -365,7 +375,6 @@ __global__ __launch_bounds__(256) void append_state_mfma_kernel(
     int chunk_tokens, float* __restrict__ part_s, float* __restrict__ part_z) {
   constexpr int RT = D / 16;        // row tiles (coordinates j)
   constexpr int CT = D / 64;        // column tiles per wavefront
-  constexpr int E = D / 64;         // elements of a row per lane (lane + 64 e)
   __shared__ StateSmem<D> sm;
   const int bh = blockIdx.y;
   const int b = bh / m.hkv;
@@ -380,76 +389,105 @@ __global__ __launch_bounds__(256) void append_state_mfma_kernel(
   for (int r = 0; r < RT; ++r)
 #pragma unroll
     for (int c = 0; c < CT; ++c) acc[r][c] = afloatx4{0.f, 0.f, 0.f, 0.f};
-  float zacc[E];
+  float zacc[8];  // phi(k) of this lane's coordinates, summed over its tokens
 #pragma unroll
-  for (int e = 0; e < E; ++e) zacc[e] = 0.f;
+  for (int i = 0; i < 8; ++i) zacc[i] = 0.f;
   const bf16_t* kb = k_new + (int64_t)bh * max_new * D;
   const bf16_t* vb = v_new + (int64_t)bh * max_new * D;
-  // wavefront w takes tokens 8 w .. 8 w + 7 of each 32-token step, lane l
-  // coordinates l + 64 e; the next step's rows are loaded while the current
-  // one is processed
-  uint16_t kx[8][E], vx[8][E];
+  // wavefront w takes tokens 8 w .. 8 w + 7 of each 32-token step as NS
+  // 16-byte loads per lane: LPR = D / 8 lanes per token (lane l holds
+  // coordinates 8 (l % LPR) .. + 7 of token 8 w + RPL s + l / LPR); the next
+  // step's rows are loaded while the current one is processed
+  constexpr int LPR = D / 8, RPL = 64 / LPR, NS = 8 / RPL;
+  const int cl = lane % LPR, tl = lane / LPR;
+  uint4 kx[NS], vx[NS];
   auto load_step = [&](int tt) {
 #pragma unroll
-    for (int r = 0; r < 8; ++r) {
-      const int row = min(tt + 8 * w + r, t1 - 1);
-#pragma unroll
-      for (int e = 0; e < E; ++e) {
-        kx[r][e] = kb[(int64_t)row * D + lane + 64 * e].bits;
-        vx[r][e] = vb[(int64_t)row * D + lane + 64 * e].bits;
-      }
+    for (int s = 0; s < NS; ++s) {
+      const int row = min(tt + 8 * w + RPL * s + tl, t1 - 1);
+      kx[s] = *reinterpret_cast<const uint4*>(kb + (int64_t)row * D + 8 * cl);
+      vx[s] = *reinterpret_cast<const uint4*>(vb + (int64_t)row * D + 8 * cl);
     }
+  };
+  // max / sum over the LPR lanes of a token (every lane gets the same bits)
+  auto row_max = [](float v) {
+    if constexpr (LPR == 16) {
+      v = fmaxf(v, dpp_rot<0x128>(v));  // row_ror:8
+      v = fmaxf(v, dpp_rot<0x124>(v));  // row_ror:4
+    } else {
+      v = fmaxf(v, dpp_rot<0x141>(v));  // row_half_mirror
+    }
+    v = fmaxf(v, dpp_rot<0x4E>(v));
+    return fmaxf(v, dpp_rot<0xB1>(v));
+  };
+  auto row_sum = [](float v) {
+    if constexpr (LPR == 16) {
+      v += dpp_rot<0x128>(v);
+      v += dpp_rot<0x124>(v);
+    } else {
+      v += dpp_rot<0x141>(v);
+    }
+    v += dpp_rot<0x4E>(v);
+    return v + dpp_rot<0xB1>(v);
   };
   if (t0 < t1) load_step(t0);
   for (int tt = t0; tt < t1; tt += kSubTokens) {
     const int nt = min(kSubTokens, t1 - tt);
-    float kf[8][E];
-    uint16_t vv[8][E];
+    uint4 kc[NS], vc[NS];
 #pragma unroll
-    for (int r = 0; r < 8; ++r)
-#pragma unroll
-      for (int e = 0; e < E; ++e) {
-        kf[r][e] = bf16_to_f32(kx[r][e]);
-        vv[r][e] = vx[r][e];
-      }
+    for (int s = 0; s < NS; ++s) {
+      kc[s] = kx[s];
+      vc[s] = vx[s];
+    }
     if (tt + kSubTokens < t1) load_step(tt + kSubTokens);
 #pragma unroll
-    for (int r = 0; r < 8; ++r) {
-      const int t = 8 * w + r;
+    for (int s = 0; s < NS; ++s) {
+      const int t = 8 * w + RPL * s + tl;
       const bool ok = t < nt;
-      float mx = -INFINITY;
+      const uint32_t kw[4] = {kc[s].x, kc[s].y, kc[s].z, kc[s].w};
+      const uint32_t vw[4] = {vc[s].x, vc[s].y, vc[s].z, vc[s].w};
+      float kf[8];
 #pragma unroll
-      for (int e = 0; e < E; ++e) mx = fmaxf(mx, kf[r][e]);
-      mx = wave_max(mx);
+      for (int i = 0; i < 8; ++i)
+        kf[i] = bf16_to_f32((uint16_t)(i & 1 ? kw[i >> 1] >> 16 : kw[i >> 1] & 0xFFFFu));
+      float mx = kf[0];
+#pragma unroll
+      for (int i = 1; i < 8; ++i) mx = fmaxf(mx, kf[i]);
+      mx = row_max(mx);
       float sum = 0.f;
 #pragma unroll
-      for (int e = 0; e < E; ++e) {
-        kf[r][e] = expf(kf[r][e] - mx);
-        sum += kf[r][e];
+      for (int i = 0; i < 8; ++i) {
+        kf[i] = expf(kf[i] - mx);
+        sum += kf[i];
       }
-      sum = wave_sum(sum);
+      sum = row_sum(sum);
       const float inv = ok ? 1.0f / sum : 0.f;
 #pragma unroll
-      for (int e = 0; e < E; ++e) {
-        const float ph = kf[r][e] * inv;
+      for (int i = 0; i < 8; ++i) {
+        const float ph = kf[i] * inv;
         const __bf16 hi = (__bf16)ph;
         const __bf16 lo = (__bf16)(ph - (float)hi);
-        const int col = lane + 64 * e;
-        sm.kT_h[col][t] = __builtin_bit_cast(uint16_t, hi);
-        sm.kT_l[col][t] = __builtin_bit_cast(uint16_t, lo);
-        sm.vT[col][t] = ok ? vv[r][e] : (uint16_t)0;
-        zacc[e] += ph;
+        const int o = StateSmem<D>::at(8 * cl + i, t);
+        sm.kT_h[o] = __builtin_bit_cast(uint16_t, hi);
+        sm.kT_l[o] = __builtin_bit_cast(uint16_t, lo);
+        sm.vT[o] = ok ? (uint16_t)(i & 1 ? vw[i >> 1] >> 16 : vw[i >> 1] & 0xFFFFu)
+                      : (uint16_t)0;
+        zacc[i] += ph;
       }
     }
     __syncthreads();
 #pragma unroll
     for (int r = 0; r < RT; ++r) {
-      const abf16x8 ah = __builtin_bit_cast(abf16x8, *reinterpret_cast<const uint4*>(&sm.kT_h[16 * r + li][8 * lg]));
-      const abf16x8 al = __builtin_bit_cast(abf16x8, *reinterpret_cast<const uint4*>(&sm.kT_l[16 * r + li][8 * lg]));
+      const int oa = StateSmem<D>::at(16 * r + li, 8 * lg);
+      const abf16x8 ah =
+          __builtin_bit_cast(abf16x8, *reinterpret_cast<const uint4*>(&sm.kT_h[oa]));
+      const abf16x8 al =
+          __builtin_bit_cast(abf16x8, *reinterpret_cast<const uint4*>(&sm.kT_l[oa]));
 #pragma unroll
       for (int c = 0; c < CT; ++c) {
         const int col = (D / 4) * w + 16 * c + li;
-        const abf16x8 bv = __builtin_bit_cast(abf16x8, *reinterpret_cast<const uint4*>(&sm.vT[col][8 * lg]));
+        const abf16x8 bv = __builtin_bit_cast(
+            abf16x8, *reinterpret_cast<const uint4*>(&sm.vT[StateSmem<D>::at(col, 8 * lg)]));
         acc[r][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bv, acc[r][c], 0, 0, 0);
         acc[r][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, bv, acc[r][c], 0, 0, 0);
       }
@@ -464,8 +502,20 @@ __global__ __launch_bounds__(256) void append_state_mfma_kernel(
 #pragma unroll
       for (int r4 = 0; r4 < 4; ++r4)
         ps[(16 * r + 4 * lg + r4) * D + (D / 4) * w + 16 * c + li] = acc[r][c][r4];
+  // the lanes of one coordinate group: l, l + LPR, ... (LPR = 16: xor 16,
+  // xor 32; LPR = 8: first the other half of the 16-lane row)
 #pragma unroll
-  for (int e = 0; e < E; ++e) sm.z[w][lane + 64 * e] = zacc[e];
+  for (int i = 0; i < 8; ++i) {
+    float v = zacc[i];
+    if constexpr (LPR == 8) v += dpp_rot<0x128>(v);
+    v += xor16(v);
+    v += xor32(v);
+    zacc[i] = v;
+  }
+  if (lane < LPR) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) sm.z[w][8 * lane + i] = zacc[i];
+  }
   __syncthreads();
   if (tid < D) {
     float z = 0.f;
