@@ -106,7 +106,8 @@ __device__ __forceinline__ void append_unit(
 // of the cache layout (8 tokens of one coordinate for bf16, 4 for fp32);
 // pieces not wholly inside the rows this unit copies are written element by
 // element. Statistics as in append_unit: two passes in fp64 over the new
-// tokens (partial sums of the token lanes added in a fixed order), Chan's
+// tokens (the token lanes' partial sums added in a fixed tree: first the
+// lanes of a wavefront by lane swaps, then the four wavefronts), Chan's
 // combination with the stored ones, rounded to fp32.
 constexpr int kAppendUnitRows = 128;  // rows a unit copies at most (us <= B <= 128)
 
@@ -117,7 +118,7 @@ __global__ __launch_bounds__(256) void append_blocks_kernel(
     const T* __restrict__ v_new, int max_new, const int32_t* __restrict__ n_new,
     const int32_t* __restrict__ table, int64_t s_bh, int64_t s_row) {
   constexpr int VEC = 16 / (int)sizeof(T);
-  __shared__ double part[256 * VEC];
+  __shared__ double part[4 * 128];  // per wavefront and coordinate
   __shared__ double smean[128];
   __shared__ __align__(16) T sV[kAppendUnitRows * 128];
   const int ux = (int)blockIdx.x, bh = (int)blockIdx.y;
@@ -173,8 +174,17 @@ __global__ __launch_bounds__(256) void append_blocks_kernel(
       }
     }
   }
+  // the token lanes of this wavefront (lanes cq, cq + NQ, ...), then one
+  // entry per wavefront and coordinate
+  const int w = tid >> 6, lane = tid & 63;
+  auto lanes_sum = [&](double (&v)[VEC]) {
 #pragma unroll
-  for (int e = 0; e < VEC; ++e) part[tl * d + c0 + e] = sum[e];
+    for (int e = 0; e < VEC; ++e) {
+      for (int sft = NQ; sft < 64; sft *= 2) v[e] += __shfl_xor(v[e], sft, 64);
+      if (lane < NQ) part[w * d + c0 + e] = v[e];
+    }
+  };
+  lanes_sum(sum);
   __syncthreads();
   // value pieces: PV tokens of one coordinate each
   if (slot >= 0) {
@@ -201,10 +211,9 @@ __global__ __launch_bounds__(256) void append_blocks_kernel(
   double mean_c[VEC];
 #pragma unroll
   for (int e = 0; e < VEC; ++e) {
-    double tot = 0.0;
-    for (int x = 0; x < TS; ++x) tot += part[x * d + c0 + e];
-    mean_c[e] = tot / nc;
-    if (tl == 0) smean[c0 + e] = mean_c[e];
+    const int c = c0 + e;
+    mean_c[e] = (((part[c] + part[d + c]) + part[2 * d + c]) + part[3 * d + c]) / nc;
+    if (tl == 0) smean[c] = mean_c[e];
   }
   __syncthreads();
   // pass 2: sum of squared deviations from the new tokens' mean
@@ -228,14 +237,12 @@ __global__ __launch_bounds__(256) void append_blocks_kernel(
       }
     }
   }
-#pragma unroll
-  for (int e = 0; e < VEC; ++e) part[tl * d + c0 + e] = m2[e];
+  lanes_sum(m2);
   __syncthreads();
   // coordinate j = tid (d threads): combine with the stored statistics
   if (tid >= d) return;
   const int j = tid;
-  double m2s = 0.0;
-  for (int x = 0; x < TS; ++x) m2s += part[x * d + j];
+  const double m2s = ((part[j] + part[d + j]) + part[2 * d + j]) + part[3 * d + j];
   const double mc = smean[j];
   const int na = t_lo - i * m.us;
   const int64_t o_mean = stats_off4(m, bh, i, 0, j / 4) + (j & 3);
