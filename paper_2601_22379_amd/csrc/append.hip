@@ -532,28 +532,31 @@ __global__ __launch_bounds__(256) void append_state_mfma_kernel(
   }
 }
 
-// S_bar += sum of the chunk partials, accumulated in fp64 in chunk order.
+// S_bar += sum of the chunk partials, accumulated in fp64 in chunk order;
+// kReduceRows rows of S_bar per workgroup (4: a thread has two entries at
+// d = 128, and 32 x bh workgroups keep every compute unit busy).
+constexpr int kReduceRows = 4;
 __global__ __launch_bounds__(256) void append_state_reduce_kernel(
     Dims m, int n_chunks, const float* __restrict__ part_s, const float* __restrict__ part_z,
     float* __restrict__ S, float* __restrict__ z) {
   const int bh = blockIdx.y;
   const int D = m.d;
-  const int row0 = blockIdx.x * 16;
-  for (int e = threadIdx.x; e < 16 * D; e += 256) {
+  const int row0 = blockIdx.x * kReduceRows;
+  for (int e = threadIdx.x; e < kReduceRows * D; e += 256) {
     const int row = row0 + e / D, col = e % D;
     const int64_t o = ((int64_t)bh * D + row) * D + col;
     double s = S[o];
     const float* p = part_s + ((int64_t)bh * n_chunks * D + row) * D + col;  // chunk c at + c D D
-    for (int c0 = 0; c0 < n_chunks; c0 += 8) {  // eight loads in flight, added in chunk order
-      float x[8];
+    for (int c0 = 0; c0 < n_chunks; c0 += 16) {  // 16 loads in flight, added in chunk order
+      float x[16];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) x[u] = p[(int64_t)min(c0 + u, n_chunks - 1) * D * D];
+      for (int u = 0; u < 16; ++u) x[u] = p[(int64_t)min(c0 + u, n_chunks - 1) * D * D];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) s += c0 + u < n_chunks ? (double)x[u] : 0.0;
+      for (int u = 0; u < 16; ++u) s += c0 + u < n_chunks ? (double)x[u] : 0.0;
     }
     S[o] = (float)s;
   }
-  if (threadIdx.x < 16) {
+  if (threadIdx.x < kReduceRows) {
     const int row = row0 + threadIdx.x;
     double s = z[(int64_t)bh * D + row];
     for (int c = 0; c < n_chunks; ++c) s += part_z[((int64_t)bh * n_chunks + c) * D + row];
@@ -749,8 +752,8 @@ hipError_t launch_append_state(const Dims& m, const spla_cache& c, const void* k
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(append_state_reduce_kernel, dim3(m.d / 16, m.bh), dim3(256), 0, st, m,
-                     ws.n_chunks, (const float*)(base + ws.part_s),
+  hipLaunchKernelGGL(append_state_reduce_kernel, dim3(m.d / kReduceRows, m.bh), dim3(256), 0,
+                     st, m, ws.n_chunks, (const float*)(base + ws.part_s),
                      (const float*)(base + ws.part_z), c.lin_state, c.lin_norm);
   return hipGetLastError();
 }
