@@ -461,10 +461,12 @@ __global__ __launch_bounds__(256) void append_state_mfma_kernel(
 #pragma unroll
       for (int i = 1; i < 8; ++i) mx = fmaxf(mx, kf[i]);
       mx = row_max(mx);
+      // exp(k - max k) as the sparse pass forms it (hardware exp2)
+      const float mxl = mx * kLog2e;
       float sum = 0.f;
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
-        kf[i] = expf(kf[i] - mx);
+        kf[i] = __builtin_amdgcn_exp2f(fmaf(kf[i], kLog2e, -mxl));
         sum += kf[i];
       }
       sum = row_sum(sum);
@@ -602,7 +604,9 @@ __device__ __forceinline__ void append_rank1_rows(const Dims& m,
     float s = 0.f;
 #pragma unroll
     for (int e = 0; e < D / 64; ++e) {
-      x[e] = expf(x[e] - mx);
+      // exp(k - max k) as the sparse pass of this element type forms it
+      x[e] = sizeof(T) == 2 ? __builtin_amdgcn_exp2f(fmaf(x[e], kLog2e, -mx * kLog2e))
+                            : expf(x[e] - mx);
       s += x[e];
     }
     s = wave_sum(s);

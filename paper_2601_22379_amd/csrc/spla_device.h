@@ -281,6 +281,9 @@ struct Mem<true> {
 // The memory clobber keeps the compiler from moving accesses across it.
 __device__ __forceinline__ void wait_memory() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
+// log2(e): exponentials are taken as the hardware exp2 of a scaled argument.
+constexpr float kLog2e = 1.4426950408889634f;
+
 // Agent-scope (whole device) relaxed atomics on int32 counters and words.
 __device__ __forceinline__ int atomic_add_agent(int32_t* p, int v) {
   return __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
