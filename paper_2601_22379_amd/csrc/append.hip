@@ -402,16 +402,19 @@ __global__ __launch_bounds__(256) void append_state_mfma_kernel(
   const bf16_t* kb = k_new + (int64_t)bh * max_new * D;
   const bf16_t* vb = v_new + (int64_t)bh * max_new * D;
   // wavefront w takes tokens 8 w .. 8 w + 7 of each 32-token step as NS
-  // 16-byte loads per lane: LPR = D / 8 lanes per token (lane l holds
-  // coordinates 8 (l % LPR) .. + 7 of token 8 w + RPL s + l / LPR); the next
+  // 16-byte loads per lane: LPR = D / 8 lanes per token, lane l holding
+  // coordinates 8 (l % LPR) .. + 7 of token tok(s) (with two loads, tokens
+  // 2 tl and 2 tl + 1, tl = l / LPR: the lane then writes both tokens of a
+  // coordinate to the transposed arrays as one 4-byte store); the next
   // step's rows are loaded while the current one is processed
   constexpr int LPR = D / 8, RPL = 64 / LPR, NS = 8 / RPL;
   const int cl = lane % LPR, tl = lane / LPR;
+  auto tok = [&](int s) { return 8 * w + (NS == 2 ? 2 * tl + s : RPL * s + tl); };
   uint4 kx[NS], vx[NS];
   auto load_step = [&](int tt) {
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
-      const int row = min(tt + 8 * w + RPL * s + tl, t1 - 1);
+      const int row = min(tt + tok(s), t1 - 1);
       kx[s] = *reinterpret_cast<const uint4*>(kb + (int64_t)row * D + 8 * cl);
       vx[s] = *reinterpret_cast<const uint4*>(vb + (int64_t)row * D + 8 * cl);
     }
@@ -447,10 +450,12 @@ __global__ __launch_bounds__(256) void append_state_mfma_kernel(
       vc[s] = vx[s];
     }
     if (tt + kSubTokens < t1) load_step(tt + kSubTokens);
+    // phi(k) hi / lo and v of coordinate 8 cl + i, the token of load s in
+    // bits 16 s .. 16 s + 15 (two loads: both tokens, one 4-byte store)
+    uint32_t hb[8] = {}, lb[8] = {}, vb2[8] = {};
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
-      const int t = 8 * w + RPL * s + tl;
-      const bool ok = t < nt;
+      const bool ok = tok(s) < nt;
       const uint32_t kw[4] = {kc[s].x, kc[s].y, kc[s].z, kc[s].w};
       const uint32_t vw[4] = {vc[s].x, vc[s].y, vc[s].z, vc[s].w};
       float kf[8];
@@ -476,12 +481,27 @@ __global__ __launch_bounds__(256) void append_state_mfma_kernel(
         const float ph = kf[i] * inv;
         const __bf16 hi = (__bf16)ph;
         const __bf16 lo = (__bf16)(ph - (float)hi);
-        const int o = StateSmem<D>::at(8 * cl + i, t);
-        sm.kT_h[o] = __builtin_bit_cast(uint16_t, hi);
-        sm.kT_l[o] = __builtin_bit_cast(uint16_t, lo);
-        sm.vT[o] = ok ? (uint16_t)(i & 1 ? vw[i >> 1] >> 16 : vw[i >> 1] & 0xFFFFu)
-                      : (uint16_t)0;
+        const uint32_t v16 = ok ? (i & 1 ? vw[i >> 1] >> 16 : vw[i >> 1] & 0xFFFFu) : 0u;
         zacc[i] += ph;
+        if constexpr (NS == 2) {
+          hb[i] |= (uint32_t)__builtin_bit_cast(uint16_t, hi) << (16 * s);
+          lb[i] |= (uint32_t)__builtin_bit_cast(uint16_t, lo) << (16 * s);
+          vb2[i] |= v16 << (16 * s);
+        } else {
+          const int o = StateSmem<D>::at(8 * cl + i, tok(s));
+          sm.kT_h[o] = __builtin_bit_cast(uint16_t, hi);
+          sm.kT_l[o] = __builtin_bit_cast(uint16_t, lo);
+          sm.vT[o] = (uint16_t)v16;
+        }
+      }
+    }
+    if constexpr (NS == 2) {  // tokens 2 tl, 2 tl + 1 of each coordinate
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int o = StateSmem<D>::at(8 * cl + i, tok(0));
+        *reinterpret_cast<uint32_t*>(&sm.kT_h[o]) = hb[i];
+        *reinterpret_cast<uint32_t*>(&sm.kT_l[o]) = lb[i];
+        *reinterpret_cast<uint32_t*>(&sm.vT[o]) = vb2[i];
       }
     }
     __syncthreads();
