@@ -359,6 +359,14 @@ __global__ __launch_bounds__(256) void append_state_partial_kernel(
 // reductions, took 146 us for a 16K-token slab at 128K). Pz accumulates
 // phi(k) in fp32 per lane.
 typedef __bf16 abf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 abf16x2 __attribute__((ext_vector_type(2)));
+typedef float afloatx2 __attribute__((ext_vector_type(2)));
+
+// Two floats rounded to bf16 (nearest even) by one packed conversion: a in
+// the low half, b in the high half.
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(afloatx2{a, b}, abf16x2));
+}
 typedef float afloatx4 __attribute__((ext_vector_type(4)));
 
 // Coordinate c's row of a transposed array starts at c TPP + 8 (c / 8): the
@@ -450,14 +458,11 @@ __global__ __launch_bounds__(256) void append_state_mfma_kernel(
       vc[s] = vx[s];
     }
     if (tt + kSubTokens < t1) load_step(tt + kSubTokens);
-    // phi(k) hi / lo and v of coordinate 8 cl + i, the token of load s in
-    // bits 16 s .. 16 s + 15 (two loads: both tokens, one 4-byte store)
-    uint32_t hb[8] = {}, lb[8] = {}, vb2[8] = {};
+    float ph[NS][8];  // phi(k) of the token of load s, coordinates 8 cl + i
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
       const bool ok = tok(s) < nt;
       const uint32_t kw[4] = {kc[s].x, kc[s].y, kc[s].z, kc[s].w};
-      const uint32_t vw[4] = {vc[s].x, vc[s].y, vc[s].z, vc[s].w};
       float kf[8];
 #pragma unroll
       for (int i = 0; i < 8; ++i)
@@ -466,7 +471,8 @@ __global__ __launch_bounds__(256) void append_state_mfma_kernel(
 #pragma unroll
       for (int i = 1; i < 8; ++i) mx = fmaxf(mx, kf[i]);
       mx = row_max(mx);
-      // exp(k - max k) as the sparse pass forms it (hardware exp2)
+      // exp(k - max k) as the sparse pass forms it (hardware exp2); the sum
+      // is in [1, D], where the hardware reciprocal is within 1 ulp
       const float mxl = mx * kLog2e;
       float sum = 0.f;
 #pragma unroll
@@ -475,33 +481,42 @@ __global__ __launch_bounds__(256) void append_state_mfma_kernel(
         sum += kf[i];
       }
       sum = row_sum(sum);
-      const float inv = ok ? 1.0f / sum : 0.f;
+      const float inv = ok ? __builtin_amdgcn_rcpf(sum) : 0.f;  // phi = 0 past the chunk
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
-        const float ph = kf[i] * inv;
-        const __bf16 hi = (__bf16)ph;
-        const __bf16 lo = (__bf16)(ph - (float)hi);
-        const uint32_t v16 = ok ? (i & 1 ? vw[i >> 1] >> 16 : vw[i >> 1] & 0xFFFFu) : 0u;
-        zacc[i] += ph;
-        if constexpr (NS == 2) {
-          hb[i] |= (uint32_t)__builtin_bit_cast(uint16_t, hi) << (16 * s);
-          lb[i] |= (uint32_t)__builtin_bit_cast(uint16_t, lo) << (16 * s);
-          vb2[i] |= v16 << (16 * s);
-        } else {
-          const int o = StateSmem<D>::at(8 * cl + i, tok(s));
-          sm.kT_h[o] = __builtin_bit_cast(uint16_t, hi);
-          sm.kT_l[o] = __builtin_bit_cast(uint16_t, lo);
-          sm.vT[o] = (uint16_t)v16;
-        }
+        ph[s][i] = kf[i] * inv;
+        zacc[i] += ph[s][i];
       }
     }
-    if constexpr (NS == 2) {  // tokens 2 tl, 2 tl + 1 of each coordinate
+    if constexpr (NS == 2) {
+      // tokens 2 tl, 2 tl + 1 of coordinate 8 cl + i as one 4-byte store
+      // each: hi pair rounded by one packed conversion, lo = phi - hi; the
+      // value pair by one byte permute (rows past the chunk hold real,
+      // finite values and meet phi = 0)
+      const uint32_t v0[4] = {vc[0].x, vc[0].y, vc[0].z, vc[0].w};
+      const uint32_t v1[4] = {vc[1].x, vc[1].y, vc[1].z, vc[1].w};
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
+        const uint32_t hp = pack_bf16x2(ph[0][i], ph[1][i]);
+        const float h0 = __uint_as_float(hp << 16), h1 = __uint_as_float(hp & 0xFFFF0000u);
+        const uint32_t lp = pack_bf16x2(ph[0][i] - h0, ph[1][i] - h1);
+        const uint32_t vp =
+            __builtin_amdgcn_perm(v1[i >> 1], v0[i >> 1], i & 1 ? 0x07060302u : 0x05040100u);
         const int o = StateSmem<D>::at(8 * cl + i, tok(0));
-        *reinterpret_cast<uint32_t*>(&sm.kT_h[o]) = hb[i];
-        *reinterpret_cast<uint32_t*>(&sm.kT_l[o]) = lb[i];
-        *reinterpret_cast<uint32_t*>(&sm.vT[o]) = vb2[i];
+        *reinterpret_cast<uint32_t*>(&sm.kT_h[o]) = hp;
+        *reinterpret_cast<uint32_t*>(&sm.kT_l[o]) = lp;
+        *reinterpret_cast<uint32_t*>(&sm.vT[o]) = vp;
+      }
+    } else {
+      const uint32_t vw[4] = {vc[0].x, vc[0].y, vc[0].z, vc[0].w};
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const __bf16 hi = (__bf16)ph[0][i];
+        const __bf16 lo = (__bf16)(ph[0][i] - (float)hi);
+        const int o = StateSmem<D>::at(8 * cl + i, tok(0));
+        sm.kT_h[o] = __builtin_bit_cast(uint16_t, hi);
+        sm.kT_l[o] = __builtin_bit_cast(uint16_t, lo);
+        sm.vT[o] = (uint16_t)(i & 1 ? vw[i >> 1] >> 16 : vw[i >> 1] & 0xFFFFu);
       }
     }
     __syncthreads();
