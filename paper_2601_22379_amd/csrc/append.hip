@@ -569,6 +569,277 @@ __global__ __launch_bounds__(256) void append_state_mfma_kernel(
   }
 }
 
+// Bulk append in one pass over the new keys and values (bf16, d = 128, one
+// statistics unit per block): one workgroup per (chunk, sequence x KV head),
+// the chunks aligned to blocks (chunk x covers positions a0 .. a0 + ct - 1,
+// a0 = L0 - L0 % B + x ct), so that every block's statistics belong to one
+// workgroup. Per 32-token step (one block holds whole steps) the workgroup
+//   * writes the step's key rows to the cache from the registers they were
+//     loaded into (a 16-byte piece of a row is one piece of the cache);
+//   * leaves phi(k) (bf16 hi + lo), the values and the keys transposed in
+//     LDS, and adds the step to the chunk's partial state on the matrix
+//     cores (as append_state_mfma_kernel, bit for bit);
+//   * writes the value pieces of the cache (8 tokens of one coordinate)
+//     from the transposed values;
+//   * adds the step's keys to the block's sums of k and k^2 per coordinate
+//     in fp64 (two threads per coordinate, 16 tokens each: exact for bf16
+//     keys over a block), and after the block's last step merges the new
+//     tokens' mean and M2 = sum k^2 - mean sum k into the stored statistics
+//     (Chan's combination, rounded to fp32).
+// Tokens outside [L0, L0 + n) (before the append point in the first block,
+// past the new tokens in the last) load a clamped real row, get phi = 0 and
+// are neither stored nor counted.
+template <int D>
+__global__ __launch_bounds__(256) void append_fused_kernel(
+    Dims m, bf16_t* __restrict__ kcache, bf16_t* __restrict__ vcache, float* __restrict__ stats,
+    const int32_t* __restrict__ seq_lens, int32_t* __restrict__ err,
+    const bf16_t* __restrict__ k_new, const bf16_t* __restrict__ v_new, int max_new,
+    const int32_t* __restrict__ n_new, const int32_t* __restrict__ table, int n_chunks,
+    int chunk_tokens, float* __restrict__ part_s, float* __restrict__ part_z) {
+  static_assert(D == 128, "two tokens per lane: d = 128");
+  constexpr int RT = D / 16;  // row tiles (coordinates j)
+  constexpr int CT = D / 64;  // column tiles per wavefront
+  __shared__ StateSmem<D> sm;
+  __shared__ __align__(16) uint16_t kR[StateSmem<D>::N];  // keys of the step, transposed
+  const int bh = blockIdx.y;
+  const int b = bh / m.hkv;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int li = lane & 15, lg = lane >> 4;
+  const int L0 = seq_lens[b];
+  bool clipped;
+  const int ne = appended_count(m, L0, max_new, n_new, b, &clipped);
+  if (clipped && err && blockIdx.x == 0 && bh % m.hkv == 0 && tid == 0)
+    atomicOr(err, (int)SPLA_DEVERR_CAPACITY);
+  const int Bk = m.B;
+  const int a0 = L0 - L0 % Bk + (int)blockIdx.x * chunk_tokens;
+  const int lo = max(a0, L0), a1n = min(a0 + chunk_tokens, L0 + ne);
+  const int a1 = lo < a1n ? a1n : a0;  // no step when the chunk holds no new token
+  afloatx4 acc[RT][CT];
+#pragma unroll
+  for (int r = 0; r < RT; ++r)
+#pragma unroll
+    for (int c = 0; c < CT; ++c) acc[r][c] = afloatx4{0.f, 0.f, 0.f, 0.f};
+  float zacc[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) zacc[i] = 0.f;
+  const bf16_t* kb = k_new + (int64_t)bh * max_new * D;
+  const bf16_t* vb = v_new + (int64_t)bh * max_new * D;
+  // lane l: coordinates 8 (l % 16) .. + 7 of tokens 8 w + 2 (l / 16) + s
+  const int cl = lane & 15, tl = lane >> 4;
+  auto tok = [&](int s) { return 8 * w + 2 * tl + s; };
+  uint4 kx[2], vx[2];
+  auto load_step = [&](int tt) {
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      const int row = min(max(tt + tok(s) - L0, 0), ne - 1);
+      kx[s] = *reinterpret_cast<const uint4*>(kb + (int64_t)row * D + 8 * cl);
+      vx[s] = *reinterpret_cast<const uint4*>(vb + (int64_t)row * D + 8 * cl);
+    }
+  };
+  auto row_max = [](float v) {
+    v = fmaxf(v, dpp_rot<0x128>(v));  // row_ror:8
+    v = fmaxf(v, dpp_rot<0x124>(v));  // row_ror:4
+    v = fmaxf(v, dpp_rot<0x4E>(v));
+    return fmaxf(v, dpp_rot<0xB1>(v));
+  };
+  auto row_sum = [](float v) {
+    v += dpp_rot<0x128>(v);
+    v += dpp_rot<0x124>(v);
+    v += dpp_rot<0x4E>(v);
+    return v + dpp_rot<0xB1>(v);
+  };
+  // statistics: thread (coordinate sc, half sh) sums tokens 16 sh .. + 15
+  const int sc = tid >> 1, sh = tid & 1;
+  double s1 = 0.0, s2 = 0.0;
+  int64_t slot = -1;
+  if (a0 < a1) load_step(a0);
+  for (int tt = a0; tt < a1; tt += kSubTokens) {
+    const int blk = tt / Bk;
+    if (tt % Bk == 0) {  // a block starts: its slot in the caches
+      if (!table) {
+        slot = (int64_t)bh * m.nb_cap + blk;
+      } else {
+        const int p = block_page(m, table, bh, blk);
+        slot = p < 0 ? -1 : (int64_t)p * m.hkv + bh % m.hkv;
+        if (p < 0 && err && tid == 0) atomicOr(err, (int)SPLA_DEVERR_PAGE);
+      }
+    }
+    uint4 kc[2], vc[2];
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      kc[s] = kx[s];
+      vc[s] = vx[s];
+    }
+    if (tt + kSubTokens < a1) load_step(tt + kSubTokens);
+    float ph[2][8];
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      const int t = tt + tok(s);
+      const bool ok = t >= lo && t < a1;
+      if (ok && slot >= 0)
+        *reinterpret_cast<uint4*>(kcache + k_off_slot(m, slot, t % Bk, 8 * cl)) = kc[s];
+      const uint32_t kw[4] = {kc[s].x, kc[s].y, kc[s].z, kc[s].w};
+      float kf[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+        kf[i] = bf16_to_f32((uint16_t)(i & 1 ? kw[i >> 1] >> 16 : kw[i >> 1] & 0xFFFFu));
+      float mx = kf[0];
+#pragma unroll
+      for (int i = 1; i < 8; ++i) mx = fmaxf(mx, kf[i]);
+      mx = row_max(mx);
+      const float mxl = mx * kLog2e;
+      float sum = 0.f;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        kf[i] = __builtin_amdgcn_exp2f(fmaf(kf[i], kLog2e, -mxl));
+        sum += kf[i];
+      }
+      sum = row_sum(sum);
+      const float inv = ok ? __builtin_amdgcn_rcpf(sum) : 0.f;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        ph[s][i] = kf[i] * inv;
+        zacc[i] += ph[s][i];
+      }
+    }
+    {
+      const uint32_t k0[4] = {kc[0].x, kc[0].y, kc[0].z, kc[0].w};
+      const uint32_t k1[4] = {kc[1].x, kc[1].y, kc[1].z, kc[1].w};
+      const uint32_t v0[4] = {vc[0].x, vc[0].y, vc[0].z, vc[0].w};
+      const uint32_t v1[4] = {vc[1].x, vc[1].y, vc[1].z, vc[1].w};
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const uint32_t sel = i & 1 ? 0x07060302u : 0x05040100u;
+        const uint32_t hp = pack_bf16x2(ph[0][i], ph[1][i]);
+        const float h0 = __uint_as_float(hp << 16), h1 = __uint_as_float(hp & 0xFFFF0000u);
+        const int o = StateSmem<D>::at(8 * cl + i, tok(0));
+        *reinterpret_cast<uint32_t*>(&sm.kT_h[o]) = hp;
+        *reinterpret_cast<uint32_t*>(&sm.kT_l[o]) = pack_bf16x2(ph[0][i] - h0, ph[1][i] - h1);
+        *reinterpret_cast<uint32_t*>(&sm.vT[o]) = __builtin_amdgcn_perm(v1[i >> 1], v0[i >> 1], sel);
+        *reinterpret_cast<uint32_t*>(&kR[o]) = __builtin_amdgcn_perm(k1[i >> 1], k0[i >> 1], sel);
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < RT; ++r) {
+      const int oa = StateSmem<D>::at(16 * r + li, 8 * lg);
+      const abf16x8 ah =
+          __builtin_bit_cast(abf16x8, *reinterpret_cast<const uint4*>(&sm.kT_h[oa]));
+      const abf16x8 al =
+          __builtin_bit_cast(abf16x8, *reinterpret_cast<const uint4*>(&sm.kT_l[oa]));
+#pragma unroll
+      for (int c = 0; c < CT; ++c) {
+        const int col = (D / 4) * w + 16 * c + li;
+        const abf16x8 bv = __builtin_bit_cast(
+            abf16x8, *reinterpret_cast<const uint4*>(&sm.vT[StateSmem<D>::at(col, 8 * lg)]));
+        acc[r][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bv, acc[r][c], 0, 0, 0);
+        acc[r][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, bv, acc[r][c], 0, 0, 0);
+      }
+    }
+    // value pieces: piece p = (c >> 4, token group g, c & 15), the order of
+    // the cache within a step, so consecutive threads write consecutive
+    // pieces
+    const bool whole = tt >= lo && tt + kSubTokens <= a1;  // uniform
+    if (slot >= 0) {
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const int p = tid + 256 * u;
+        const int c = ((p >> 6) << 4) + (p & 15), g = (p >> 4) & 3;
+        const uint4 x = *reinterpret_cast<const uint4*>(&sm.vT[StateSmem<D>::at(c, 8 * g)]);
+        const int tb = (tt + 8 * g) % Bk;
+        if (whole) {
+          *reinterpret_cast<uint4*>(vcache + v_off_slot(m, slot, tb, c)) = x;
+        } else {
+          const uint16_t* xe = reinterpret_cast<const uint16_t*>(&x);
+          for (int e = 0; e < 8; ++e) {
+            const int t = tt + 8 * g + e;
+            if (t >= lo && t < a1)
+              reinterpret_cast<uint16_t*>(vcache)[v_off_slot(m, slot, tb + e, c)] = xe[e];
+          }
+        }
+      }
+    }
+    // the block's sums of k and k^2 (coordinate sc, tokens 16 sh .. + 15)
+    {
+      const int ob = StateSmem<D>::at(sc, 16 * sh);
+      const uint4 r0 = *reinterpret_cast<const uint4*>(&kR[ob]);
+      const uint4 r1 = *reinterpret_cast<const uint4*>(&kR[ob + 8]);
+      const uint32_t kw[8] = {r0.x, r0.y, r0.z, r0.w, r1.x, r1.y, r1.z, r1.w};
+      if (whole) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const double x =
+              (double)bf16_to_f32((uint16_t)(e & 1 ? kw[e >> 1] >> 16 : kw[e >> 1] & 0xFFFFu));
+          s1 += x;
+          s2 = fma(x, x, s2);
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int t = tt + 16 * sh + e;
+          const double x =
+              (t >= lo && t < a1)
+                  ? (double)bf16_to_f32((uint16_t)(e & 1 ? kw[e >> 1] >> 16 : kw[e >> 1] & 0xFFFFu))
+                  : 0.0;
+          s1 += x;
+          s2 = fma(x, x, s2);
+        }
+      }
+    }
+    if ((tt + kSubTokens) % Bk == 0 || tt + kSubTokens >= a1) {  // the block's last step
+      s1 += __shfl_xor(s1, 1, 64);
+      s2 += __shfl_xor(s2, 1, 64);
+      if (sh == 0) {
+        const int nc = min((blk + 1) * Bk, a1) - max(blk * Bk, lo);
+        const int na = max(L0 - blk * Bk, 0);
+        const double mc = s1 / nc;
+        const double m2s = s2 - mc * s1;
+        const int64_t o_mean = stats_off4(m, bh, blk, 0, sc / 4) + (sc & 3);
+        const int64_t o_m2 = stats_off4(m, bh, blk, 1, sc / 4) + (sc & 3);
+        double mean = mc, m2v = m2s;
+        if (na > 0) {
+          const double mean_a = stats[o_mean], m2_a = stats[o_m2];
+          const double n = (double)(na + nc);
+          const double delta = mc - mean_a;
+          mean = mean_a + delta * (nc / n);
+          m2v = m2_a + m2s + delta * delta * ((double)na * nc / n);
+        }
+        stats[o_mean] = (float)mean;
+        stats[o_m2] = (float)m2v;
+      }
+      s1 = 0.0;
+      s2 = 0.0;
+    }
+    __syncthreads();
+  }
+  float* ps = part_s + ((int64_t)bh * n_chunks + blockIdx.x) * D * D;
+#pragma unroll
+  for (int r = 0; r < RT; ++r)
+#pragma unroll
+    for (int c = 0; c < CT; ++c)
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4)
+        ps[(16 * r + 4 * lg + r4) * D + (D / 4) * w + 16 * c + li] = acc[r][c][r4];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    float v = zacc[i];
+    v += xor16(v);
+    v += xor32(v);
+    zacc[i] = v;
+  }
+  if (lane < 16) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) sm.z[w][8 * lane + i] = zacc[i];
+  }
+  __syncthreads();
+  if (tid < D) {
+    float z = 0.f;
+#pragma unroll
+    for (int x = 0; x < 4; ++x) z += sm.z[x][tid];
+    part_z[((int64_t)bh * n_chunks + blockIdx.x) * D + tid] = z;
+  }
+}
+
 // S_bar += sum of the chunk partials, accumulated in fp64 in chunk order;
 // kReduceRows rows of S_bar per workgroup (4: a thread has two entries at
 // d = 128, and 32 x bh workgroups keep every compute unit busy).
@@ -789,6 +1060,29 @@ hipError_t launch_append_state(const Dims& m, const spla_cache& c, const void* k
     if (m.d == 64) state_partial<bf16_t, 64>(m, c, k_new, v_new, max_new, n_new, ws, base, st);
     else state_partial<bf16_t, 128>(m, c, k_new, v_new, max_new, n_new, ws, base, st);
   }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(append_state_reduce_kernel, dim3(m.d / kReduceRows, m.bh), dim3(256), 0,
+                     st, m, ws.n_chunks, (const float*)(base + ws.part_s),
+                     (const float*)(base + ws.part_z), c.lin_state, c.lin_norm);
+  return hipGetLastError();
+}
+
+bool append_fusable(const Dims& m) { return m.elem == 2 && m.d == 128 && !windowed(m); }
+
+hipError_t launch_append_fused(const Dims& m, const spla_cache& c, const void* k_new,
+                               const void* v_new, int max_new, const int32_t* n_new,
+                               const AppendWs& ws, char* base, hipStream_t st) {
+  if (!append_fusable(m)) return hipErrorInvalidValue;
+  // block-aligned chunks: the first starts up to B - 1 positions before the
+  // append point, so n_chunks chunks of ct tokens cover B - 1 + max_new
+  const int ct = (int)align_up(ceil_div((int64_t)max_new + m.B - 1, ws.n_chunks),
+                               m.B > kSubTokens ? m.B : kSubTokens);
+  hipLaunchKernelGGL(append_fused_kernel<128>, dim3(ws.n_chunks, m.bh), dim3(256), 0, st, m,
+                     (bf16_t*)c.k_cache, (bf16_t*)c.v_cache, c.blk_stats, c.seq_lens, c.err_flags,
+                     (const bf16_t*)k_new, (const bf16_t*)v_new, max_new, n_new,
+                     m.pages > 0 ? c.block_table : nullptr, ws.n_chunks, ct,
+                     (float*)(base + ws.part_s), (float*)(base + ws.part_z));
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(append_state_reduce_kernel, dim3(m.d / kReduceRows, m.bh), dim3(256), 0,

@@ -27,6 +27,14 @@ hipError_t launch_append_blocks(const Dims& m, const spla_cache& c, const void* 
 hipError_t launch_append_state(const Dims& m, const spla_cache& c, const void* k_new,
                                const void* v_new, int max_new, const int32_t* n_new,
                                const AppendWs& ws, char* wsbase, hipStream_t st);
+// rows, block statistics and state partials of a bulk append in one pass over
+// the new keys and values (append_fusable shapes: bf16, d = 128, blocks as
+// the statistics units), then the state reduce; in place of
+// launch_append_blocks + launch_append_state
+bool append_fusable(const Dims& m);
+hipError_t launch_append_fused(const Dims& m, const spla_cache& c, const void* k_new,
+                               const void* v_new, int max_new, const int32_t* n_new,
+                               const AppendWs& ws, char* wsbase, hipStream_t st);
 // the single-token append of a step (statistics, K/V rows and, with rank1,
 // the rank-one update of S_bar and z_bar) in one launch. With fin_ctr (the
 // items_done lines of a decode workspace's synchronisation area) the last
