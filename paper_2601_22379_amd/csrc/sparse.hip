@@ -33,11 +33,11 @@ __global__ __launch_bounds__(64) void merge_kernel(
 
 // ------------------------------------------------------------ VALU pass
 template <typename T, int D>
-__global__ __launch_bounds__(256) void sparse_valu_kernel(
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void sparse_valu_kernel(
     Dims m, float s, float eps, uint32_t flags, const T* __restrict__ kc,
     const T* __restrict__ vc, const T* __restrict__ q, const float* __restrict__ gamma,
     const float* __restrict__ S, const float* __restrict__ zbar,
-    const int32_t* __restrict__ sel, const int32_t* __restrict__ meta, int bps, int stride,
+    const int32_t* __restrict__ sel, const int32_t* __restrict__ meta, int stride,
     float* __restrict__ part, const int32_t* __restrict__ table) {
   constexpr int MG = SPLA_MAX_GROUP;
   constexpr int PER = (MG * D + 255) / 256;  // (head, coord) pairs per thread
@@ -56,7 +56,10 @@ __global__ __launch_bounds__(256) void sparse_valu_kernel(
   const int nsel = meta[bh * 4 + 0];
   const int L = meta[bh * 4 + 2];
   const int nb = (L + m.B - 1) / m.B;
-  const int p0 = split * bps, p1 = min(p0 + bps, nsel);
+  // workgroup split: sub-tile sub0 of selection entry p0 (B / 32 sub-tiles
+  // per block), so a block's sub-tiles run side by side
+  const int spb = m.B / kSubTokens;
+  const int p0 = split / spb, sub0 = split % spb, p1 = min(p0 + 1, nsel);
   // this workgroup's rows of S_bar and z_bar for the global linear term: the
   // first kLinPre rows loaded now (they land while the blocks are processed),
   // any further ones at the end, kLinPre rows per batch of loads
@@ -116,7 +119,7 @@ __global__ __launch_bounds__(256) void sparse_valu_kernel(
       const int pg = block_page(m, table, bh, blk);
       slot = (int64_t)(pg < 0 ? 0 : pg) * m.hkv + h;
     }
-    for (int sub = 0; sub * kSubTokens < n_i; ++sub) {
+    for (int sub = sub0; sub == sub0 && sub * kSubTokens < n_i; ++sub) {
       const int tb0 = sub * kSubTokens;
       const int nt = min(kSubTokens, n_i - sub * kSubTokens);
       // every load of the sub-tile issued before any is used (rows past nt
@@ -138,37 +141,59 @@ __global__ __launch_bounds__(256) void sparse_valu_kernel(
         sV[c2][r2] = r2 < nt ? vx[i] : 0.f;
       }
       __syncthreads();
-      for (int r = 0; r < kSubTokens / 4; ++r) {  // phi(k) rows
-        const int row = w * (kSubTokens / 4) + r;
-        float x[D / 64];
+      // phi(k) rows: wavefront w takes rows 8 w .. 8 w + 7 at once, eight
+      // lanes per row (lane 8 r + u: coordinates u D / 8 ..), the softmax's
+      // max and sum over the row's lanes by lane swaps
+      {
+        static_assert(kSubTokens == 32, "four wavefronts of eight rows");
+        constexpr int DE = D / 8;
+        const int row = 8 * w + (lane >> 3), c0 = DE * (lane & 7);
+        float x[DE];
         float mx = -INFINITY;
 #pragma unroll
-        for (int e = 0; e < D / 64; ++e) {
-          x[e] = sK[row][lane + 64 * e];
+        for (int e = 0; e < DE; ++e) {
+          x[e] = sK[row][c0 + e];
           mx = fmaxf(mx, x[e]);
         }
-        mx = wave_max(mx);
+        mx = fmaxf(mx, __shfl_xor(mx, 1, 64));
+        mx = fmaxf(mx, __shfl_xor(mx, 2, 64));
+        mx = fmaxf(mx, __shfl_xor(mx, 4, 64));
         float sum = 0.f;
 #pragma unroll
-        for (int e = 0; e < D / 64; ++e) {
+        for (int e = 0; e < DE; ++e) {
           x[e] = expf(x[e] - mx);
           sum += x[e];
         }
-        sum = wave_sum(sum);
+        sum += __shfl_xor(sum, 1, 64);
+        sum += __shfl_xor(sum, 2, 64);
+        sum += __shfl_xor(sum, 4, 64);
         const float inv = row < nt ? 1.0f / sum : 0.f;
 #pragma unroll
-        for (int e = 0; e < D / 64; ++e) sE[row][lane + 64 * e] = x[e] * inv;
+        for (int e = 0; e < DE; ++e) sE[row][c0 + e] = x[e] * inv;
       }
       __syncthreads();
-      for (int e = tid; e < G * kSubTokens; e += 256) {  // logits and linear weights
+      // logits and linear weights: eight lanes per (head, token), each over
+      // D / 8 coordinates, added by lane swaps; G passes of 32 products
+      for (int e0 = 0; e0 < G * kSubTokens; e0 += 32) {
+        constexpr int DE = D / 8;
+        const int e = e0 + (tid >> 3), c0 = DE * (tid & 7);
         const int mm = e / kSubTokens, t = e % kSubTokens;
         float a = 0.f, wl = 0.f;
-        for (int j = 0; j < D; ++j) {
-          a = fmaf(sq[mm][j], sK[t][j], a);
-          wl = fmaf(sphq[mm][j], sE[t][j], wl);
+#pragma unroll 8
+        for (int j = 0; j < DE; ++j) {
+          a = fmaf(sq[mm][c0 + j], sK[t][c0 + j], a);
+          wl = fmaf(sphq[mm][c0 + j], sE[t][c0 + j], wl);
         }
-        sP[mm][t] = t < nt ? a : -INFINITY;
-        sW[mm][t] = t < nt ? wl : 0.f;
+        a += __shfl_xor(a, 1, 64);
+        wl += __shfl_xor(wl, 1, 64);
+        a += __shfl_xor(a, 2, 64);
+        wl += __shfl_xor(wl, 2, 64);
+        a += __shfl_xor(a, 4, 64);
+        wl += __shfl_xor(wl, 4, 64);
+        if ((tid & 7) == 0) {
+          sP[mm][t] = t < nt ? a : -INFINITY;
+          sW[mm][t] = t < nt ? wl : 0.f;
+        }
       }
       __syncthreads();
       // online softmax bookkeeping: wavefront w takes heads w, w + 4, ..., lane
@@ -197,7 +222,9 @@ __global__ __launch_bounds__(256) void sparse_valu_kernel(
         if (idx < G * D) {
           const int mm = idx / D, c = idx % D;
           float a = acc[r] * s_alpha[mm], aw = accw[r];
-          for (int t = 0; t < nt; ++t) {
+          // tokens past nt add exact zeros (p, w and v are 0 there)
+#pragma unroll 8
+          for (int t = 0; t < kSubTokens; ++t) {
             a = fmaf(sP[mm][t], sV[c][t], a);
             aw = fmaf(sW[mm][t], sV[c][t], aw);
           }
@@ -218,7 +245,7 @@ __global__ __launch_bounds__(256) void sparse_valu_kernel(
 #pragma unroll
     for (int u = 0; u < kLinPre; ++u) {
       const bool ok = j0 + u < rend;
-      const int jc = ok ? j0 + u : row0;
+      const int jc = ok ? j0 + u : 0;
 #pragma unroll
       for (int r = 0; r < PER; ++r) {
         const int mm = (tid + 256 * r) / D;
@@ -336,7 +363,7 @@ static void valu_td(const Dims& m, const spla_config& cfg, float s, const spla_c
                      cfg.rms_eps, cfg.flags, (const T*)c.k_cache, (const T*)c.v_cache,
                      (const T*)q, gamma, (const float*)c.lin_state, (const float*)c.lin_norm,
                      (const int32_t*)(base + ws.sel), (const int32_t*)(base + ws.meta),
-                     ws.blocks_per_wg, ws.part_stride, (float*)(base + ws.part),
+                     ws.part_stride, (float*)(base + ws.part),
                      m.pages > 0 ? c.block_table : nullptr);
 }
 

@@ -134,7 +134,6 @@ struct DecodeWs {
   int64_t total;
   int n_sl;           // slices of the two-stage selection
   int n_wg;           // sparse workgroups per (sequence, kv head)
-  int blocks_per_wg;  // selected blocks per VALU-pass workgroup
   int part_stride;    // floats per record: header + acc[G][d] + accw[G][d]
 };
 
@@ -192,9 +191,10 @@ SPLA_HD DecodeWs decode_ws_layout(const Dims& m) {
     off = align_up(off + bytes, A);
     return o;
   };
-  // MFMA pass: one 32-token step per wavefront; VALU pass: one block per workgroup
-  w.blocks_per_wg = 1;
-  w.n_wg = use_mfma_sparse(m) ? (int)ceil_div((int64_t)m.k * (m.B / 32), kSparseWaves) : m.k;
+  // MFMA pass: one 32-token step per wavefront; VALU pass: one 32-token
+  // sub-tile of a selected block per workgroup
+  w.n_wg = use_mfma_sparse(m) ? (int)ceil_div((int64_t)m.k * (m.B / 32), kSparseWaves)
+                              : m.k * (m.B / kSubTokens);
   w.part_stride = kPartHead + 2 * m.group * m.d;
   w.e_vals = take((int64_t)m.bh * m.group * m.n_tiles * kTileBlocks * 4);
   w.tile_part = take((int64_t)m.bh * m.n_tiles * m.group * 2 * 8);
