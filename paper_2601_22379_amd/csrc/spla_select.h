@@ -346,22 +346,18 @@ __device__ void select_blocks(const Dims& m, int bh, int seq_len,
           if (u < nu) wsc[u] = (float)g[j][c];
         }
       __syncthreads();
-      // windows u_lo .. u_lo + nv - 1 touch this thread's blocks; each is
-      // pooled into every one of the thread's blocks it shares a token with
-      const int bpw = m.B / m.us, wpb = m.ul / m.us;
-      const int u_lo = i0 * bpw - (wpb - 1), nv = R * bpw + wpb - 1;
+      // the windows sharing a token with block i (s divides B and C) are
+      // i B / s - (C / s - 1) .. (i + 1) B / s - 1: a run of B / s + C / s - 1
+      const int bpw = m.B / m.us, wpb = m.ul / m.us, nvb = bpw + wpb - 1;
 #pragma unroll
-      for (int r = 0; r < R; ++r) best[r] = 0.f;
-      for (int v = 0; v < nv; ++v) {
-        const int u = u_lo + v;
-        if (u < 0 || u >= nu) continue;
-        const float f = wsc[u];
-        const int64_t a = (int64_t)u * m.us, b = a + m.ul;
-#pragma unroll
-        for (int r = 0; r < R; ++r) {
-          const int64_t lo = (int64_t)(i0 + r) * m.B;
-          if (a < lo + m.B && b > lo) best[r] = fmaxf(best[r], f);
+      for (int r = 0; r < R; ++r) {
+        const int u0 = (i0 + r) * bpw - (wpb - 1);
+        float bst = 0.f;
+        for (int v = 0; v < nvb; ++v) {
+          const int u = u0 + v;
+          if (u >= 0 && u < nu) bst = fmaxf(bst, wsc[u]);
         }
+        best[r] = bst;
       }
     } else {
     const int t = i0 / kTileBlocks;  // R <= 64: one tile per thread
