@@ -140,6 +140,36 @@ def test_append_statistics_and_state(dev):
             assert np.array_equal(kl, K) and np.array_equal(vl, V)
 
 
+@pytest.mark.parametrize("B,slab", [(32, 1000), (128, 1500)])
+def test_one_pass_append_block_sizes(dev, B, slab):
+    """The bulk append's one pass (bf16, d = 128) at one and four 32-token
+    steps per block: uneven slabs start mid-block, and the shorter sequence
+    receives nothing in the last calls; block mean / M2, S_bar, z_bar and the
+    K/V rows equal the oracle's."""
+    w = si.custom(f"onepass_B{B}", 2, 4, 2, 128, B, 8, [4321, 1234], kind="drift",
+                  code=180 + B // 32)
+    cache, q, gamma, out, sel = run_decode(w, dev, slab=slab)
+    mean, m2 = (x.cpu().numpy() for x in cache.stats_logical())
+    S, z = (x.cpu().numpy() for x in cache.state_logical())
+    assert list(cache.seq_lens.cpu().numpy()) == list(w.lengths)
+    assert cache.err.item() == 0
+    for b in range(w.batch):
+        for h in range(w.n_kv_heads):
+            L = w.lengths[b]
+            K, V = si.gen_kv(w, b, h, 0, L)
+            st = O.build_state(K, V, L, w.block_size)
+            nb = len(st.counts)
+            np.testing.assert_allclose(mean[b, h, :nb], st.mean, rtol=0, atol=2e-6)
+            np.testing.assert_allclose(m2[b, h, :nb] / st.counts[:, None], st.var, rtol=2e-5,
+                                       atol=1e-6)
+            np.testing.assert_allclose(S[b, h], st.s_bar, rtol=2e-5, atol=2e-5)
+            np.testing.assert_allclose(z[b, h], st.z_bar, rtol=2e-5, atol=1e-5)
+            kl = cache.k_logical()[b, h, :L].float().cpu().numpy()
+            vl = cache.v_logical()[b, h, :L].float().cpu().numpy()
+            assert np.array_equal(kl, K) and np.array_equal(vl, V)
+    check_all(w, q, gamma, out, sel, H.params_of(w))
+
+
 def test_append_chunking_invariance(dev):
     w = si.custom("chunks", 2, 8, 2, 128, 64, 8, [3333, 2049], kind="block_offsets", code=123)
     a = run_decode(w, dev, slab=4096)
