@@ -844,11 +844,21 @@ __global__ __launch_bounds__(256) void append_fused_kernel(
 // kReduceRows rows of S_bar per workgroup (4: a thread has two entries at
 // d = 128, and 32 x bh workgroups keep every compute unit busy).
 constexpr int kReduceRows = 4;
+// With seq_lens (the one-pass append), the first workgroup of each sequence
+// also advances its length by the tokens appended (the append's last step:
+// nothing in this kernel reads the lengths otherwise).
 __global__ __launch_bounds__(256) void append_state_reduce_kernel(
     Dims m, int n_chunks, const float* __restrict__ part_s, const float* __restrict__ part_z,
-    float* __restrict__ S, float* __restrict__ z) {
+    float* __restrict__ S, float* __restrict__ z, int32_t* __restrict__ seq_lens, int max_new,
+    const int32_t* __restrict__ n_new) {
   const int bh = blockIdx.y;
   const int D = m.d;
+  if (seq_lens && blockIdx.x == 0 && bh % m.hkv == 0 && threadIdx.x == 0) {
+    const int b = bh / m.hkv;
+    bool clipped;
+    const int L0 = seq_lens[b];
+    seq_lens[b] = L0 + appended_count(m, L0, max_new, n_new, b, &clipped);
+  }
   const int row0 = blockIdx.x * kReduceRows;
   for (int e = threadIdx.x; e < kReduceRows * D; e += 256) {
     const int row = row0 + e / D, col = e % D;
@@ -1064,7 +1074,8 @@ hipError_t launch_append_state(const Dims& m, const spla_cache& c, const void* k
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(append_state_reduce_kernel, dim3(m.d / kReduceRows, m.bh), dim3(256), 0,
                      st, m, ws.n_chunks, (const float*)(base + ws.part_s),
-                     (const float*)(base + ws.part_z), c.lin_state, c.lin_norm);
+                     (const float*)(base + ws.part_z), c.lin_state, c.lin_norm, nullptr, 0,
+                     nullptr);
   return hipGetLastError();
 }
 
@@ -1087,7 +1098,8 @@ hipError_t launch_append_fused(const Dims& m, const spla_cache& c, const void* k
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(append_state_reduce_kernel, dim3(m.d / kReduceRows, m.bh), dim3(256), 0,
                      st, m, ws.n_chunks, (const float*)(base + ws.part_s),
-                     (const float*)(base + ws.part_z), c.lin_state, c.lin_norm);
+                     (const float*)(base + ws.part_z), c.lin_state, c.lin_norm, c.seq_lens,
+                     max_new, n_new);
   return hipGetLastError();
 }
 

@@ -156,15 +156,15 @@ extern "C" int32_t spla_append(const spla_config* cfg, const spla_cache* cache, 
   const Dims m = spla::make_dims(*cfg);
   const spla::AppendWs L = spla::append_ws_layout(m, max_new);
   hipStream_t st = static_cast<hipStream_t>(stream);
-  if (spla::append_fusable(m)) {
+  if (spla::append_fusable(m)) {  // the lengths advance in its last launch
     SPLA_TRY(spla::launch_append_fused(m, *cache, k_new, v_new, max_new, n_new, L,
                                        static_cast<char*>(workspace), st));
   } else {
     SPLA_TRY(spla::launch_append_blocks(m, *cache, k_new, v_new, max_new, n_new, st));
     SPLA_TRY(spla::launch_append_state(m, *cache, k_new, v_new, max_new, n_new, L,
                                        static_cast<char*>(workspace), st));
+    SPLA_TRY(spla::launch_append_finish(m, *cache, max_new, n_new, st));
   }
-  SPLA_TRY(spla::launch_append_finish(m, *cache, max_new, n_new, st));
   return SPLA_OK;
 }
 

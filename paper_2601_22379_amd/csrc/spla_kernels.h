@@ -29,8 +29,8 @@ hipError_t launch_append_state(const Dims& m, const spla_cache& c, const void* k
                                const AppendWs& ws, char* wsbase, hipStream_t st);
 // rows, block statistics and state partials of a bulk append in one pass over
 // the new keys and values (append_fusable shapes: bf16, d = 128, blocks as
-// the statistics units), then the state reduce; in place of
-// launch_append_blocks + launch_append_state
+// the statistics units), then the state reduce, which also advances seq_lens;
+// in place of launch_append_blocks + launch_append_state + launch_append_finish
 bool append_fusable(const Dims& m);
 hipError_t launch_append_fused(const Dims& m, const spla_cache& c, const void* k_new,
                                const void* v_new, int max_new, const int32_t* n_new,
