@@ -180,9 +180,9 @@ void prefill_sparse_kernel(
   sparse_prologue<D, GC, false>(m, q + (int64_t)i * m.batch * m.hq * D, nullptr, nullptr, bh, x,
                                 n_wg, r, sm);
   sparse_linear<D, GC, false>(m, nullptr, bh, r, sm);
-  const int e = sparse_step_entry<BLK>(x);
-  sparse_body<D, BLK, false, GC>(m, s, kc, vc, e < m.k ? sel[(int64_t)vh * m.k + e] : -1,
-                                 meta[vh * 4 + 2], bh, x, n_wg, r, sm, part, stride, table, vh);
+  sparse_body_steps<D, BLK, false, GC, kPrefillStepsPerWave>(
+      m, s, kc, vc, sel + (int64_t)vh * m.k, meta[vh * 4 + 2], bh, x, n_wg, r, sm, part, stride,
+      table, vh);
 }
 
 // ---------------------------------------------------------------- merge

@@ -222,6 +222,7 @@ SPLA_HD bool step_fusable(const Dims& m) {
 
 // ---- chunked prefill workspace ------------------------------------------------
 constexpr int kPrefillChunk = 32;  // positions per chunk of the chunked prefill
+constexpr int kPrefillStepsPerWave = 2;  // 32-token steps per wavefront of its sparse pass
 
 // The chunked prefill covers the matrix-core shapes (bf16, G <= 8); the other
 // shapes run position by position (the single-token append, then a decode).
@@ -230,7 +231,7 @@ SPLA_HD bool use_chunked_prefill(const Dims& m) { return use_mfma_sparse(m); }
 struct PrefillWs {
   int T;            // positions per chunk
   int nu_touch;     // statistics units that T consecutive tokens can touch
-  int n_wg;         // sparse workgroups per query (as in the decode)
+  int n_wg;         // sparse workgroups per query (kPrefillStepsPerWave steps per wavefront)
   int part_stride;  // floats per record
   int64_t ustat;    // f32 [bh][nu_touch][T][2][d]  running (mean, M2) of the touched units
   int64_t e_vals;   // f32 [bh T][G][n_tiles*64]    per query, as the decode's
@@ -256,7 +257,7 @@ SPLA_HD PrefillWs prefill_ws_layout(const Dims& m, int n_tokens) {
   // units u with u us < L0 + T and u us + ul > L0
   w.nu_touch = (int)ceil_div(w.T + m.ul, m.us) + 1;
   const DecodeWs d = decode_ws_layout(m);
-  w.n_wg = d.n_wg;
+  w.n_wg = (int)ceil_div((int64_t)m.k * (m.B / 32), kSparseWaves * kPrefillStepsPerWave);
   w.part_stride = d.part_stride;
   const int64_t nq = (int64_t)m.bh * w.T;
   w.ustat = take((int64_t)m.bh * w.nu_touch * w.T * 2 * m.d * 4);

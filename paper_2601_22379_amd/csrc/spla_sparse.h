@@ -577,8 +577,8 @@ struct SparseKV {
 // none; clipped to the last block) and its valid token count (0: nothing).
 template <int BLK>
 __device__ __forceinline__ int sparse_step_block(const Dims& m, int blk_sel, int& L, int x,
-                                                 int* n_valid) {
-  const int ch = (x * kSparseWaves + (int)(threadIdx.x >> 6)) % (BLK / 32);
+                                                 int* n_valid, int ch_in = -1) {
+  const int ch = ch_in >= 0 ? ch_in : (x * kSparseWaves + (int)(threadIdx.x >> 6)) % (BLK / 32);
   L = min(max(L, 0), m.cap);
   const int nb = (L + BLK - 1) / BLK;
   const int blk = blk_sel >= nb ? nb - 1 : blk_sel;
@@ -593,10 +593,10 @@ template <int D, int BLK>
 __device__ __forceinline__ void sparse_load(const Dims& m, const bf16_t* __restrict__ kc,
                                             const bf16_t* __restrict__ vc, int blk, int bh,
                                             int x, const int32_t* __restrict__ table,
-                                            SparseKV<D>& kv) {
+                                            SparseKV<D>& kv, int ch_in = -1) {
   constexpr int KS = D / 32, MT = D / 16;
   const int lane = threadIdx.x & 63;
-  const int ch = (x * kSparseWaves + (int)(threadIdx.x >> 6)) % (BLK / 32);
+  const int ch = ch_in >= 0 ? ch_in : (x * kSparseWaves + (int)(threadIdx.x >> 6)) % (BLK / 32);
   int64_t step0;
   if (table) {
     const int p = block_page(m, table, bh, blk);
@@ -617,7 +617,9 @@ __device__ __forceinline__ void sparse_load(const Dims& m, const bf16_t* __restr
 // The two products of one step (n_valid > 0): S = K [q | phi(q)]^T, the
 // step's softmax over the exact columns, and acc_o = V^T P; m_run / l_run get
 // the step's max and sum (exact columns) or the sum of the linear weights.
-template <int D, int GC>
+// ONLINE: acc_o, m_run and l_run already hold earlier steps of this
+// wavefront; the exact columns are rescaled to the running max first.
+template <int D, int GC, bool ONLINE = false>
 __device__ __forceinline__ void sparse_mma(float s, SparseKV<D>& kv, SparseSmem<D, GC>& sm,
                                            floatx4 (&acc_o)[D / 16], float& m_run,
                                            float& l_run) {
@@ -683,6 +685,14 @@ __device__ __forceinline__ void sparse_mma(float s, SparseKV<D>& kv, SparseSmem<
   }
   cmax = fmaxf(cmax, xor16(cmax));
   cmax = fmaxf(cmax, xor32(cmax));
+  float alpha = 1.f;  // ONLINE: the earlier steps' scale (exact columns)
+  if constexpr (ONLINE) {
+    if (exact_col) {
+      const float mn = fmaxf(m_run, cmax);
+      alpha = m_run == -INFINITY ? 0.f : __expf(m_run - mn);
+      cmax = mn;
+    }
+  }
   float psum = 0.f;
   bf16x8 bh8, bl8;
   float pv[8];
@@ -694,8 +704,14 @@ __device__ __forceinline__ void sparse_mma(float s, SparseKV<D>& kv, SparseSmem<
   split_bf16x8(pv, bh8, bl8);
   psum += xor16(psum);
   psum += xor32(psum);
+  if constexpr (ONLINE) {
+#pragma unroll
+    for (int t = 0; t < MT; ++t) acc_o[t] = acc_o[t] * alpha;
+    l_run = fmaf(l_run, alpha, psum);
+  } else {
+    l_run = psum;
+  }
   m_run = exact_col ? cmax : -INFINITY;
-  l_run = psum;
   if (n_valid < 32) {  // rows past the sequence end may hold anything: zero them
 #pragma unroll
     for (int t = 0; t < MT; ++t)
@@ -811,6 +827,43 @@ __device__ __forceinline__ void sparse_body(const Dims& m, float s,
   if (kv.n_valid > 0) {
     sparse_load<D, BLK>(m, kc, vc, blk, bh, x, table, kv);
     sparse_mma<D, GC>(s, kv, sm, acc_o, m_run, l_run);
+  }
+  sparse_record<D, CO, GC>(m, acc_o, m_run, l_run, bh, x, n_wg, r, sm, part, stride, rec_row);
+}
+
+// sparse_body with SPW consecutive 32-token steps per wavefront: step
+// (x kSparseWaves + w) SPW + j of the selection (B / 32 steps per selected
+// block, entries of sel_row), accumulated online, then one record per
+// workgroup (n_wg = k B / (32 kSparseWaves SPW) records per query).
+template <int D, int BLK, bool CO, int GC, int SPW>
+__device__ __forceinline__ void sparse_body_steps(const Dims& m, float s,
+                                                  const bf16_t* __restrict__ kc,
+                                                  const bf16_t* __restrict__ vc,
+                                                  const int32_t* __restrict__ sel_row, int L,
+                                                  int bh, int x, int n_wg, const SparseRegs& r,
+                                                  SparseSmem<D, GC>& sm, float* __restrict__ part,
+                                                  int stride,
+                                                  const int32_t* __restrict__ table,
+                                                  int64_t rec_row) {
+  constexpr int MT = D / 16, CPB = BLK / 32;
+  floatx4 acc_o[MT];
+#pragma unroll
+  for (int t = 0; t < MT; ++t) acc_o[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+  float m_run = -INFINITY, l_run = 0.f;
+  const int g0 = (x * kSparseWaves + (int)(threadIdx.x >> 6)) * SPW;
+#pragma unroll
+  for (int j = 0; j < SPW; ++j) {
+    const int gs = g0 + j, e = gs / CPB, ch = gs % CPB;
+    const int v = e < m.k ? sel_row[e] : -1;
+    const int blk_sel = __builtin_amdgcn_readfirstlane(v);
+    SparseKV<D> kv;
+    int Lj = L;
+    const int blk = sparse_step_block<BLK>(m, blk_sel, Lj, x, &kv.n_valid, ch);
+    if (kv.n_valid > 0) {
+      sparse_load<D, BLK>(m, kc, vc, blk, bh, x, table, kv, ch);
+      if (j == 0) sparse_mma<D, GC>(s, kv, sm, acc_o, m_run, l_run);
+      else sparse_mma<D, GC, true>(s, kv, sm, acc_o, m_run, l_run);
+    }
   }
   sparse_record<D, CO, GC>(m, acc_o, m_run, l_run, bh, x, n_wg, r, sm, part, stride, rec_row);
 }
