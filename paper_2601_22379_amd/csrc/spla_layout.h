@@ -222,7 +222,7 @@ SPLA_HD bool step_fusable(const Dims& m) {
 
 // ---- chunked prefill workspace ------------------------------------------------
 constexpr int kPrefillChunk = 32;  // positions per chunk of the chunked prefill
-constexpr int kPrefillStepsPerWave = 2;  // 32-token steps per wavefront of its sparse pass
+constexpr int kPrefillStepsPerWave = 8;  // 32-token steps per wavefront of its sparse pass
 
 // The chunked prefill covers the matrix-core shapes (bf16, G <= 8); the other
 // shapes run position by position (the single-token append, then a decode).
