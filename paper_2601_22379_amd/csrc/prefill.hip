@@ -255,33 +255,46 @@ __device__ __forceinline__ float row16_sum(float v) {
 
 // One row of D elements, lane holding elements lane + 64 e (row 0 when !ok,
 // so that the load is issued either way).
-template <int D>
-__device__ __forceinline__ void load_row(const bf16_t* __restrict__ src, float (&x)[D / 64]) {
-  const int lane = threadIdx.x & 63;
+// DE = D / 8 consecutive elements of a bf16 row (16-byte loads), as floats.
+template <int DE>
+__device__ __forceinline__ void load_part(const bf16_t* __restrict__ src, float (&x)[DE]) {
+  static_assert(DE % 8 == 0, "whole 16-byte pieces");
 #pragma unroll
-  for (int e = 0; e < D / 64; ++e) x[e] = bf16_to_f32(src[lane + 64 * e].bits);
+  for (int u = 0; u < DE / 8; ++u) {
+    const uint4 v = *reinterpret_cast<const uint4*>(src + 8 * u);
+    const uint32_t w4[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      x[8 * u + e] = bf16_to_f32((uint16_t)(e & 1 ? w4[e >> 1] >> 16 : w4[e >> 1] & 0xFFFFu));
+  }
 }
 
-// phi(x) of such a row (softmax over the features); zero when !ok.
-template <int D>
-__device__ __forceinline__ void phi_row(float (&x)[D / 64], bool ok, float (&ph)[D / 64]) {
+// phi of a row held by eight consecutive lanes (DE elements each): softmax
+// over the row, the max and sum over the eight lanes by lane swaps; zero
+// when !ok.
+template <int DE>
+__device__ __forceinline__ void phi_part(float (&x)[DE], bool ok) {
   float mx = -INFINITY;
 #pragma unroll
-  for (int e = 0; e < D / 64; ++e) {
+  for (int e = 0; e < DE; ++e) {
     x[e] = ok ? x[e] : 0.f;
     mx = fmaxf(mx, x[e]);
   }
-  mx = wave_max(mx);
+  mx = fmaxf(mx, __shfl_xor(mx, 1, 64));
+  mx = fmaxf(mx, __shfl_xor(mx, 2, 64));
+  mx = fmaxf(mx, __shfl_xor(mx, 4, 64));
   float sum = 0.f;
 #pragma unroll
-  for (int e = 0; e < D / 64; ++e) {
+  for (int e = 0; e < DE; ++e) {
     x[e] = expf(x[e] - mx);
     sum += x[e];
   }
-  sum = wave_sum(sum);
+  sum += __shfl_xor(sum, 1, 64);
+  sum += __shfl_xor(sum, 2, 64);
+  sum += __shfl_xor(sum, 4, 64);
   const float inv = ok ? 1.0f / sum : 0.f;
 #pragma unroll
-  for (int e = 0; e < D / 64; ++e) ph[e] = x[e] * inv;
+  for (int e = 0; e < DE; ++e) x[e] *= inv;
 }
 
 template <int D>
@@ -300,27 +313,26 @@ __global__ __launch_bounds__(256) void prefill_linear_kernel(
   int L0, nv;
   chunk_bounds(m, seq_lens, b, T_, &L0, &nv);
 
-  // phi(K) of the chunk's keys (rows past nv, or past T, are zero); every
-  // row's loads are issued before the first softmax
-  float kx[TP / 4][D / 64];
+  // phi(K) of the chunk's keys (rows past nv, or past T, are zero):
+  // wavefront w takes rows 8 w .. 8 w + 7 at once, eight lanes per row (lane
+  // 8 r + u: coordinates u D / 8 ..)
+  constexpr int DE = D / 8;
+  static_assert(TP == 32, "four wavefronts of eight key rows");
+  {
+    const int i = 8 * w + (lane >> 3), ce = DE * (lane & 7);
+    float kx[DE];
+    load_part<DE>(k_new + ((int64_t)min(i, T_ - 1) * m.bh + bh) * D + ce, kx);
+    phi_part<DE>(kx, i < nv);
 #pragma unroll
-  for (int r = 0; r < TP / 4; ++r)
-    load_row<D>(k_new + ((int64_t)min(w + 4 * r, T_ - 1) * m.bh + bh) * D, kx[r]);
-#pragma unroll
-  for (int r = 0; r < TP / 4; ++r) {
-    const int i = w + 4 * r;
-    float ph[D / 64];
-    phi_row<D>(kx[r], i < nv, ph);
-#pragma unroll
-    for (int e = 0; e < D / 64; ++e) {
-      const int col = lane + 64 * e;
+    for (int e = 0; e < DE; ++e) {
+      const int col = ce + e;
       uint16_t hh, ll;
-      split_bf16(ph[e], hh, ll);
+      split_bf16(kx[e], hh, ll);
       sm.phk_h[i][col] = hh;
       sm.phk_l[i][col] = ll;
       sm.phkT_h[col][i] = hh;
       sm.phkT_l[col][i] = ll;
-      sm.phk_f[i][col] = ph[e];
+      sm.phk_f[i][col] = kx[e];
     }
   }
   for (int e = tid; e < TP * CB; e += 256) {
@@ -342,23 +354,24 @@ __global__ __launch_bounds__(256) void prefill_linear_kernel(
   for (int rt0 = 0; rt0 < n_rt; rt0 += 4) {
     const int rt = rt0 + w;
     const bool act = rt < n_rt;
-    float qx[16][D / 64];  // the tile's 16 query rows, all loads issued first
+    // the tile's 16 query rows, eight at a time with eight lanes per row
+    // (both halves' loads issued first)
+    float qx[2][DE];
+    const int ce = DE * (lane & 7);
 #pragma unroll
-    for (int rr = 0; rr < 16; ++rr) {
-      const int row = rt * 16 + rr;
+    for (int hp = 0; hp < 2; ++hp) {
+      const int row = rt * 16 + 8 * hp + (lane >> 3);
       const bool ok = act && row < R;
       const int i = ok ? row / G : 0, g = ok ? row % G : 0;
-      load_row<D>(q + (((int64_t)i * m.batch + b) * m.hq + h * G + g) * D, qx[rr]);
+      load_part<DE>(q + (((int64_t)i * m.batch + b) * m.hq + h * G + g) * D + ce, qx[hp]);
     }
 #pragma unroll
-    for (int rr = 0; rr < 16; ++rr) {
-      const int row = rt * 16 + rr;
-      const bool ok = act && row < R;
-      float ph[D / 64];
-      phi_row<D>(qx[rr], ok, ph);
+    for (int hp = 0; hp < 2; ++hp) {
+      const int rr = 8 * hp + (lane >> 3), row = rt * 16 + rr;
+      phi_part<DE>(qx[hp], act && row < R);
 #pragma unroll
-      for (int e = 0; e < D / 64; ++e)
-        split_bf16(ph[e], sm.pq_h[w][rr][lane + 64 * e], sm.pq_l[w][rr][lane + 64 * e]);
+      for (int e = 0; e < DE; ++e)
+        split_bf16(qx[hp][e], sm.pq_h[w][rr][ce + e], sm.pq_l[w][rr][ce + e]);
     }
     __syncthreads();
     // A = phi(Q) phi(K)^T, masked, row sums
@@ -420,19 +433,23 @@ __global__ __launch_bounds__(256) void prefill_linear_kernel(
         if (act && row < R) obar[((int64_t)bh * R + row) * D + c0 + cc * 16 + li] = acc[r4];
       }
     }
-    if (cb == 0) {  // zq = phi(Q) . z_bar + the row sums of A
-      for (int rr = 0; rr < 16; ++rr) {
+    if (cb == 0) {  // zq = phi(Q) . z_bar + the row sums of A, eight lanes per row
+#pragma unroll
+      for (int hp = 0; hp < 2; ++hp) {
+        const int rr = 8 * hp + (lane >> 3);
         float p = 0.f;
 #pragma unroll
-        for (int e = 0; e < D / 64; ++e) {
-          const int col = lane + 64 * e;
+        for (int e = 0; e < DE; ++e) {
+          const int col = ce + e;
           const float ph = __builtin_bit_cast(float, (uint32_t)sm.pq_h[w][rr][col] << 16) +
                            __builtin_bit_cast(float, (uint32_t)sm.pq_l[w][rr][col] << 16);
           p = fmaf(ph, sm.zb[col], p);
         }
-        p = wave_sum(p);
+        p += __shfl_xor(p, 1, 64);
+        p += __shfl_xor(p, 2, 64);
+        p += __shfl_xor(p, 4, 64);
         const int row = rt * 16 + rr;
-        if (act && row < R && lane == 0) zq[(int64_t)bh * R + row] = p + sm.rsum[w][rr];
+        if (act && row < R && (lane & 7) == 0) zq[(int64_t)bh * R + row] = p + sm.rsum[w][rr];
       }
     }
     __syncthreads();
