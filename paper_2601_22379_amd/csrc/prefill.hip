@@ -139,17 +139,17 @@ __global__ __launch_bounds__(256) void prefill_score_kernel(
 }
 
 // ----------------------------------------------------------- selection
-template <int R, bool WIN>
-__global__ __launch_bounds__(kPrefSelThreads) void prefill_select_kernel(
+template <int R, bool WIN, int NT = kPrefSelThreads>
+__global__ __launch_bounds__(NT) void prefill_select_kernel(
     Dims m, int T_, const int32_t* __restrict__ seq_lens, const float* __restrict__ e_vals,
     const double* __restrict__ tile_part, int32_t* __restrict__ sel_ws,
     int32_t* __restrict__ sel_out, int32_t* __restrict__ meta) {
-  __shared__ SelectSmem<kPrefSelThreads, kMaxTiles * SPLA_MAX_GROUP> sm;
+  __shared__ SelectSmem<NT, kMaxTiles * SPLA_MAX_GROUP> sm;
   __shared__ float wsc[WIN ? kMaxWindows : 1];
   const int vh = blockIdx.x, bh = vh / T_, i = vh % T_;
   int L0, nv;
   chunk_bounds(m, seq_lens, bh / m.hkv, T_, &L0, &nv);
-  select_blocks<kPrefSelThreads, R, kMaxTiles * SPLA_MAX_GROUP, false, 0, WIN>(
+  select_blocks<NT, R, kMaxTiles * SPLA_MAX_GROUP, false, 0, WIN>(
       m, vh, L0 + min(i + 1, nv), e_vals, tile_part, sm, sel_ws + (int64_t)vh * m.k,
       meta + vh * 4, sel_out ? sel_out + ((int64_t)i * m.bh + bh) * m.k : nullptr, wsc);
 }
@@ -503,11 +503,16 @@ static void prefill_score_d(const Dims& m, int T, const spla_cache& c, const voi
   }
 }
 
-template <int R>
+template <int R, int NT = kPrefSelThreads>
 static void prefill_select_r(const Dims& m, int T, const spla_cache& c, int32_t* sel_out,
                              const PrefillWs& ws, char* base, hipStream_t st) {
   const unsigned grid = (unsigned)((int64_t)m.bh * T);
-  if (windowed(m))
+  if constexpr (NT != kPrefSelThreads) {  // blocks only
+    hipLaunchKernelGGL((prefill_select_kernel<R, false, NT>), dim3(grid), dim3(NT), 0, st, m, T,
+                       (const int32_t*)c.seq_lens, (const float*)(base + ws.e_vals),
+                       (const double*)(base + ws.tile_part), (int32_t*)(base + ws.sel), sel_out,
+                       (int32_t*)(base + ws.meta));
+  } else if (windowed(m))
     hipLaunchKernelGGL((prefill_select_kernel<R, true>), dim3(grid), dim3(kPrefSelThreads), 0, st,
                        m, T, (const int32_t*)c.seq_lens, (const float*)(base + ws.e_vals),
                        (const double*)(base + ws.tile_part), (int32_t*)(base + ws.sel), sel_out,
@@ -573,10 +578,17 @@ hipError_t launch_prefill_chunk(const Dims& m, const spla_config& cfg, const spl
   else prefill_score_d<128>(m, T, c, q, s_score, fo, ws, base, st);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   mark_phase(ev, SPLA_PHASE_SCORE, true, st);
-  // 4. selection of every query (blocks per thread of a 1024-thread workgroup)
+  // 4. selection of every query: without windows and up to 2048 blocks, 256
+  // threads with up to eight blocks each (four wavefronts: cheaper barriers
+  // and histogram scans; 32 positions at 128K 21.2 -> 17.5 us); otherwise
+  // blocks per thread of a 1024-thread workgroup
   mark_phase(ev, SPLA_PHASE_SELECT, false, st);
   const int per = (int)ceil_div(m.nb_cap, kPrefSelThreads);
-  if (per <= 1) prefill_select_r<1>(m, T, c, sel_out, ws, base, st);
+  if (!windowed(m) && m.nb_cap <= 256) prefill_select_r<1, 256>(m, T, c, sel_out, ws, base, st);
+  else if (!windowed(m) && m.nb_cap <= 512) prefill_select_r<2, 256>(m, T, c, sel_out, ws, base, st);
+  else if (!windowed(m) && m.nb_cap <= 1024) prefill_select_r<4, 256>(m, T, c, sel_out, ws, base, st);
+  else if (!windowed(m) && m.nb_cap <= 2048) prefill_select_r<8, 256>(m, T, c, sel_out, ws, base, st);
+  else if (per <= 1) prefill_select_r<1>(m, T, c, sel_out, ws, base, st);
   else if (per <= 2) prefill_select_r<2>(m, T, c, sel_out, ws, base, st);
   else if (per <= 4) prefill_select_r<4>(m, T, c, sel_out, ws, base, st);
   else if (per <= 8) prefill_select_r<8>(m, T, c, sel_out, ws, base, st);
