@@ -25,6 +25,10 @@ __global__ __launch_bounds__(64) void merge_kernel(
     merge_head<T, D, false, false, true>(m, eps, flags, gamma, meta[bh * 4 + 1],
                                          meta[bh * 4 + 2], part + (int64_t)bh * n_rec * stride,
                                          n_rec, stride, out, bh, 2 * (int)blockIdx.y);
+  else if (n_rec > 16)  // uniform: every record's loads in one batch (32 records)
+    merge_head<T, D, false, false, false, 16>(m, eps, flags, gamma, meta[bh * 4 + 1],
+                                              meta[bh * 4 + 2], part + (int64_t)bh * n_rec * stride,
+                                              n_rec, stride, out, bh, (int)blockIdx.y);
   else
     merge_head<T, D, false>(m, eps, flags, gamma, meta[bh * 4 + 1], meta[bh * 4 + 2],
                             part + (int64_t)bh * n_rec * stride, n_rec, stride, out, bh,

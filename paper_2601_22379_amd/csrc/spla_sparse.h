@@ -98,7 +98,7 @@ __device__ __forceinline__ void load_vec(const float* base, uint32_t off, float 
 // computes o_bar and <phi(q), z_bar> for every query in a kernel of its own);
 // obar_add (this query's G x D rows) and zq_add (its G values) are added to
 // the sums of the records' linear fields instead.
-template <typename T, int D, bool CO, bool ADD = false, bool HALF = false>
+template <typename T, int D, bool CO, bool ADD = false, bool HALF = false, int NP = 8>
 __device__ __forceinline__ void merge_head(const Dims& m, float eps, uint32_t flags,
                                            const float* __restrict__ gamma, int all_sel, int L,
                                            const float* rec, int n_rec, int stride,
@@ -107,7 +107,7 @@ __device__ __forceinline__ void merge_head(const Dims& m, float eps, uint32_t fl
                                            const float* __restrict__ zq_add = nullptr) {
   static_assert(!(ADD && HALF), "one head per wavefront with ADD");
   constexpr int E = D / 32;            // coordinates per lane
-  constexpr int NP = 8;                // record pairs (HALF: records) per load batch
+  // NP: record pairs (HALF: records) per load batch
   constexpr int HB = HALF ? 32 : 64;   // records per batch of headers
   constexpr int RS = HALF ? NP : 2 * NP;  // records per batch of bodies
   const int b = bh / m.hkv, h = bh % m.hkv;
