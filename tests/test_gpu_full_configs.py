@@ -17,7 +17,7 @@ from paper_2601_22379_amd import spla
 
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 
-SAMPLES = {"1": 1, "2": 3, "3": 3, "4": 4, "5": 2, "g5": 2}
+SAMPLES = {"1": 1, "2": 32, "3": 32, "4": 32, "5": 8, "g5": 8}
 
 
 @pytest.fixture(scope="module")
