@@ -124,7 +124,7 @@ def test_full_size_strided_selection(dev):
     sel = sel.cpu().numpy()
     check_properties(w, sel, out, w.lengths)
     p = H.params_of(w, window=C, stride=s)
-    pairs = sample_pairs(w, 2, 1)
+    pairs = sample_pairs(w, 8, 1)
     H.log(f"strided config 3: oracle on {pairs}")
     infos = [H.check_kv_head(w, b, h, out[b], sel[b, h], q[b], gamma, p) for b, h in pairs]
     H.log(f"strided config 3: worst rel err {max(i['rel_err'] for i in infos):.3e}, "
@@ -161,6 +161,6 @@ def test_full_size_paged_cache(dev):
     sel = sel_p.cpu().numpy()
     check_properties(w, sel, out, w.lengths)
     p = H.params_of(w)
-    pairs = sample_pairs(w, 2, 2)
+    pairs = sample_pairs(w, 8, 2)
     infos = [H.check_kv_head(w, b, h, out[b], sel[b, h], q[b], gamma, p) for b, h in pairs]
     H.log(f"paged config 3: worst rel err {max(i['rel_err'] for i in infos):.3e}")
