@@ -380,9 +380,9 @@ enum { SPLA_NOALLOC_SCRATCH_BYTES = 64 << 20 };
  * GPU the library runs on holds one copy until the process ends. The first
  * call on a device takes its address (hipGetSymbolAddress, with that device
  * current) and zero-fills it on `stream`; later calls allocate nothing and
- * call no allocating routine. Every call clears the single-launch decode's
- * counters in the scratch with a fill kernel before the decode (the previous
- * call may have used another shape). All calls on one device share the
+ * call no allocating routine. Every call clears the decode's counters (its
+ * synchronisation area) in the scratch with a fill kernel before the decode
+ * (the previous call may have used another shape). All calls on one device share the
  * scratch and it keeps the last call's contents: calls that overlap on one
  * GPU (other streams or threads) race, and their outputs are undefined. */
 int32_t spla_decode_noalloc(const spla_config* cfg, const spla_cache* cache, const void* q,

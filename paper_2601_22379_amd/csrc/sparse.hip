@@ -57,8 +57,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void s
   const int b = bh / m.hkv, h = bh % m.hkv;
   const int G = m.group;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int nsel = meta[bh * 4 + 0];
-  const int L = meta[bh * 4 + 2];
+  const int nsel = min(max(meta[bh * 4 + 0], 0), m.k);
+  const int L = min(max(meta[bh * 4 + 2], 0), m.cap);  // as the matrix-core pass clips it
   const int nb = (L + m.B - 1) / m.B;
   // workgroup split: sub-tile sub0 of selection entry p0 (B / 32 sub-tiles
   // per block), so a block's sub-tiles run side by side

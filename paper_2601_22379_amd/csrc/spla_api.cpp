@@ -79,15 +79,20 @@ int32_t run_decode(const spla_config* cfg, const spla_cache* cache, const void* 
       SPLA_TRY(spla::launch_decode_fused(m, *cfg, *cache, q, w, out, sel_idx, L, base, st));
     return SPLA_OK;
   }
+  // the selection runs in its own launch, or in the scoring launch's last
+  // workgroup of each head, or in the sparse launch (the select phase empty)
+  const bool in_sparse = spla::sparse_selects(m, k_step != nullptr);
+  const bool in_score = !in_sparse && spla::score_selects(m);
   {
     PhaseMark pm(ev, st, SPLA_PHASE_SCORE);
-    SPLA_TRY(spla::launch_score(m, *cfg, *cache, q, L, base, st));
+    if (in_score)
+      SPLA_TRY(spla::launch_score_select(m, *cfg, *cache, q, L, base, sel_idx, st));
+    else
+      SPLA_TRY(spla::launch_score(m, *cfg, *cache, q, L, base, st));
   }
-  if (!spla::sparse_selects(m, k_step != nullptr)) {
-    PhaseMark pm(ev, st, SPLA_PHASE_SELECT);
-    SPLA_TRY(spla::launch_select(m, *cache, L, base, sel_idx, st));
-  } else {
-    PhaseMark pm(ev, st, SPLA_PHASE_SELECT);  // folded into the sparse launch: empty
+  {
+    PhaseMark pm(ev, st, SPLA_PHASE_SELECT);  // empty when folded into another launch
+    if (!in_sparse && !in_score) SPLA_TRY(spla::launch_select(m, *cache, L, base, sel_idx, st));
   }
   {
     PhaseMark pm(ev, st, SPLA_PHASE_SPARSE);
@@ -331,11 +336,11 @@ extern "C" int32_t spla_decode_noalloc(const spla_config* cfg, const spla_cache*
   if ((s = device_scratch(st, &base)) != SPLA_OK) return s;
   const Dims m = spla::make_dims(*cfg);
   const spla::DecodeWs L = spla::decode_ws_layout(m);
-  // the single-launch decode needs its counters at zero; the previous call
-  // may have left other data there (another layout), so they are cleared
-  // with a fill kernel on every call
-  if (spla::use_fused_decode(m) && !(cfg->flags & SPLA_FLAG_SEPARATE_KERNELS))
-    SPLA_TRY(spla::launch_fill_zero(static_cast<char*>(base) + L.sync, (size_t)(L.total - L.sync),
-                                    st));
+  // the counters (single launch, selection folded into the scoring launch,
+  // two-stage selection) must start at zero; the previous call may have
+  // left other data there (another layout), so the synchronisation area is
+  // cleared with a fill kernel on every call
+  SPLA_TRY(spla::launch_fill_zero(static_cast<char*>(base) + L.sync, (size_t)(L.total - L.sync),
+                                  st));
   return run_decode(cfg, cache, q, w, out, sel_idx, base, need, nullptr, st);
 }

@@ -50,6 +50,12 @@ hipError_t launch_append_finish(const Dims& m, const spla_cache& c, int max_new,
 hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t st);
 
 // score.hip: block scoring
+// the scoring launch with the selection folded in (score_selects shapes; in
+// place of launch_score + launch_select)
+bool score_selects(const Dims& m);
+hipError_t launch_score_select(const Dims& m, const spla_config& cfg, const spla_cache& c,
+                               const void* q, const DecodeWs& ws, char* wsbase, int32_t* sel_out,
+                               hipStream_t st);
 hipError_t launch_score(const Dims& m, const spla_config& cfg, const spla_cache& c,
                         const void* q, const DecodeWs& ws, char* wsbase, hipStream_t st);
 

@@ -129,8 +129,9 @@ struct DecodeWs {
   int64_t cand_key;   // u32 [bh][n_sl][k]         two-stage selection: slice candidates' keys
   int64_t cand_id;    // i32 [bh][n_sl][k]         ... their block ids (ascending per slice)
   int64_t cand_n;     // i32 [bh][n_sl]            ... their count per slice
-  int64_t sync;       // i32 [sync_layout(m).words]  counters of the single-launch decode;
-                      //   zero between calls
+  int64_t sync;       // i32 [sync_layout(m).words]  counters of the single-launch decode,
+                      //   of the scoring launch that selects and of the two-stage
+                      //   selection; zero between calls
   int64_t total;
   int n_sl;           // slices of the two-stage selection
   int n_wg;           // sparse workgroups per (sequence, kv head)
